@@ -1,0 +1,167 @@
+"""CPU oracle for the tree-verification step -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the package smoke check and the benchmark's CPU-baseline leg may import this package.
+The product (the HIP library and its Python binding) never imports, links or calls it.
+
+Thin ctypes wrapper over ``oracle.c`` (plain C, fp64 accumulation; that file states what each function
+computes and which passage of the paper it follows).  The shared library is built with gcc by :func:`build`
+-- no hipcc, no header shared with the HIP path.  :class:`Oracle` can also wrap a differently built copy of
+the source (the mutation tests compile copies with planted mistakes to show that the pins catch them).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_DIR = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(_DIR, "oracle.c")
+LIBRARY = os.path.join(_DIR, "liboracle.so")
+
+
+def compile_source(src_path: str, lib_path: str) -> str:
+    """Compile an oracle C source with gcc -O2 (no fast-math) and OpenMP into a shared library."""
+    tmp = lib_path + ".tmp%d" % os.getpid()
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+                           "-o", tmp, src_path, "-lm"])
+    os.replace(tmp, lib_path)
+    return lib_path
+
+
+def build(force: bool = True) -> str:
+    """Build liboracle.so next to oracle.c."""
+    if force or not os.path.exists(LIBRARY):
+        compile_source(SOURCE, LIBRARY)
+    return LIBRARY
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise OracleError("%s failed with code %d" % (what, rc))
+
+
+class Oracle:
+    """The oracle's four entry points over one built library."""
+
+    def __init__(self, lib_path: str):
+        lib = ctypes.CDLL(lib_path)
+        P, I = ctypes.c_void_p, ctypes.c_int
+        lib.oracle_tree_attn.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, P, P, P]
+        lib.oracle_tree_attn_rows.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, P, I, P, P, P]
+        lib.oracle_tree_accept.argtypes = [I, I, I, P, P, P, P, P, P, P]
+        lib.oracle_kv_commit.argtypes = [I, ctypes.c_int64, I, I, I, I, I, P, P, P, P, P, I, P]
+        for f in (lib.oracle_tree_attn, lib.oracle_tree_attn_rows, lib.oracle_tree_accept, lib.oracle_kv_commit):
+            f.restype = ctypes.c_int
+        self.lib = lib
+        self.path = lib_path
+
+    def tree_attn(self, q, k_cache, v_cache, kv_len, parent, scale: float, num_kv_heads: int,
+                  tree_mask=None, with_lse: bool = True):
+        """q [B,Hq,T,D]; k/v [B,Hkv,S_cap,D] (fp32 values); kv_len [B]; parent [B,T] (or None together with
+        tree_mask [B,T,ceil(T/64)] uint64).  Returns (out [B,Hq,T,D] float64, lse [B,Hq,T] float64)."""
+        q = _c(q, np.float32)
+        k_cache = _c(k_cache, np.float32)
+        v_cache = _c(v_cache, np.float32)
+        B, Hq, T, D = q.shape
+        S_cap = k_cache.shape[2]
+        assert k_cache.shape == (B, num_kv_heads, S_cap, D) and v_cache.shape == k_cache.shape
+        kv_len = _c(kv_len, np.int32)
+        parent = _c(parent, np.int32)
+        tree_mask = _c(tree_mask, np.uint64)
+        out = np.empty((B, Hq, T, D), dtype=np.float64)
+        lse = np.empty((B, Hq, T), dtype=np.float64) if with_lse else None
+        rc = self.lib.oracle_tree_attn(B, Hq, num_kv_heads, T, D, S_cap, float(scale), _p(q), _p(k_cache),
+                                       _p(v_cache), _p(kv_len), _p(parent), _p(tree_mask), _p(out), _p(lse))
+        _check(rc, "oracle_tree_attn")
+        return out, lse
+
+    def tree_attn_rows(self, q, k_cache, v_cache, kv_len, parent, scale: float, num_kv_heads: int, rows,
+                       tree_mask=None):
+        """Selected rows only: rows is an [n, 3] array of (b, h, i).  Returns (out [n, D], lse [n])."""
+        q = _c(q, np.float32)
+        k_cache = _c(k_cache, np.float32)
+        v_cache = _c(v_cache, np.float32)
+        B, Hq, T, D = q.shape
+        S_cap = k_cache.shape[2]
+        rows = _c(rows, np.int32).reshape(-1, 3)
+        kv_len = _c(kv_len, np.int32)
+        parent = _c(parent, np.int32)
+        tree_mask = _c(tree_mask, np.uint64)
+        out = np.empty((rows.shape[0], D), dtype=np.float64)
+        lse = np.empty(rows.shape[0], dtype=np.float64)
+        rc = self.lib.oracle_tree_attn_rows(B, Hq, num_kv_heads, T, D, S_cap, float(scale), _p(q),
+                                            _p(k_cache), _p(v_cache), _p(kv_len), _p(parent), _p(tree_mask),
+                                            rows.shape[0], _p(rows), _p(out), _p(lse))
+        _check(rc, "oracle_tree_attn_rows")
+        return out, lse
+
+    def tree_accept(self, logits, tokens, parent):
+        """Returns (accept_len [B], accept_path [B,T], next_token [B], target_argmax [B,T]), all int32."""
+        logits = _c(logits, np.float32)
+        B, T, V = logits.shape
+        tokens = _c(tokens, np.int32)
+        parent = _c(parent, np.int32)
+        alen = np.empty(B, dtype=np.int32)
+        path = np.empty((B, T), dtype=np.int32)
+        nxt = np.empty(B, dtype=np.int32)
+        am = np.empty((B, T), dtype=np.int32)
+        rc = self.lib.oracle_tree_accept(B, T, V, _p(logits), _p(tokens), _p(parent), _p(alen), _p(path),
+                                         _p(nxt), _p(am))
+        _check(rc, "oracle_tree_accept")
+        return alen, path, nxt, am
+
+    def kv_commit(self, k_cache: np.ndarray, v_cache: np.ndarray, kv_len_in, accept_path, accept_len):
+        """In place on k_cache / v_cache of shape [NL, B, Hkv, S_cap, D] (uint16 bf16 bits or float32).
+        Returns kv_len_out [B]."""
+        assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous and k_cache.shape == v_cache.shape
+        NL, B, Hkv, S_cap, D = k_cache.shape
+        accept_path = _c(accept_path, np.int32)
+        out = np.empty(B, dtype=np.int32)
+        rc = self.lib.oracle_kv_commit(NL, B * Hkv * S_cap * D, B, Hkv, D, S_cap, k_cache.dtype.itemsize,
+                                       _p(k_cache), _p(v_cache), _p(_c(kv_len_in, np.int32)), _p(accept_path),
+                                       _p(_c(accept_len, np.int32)), accept_path.shape[1], _p(out))
+        _check(rc, "oracle_kv_commit")
+        return out
+
+
+_default: Optional[Oracle] = None
+
+
+def default() -> Oracle:
+    global _default
+    if _default is None:
+        if not os.path.exists(LIBRARY):
+            build(force=False)
+        _default = Oracle(LIBRARY)
+    return _default
+
+
+def tree_attn(*a, **kw):
+    return default().tree_attn(*a, **kw)
+
+
+def tree_attn_rows(*a, **kw):
+    return default().tree_attn_rows(*a, **kw)
+
+
+def tree_accept(*a, **kw):
+    return default().tree_accept(*a, **kw)
+
+
+def kv_commit(*a, **kw):
+    return default().kv_commit(*a, **kw)

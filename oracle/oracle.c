@@ -1,0 +1,255 @@
+/*
+ * oracle.c -- plain, slow CPU oracle for the DREAM-S tree-verification step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or load this file: only the test
+ * suite, the package smoke check and the benchmark's CPU-baseline leg use it.  It shares no code, header or
+ * constant with the HIP library; both are fed from the same seeded input generator.
+ *
+ * Everything here is the plain definition of what the verification step computes, written out with
+ * scalar loops and fp64 accumulation (inputs are fp32 values; bf16 inputs arrive already widened, which is
+ * exact).  No blocking, no online softmax, no split of the key axis, no fast-math.
+ *
+ *  oracle_tree_attn / oracle_tree_attn_row
+ *      Masked softmax attention  A = softmax(Q K^T * scale), out = A V  (the attention matrix as the paper
+ *      defines it in Section 3.2, "Adaptive Intermediate Feature Distillation"; scale = 1/sqrt(head_dim)
+ *      is passed explicitly).  Each tree node attends to every committed prefix slot -- image and text
+ *      tokens alike, since the paper's Section 2 ("Vision-Language Models") notes that all visual tokens sit
+ *      in the KV cache and are attended at every decoding step -- plus the tree slots of its own ancestors
+ *      and itself, so that each root-to-node path is verified exactly as the sequential draft it stands for
+ *      (Section 2, "Speculative decoding": drafts are verified in one parallel pass).
+ *      Softmax is taken in two passes (max, then exp/sum), the textbook way.
+ *
+ *  oracle_tree_accept
+ *      Greedy verification (Section 2, "Speculative decoding"): a draft token is kept while it equals the
+ *      target's own choice at its position; at the first mismatch the target's token replaces it.  On a tree
+ *      this is applied along every root-to-node path; the longest consistent path wins (deepest node,
+ *      smallest index on ties) and the target's token at its end is emitted as the bonus token, so one
+ *      step emits depth+1 tokens (the paper's Table 6 prints acceptance lengths above the draft window,
+ *      which counts that bonus token).
+ *
+ *  oracle_kv_commit
+ *      Keeps the root and the accepted nodes' K/V as the next contiguous cache slots, in path order.
+ *
+ * Return value of every entry point: 0 on success, negative on invalid input (nothing written then).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_BAD_ARG (-1)
+#define ORACLE_BAD_TREE (-2)
+#define ORACLE_NONFINITE (-3)
+
+/* parent[0] = -1 and 0 <= parent[i] < i for i >= 1. */
+static int tree_ok(const int32_t* parent, int T) {
+  if (T < 1 || parent[0] != -1) return 0;
+  for (int i = 1; i < T; ++i)
+    if (parent[i] < 0 || parent[i] >= i) return 0;
+  return 1;
+}
+
+/* visible[j] = 1 iff tree node j may be attended by tree node i. */
+static void visible_nodes(const int32_t* parent, const uint64_t* mask_row, int T, int i, unsigned char* visible) {
+  memset(visible, 0, (size_t)T);
+  if (mask_row) {
+    for (int j = 0; j < T; ++j) visible[j] = (unsigned char)((mask_row[j / 64] >> (j % 64)) & 1u);
+  } else {
+    for (int j = i; j >= 0; j = parent[j]) visible[j] = 1;   /* i, its parent, ..., the root */
+  }
+}
+
+/* One output row: sequence b, query head h, tree node i. */
+static void attn_row(int Hq, int Hkv, int T, int D, int S_cap, double scale, const float* q, const float* k,
+                     const float* v, const int32_t* kv_len, const int32_t* parent, const uint64_t* tree_mask,
+                     int b, int h, int i, double* out_row, double* lse_out, unsigned char* visible,
+                     double* score) {
+  const int G = Hq / Hkv;
+  const int g = h / G;                      /* KV head shared by query head h */
+  const int L = kv_len[b];
+  const int W = (T + 63) / 64;
+  const float* qi = q + (((size_t)b * Hq + h) * T + i) * D;
+  const float* kb = k + ((size_t)b * Hkv + g) * (size_t)S_cap * D;
+  const float* vb = v + ((size_t)b * Hkv + g) * (size_t)S_cap * D;
+  visible_nodes(parent ? parent + (size_t)b * T : NULL,
+                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);
+
+  /* slots 0..L-1 are the committed prefix; slot L+j holds tree node j */
+  const int n = L + T;
+  double m = -INFINITY;
+  for (int s = 0; s < n; ++s) {
+    if (s >= L && !visible[s - L]) continue;
+    double dot = 0.0;
+    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];
+    score[s] = scale * dot;
+    if (score[s] > m) m = score[s];
+  }
+  for (int d = 0; d < D; ++d) out_row[d] = 0.0;
+  if (m == -INFINITY) { /* nothing visible: defined as a zero row with lse = -inf */
+    *lse_out = -INFINITY;
+    return;
+  }
+  double l = 0.0;
+  for (int s = 0; s < n; ++s) {
+    if (s >= L && !visible[s - L]) continue;
+    double p = exp(score[s] - m);
+    l += p;
+    for (int d = 0; d < D; ++d) out_row[d] += p * (double)vb[(size_t)s * D + d];
+  }
+  for (int d = 0; d < D; ++d) out_row[d] /= l;
+  *lse_out = m + log(l);
+}
+
+static int attn_args_ok(int B, int Hq, int Hkv, int T, int D, int S_cap, const int32_t* kv_len,
+                        const int32_t* parent, const uint64_t* tree_mask) {
+  if (B < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || T < 1 || D < 1 || S_cap < T) return ORACLE_BAD_ARG;
+  if (!parent && !tree_mask) return ORACLE_BAD_ARG;
+  for (int b = 0; b < B; ++b) {
+    if (kv_len[b] < 0 || kv_len[b] + T > S_cap) return ORACLE_BAD_ARG;
+    if (!tree_mask && !tree_ok(parent + (size_t)b * T, T)) return ORACLE_BAD_TREE;
+  }
+  return 0;
+}
+
+/* Layouts: q, out [B,Hq,T,D]; k, v [B,Hkv,S_cap,D]; lse [B,Hq,T]; tree_mask [B,T,ceil(T/64)] or NULL. */
+int oracle_tree_attn(int B, int Hq, int Hkv, int T, int D, int S_cap, double scale, const float* q,
+                     const float* k, const float* v, const int32_t* kv_len, const int32_t* parent,
+                     const uint64_t* tree_mask, double* out, double* lse) {
+  int rc = attn_args_ok(B, Hq, Hkv, T, D, S_cap, kv_len, parent, tree_mask);
+  if (rc) return rc;
+#pragma omp parallel
+  {
+    unsigned char* visible = (unsigned char*)malloc((size_t)T);
+    double* score = (double*)malloc(sizeof(double) * (size_t)(S_cap + 1));
+#pragma omp for collapse(2) schedule(dynamic)
+    for (int b = 0; b < B; ++b)
+      for (int h = 0; h < Hq; ++h)
+        for (int i = 0; i < T; ++i) {
+          size_t r = ((size_t)b * Hq + h) * T + i;
+          double lse_r;
+          attn_row(Hq, Hkv, T, D, S_cap, scale, q, k, v, kv_len, parent, tree_mask, b, h, i,
+                   out + r * D, &lse_r, visible, score);
+          if (lse) lse[r] = lse_r;
+        }
+    free(visible);
+    free(score);
+  }
+  return 0;
+}
+
+/* Selected rows only: rows[3*n + {0,1,2}] = (b, h, i); out_rows [n, D], lse_rows [n]. */
+int oracle_tree_attn_rows(int B, int Hq, int Hkv, int T, int D, int S_cap, double scale, const float* q,
+                          const float* k, const float* v, const int32_t* kv_len, const int32_t* parent,
+                          const uint64_t* tree_mask, int n_rows, const int32_t* rows, double* out_rows,
+                          double* lse_rows) {
+  int rc = attn_args_ok(B, Hq, Hkv, T, D, S_cap, kv_len, parent, tree_mask);
+  if (rc) return rc;
+  for (int r = 0; r < n_rows; ++r) {
+    int b = rows[3 * r], h = rows[3 * r + 1], i = rows[3 * r + 2];
+    if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= T) return ORACLE_BAD_ARG;
+  }
+#pragma omp parallel
+  {
+    unsigned char* visible = (unsigned char*)malloc((size_t)T);
+    double* score = (double*)malloc(sizeof(double) * (size_t)(S_cap + 1));
+#pragma omp for schedule(dynamic)
+    for (int r = 0; r < n_rows; ++r) {
+      double lse_r;
+      attn_row(Hq, Hkv, T, D, S_cap, scale, q, k, v, kv_len, parent, tree_mask, rows[3 * r], rows[3 * r + 1],
+               rows[3 * r + 2], out_rows + (size_t)r * D, &lse_r, visible, score);
+      if (lse_rows) lse_rows[r] = lse_r;
+    }
+    free(visible);
+    free(score);
+  }
+  return 0;
+}
+
+/*
+ * Greedy tree acceptance.  logits [B,T,V] (target logits at every node), tokens [B,T] (draft token of every
+ * node; tokens[b][0] is the root, already emitted), parent [B,T].
+ * Outputs: accept_len [B] = number of accepted draft tokens a (the depth of the last accepted node);
+ * accept_path [B,T] = node ids root..last then -1; next_token [B] = target token after the last accepted
+ * node; target_argmax [B,T] (may be NULL) = the target's token at every node.
+ */
+int oracle_tree_accept(int B, int T, int V, const float* logits, const int32_t* tokens, const int32_t* parent,
+                       int32_t* accept_len, int32_t* accept_path, int32_t* next_token, int32_t* target_argmax) {
+  if (B < 0 || T < 1 || V < 1) return ORACLE_BAD_ARG;
+  for (int b = 0; b < B; ++b)
+    if (!tree_ok(parent + (size_t)b * T, T)) return ORACLE_BAD_TREE;
+  for (size_t e = 0; e < (size_t)B * T * V; ++e)
+    if (!isfinite(logits[e])) return ORACLE_NONFINITE;
+
+  int* am = (int*)malloc(sizeof(int) * (size_t)T);
+  int* ok = (int*)malloc(sizeof(int) * (size_t)T);
+  int* depth = (int*)malloc(sizeof(int) * (size_t)T);
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int32_t* tok = tokens + (size_t)b * T;
+    /* the target's token at node i: the smallest index attaining the row maximum */
+    for (int i = 0; i < T; ++i) {
+      const float* row = logits + ((size_t)b * T + i) * V;
+      int best = 0;
+      for (int x = 1; x < V; ++x)
+        if (row[x] > row[best]) best = x;
+      am[i] = best;
+    }
+    /* a node is consistent iff its parent is and its token is the target's token at the parent */
+    ok[0] = 1;
+    depth[0] = 0;
+    for (int i = 1; i < T; ++i) {
+      ok[i] = ok[par[i]] && tok[i] == am[par[i]];
+      depth[i] = depth[par[i]] + 1;
+    }
+    int last = 0;
+    for (int i = 1; i < T; ++i)
+      if (ok[i] && depth[i] > depth[last]) last = i;
+    const int a = depth[last];
+    int32_t* path = accept_path + (size_t)b * T;
+    for (int k = 0; k < T; ++k) path[k] = -1;
+    for (int j = last; j >= 0; j = par[j]) path[depth[j]] = j;
+    accept_len[b] = a;
+    next_token[b] = am[last];
+    if (target_argmax)
+      for (int i = 0; i < T; ++i) target_argmax[(size_t)b * T + i] = am[i];
+  }
+  free(am);
+  free(ok);
+  free(depth);
+  return 0;
+}
+
+/*
+ * KV commit.  Cache layers are layer_stride_elems elements apart; inside a layer the layout is
+ * [B, Hkv, S_cap, D] with elements of elem_bytes bytes.  For k = 0..a (increasing), slot L+path[k] is copied
+ * to slot L+k for every layer and KV head; kv_len_out[b] = L + a + 1.  Copies are bytewise.
+ */
+int oracle_kv_commit(int NL, int64_t layer_stride_elems, int B, int Hkv, int D, int S_cap, int elem_bytes,
+                     void* k_cache, void* v_cache, const int32_t* kv_len_in, const int32_t* accept_path,
+                     const int32_t* accept_len, int path_stride, int32_t* kv_len_out) {
+  if (NL < 1 || B < 0 || Hkv < 1 || D < 1 || S_cap < 1 || (elem_bytes != 2 && elem_bytes != 4)) return ORACLE_BAD_ARG;
+  for (int b = 0; b < B; ++b) {
+    const int a = accept_len[b];
+    const int32_t* path = accept_path + (size_t)b * path_stride;
+    if (a < 0 || a >= path_stride || path[0] != 0) return ORACLE_BAD_ARG;
+    for (int k = 1; k <= a; ++k)
+      if (path[k] < k || path[k] <= path[k - 1]) return ORACLE_BAD_ARG;
+    if (kv_len_in[b] + path[a] >= S_cap) return ORACLE_BAD_ARG;
+  }
+  const size_t row = (size_t)D * elem_bytes;
+  for (int layer = 0; layer < NL; ++layer)
+    for (int b = 0; b < B; ++b)
+      for (int g = 0; g < Hkv; ++g) {
+        const size_t base = ((size_t)layer * layer_stride_elems + ((size_t)b * Hkv + g) * (size_t)S_cap * D) * elem_bytes;
+        const int L = kv_len_in[b];
+        const int32_t* path = accept_path + (size_t)b * path_stride;
+        for (int k = 0; k <= accept_len[b]; ++k) {
+          char* kc = (char*)k_cache + base;
+          char* vc = (char*)v_cache + base;
+          memmove(kc + (size_t)(L + k) * row, kc + (size_t)(L + path[k]) * row, row);
+          memmove(vc + (size_t)(L + k) * row, vc + (size_t)(L + path[k]) * row, row);
+        }
+      }
+  for (int b = 0; b < B; ++b) kv_len_out[b] = kv_len_in[b] + accept_len[b] + 1;
+  return 0;
+}

@@ -1,0 +1,498 @@
+"""Pins for the CPU oracle: checks against what the paper and the mathematics fix, independent of the oracle's
+own code.  Each pin is a function of an ``oracle.Oracle`` instance so that the same checks can be run against
+copies of the oracle with planted mistakes (tests/test_oracle_mutants.py) to show that they would catch them.
+
+Sources of truth used here: brute-force dense masked softmax (numpy, fp64) with the ancestor relation built
+as a transitive closure; library attention (torch scaled_dot_product_attention, fp64) for the chain and
+single-node special cases; closed forms; invariants (non-ancestor perturbation, relabelling); exhaustive
+enumeration of root-to-node paths for acceptance; the greedy rule's worked instances in tests/golden; the exact
+expected acceptance length of the independent-agreement model; and a direct numpy gather for the commit.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+from scipy.special import logsumexp
+
+from paper_2606_00535_amd import workload as W
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ------------------------------------------------------------------------------------------ helpers (numpy)
+def ancestor_closure(parent: np.ndarray) -> np.ndarray:
+    """C[i, j] = True iff node j is node i or one of its ancestors (reflexive-transitive closure of the
+    child->parent relation, by repeated boolean matrix products)."""
+    T = len(parent)
+    A = np.zeros((T, T), dtype=bool)
+    for i in range(1, T):
+        A[i, parent[i]] = True
+    C = np.eye(T, dtype=bool)
+    for _ in range(T):
+        C = C | ((C.astype(np.int64) @ A.astype(np.int64)) > 0)
+    return C
+
+
+def mask_bits_from_closure(C: np.ndarray) -> np.ndarray:
+    T = C.shape[0]
+    Wd = (T + 63) // 64
+    bits = np.zeros((T, Wd), dtype=np.uint64)
+    for i in range(T):
+        for j in range(T):
+            if C[i, j]:
+                bits[i, j // 64] |= np.uint64(1) << np.uint64(j % 64)
+    return bits
+
+
+def dense_tree_attention(q, k, v, kv_len, parent, scale, Hkv):
+    """Brute force: per (b, h) a dense [T, L+T] score matrix, -inf outside the visibility mask, softmax, @V."""
+    q = q.astype(np.float64)
+    B, Hq, T, D = q.shape
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, T, D))
+    lse = np.zeros((B, Hq, T))
+    for b in range(B):
+        L = int(kv_len[b])
+        C = ancestor_closure(parent[b])
+        vis = np.concatenate([np.ones((T, L), dtype=bool), C], axis=1)
+        for h in range(Hq):
+            g = h // G
+            K = k[b, g, :L + T].astype(np.float64)
+            V = v[b, g, :L + T].astype(np.float64)
+            s = scale * (q[b, h] @ K.T)
+            s[~vis] = -np.inf
+            lse[b, h] = logsumexp(s, axis=1)
+            out[b, h] = np.exp(s - lse[b, h][:, None]) @ V
+    return out, lse
+
+
+def random_inputs(rng, B, Hq, Hkv, T, D, L, extra=0, dtype=np.float32):
+    S = L + T + extra
+    q = rng.standard_normal((B, Hq, T, D)).astype(dtype)
+    k = rng.standard_normal((B, Hkv, S, D)).astype(dtype)
+    v = rng.standard_normal((B, Hkv, S, D)).astype(dtype)
+    return q, k, v
+
+
+def random_parent(rng, T, max_branch=3):
+    if T == 1:
+        return np.array([-1], dtype=np.int32)
+    depth = int(rng.integers(1, T))
+    b = max_branch
+    while sum(b ** d for d in range(depth + 1)) < T:
+        b += 1
+    return W.random_tree(rng, T, depth, b)
+
+
+# ---------------------------------------------------------------------------------------- attention pins
+def pin_attn_bruteforce(orc):
+    rng = np.random.default_rng(1234)
+    for (B, Hq, Hkv, D) in [(1, 2, 2, 8), (2, 4, 2, 8), (1, 3, 1, 16)]:
+        for L in (0, 1, 5, 17):
+            for T in (1, 2, 5, 16):
+                q, k, v = random_inputs(rng, B, Hq, Hkv, T, D, L, extra=3)
+                parent = np.stack([random_parent(rng, T) for _ in range(B)])
+                kv_len = np.full(B, L, dtype=np.int32)
+                scale = 1.0 / np.sqrt(D)
+                o, lse = orc.tree_attn(q, k, v, kv_len, parent, scale, Hkv)
+                eo, else_ = dense_tree_attention(q, k, v, kv_len, parent, scale, Hkv)
+                assert np.max(np.abs(o - eo)) <= 1e-12, (B, Hq, Hkv, D, L, T)
+                assert np.max(np.abs(lse - else_)) <= 1e-12, (B, Hq, Hkv, D, L, T)
+    # ragged prefix lengths inside one batch
+    B, Hq, Hkv, D, T = 3, 2, 1, 8, 7
+    q, k, v = random_inputs(rng, B, Hq, Hkv, T, D, 20)
+    parent = np.stack([random_parent(rng, T) for _ in range(B)])
+    kv_len = np.array([0, 20, 9], dtype=np.int32)
+    o, lse = orc.tree_attn(q, k, v, kv_len, parent, 0.3, Hkv)
+    eo, else_ = dense_tree_attention(q, k, v, kv_len, parent, 0.3, Hkv)
+    assert np.max(np.abs(o - eo)) <= 1e-12 and np.max(np.abs(lse - else_)) <= 1e-12
+
+
+def _torch_sdpa(q, k, v, mask, scale):
+    import torch
+    tq = torch.from_numpy(np.asarray(q, dtype=np.float64))
+    tk = torch.from_numpy(np.asarray(k, dtype=np.float64))
+    tv = torch.from_numpy(np.asarray(v, dtype=np.float64))
+    tm = None if mask is None else torch.from_numpy(mask)
+    return torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=tm, scale=scale).numpy()
+
+
+def pin_attn_chain_is_causal(orc):
+    """A chain-shaped tree is ordinary causal attention of T new tokens after an L-token prefix (explicit
+    bottom-right-aligned causal mask: new token i sees the prefix and new tokens 0..i)."""
+    rng = np.random.default_rng(7)
+    for (L, T, D) in [(0, 6, 16), (11, 9, 16), (40, 16, 32)]:
+        q, k, v = random_inputs(rng, 1, 2, 2, T, D, L)
+        parent = W.chain_tree(T)[None]
+        o, _ = orc.tree_attn(q, k, v, np.array([L], np.int32), parent, 1.0 / np.sqrt(D), 2)
+        mask = np.zeros((T, L + T), dtype=bool)
+        for i in range(T):
+            mask[i, :L + i + 1] = True
+        ref = _torch_sdpa(q[0], k[0, :, :L + T], v[0, :, :L + T], mask, 1.0 / np.sqrt(D))
+        assert np.max(np.abs(o[0] - ref)) <= 1e-12, (L, T)
+
+
+def pin_attn_single_node_is_decode(orc):
+    """T = 1 is one decode step: plain softmax attention over the L prefix keys plus the node's own key."""
+    rng = np.random.default_rng(8)
+    for L in (0, 1, 33, 200):
+        q, k, v = random_inputs(rng, 1, 4, 2, 1, 16, L)
+        o, _ = orc.tree_attn(q, k, v, np.array([L], np.int32), np.array([[-1]], np.int32), 0.25, 2)
+        kk = np.repeat(k[0, :, :L + 1], 2, axis=0)      # query head h reads KV head h // 2
+        vv = np.repeat(v[0, :, :L + 1], 2, axis=0)
+        ref = _torch_sdpa(q[0], kk, vv, None, 0.25)
+        assert np.max(np.abs(o[0] - ref)) <= 1e-12, L
+
+
+def pin_attn_star(orc):
+    """Star tree: node i > 0 sees the prefix, the root and itself; the root sees the prefix and itself."""
+    rng = np.random.default_rng(9)
+    L, T, D = 13, 6, 8
+    q, k, v = random_inputs(rng, 1, 1, 1, T, D, L)
+    o, _ = orc.tree_attn(q, k, v, np.array([L], np.int32), W.star_tree(T)[None], 0.5, 1)
+    for i in range(T):
+        keys = list(range(L)) + [L] + ([L + i] if i > 0 else [])
+        s = 0.5 * (k[0, 0, keys].astype(np.float64) @ q[0, 0, i].astype(np.float64))
+        p = np.exp(s - s.max())
+        ref = (p / p.sum()) @ v[0, 0, keys].astype(np.float64)
+        assert np.max(np.abs(o[0, 0, i] - ref)) <= 1e-12, i
+
+
+def pin_attn_nonancestor_perturbation(orc):
+    """Changing K/V of tree nodes that are not ancestors-or-self of node i leaves row i bitwise unchanged;
+    changing one of its ancestors changes it."""
+    rng = np.random.default_rng(10)
+    L, T, D, Hkv = 9, 12, 8, 2
+    q, k, v = random_inputs(rng, 1, 2, Hkv, T, D, L)
+    parent = W.random_tree(rng, T, 4, 3)[None]
+    kv = np.array([L], np.int32)
+    o, lse = orc.tree_attn(q, k, v, kv, parent, 0.35, Hkv)
+    C = ancestor_closure(parent[0])
+    for i in range(T):
+        k2, v2 = k.copy(), v.copy()
+        for j in range(T):
+            if not C[i, j]:
+                k2[0, :, L + j] = rng.standard_normal((Hkv, D))
+                v2[0, :, L + j] = rng.standard_normal((Hkv, D))
+        o2, lse2 = orc.tree_attn(q, k2, v2, kv, parent, 0.35, Hkv)
+        assert np.array_equal(o2[0, :, i], o[0, :, i]) and np.array_equal(lse2[0, :, i], lse[0, :, i]), i
+        anc = [j for j in range(T) if C[i, j]]
+        j = anc[int(rng.integers(len(anc)))]
+        v3 = v.copy()
+        v3[0, :, L + j] += 1.0
+        o3, _ = orc.tree_attn(q, k, v3, kv, parent, 0.35, Hkv)
+        assert np.all(np.abs(o3[0, :, i] - o[0, :, i]) > 1e-9), (i, j)
+
+
+def pin_attn_closed_forms(orc):
+    """V constant => out equals that constant; K constant => out is the plain mean of the visible V rows and
+    lse = scale*q.k + log(#visible)."""
+    rng = np.random.default_rng(11)
+    L, T, D = 21, 10, 8
+    q, k, v = random_inputs(rng, 1, 2, 1, T, D, L)
+    parent = W.random_tree(rng, T, 3, 4)[None]
+    kv = np.array([L], np.int32)
+    vc = np.full_like(v, 0.625)
+    o, _ = orc.tree_attn(q, k, vc, kv, parent, 0.4, 1)
+    assert np.max(np.abs(o - 0.625)) <= 1e-14
+    kc = np.broadcast_to(k[:, :, :1], k.shape).copy()
+    o, lse = orc.tree_attn(q, kc, v, kv, parent, 0.4, 1)
+    C = ancestor_closure(parent[0])
+    for h in range(2):
+        for i in range(T):
+            rows = list(range(L)) + [L + j for j in range(T) if C[i, j]]
+            ref = v[0, 0, rows].astype(np.float64).mean(axis=0)
+            assert np.max(np.abs(o[0, h, i] - ref)) <= 1e-12
+            ref_lse = 0.4 * float(q[0, h, i].astype(np.float64) @ kc[0, 0, 0].astype(np.float64)) + np.log(len(rows))
+            assert abs(lse[0, h, i] - ref_lse) <= 1e-12
+
+
+def pin_attn_relabelling(orc):
+    """Renumbering the tree in another topological order (children before ... any order with parents first)
+    permutes the output rows the same way."""
+    rng = np.random.default_rng(12)
+    L, T, D = 15, 14, 8
+    q, k, v = random_inputs(rng, 1, 2, 2, T, D, L)
+    parent = W.random_tree(rng, T, 5, 3)
+    o, lse = orc.tree_attn(q, k, v, np.array([L], np.int32), parent[None], 0.3, 2)
+    # depth-first order (pre-order, last child first) is another valid topological numbering
+    children = [[] for _ in range(T)]
+    for i in range(1, T):
+        children[parent[i]].append(i)
+    order, stack = [], [0]
+    while stack:
+        n = stack.pop()
+        order.append(n)
+        stack.extend(children[n])
+    new_of = {old: new for new, old in enumerate(order)}
+    p2 = np.array([-1 if parent[old] < 0 else new_of[parent[old]] for old in order], dtype=np.int32)
+    q2 = q[:, :, order]
+    k2, v2 = k.copy(), v.copy()
+    k2[:, :, L:L + T] = k[:, :, L + np.array(order)]
+    v2[:, :, L:L + T] = v[:, :, L + np.array(order)]
+    o2, lse2 = orc.tree_attn(q2, k2, v2, np.array([L], np.int32), p2[None], 0.3, 2)
+    assert np.max(np.abs(o2 - o[:, :, order])) <= 1e-12
+    assert np.max(np.abs(lse2 - lse[:, :, order])) <= 1e-12
+
+
+def pin_attn_mask_input(orc):
+    """An explicit ancestor-or-self bit mask gives the same result as the parent array; an all-zero mask row
+    over an empty prefix has no visible key and is defined as a zero row with lse = -inf."""
+    rng = np.random.default_rng(13)
+    for T in (5, 64, 70):
+        L, D = 6, 8
+        q, k, v = random_inputs(rng, 1, 1, 1, T, D, L)
+        parent = random_parent(rng, T)
+        bits = mask_bits_from_closure(ancestor_closure(parent))[None]
+        kv = np.array([L], np.int32)
+        o1, l1 = orc.tree_attn(q, k, v, kv, parent[None], 0.3, 1)
+        o2, l2 = orc.tree_attn(q, k, v, kv, None, 0.3, 1, tree_mask=bits)
+        assert np.array_equal(o1, o2) and np.array_equal(l1, l2), T
+    q, k, v = random_inputs(rng, 1, 1, 1, 3, 8, 0)
+    bits = np.zeros((1, 3, 1), dtype=np.uint64)
+    bits[0, 1, 0] = 0b011
+    o, lse = orc.tree_attn(q, k, v, np.array([0], np.int32), None, 0.3, 1, tree_mask=bits)
+    assert np.all(o[0, 0, 0] == 0) and lse[0, 0, 0] == -np.inf
+    assert np.all(o[0, 0, 2] == 0) and lse[0, 0, 2] == -np.inf
+    s = 0.3 * (k[0, 0, :2].astype(np.float64) @ q[0, 0, 1].astype(np.float64))
+    p = np.exp(s - s.max())
+    assert np.max(np.abs(o[0, 0, 1] - (p / p.sum()) @ v[0, 0, :2].astype(np.float64))) <= 1e-12
+
+
+def pin_attn_rows_entry(orc):
+    """The selected-rows entry point agrees exactly with the full one."""
+    rng = np.random.default_rng(14)
+    B, Hq, Hkv, T, D, L = 2, 4, 2, 9, 8, 12
+    q, k, v = random_inputs(rng, B, Hq, Hkv, T, D, L)
+    parent = np.stack([random_parent(rng, T) for _ in range(B)])
+    kv = np.array([L, 5], np.int32)
+    o, lse = orc.tree_attn(q, k, v, kv, parent, 0.3, Hkv)
+    rows = np.array([[0, 0, 0], [1, 3, 8], [1, 2, 4], [0, 1, 7]], dtype=np.int32)
+    orow, lrow = orc.tree_attn_rows(q, k, v, kv, parent, 0.3, Hkv, rows)
+    for n, (b, h, i) in enumerate(rows):
+        assert np.array_equal(orow[n], o[b, h, i]) and lrow[n] == lse[b, h, i]
+
+
+ATTN_PINS = [pin_attn_bruteforce, pin_attn_chain_is_causal, pin_attn_single_node_is_decode, pin_attn_star,
+             pin_attn_nonancestor_perturbation, pin_attn_closed_forms, pin_attn_relabelling,
+             pin_attn_mask_input, pin_attn_rows_entry]
+
+
+# ----------------------------------------------------------------------------------------- acceptance pins
+def brute_force_accept(logits, tokens, parent):
+    """Enumerate every node; it is acceptable iff each node on its root path (root excluded) carries the
+    target's token at its parent (numpy argmax: first maximal index).  Take the deepest, smallest index."""
+    T = len(parent)
+    am = [int(np.argmax(logits[i])) for i in range(T)]
+    best, best_depth = 0, 0
+    for i in range(T):
+        path = [i]
+        while path[-1] != 0:
+            path.append(int(parent[path[-1]]))
+        path = path[::-1]
+        if all(tokens[path[d]] == am[path[d - 1]] for d in range(1, len(path))):
+            if len(path) - 1 > best_depth:
+                best, best_depth = i, len(path) - 1
+    path = [best]
+    while path[-1] != 0:
+        path.append(int(parent[path[-1]]))
+    return best_depth, path[::-1], am[best], am
+
+
+def pin_accept_bruteforce(orc):
+    rng = np.random.default_rng(21)
+    B = 256
+    for V in (2, 3, 4, 7):
+        for T in (1, 2, 5, 9, 16):
+            parent = np.stack([random_parent(rng, T, max_branch=4) for _ in range(B)])
+            # values from a tiny set force argmax ties, including -0.0 against +0.0
+            logits = rng.choice(np.array([-1.0, -0.0, 0.0, 0.5, 1.0], dtype=np.float32), size=(B, T, V))
+            tokens = rng.integers(0, V, size=(B, T)).astype(np.int32)
+            alen, path, nxt, am = orc.tree_accept(logits, tokens, parent)
+            for b in range(B):
+                a, p, n, ref_am = brute_force_accept(logits[b], tokens[b], parent[b])
+                assert alen[b] == a and nxt[b] == n, (V, T, b)
+                assert list(path[b, :a + 1]) == p and np.all(path[b, a + 1:] == -1), (V, T, b)
+                assert list(am[b]) == ref_am
+
+
+def load_golden_chain_cases():
+    cases = []
+    with open(os.path.join(GOLDEN, "greedy_rule_chain.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            name, draft, target, emitted = [x.strip() for x in line.split("|")]
+            cases.append((name, [int(x) for x in draft.split()], [int(x) for x in target.split()],
+                          [int(x) for x in emitted.split()]))
+    return cases
+
+
+def pin_accept_golden_chain(orc):
+    """The paper's greedy rule on its own terms (tests/golden/greedy_rule_chain.txt): a chain of drafts
+    t_1..t_6 with the target's tokens t'_1..t'_7 planted as the unique row maxima."""
+    V = 10
+    for name, draft, target, emitted in load_golden_chain_cases():
+        T = len(draft) + 1
+        parent = W.chain_tree(T)[None]
+        tokens = np.array([[0] + draft], dtype=np.int32)
+        logits = np.zeros((1, T, V), dtype=np.float32)
+        for r, t in enumerate(target):
+            logits[0, r, t] = 1.0
+        alen, path, nxt, _ = orc.tree_accept(logits, tokens, parent)
+        got = [int(tokens[0, path[0, d]]) for d in range(1, alen[0] + 1)] + [int(nxt[0])]
+        assert got == emitted, (name, got, emitted)
+
+
+def pin_accept_chain_rule(orc):
+    """On random chains the result equals a direct transcription of the sequential rule."""
+    rng = np.random.default_rng(22)
+    B, T, V = 500, 7, 5
+    logits = rng.standard_normal((B, T, V)).astype(np.float32)
+    tokens = rng.integers(0, V, size=(B, T)).astype(np.int32)
+    tgt = np.argmax(logits, axis=2)
+    tokens[rng.random((B, T)) < 0.6] = -1
+    tokens = np.where(tokens < 0, np.roll(tgt, 1, axis=1), tokens).astype(np.int32)
+    alen, path, nxt, _ = orc.tree_accept(logits, tokens, np.tile(W.chain_tree(T), (B, 1)))
+    for b in range(B):
+        emitted = []
+        for i in range(1, T):
+            if tokens[b, i] != tgt[b, i - 1]:
+                emitted.append(int(tgt[b, i - 1]))
+                break
+            emitted.append(int(tokens[b, i]))
+        else:
+            emitted.append(int(tgt[b, T - 1]))
+        got = [int(tokens[b, path[b, d]]) for d in range(1, alen[b] + 1)] + [int(nxt[b])]
+        assert got == emitted, b
+        assert 1 <= alen[b] + 1 <= T          # tau within [1, gamma + 1]
+
+
+def pin_accept_special_cases(orc):
+    """Every draft agrees => the deepest node with the smallest index is accepted (a = depth); no draft
+    agrees => a = 0, path = [root] and the bonus token is the target's token at the root."""
+    rng = np.random.default_rng(23)
+    for _ in range(20):
+        T, V = 30, 11
+        parent = W.random_tree(rng, T, 5, 3)
+        logits = rng.standard_normal((1, T, V)).astype(np.float32)
+        am = np.argmax(logits[0], axis=1)
+        depth = W.tree_depths_for_generator_checks(parent)
+        tok = np.array([0] + [am[parent[i]] for i in range(1, T)], dtype=np.int32)[None]
+        alen, path, nxt, _ = orc.tree_accept(logits, tok, parent[None])
+        last = int(np.flatnonzero(depth == depth.max())[0])
+        assert alen[0] == depth.max() and path[0, alen[0]] == last and nxt[0] == am[last]
+        tok2 = np.array([0] + [(am[parent[i]] + 1) % V for i in range(1, T)], dtype=np.int32)[None]
+        alen, path, nxt, _ = orc.tree_accept(logits, tok2, parent[None])
+        assert alen[0] == 0 and path[0, 0] == 0 and np.all(path[0, 1:] == -1) and nxt[0] == am[0]
+
+
+def pin_accept_signed_zero_ties(orc):
+    logits = np.array([[[-0.0, 0.0, -1.0], [0.0, -0.0, -1.0], [-3.0, 0.0, -0.0]]], dtype=np.float32)
+    tokens = np.array([[2, 0, 1]], dtype=np.int32)
+    _, _, _, am = orc.tree_accept(logits, tokens, np.array([[-1, 0, 1]], np.int32))
+    assert list(am[0]) == [0, 0, 1]
+
+
+def expected_accept_length(parent: np.ndarray, p_eff: float) -> float:
+    """E[a] when every non-root node independently carries its parent's target token with probability p_eff:
+    with F_i(d) = P(consistent descendants of i reach at most d levels below i),
+    F_i(d) = prod_{c child of i} (1 - p_eff + p_eff * F_c(d - 1)), F_c(-1) = 0, and E[a] = sum_{d>=1} (1 - F_0(d-1))."""
+    T = len(parent)
+    children = [[] for _ in range(T)]
+    for i in range(1, T):
+        children[parent[i]].append(i)
+    maxd = T
+    F = np.ones((T, maxd + 1))
+    for i in reversed(range(T)):
+        for d in range(maxd + 1):
+            prod = 1.0
+            for c in children[i]:
+                Fc = F[c, d - 1] if d >= 1 else 0.0
+                prod *= 1.0 - p_eff + p_eff * Fc
+            F[i, d] = prod
+    return float(sum(1.0 - F[0, d - 1] for d in range(1, maxd + 1)))
+
+
+def pin_accept_expected_length(orc):
+    """Statistical pin: the mean accepted length over many independent token draws matches the exact
+    expectation of the independent-agreement model (within 4 standard errors)."""
+    rng = np.random.default_rng(24)
+    T, V, p, N = 16, 8, 0.7, 20000
+    parent = W.random_tree(rng, T, 4, 3)
+    row = rng.standard_normal((T, V)).astype(np.float32)
+    am = np.argmax(row, axis=1)
+    logits = np.broadcast_to(row, (N, T, V)).copy()
+    hit = rng.random((N, T)) < p
+    uni = rng.integers(0, V, size=(N, T))
+    tokens = np.where(hit, am[np.maximum(parent, 0)][None, :], uni).astype(np.int32)
+    alen, _, _, _ = orc.tree_accept(logits, tokens, np.tile(parent, (N, 1)))
+    exact = expected_accept_length(parent, p + (1 - p) / V)
+    se = alen.std() / np.sqrt(N)
+    assert abs(alen.mean() - exact) <= 4 * se, (alen.mean(), exact, se)
+
+
+ACCEPT_PINS = [pin_accept_bruteforce, pin_accept_golden_chain, pin_accept_chain_rule, pin_accept_special_cases,
+               pin_accept_signed_zero_ties, pin_accept_expected_length]
+
+
+# ---------------------------------------------------------------------------------------------- commit pins
+def pin_commit_gather(orc):
+    """Direct gather from a snapshot: slot L+k <- old slot L+path[k] for k <= a; everything else untouched;
+    includes aliasing paths such as [0, 2, 5] (slot L+2 is both a source and a destination)."""
+    rng = np.random.default_rng(31)
+    for dtype in (np.uint16, np.float32):
+        NL, B, Hkv, T, D = 3, 4, 2, 9, 8
+        S = 64
+        # paths of the tree with parent array [-1, 0, 0, 2, 1, 3, 5, 5, 6]
+        paths = [[0, 2, 5, 7], [0], [0, 1, 4], [0, 2, 3]]
+        kv_in = np.array([10, 0, 33, 54], np.int32)
+        alen = np.array([len(p) - 1 for p in paths], np.int32)
+        path = np.full((B, T), -1, np.int32)
+        for b, p in enumerate(paths):
+            path[b, :len(p)] = p
+        if dtype == np.uint16:
+            k = rng.integers(0, 65535, size=(NL, B, Hkv, S, D)).astype(np.uint16)
+            v = rng.integers(0, 65535, size=(NL, B, Hkv, S, D)).astype(np.uint16)
+        else:
+            k = rng.standard_normal((NL, B, Hkv, S, D)).astype(np.float32)
+            v = rng.standard_normal((NL, B, Hkv, S, D)).astype(np.float32)
+        k0, v0 = k.copy(), v.copy()
+        out = orc.kv_commit(k, v, kv_in, path, alen)
+        ek, ev = k0.copy(), v0.copy()
+        for b, p in enumerate(paths):
+            L = kv_in[b]
+            ek[:, b, :, L:L + len(p)] = k0[:, b][:, :, L + np.array(p)]
+            ev[:, b, :, L:L + len(p)] = v0[:, b][:, :, L + np.array(p)]
+        assert np.array_equal(k.view(np.uint8), ek.view(np.uint8)) and np.array_equal(v.view(np.uint8), ev.view(np.uint8))
+        assert list(out) == [kv_in[b] + alen[b] + 1 for b in range(B)]
+
+
+def pin_commit_composition(orc):
+    """After commit, one decode step of the last accepted node's query over the committed cache (prefix of
+    length L+a, then the node itself) equals that node's row of the tree attention before the commit."""
+    rng = np.random.default_rng(32)
+    for trial in range(6):
+        T, D, Hkv, Hq, L = 20, 16, 2, 4, 25
+        parent = W.random_tree(rng, T, 5, 3)
+        q, k, v = random_inputs(rng, 1, Hq, Hkv, T, D, L, extra=5)
+        logits = rng.standard_normal((1, T, 6)).astype(np.float32)
+        am = np.argmax(logits[0], axis=1)
+        tok = np.array([0] + [am[parent[i]] if rng.random() < 0.8 else rng.integers(6) for i in range(1, T)],
+                       dtype=np.int32)[None]
+        alen, path, _, _ = orc.tree_accept(logits, tok, parent[None])
+        a, last = int(alen[0]), int(path[0, alen[0]])
+        o_tree, lse_tree = orc.tree_attn(q, k, v, np.array([L], np.int32), parent[None], 0.25, Hkv)
+        kc, vc = k[None].copy(), v[None].copy()
+        out_len = orc.kv_commit(kc, vc, np.array([L], np.int32), path, alen)
+        assert out_len[0] == L + a + 1
+        o_dec, lse_dec = orc.tree_attn(q[:, :, last:last + 1], kc[0], vc[0], np.array([L + a], np.int32),
+                                       np.array([[-1]], np.int32), 0.25, Hkv)
+        assert np.max(np.abs(o_dec[0, :, 0] - o_tree[0, :, last])) <= 1e-12, trial
+        assert np.max(np.abs(lse_dec[0, :, 0] - lse_tree[0, :, last])) <= 1e-12, trial
+
+
+COMMIT_PINS = [pin_commit_gather, pin_commit_composition]
+ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS

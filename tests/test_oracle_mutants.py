@@ -1,0 +1,62 @@
+"""The pins would catch plausible mistakes in the oracle: each case below plants one mistake in a copy of
+oracle.c (a dropped term, a wrong index, a wrong tie rule, a transposed operand, ...), builds it with gcc, and
+requires at least one pin of the matching group to fail on it.  Runs on the CPU only."""
+import os
+
+import pytest
+
+import oracle
+import pins
+
+ATTN, ACC, COM = "attn", "accept", "commit"
+MUTANTS = [
+    ("drop_scale", ATTN, "score[s] = scale * dot;", "score[s] = dot;"),
+    ("wrong_kv_head", ATTN, "const int g = h / G;", "const int g = h % Hkv;"),
+    ("self_not_visible", ATTN, "for (int j = i; j >= 0; j = parent[j]) visible[j] = 1;",
+     "for (int j = parent[i]; j >= 0; j = parent[j]) visible[j] = 1;"),
+    ("whole_tree_visible", ATTN, "for (int j = i; j >= 0; j = parent[j]) visible[j] = 1;",
+     "for (int j = 0; j < T; ++j) visible[j] = 1;"),
+    ("last_slot_dropped", ATTN, "const int n = L + T;", "const int n = L + T - 1;"),
+    ("values_shifted", ATTN, "out_row[d] += p * (double)vb[(size_t)s * D + d];",
+     "out_row[d] += p * (double)vb[(size_t)(s + 1) * D + d];"),
+    ("keys_as_values", ATTN, "out_row[d] += p * (double)vb[(size_t)s * D + d];",
+     "out_row[d] += p * (double)kb[(size_t)s * D + d];"),
+    ("lse_without_max", ATTN, "*lse_out = m + log(l);", "*lse_out = log(l);"),
+    ("no_normalisation", ATTN, "for (int d = 0; d < D; ++d) out_row[d] /= l;", ""),
+    ("mask_bit_index", ATTN, "(mask_row[j / 64] >> (j % 64))", "(mask_row[j / 64] >> (j % 63))"),
+    ("query_row_of_root", ATTN, "const float* qi = q + (((size_t)b * Hq + h) * T + i) * D;",
+     "const float* qi = q + (((size_t)b * Hq + h) * T) * D;"),
+    ("argmax_ties_high", ACC, "if (row[x] > row[best]) best = x;", "if (row[x] >= row[best]) best = x;"),
+    ("own_argmax", ACC, "ok[i] = ok[par[i]] && tok[i] == am[par[i]];", "ok[i] = ok[par[i]] && tok[i] == am[i];"),
+    ("ok_ignores_parent", ACC, "ok[i] = ok[par[i]] && tok[i] == am[par[i]];", "ok[i] = tok[i] == am[par[i]];"),
+    ("last_ties_high", ACC, "if (ok[i] && depth[i] > depth[last]) last = i;",
+     "if (ok[i] && depth[i] >= depth[last]) last = i;"),
+    ("bonus_from_parent", ACC, "next_token[b] = am[last];", "next_token[b] = am[par[last] < 0 ? 0 : par[last]];"),
+    ("accept_len_counts_bonus", ACC, "accept_len[b] = a;", "accept_len[b] = a + 1;"),
+    ("kv_len_without_root", COM, "kv_len_out[b] = kv_len_in[b] + accept_len[b] + 1;",
+     "kv_len_out[b] = kv_len_in[b] + accept_len[b];"),
+    ("commit_reversed", COM, "for (int k = 0; k <= accept_len[b]; ++k) {",
+     "for (int k = accept_len[b]; k >= 0; --k) {"),
+    ("commit_skips_v", COM, "memmove(vc + (size_t)(L + k) * row, vc + (size_t)(L + path[k]) * row, row);", ""),
+    ("commit_drops_last", COM, "for (int k = 0; k <= accept_len[b]; ++k) {",
+     "for (int k = 0; k < accept_len[b]; ++k) {"),
+]
+GROUPS = {ATTN: pins.ATTN_PINS, ACC: pins.ACCEPT_PINS, COM: pins.COMMIT_PINS}
+
+
+@pytest.mark.parametrize("name,group,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(tmp_path, name, group, old, new):
+    src = open(oracle.SOURCE).read()
+    assert src.count(old) >= 1, "mutation site not found: %s" % name
+    mutated = src.replace(old, new)
+    path_c = os.path.join(tmp_path, "mutant.c")
+    open(path_c, "w").write(mutated)
+    lib = oracle.compile_source(path_c, os.path.join(tmp_path, "libmutant.so"))
+    orc = oracle.Oracle(lib)
+    caught = []
+    for pin in GROUPS[group]:
+        try:
+            pin(orc)
+        except (AssertionError, oracle.OracleError, ValueError, IndexError) as e:
+            caught.append((pin.__name__, type(e).__name__))
+    assert caught, "no pin caught mutant %s" % name
