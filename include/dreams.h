@@ -1,0 +1,182 @@
+/*
+ * dreams.h -- C ABI of libdreams.so, the MI355X (gfx950) tree-verification step of DREAM-S speculative
+ * decoding for vision-language models.
+ *
+ * The step has three verbs, run back to back on one HIP stream:
+ *   dreams_tree_verify_attn  tree-masked attention of the draft-token tree against the KV cache
+ *   dreams_tree_accept       greedy acceptance of the longest target-consistent root-to-node path
+ *   dreams_kv_commit         compaction of the accepted path's K/V into the cache
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named as "device" point to device memory the caller owns (allocated on the current HIP
+ *     device).  The library never allocates or frees inside a call; scratch memory comes in through a
+ *     caller-owned workspace sized by the matching *_workspace_size query.
+ *   - Calls are asynchronous and stream-ordered: they enqueue kernels on `stream` and return.  Outputs are
+ *     valid once the stream has reached that point.  Calls that share a workspace must be ordered (same
+ *     stream, or synchronised streams).
+ *   - Host-visible arguments (sizes, flags, null pointers) are checked before anything is enqueued; on a
+ *     failed check the call returns a negative status, sets the thread's last error message and enqueues
+ *     nothing.  Values that live in device memory (kv_len, parent, accept_path, ...) cannot be checked on the
+ *     host; the kernels clamp or skip out-of-range entries so that no access leaves the caller's buffers,
+ *     and the results for such entries are unspecified.
+ *   - A HIP launch error returns DREAMS_ERR_HIP.
+ *   - Element types: DREAMS_BF16 tensors hold bfloat16 bit patterns (round-to-nearest-even); DREAMS_F32
+ *     tensors hold IEEE binary32.
+ */
+#ifndef DREAMS_H
+#define DREAMS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DREAMS_OK = 0,
+  DREAMS_ERR_INVALID_ARG = -1,  /* a host-visible argument is out of range or a required pointer is NULL */
+  DREAMS_ERR_UNSUPPORTED = -2,  /* valid in principle but not built (e.g. a head_dim other than 64/128)   */
+  DREAMS_ERR_WORKSPACE = -3,    /* workspace NULL or smaller than the matching *_workspace_size           */
+  DREAMS_ERR_HIP = -4           /* the HIP runtime reported an error (device query or kernel launch)     */
+} dreams_status_t;
+
+typedef enum { DREAMS_F32 = 0, DREAMS_BF16 = 1 } dreams_dtype_t;
+
+/*
+ * Shape of one tree-verification attention call.
+ *   batch            B >= 0 sequences
+ *   num_q_heads      Hq >= 1 query heads
+ *   num_kv_heads     Hkv >= 1 KV heads, Hq % Hkv == 0 (query head h reads KV head h / (Hq/Hkv))
+ *   head_dim         D, 64 or 128
+ *   num_nodes        T, 1..128 tree nodes per sequence, root included (node 0 = the last emitted token)
+ *   cache_capacity   S_cap >= T slots per (sequence, KV head)
+ *   max_kv_len       host-side upper bound on every kv_len[b], used only to plan the work split;
+ *                    0 means S_cap - T.  Must satisfy 0 <= max_kv_len <= S_cap - T.
+ *   num_splits       number of pieces the key axis of each (sequence, KV head) is cut into; 0 lets the
+ *                    library choose from the shape and the device's compute-unit count.  Any value gives
+ *                    the same result up to floating-point rounding order.
+ *   dtype            type of q, the caches and out: DREAMS_BF16 (matrix-core path) or DREAMS_F32
+ *   scale            softmax scale applied to q.k (normally 1/sqrt(D))
+ */
+typedef struct {
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t num_nodes;
+  int32_t cache_capacity;
+  int32_t max_kv_len;
+  int32_t num_splits;
+  dreams_dtype_t dtype;
+  float scale;
+} dreams_attn_desc_t;
+
+/* Bytes of workspace dreams_tree_verify_attn needs for `desc` on the current device (may be 0). */
+dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t* desc, size_t* bytes);
+
+/*
+ * dreams_tree_verify_attn -- the target model's parallel verification pass, attention part (the paper,
+ * Section 2, "Speculative decoding": the target checks all draft tokens in one pass; Section 3.2 defines the
+ * attention matrix softmax(Q K^T / sqrt(z))).  For every sequence b, query head h and tree node i:
+ *
+ *     out[b,h,i,:] = softmax_j( scale * q[b,h,i,:] . k[b,g,j,:] ) v[b,g,j,:],   g = h / (Hq/Hkv)
+ *
+ * over the visible slots j: every committed prefix slot 0..L_b-1 (image and text tokens alike -- the
+ * paper's Section 2, "Vision-Language Models", notes every visual token stays in the KV cache and is
+ * attended at each decoding step), plus slot L_b + n for every tree node n that is node i itself or one of
+ * its ancestors.  lse[b,h,i] = log(sum_j exp(scale * q.k_j)) (natural log).  A row with no visible slot
+ * (possible only with a tree_mask and L_b = 0) gives out = 0 and lse = -inf.
+ *
+ *   q          device [B, Hq, T, D]      queries of the tree nodes (after any positional rotation)
+ *   k_cache    device [B, Hkv, S_cap, D] keys: slots [0, L_b) committed prefix, [L_b, L_b+T) the tree
+ *                                         nodes' own keys in node order (written by the caller beforehand)
+ *   v_cache    device [B, Hkv, S_cap, D] values, same layout
+ *   kv_len     device [B] int32          L_b; the kernel clamps it into [0, S_cap - T]
+ *   parent     device [B, T] int32       parent[b,0] = -1, 0 <= parent[b,i] < i; ignored when tree_mask is
+ *                                         given.  An entry breaking these rules ends that node's ancestor walk.
+ *   tree_mask  device [B, T, ceil(T/64)] uint64, or NULL: bit n of row i set <=> slot L_b+n is visible to
+ *                                         node i.  Takes precedence over parent.
+ *   out        device [B, Hq, T, D]      same dtype as q
+ *   lse        device [B, Hq, T] float, or NULL
+ *   workspace  device, >= dreams_tree_verify_attn_workspace_size bytes.  Must be zero-filled before its
+ *              first use; every call leaves the part it relies on zero again when it completes.
+ * Arithmetic: bf16 products accumulated in fp32 on the matrix cores, softmax statistics in fp32, one
+ * rounding of the probabilities to bf16 before the value product; output rounded to the nearest bf16.
+ */
+dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                        const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                        const uint64_t* tree_mask, void* out, float* lse, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace dreams_tree_accept needs (may be 0). */
+dreams_status_t dreams_tree_accept_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
+                                                  size_t* bytes);
+
+/*
+ * dreams_tree_accept -- greedy acceptance (the paper, Section 2, "Speculative decoding": a draft token is
+ * kept while it equals the target's own token at its position; at the first mismatch the target's token is
+ * used instead), applied to every root-to-node path of the tree.
+ *
+ *   tgt[i]  = the smallest vocabulary index attaining max_v target_logits[b,i,v]   (-0.0 equals +0.0)
+ *   node i is consistent iff i = 0, or its parent is consistent and draft_tokens[b,i] == tgt[parent[i]]
+ *   last    = the consistent node of greatest depth, smallest index among equals
+ *   accept_len[b]  = depth(last) = number of accepted draft tokens a  (the step emits a + 1 tokens)
+ *   accept_path[b] = node ids root .. last (a + 1 entries), then -1 up to T entries
+ *   next_token[b]  = tgt[last], the target's token emitted after the accepted drafts
+ *
+ *   target_logits  device [B, T, V] float, finite (NaN gives unspecified results)
+ *   draft_tokens   device [B, T] int32 (entry 0 = root token, not checked)
+ *   parent         device [B, T] int32, as for dreams_tree_verify_attn; a node whose ancestor walk
+ *                  breaks the parent rules is never consistent
+ *   accept_len     device [B] int32 (out)
+ *   accept_path    device [B, T] int32 (out)
+ *   next_token     device [B] int32 (out)
+ *   target_argmax  device [B, T] int32 (out) or NULL: tgt[i] for every node
+ *   workspace      device, >= dreams_tree_accept_workspace_size bytes, zero-filled before first use; every
+ *                  call leaves it zero again.
+ * Bit-exact: integer results only; every comparison is an fp32 comparison of the caller's logits.
+ */
+dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t vocab, const float* target_logits,
+                                   const int32_t* draft_tokens, const int32_t* parent, int32_t* accept_len,
+                                   int32_t* accept_path, int32_t* next_token, int32_t* target_argmax,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * dreams_kv_commit -- keeps the accepted path in the cache: for every layer, sequence b and KV head, and
+ * k = 0 .. accept_len[b], slot kv_len_in[b] + k receives (bit for bit) the K and V rows of slot
+ * kv_len_in[b] + accept_path[b,k]; then kv_len_out[b] = kv_len_in[b] + accept_len[b] + 1 (the root and the
+ * accepted drafts are now committed; the bonus token's K/V is produced by the next step, where it is the
+ * root).  Slots outside [kv_len_in[b], kv_len_in[b] + accept_len[b]] are not written.
+ *
+ *   num_layers          NL >= 1 caches; layer l starts layer_stride_elems elements after layer l-1
+ *   k_cache, v_cache    device, per layer [B, Hkv, S_cap, D] of `dtype` (in place)
+ *   kv_len_in           device [B] int32
+ *   accept_path         device [B, path_stride] int32, as written by dreams_tree_accept
+ *   accept_len          device [B] int32, clamped into [0, path_stride - 1]
+ *   kv_len_out          device [B] int32 (out); must not alias kv_len_in
+ * A path entry that is not a valid source (accept_path[b,k] < k, or kv_len_in[b] + accept_path[b,k] outside
+ * the cache) is skipped.
+ */
+dreams_status_t dreams_kv_commit(int32_t num_layers, int64_t layer_stride_elems, int32_t batch,
+                                 int32_t num_kv_heads, int32_t head_dim, int32_t cache_capacity,
+                                 dreams_dtype_t dtype, void* k_cache, void* v_cache, const int32_t* kv_len_in,
+                                 const int32_t* accept_path, const int32_t* accept_len, int32_t path_stride,
+                                 int32_t* kv_len_out, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* dreams_status_string(dreams_status_t status);
+
+/* Message describing the calling thread's most recent failure ("" if none). Valid until its next call. */
+const char* dreams_last_error_message(void);
+
+/* Host-side check of a parent array (host memory): DREAMS_OK iff parent[0] == -1 and 0 <= parent[i] < i. */
+dreams_status_t dreams_check_tree_host(const int32_t* parent, int32_t num_nodes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DREAMS_H */

@@ -67,8 +67,13 @@ class Oracle:
         lib.oracle_kv_commit.argtypes = [I, ctypes.c_int64, I, I, I, I, I, P, P, P, P, P, I, P]
         for f in (lib.oracle_tree_attn, lib.oracle_tree_attn_rows, lib.oracle_tree_accept, lib.oracle_kv_commit):
             f.restype = ctypes.c_int
+        lib.oracle_num_threads.argtypes = []
+        lib.oracle_num_threads.restype = ctypes.c_int
         self.lib = lib
         self.path = lib_path
+
+    def num_threads(self) -> int:
+        return int(self.lib.oracle_num_threads())
 
     def tree_attn(self, q, k_cache, v_cache, kv_len, parent, scale: float, num_kv_heads: int,
                   tree_mask=None, with_lse: bool = True):
@@ -149,6 +154,10 @@ def default() -> Oracle:
             build(force=False)
         _default = Oracle(LIBRARY)
     return _default
+
+
+def num_threads() -> int:
+    return default().num_threads()
 
 
 def tree_attn(*a, **kw):

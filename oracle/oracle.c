@@ -33,6 +33,7 @@
  * Return value of every entry point: 0 on success, negative on invalid input (nothing written then).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -253,3 +254,6 @@ int oracle_kv_commit(int NL, int64_t layer_stride_elems, int B, int Hkv, int D, 
   for (int b = 0; b < B; ++b) kv_len_out[b] = kv_len_in[b] + accept_len[b] + 1;
   return 0;
 }
+
+/* Number of threads the parallel loops above use (reported beside CPU timings). */
+int oracle_num_threads(void) { return omp_get_max_threads(); }

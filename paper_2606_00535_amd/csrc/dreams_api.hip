@@ -1,0 +1,371 @@
+// Host side of libdreams.so: argument checks, work planning, workspace layout, launches, error reporting.
+// Every check that can be made on the host is made before anything is enqueued.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <mutex>
+#include <string>
+
+#include "dreams.h"
+#include "kernels.h"
+
+using namespace dreams;
+
+namespace {
+
+thread_local std::string g_error;
+
+dreams_status_t fail(dreams_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return st;
+}
+
+dreams_status_t ok() {
+  g_error.clear();
+  return DREAMS_OK;
+}
+
+dreams_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(DREAMS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t n) { return ((uintptr_t)p % n) == 0; }
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Compute-unit count of the current device, cached per device.
+dreams_status_t device_cus(int* cus) {
+  static std::mutex mu;
+  static int cache[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(DREAMS_ERR_HIP, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (cache[dev] == 0) {
+    int n = 0;
+    e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute(multiprocessor count)");
+    cache[dev] = n > 0 ? n : 1;
+  }
+  *cus = cache[dev];
+  return DREAMS_OK;
+}
+
+// ------------------------------------------------------------------------------------------ attention
+struct AttnPlan {
+  int G, rows_total, row_groups, units, splits, key_tile;
+  size_t acc_off, ml_off, cnt_off, bytes;
+};
+
+constexpr int kMaxSplitsRequest = 4096;
+
+dreams_status_t check_attn_desc(const dreams_attn_desc_t* d) {
+  if (!d) return fail(DREAMS_ERR_INVALID_ARG, "desc is NULL");
+  if (d->batch < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", d->batch);
+  if (d->num_q_heads < 1 || d->num_kv_heads < 1)
+    return fail(DREAMS_ERR_INVALID_ARG, "num_q_heads = %d and num_kv_heads = %d must be >= 1", d->num_q_heads,
+                d->num_kv_heads);
+  if (d->num_q_heads % d->num_kv_heads != 0)
+    return fail(DREAMS_ERR_INVALID_ARG, "num_q_heads = %d is not a multiple of num_kv_heads = %d", d->num_q_heads,
+                d->num_kv_heads);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(DREAMS_ERR_UNSUPPORTED, "head_dim = %d (supported: 64, 128)", d->head_dim);
+  if (d->num_nodes < 1 || d->num_nodes > kMaxNodes)
+    return fail(DREAMS_ERR_INVALID_ARG, "num_nodes = %d outside [1, %d]", d->num_nodes, kMaxNodes);
+  if (d->cache_capacity < d->num_nodes)
+    return fail(DREAMS_ERR_INVALID_ARG, "cache_capacity = %d < num_nodes = %d", d->cache_capacity, d->num_nodes);
+  if (d->max_kv_len < 0 || d->max_kv_len > d->cache_capacity - d->num_nodes)
+    return fail(DREAMS_ERR_INVALID_ARG, "max_kv_len = %d outside [0, cache_capacity - num_nodes = %d]",
+                d->max_kv_len, d->cache_capacity - d->num_nodes);
+  if (d->num_splits < 0 || d->num_splits > kMaxSplitsRequest)
+    return fail(DREAMS_ERR_INVALID_ARG, "num_splits = %d outside [0, %d]", d->num_splits, kMaxSplitsRequest);
+  if (d->dtype != DREAMS_BF16 && d->dtype != DREAMS_F32)
+    return fail(DREAMS_ERR_INVALID_ARG, "dtype = %d is not DREAMS_BF16 or DREAMS_F32", (int)d->dtype);
+  if (!isfinite(d->scale)) return fail(DREAMS_ERR_INVALID_ARG, "scale is not finite");
+  return DREAMS_OK;
+}
+
+dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
+  dreams_status_t st = check_attn_desc(d);
+  if (st != DREAMS_OK) return st;
+  *p = AttnPlan{};
+  p->G = d->num_q_heads / d->num_kv_heads;
+  p->rows_total = p->G * d->num_nodes;
+  p->row_groups = (p->rows_total + kAttnRows - 1) / kAttnRows;
+  p->units = d->batch * d->num_kv_heads;
+  p->key_tile = 64;
+  p->splits = 1;
+  if (d->dtype == DREAMS_F32 || p->units == 0) return DREAMS_OK;
+
+  const int max_len = d->max_kv_len > 0 ? d->max_kv_len : d->cache_capacity - d->num_nodes;
+  const int n_keys = max_len + d->num_nodes;
+  const int max_splits = (n_keys + p->key_tile - 1) / p->key_tile;
+  int splits = d->num_splits;
+  if (splits == 0) {
+    int cus = 0;
+    st = device_cus(&cus);
+    if (st != DREAMS_OK) return st;
+    const long long wgs = (long long)p->units * p->row_groups;
+    splits = (int)((cus + wgs - 1) / wgs);
+  }
+  splits = splits < 1 ? 1 : (splits > max_splits ? max_splits : splits);
+  p->splits = splits;
+  const long long grid = 8LL * ((p->units + 7) / 8) * splits * p->row_groups;
+  if (grid > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large: %lld workgroups", grid);
+  if (splits > 1) {
+    const size_t sets = (size_t)p->units * p->row_groups;
+    const size_t rows = sets * splits * kAttnRows;
+    p->acc_off = 0;
+    p->ml_off = align_up(rows * d->head_dim * sizeof(float), 256);
+    p->cnt_off = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
+    p->bytes = p->cnt_off + align_up(sets * sizeof(uint32_t), 256);
+  }
+  return DREAMS_OK;
+}
+
+// ----------------------------------------------------------------------------------------- acceptance
+struct AcceptPlan {
+  int chunks, chunk;
+  size_t val_off, idx_off, cnt_off, bytes;
+};
+
+constexpr int kAcceptTargetWgs = 2048;
+constexpr int kAcceptMinPiece = 2048;
+
+dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
+  if (B < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", B);
+  if (T < 1 || T > kMaxNodes) return fail(DREAMS_ERR_INVALID_ARG, "num_nodes = %d outside [1, %d]", T, kMaxNodes);
+  if (V < 1) return fail(DREAMS_ERR_INVALID_ARG, "vocab = %d < 1", V);
+  *p = AcceptPlan{};
+  const long long rows = (long long)B * T;
+  if (rows == 0) return DREAMS_OK;
+  long long chunks = (kAcceptTargetWgs + rows - 1) / rows;
+  const long long max_chunks = (V + kAcceptMinPiece - 1) / kAcceptMinPiece;
+  if (chunks > max_chunks) chunks = max_chunks;
+  if (chunks < 1) chunks = 1;
+  long long chunk = (V + chunks - 1) / chunks;
+  chunk = (chunk + 3) / 4 * 4;
+  chunks = (V + chunk - 1) / chunk;
+  if (rows * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  p->chunks = (int)chunks;
+  p->chunk = (int)chunk;
+  const size_t parts = (size_t)rows * chunks;
+  p->val_off = 0;
+  p->idx_off = align_up(parts * sizeof(float), 256);
+  p->cnt_off = p->idx_off + align_up(parts * sizeof(int32_t), 256);
+  p->bytes = p->cnt_off + align_up((size_t)B * sizeof(uint32_t), 256);
+  return DREAMS_OK;
+}
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const char* pa = (const char*)a;
+  const char* pb = (const char*)b;
+  return pa < pb + nb && pb < pa + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t* desc, size_t* bytes) {
+  if (!bytes) return fail(DREAMS_ERR_INVALID_ARG, "bytes is NULL");
+  AttnPlan p;
+  dreams_status_t st = plan_attn(desc, &p);
+  if (st != DREAMS_OK) return st;
+  *bytes = p.bytes;
+  return ok();
+}
+
+dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                        const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                        const uint64_t* tree_mask, void* out, float* lse, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  dreams_status_t st = check_attn_desc(desc);
+  if (st != DREAMS_OK) return st;
+  if (desc->batch == 0) return ok();
+  if (!q || !k_cache || !v_cache || !kv_len || !out)
+    return fail(DREAMS_ERR_INVALID_ARG, "q, k_cache, v_cache, kv_len and out must not be NULL");
+  if (!parent && !tree_mask) return fail(DREAMS_ERR_INVALID_ARG, "either parent or tree_mask must be given");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16))
+    return fail(DREAMS_ERR_INVALID_ARG, "q, k_cache, v_cache and out must be 16-byte aligned");
+  if (!aligned(kv_len, 4) || (parent && !aligned(parent, 4)) || (lse && !aligned(lse, 4)) ||
+      (tree_mask && !aligned(tree_mask, 8)))
+    return fail(DREAMS_ERR_INVALID_ARG, "kv_len, parent, lse or tree_mask is misaligned");
+  AttnPlan p;
+  st = plan_attn(desc, &p);
+  if (st != DREAMS_OK) return st;
+  if (p.bytes > 0) {
+    if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", p.bytes);
+    if (workspace_bytes < p.bytes)
+      return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, p.bytes);
+    if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  }
+  if (desc->dtype == DREAMS_F32 && (long long)desc->batch * desc->num_q_heads * desc->num_nodes > 0x7fffffffLL)
+    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+
+  AttnArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.kv_len = kv_len;
+  a.parent = parent;
+  a.mask = tree_mask;
+  a.out = out;
+  a.lse = lse;
+  char* ws = (char*)workspace;
+  a.part_acc = p.bytes ? (float*)(ws + p.acc_off) : nullptr;
+  a.part_ml = p.bytes ? (float*)(ws + p.ml_off) : nullptr;
+  a.counters = p.bytes ? (uint32_t*)(ws + p.cnt_off) : nullptr;
+  a.B = desc->batch;
+  a.Hq = desc->num_q_heads;
+  a.Hkv = desc->num_kv_heads;
+  a.G = p.G;
+  a.T = desc->num_nodes;
+  a.D = desc->head_dim;
+  a.S_cap = desc->cache_capacity;
+  a.units = p.units;
+  a.row_groups = p.row_groups;
+  a.splits = p.splits;
+  a.key_tile = p.key_tile;
+  a.scale_log2 = desc->scale * 1.4426950408889634f;
+  hipError_t e = desc->dtype == DREAMS_BF16 ? launch_tree_attn_bf16(a, stream) : launch_tree_attn_f32(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "tree attention launch");
+  return ok();
+}
+
+dreams_status_t dreams_tree_accept_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab, size_t* bytes) {
+  if (!bytes) return fail(DREAMS_ERR_INVALID_ARG, "bytes is NULL");
+  AcceptPlan p;
+  dreams_status_t st = plan_accept(batch, num_nodes, vocab, &p);
+  if (st != DREAMS_OK) return st;
+  *bytes = p.bytes;
+  return ok();
+}
+
+dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t vocab, const float* target_logits,
+                                   const int32_t* draft_tokens, const int32_t* parent, int32_t* accept_len,
+                                   int32_t* accept_path, int32_t* next_token, int32_t* target_argmax,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  AcceptPlan p;
+  dreams_status_t st = plan_accept(batch, num_nodes, vocab, &p);
+  if (st != DREAMS_OK) return st;
+  if (batch == 0) return ok();
+  if (!target_logits || !draft_tokens || !parent || !accept_len || !accept_path || !next_token)
+    return fail(DREAMS_ERR_INVALID_ARG,
+                "target_logits, draft_tokens, parent, accept_len, accept_path and next_token must not be NULL");
+  if (!aligned(target_logits, 4) || !aligned(draft_tokens, 4) || !aligned(parent, 4) || !aligned(accept_len, 4) ||
+      !aligned(accept_path, 4) || !aligned(next_token, 4) || (target_argmax && !aligned(target_argmax, 4)))
+    return fail(DREAMS_ERR_INVALID_ARG, "an int32/float argument is not 4-byte aligned");
+  if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", p.bytes);
+  if (workspace_bytes < p.bytes)
+    return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, p.bytes);
+  if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  AcceptArgs a{};
+  a.logits = target_logits;
+  a.tokens = draft_tokens;
+  a.parent = parent;
+  a.accept_len = accept_len;
+  a.accept_path = accept_path;
+  a.next_token = next_token;
+  a.target_argmax = target_argmax;
+  char* ws = (char*)workspace;
+  a.part_val = (float*)(ws + p.val_off);
+  a.part_idx = (int32_t*)(ws + p.idx_off);
+  a.counters = (uint32_t*)(ws + p.cnt_off);
+  a.B = batch;
+  a.T = num_nodes;
+  a.V = vocab;
+  a.chunks = p.chunks;
+  a.chunk = p.chunk;
+  a.vec4 = (vocab % 4 == 0) && aligned(target_logits, 16);
+  hipError_t e = launch_tree_accept(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "tree accept launch");
+  return ok();
+}
+
+dreams_status_t dreams_kv_commit(int32_t num_layers, int64_t layer_stride_elems, int32_t batch,
+                                 int32_t num_kv_heads, int32_t head_dim, int32_t cache_capacity,
+                                 dreams_dtype_t dtype, void* k_cache, void* v_cache, const int32_t* kv_len_in,
+                                 const int32_t* accept_path, const int32_t* accept_len, int32_t path_stride,
+                                 int32_t* kv_len_out, hipStream_t stream) {
+  if (num_layers < 1) return fail(DREAMS_ERR_INVALID_ARG, "num_layers = %d < 1", num_layers);
+  if (batch < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", batch);
+  if (num_kv_heads < 1 || head_dim < 1 || cache_capacity < 1 || path_stride < 1)
+    return fail(DREAMS_ERR_INVALID_ARG, "num_kv_heads, head_dim, cache_capacity and path_stride must be >= 1");
+  if (dtype != DREAMS_BF16 && dtype != DREAMS_F32)
+    return fail(DREAMS_ERR_INVALID_ARG, "dtype = %d is not DREAMS_BF16 or DREAMS_F32", (int)dtype);
+  const int elem = dtype == DREAMS_BF16 ? 2 : 4;
+  const long long row_bytes = (long long)head_dim * elem;
+  if (row_bytes % 16 != 0 || row_bytes > kCommitMaxRowBytes)
+    return fail(DREAMS_ERR_UNSUPPORTED, "head_dim * element size = %lld bytes (must be a multiple of 16, <= %d)",
+                row_bytes, kCommitMaxRowBytes);
+  const long long layer_elems = (long long)batch * num_kv_heads * cache_capacity * head_dim;
+  if (num_layers > 1 && layer_stride_elems < layer_elems)
+    return fail(DREAMS_ERR_INVALID_ARG, "layer_stride_elems = %lld is smaller than one layer (%lld elements)",
+                (long long)layer_stride_elems, layer_elems);
+  if (layer_stride_elems < 0) return fail(DREAMS_ERR_INVALID_ARG, "layer_stride_elems < 0");
+  if (batch == 0) return ok();
+  if (!k_cache || !v_cache || !kv_len_in || !accept_path || !accept_len || !kv_len_out)
+    return fail(DREAMS_ERR_INVALID_ARG, "cache, length and path pointers must not be NULL");
+  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || ((layer_stride_elems * elem) % 16) != 0)
+    return fail(DREAMS_ERR_INVALID_ARG, "k_cache, v_cache and the layer stride must be 16-byte aligned");
+  if (!aligned(kv_len_in, 4) || !aligned(accept_path, 4) || !aligned(accept_len, 4) || !aligned(kv_len_out, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "an int32 argument is not 4-byte aligned");
+  if (overlap(kv_len_out, (size_t)batch * 4, kv_len_in, (size_t)batch * 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "kv_len_out must not overlap kv_len_in");
+  if ((long long)num_layers * batch * num_kv_heads > 0x7fffffffLL)
+    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+
+  CommitArgs a{};
+  a.k = (char*)k_cache;
+  a.v = (char*)v_cache;
+  a.kv_len_in = kv_len_in;
+  a.path = accept_path;
+  a.accept_len = accept_len;
+  a.kv_len_out = kv_len_out;
+  a.layer_stride_bytes = layer_stride_elems * elem;
+  a.NL = num_layers;
+  a.B = batch;
+  a.Hkv = num_kv_heads;
+  a.S_cap = cache_capacity;
+  a.path_stride = path_stride;
+  a.row_bytes = (int)row_bytes;
+  hipError_t e = launch_kv_commit(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "kv commit launch");
+  return ok();
+}
+
+const char* dreams_status_string(dreams_status_t status) {
+  switch (status) {
+    case DREAMS_OK: return "DREAMS_OK";
+    case DREAMS_ERR_INVALID_ARG: return "DREAMS_ERR_INVALID_ARG: an argument is out of range or NULL";
+    case DREAMS_ERR_UNSUPPORTED: return "DREAMS_ERR_UNSUPPORTED: shape or type not supported by this build";
+    case DREAMS_ERR_WORKSPACE: return "DREAMS_ERR_WORKSPACE: workspace missing or too small";
+    case DREAMS_ERR_HIP: return "DREAMS_ERR_HIP: the HIP runtime reported an error";
+  }
+  return "unknown dreams status";
+}
+
+const char* dreams_last_error_message(void) { return g_error.c_str(); }
+
+dreams_status_t dreams_check_tree_host(const int32_t* parent, int32_t num_nodes) {
+  if (!parent) return fail(DREAMS_ERR_INVALID_ARG, "parent is NULL");
+  if (num_nodes < 1) return fail(DREAMS_ERR_INVALID_ARG, "num_nodes = %d < 1", num_nodes);
+  if (parent[0] != -1) return fail(DREAMS_ERR_INVALID_ARG, "parent[0] = %d, the root must have parent -1", parent[0]);
+  for (int i = 1; i < num_nodes; ++i)
+    if (parent[i] < 0 || parent[i] >= i)
+      return fail(DREAMS_ERR_INVALID_ARG, "parent[%d] = %d is not in [0, %d)", i, parent[i], i);
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+// Internal interface between the host layer (dreams_api.hip) and the gfx950 kernels.  Not installed.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dreams {
+
+// ------------------------------------------------------------------------------------ tree attention
+// Matrix-core (bf16) path: one workgroup = 4 waves, each wave owns 16 query rows of one KV head, so a
+// workgroup covers kAttnRows rows; the key axis of every (sequence, KV head) is cut into `splits` pieces.
+constexpr int kAttnWaves = 4;
+constexpr int kAttnRows = 16 * kAttnWaves;
+constexpr int kAttnThreads = 64 * kAttnWaves;
+constexpr int kMaxNodes = 128;
+
+struct AttnArgs {
+  const void* q;          // [B, Hq, T, D]
+  const void* k;          // [B, Hkv, S_cap, D]
+  const void* v;
+  const int32_t* kv_len;  // [B]
+  const int32_t* parent;  // [B, T] (unused when mask != nullptr)
+  const uint64_t* mask;   // [B, T, ceil(T/64)] or nullptr
+  void* out;              // [B, Hq, T, D]
+  float* lse;             // [B, Hq, T] or nullptr
+  float* part_acc;        // [units * row_groups, splits, kAttnRows, D]   (splits > 1 only)
+  float* part_ml;         // [units * row_groups, splits, kAttnRows, 2]
+  uint32_t* counters;     // [units * row_groups], zero between calls
+  int B, Hq, Hkv, G, T, D, S_cap;
+  int units;              // B * Hkv
+  int row_groups;         // ceil(G*T / kAttnRows)
+  int splits;
+  int key_tile;           // keys per LDS tile (64 or 128)
+  float scale_log2;       // scale * log2(e)
+};
+
+// Grid size (in workgroups) of the bf16 kernel for this plan.
+int tree_attn_bf16_grid(const AttnArgs& a);
+hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
+
+// ---------------------------------------------------------------------------------------- acceptance
+constexpr int kAcceptThreads = 256;
+
+struct AcceptArgs {
+  const float* logits;    // [B, T, V]
+  const int32_t* tokens;  // [B, T]
+  const int32_t* parent;  // [B, T]
+  int32_t* accept_len;    // [B]
+  int32_t* accept_path;   // [B, T]
+  int32_t* next_token;    // [B]
+  int32_t* target_argmax; // [B, T] or nullptr
+  float* part_val;        // [B, T, chunks]
+  int32_t* part_idx;      // [B, T, chunks]
+  uint32_t* counters;     // [B], zero between calls
+  int B, T, V;
+  int chunks;             // vocabulary pieces per row
+  int chunk;              // elements per piece (multiple of 4 when vectorised)
+  int vec4;               // logits rows are 16-byte aligned and V % 4 == 0
+};
+
+hipError_t launch_tree_accept(const AcceptArgs& a, hipStream_t stream);
+
+// ------------------------------------------------------------------------------------------ commit
+constexpr int kCommitThreads = 256;
+constexpr int kCommitRowsPerPass = 32;
+constexpr int kCommitMaxRowBytes = 512;
+
+struct CommitArgs {
+  char* k;
+  char* v;
+  const int32_t* kv_len_in;
+  const int32_t* path;
+  const int32_t* accept_len;
+  int32_t* kv_len_out;
+  int64_t layer_stride_bytes;
+  int NL, B, Hkv, S_cap, path_stride;
+  int row_bytes;          // D * element size, multiple of 16, <= kCommitMaxRowBytes
+};
+
+hipError_t launch_kv_commit(const CommitArgs& a, hipStream_t stream);
+
+}  // namespace dreams

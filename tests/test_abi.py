@@ -1,0 +1,163 @@
+"""C ABI of libdreams.so on the CPU: the library loads, exports every symbol include/dreams.h declares, and
+rejects bad host-visible arguments (with a message) before anything is enqueued.  No kernel runs here."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dreams.h")
+
+
+@pytest.fixture(scope="module")
+def D():
+    from paper_2606_00535_amd import dreams
+    if not os.path.exists(dreams.LIBRARY):
+        from paper_2606_00535_amd import build
+        build.build()
+    return dreams
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(dreams_\w+)\s*\(", text, re.M)))
+
+
+def test_header_and_binding_agree(D):
+    assert declared_functions() == sorted(D.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(D):
+    out = subprocess.run(["nm", "-D", "--defined-only", D.LIBRARY], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT\s+(dreams_\w+)$", out, re.M))
+    missing = set(declared_functions()) - exported
+    assert not missing, missing
+    lib = D.lib()
+    for name in declared_functions():
+        assert getattr(lib, name) is not None
+
+
+def test_header_compiles_as_c():
+    r = subprocess.run(["gcc", "-std=c99", "-fsyntax-only", "-Wall", "-Werror", "-I/opt/rocm/include",
+                        "-D__HIP_PLATFORM_AMD__", "-x", "c", "-"], input='#include "%s"\nint main(void){return 0;}\n'
+                       % HEADER, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+def _desc(D, **kw):
+    base = dict(batch=1, num_q_heads=32, num_kv_heads=32, head_dim=128, num_nodes=60, cache_capacity=3200,
+                max_kv_len=0, num_splits=8, dtype=D.DREAMS_BF16, scale=0.088)
+    base.update(kw)
+    return D.AttnDesc(**base)
+
+
+def _ws(D, desc):
+    n = ctypes.c_size_t(123)
+    st = D.lib().dreams_tree_verify_attn_workspace_size(ctypes.byref(desc), ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), -1), (dict(num_q_heads=0), -1), (dict(num_kv_heads=0), -1),
+    (dict(num_q_heads=30, num_kv_heads=4), -1), (dict(head_dim=96), -2), (dict(num_nodes=0), -1),
+    (dict(num_nodes=129), -1), (dict(cache_capacity=59), -1), (dict(max_kv_len=3141), -1),
+    (dict(max_kv_len=-5), -1), (dict(num_splits=-1), -1), (dict(num_splits=5000), -1), (dict(dtype=7), -1),
+    (dict(scale=float("inf")), -1), (dict(scale=float("nan")), -1),
+])
+def test_attn_desc_rejected(D, kw, status):
+    st, _ = _ws(D, _desc(D, **kw))
+    assert st == status
+    assert D.lib().dreams_last_error_message().decode() != ""
+
+
+def test_attn_workspace_size_formula(D):
+    # explicit split count: no device query needed; partial accumulators + (m, l) + counters, 256-aligned
+    desc = _desc(D, num_splits=8)
+    st, n = _ws(D, desc)
+    assert st == 0
+    rows = 32 * 1 * 8 * 64
+    up = lambda x: (x + 255) // 256 * 256
+    assert n == up(rows * 128 * 4) + up(rows * 2 * 4) + up(32 * 4)
+    assert D.lib().dreams_last_error_message().decode() == ""
+    assert _ws(D, _desc(D, num_splits=1))[1] == 0
+    assert _ws(D, _desc(D, dtype=D.DREAMS_F32, num_splits=4))[1] == 0
+    # a request above the number of 64-key tiles is reduced to it: 3200 slots -> 50 tiles
+    assert _ws(D, _desc(D, num_splits=4000)) == _ws(D, _desc(D, num_splits=50))
+
+
+def test_attn_call_rejections(D):
+    lib = D.lib()
+    desc = _desc(D, num_splits=1)
+    fake = ctypes.c_void_p(0x100000)
+    # batch 0: nothing to do, nothing enqueued
+    assert lib.dreams_tree_verify_attn(ctypes.byref(_desc(D, batch=0)), None, None, None, None, None, None, None,
+                                       None, None, 0, None) == 0
+    assert lib.dreams_tree_verify_attn(ctypes.byref(desc), None, fake, fake, fake, fake, None, fake, None, None, 0,
+                                       None) == -1
+    assert lib.dreams_tree_verify_attn(ctypes.byref(desc), fake, fake, fake, fake, None, None, fake, None, None, 0,
+                                       None) == -1
+    assert "parent or tree_mask" in lib.dreams_last_error_message().decode()
+    mis = ctypes.c_void_p(0x100002)
+    assert lib.dreams_tree_verify_attn(ctypes.byref(desc), mis, fake, fake, fake, fake, None, fake, None, None, 0,
+                                       None) == -1
+    desc8 = _desc(D, num_splits=8)
+    assert lib.dreams_tree_verify_attn(ctypes.byref(desc8), fake, fake, fake, fake, fake, None, fake, None, None, 0,
+                                       None) == -3
+    assert lib.dreams_tree_verify_attn(ctypes.byref(desc8), fake, fake, fake, fake, fake, None, fake, None, fake, 16,
+                                       None) == -3
+    assert "needed" in lib.dreams_last_error_message().decode()
+    assert lib.dreams_tree_verify_attn(None, fake, fake, fake, fake, fake, None, fake, None, None, 0, None) == -1
+
+
+def test_accept_rejections_and_sizes(D):
+    lib = D.lib()
+    n = ctypes.c_size_t(0)
+    assert lib.dreams_tree_accept_workspace_size(1, 60, 32000, ctypes.byref(n)) == 0 and n.value > 0
+    assert lib.dreams_tree_accept_workspace_size(1, 0, 32000, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_workspace_size(1, 129, 32000, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_workspace_size(1, 60, 0, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_workspace_size(-1, 60, 10, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_workspace_size(1, 60, 10, None) == -1
+    fake = ctypes.c_void_p(0x100000)
+    assert lib.dreams_tree_accept(0, 60, 10, None, None, None, None, None, None, None, None, 0, None) == 0
+    assert lib.dreams_tree_accept(1, 60, 10, fake, fake, None, fake, fake, fake, None, fake, 1 << 20, None) == -1
+    assert lib.dreams_tree_accept(1, 60, 10, fake, fake, fake, fake, fake, fake, None, None, 0, None) == -3
+
+
+def test_commit_rejections(D):
+    lib = D.lib()
+    fake = ctypes.c_void_p(0x100000)
+    other = ctypes.c_void_p(0x200000)
+    args = lambda **kw: dict(dict(NL=2, stride=4 * 2 * 64 * 128, B=4, Hkv=2, Dh=128, S=64, dt=D.DREAMS_BF16,
+                                  k=fake, v=fake, lin=fake, path=fake, alen=fake, ps=60, lout=other), **kw)
+
+    def call(a):
+        return lib.dreams_kv_commit(a["NL"], a["stride"], a["B"], a["Hkv"], a["Dh"], a["S"], a["dt"], a["k"], a["v"],
+                                    a["lin"], a["path"], a["alen"], a["ps"], a["lout"], None)
+    assert call(args(NL=0)) == -1
+    assert call(args(Dh=4)) == -2                       # 8-byte rows are not a multiple of 16 bytes
+    assert call(args(Dh=256, dt=D.DREAMS_F32)) == -2    # 1 KiB rows
+    assert call(args(stride=100)) == -1                 # layers would overlap
+    assert call(args(lout=fake)) == -1                  # kv_len_out aliases kv_len_in
+    assert "overlap" in lib.dreams_last_error_message().decode()
+    assert call(args(k=None)) == -1
+    assert call(args(dt=5)) == -1
+    assert call(args(B=0)) == 0
+
+
+def test_check_tree_host(D):
+    D.check_tree_host(np.array([-1, 0, 0, 1, 2], np.int32))
+    D.check_tree_host(np.array([-1], np.int32))
+    for bad in ([0, 0], [-1, 1], [-1, 0, 3], [-1, -1], [-1, 0, -2]):
+        with pytest.raises(D.DreamsError):
+            D.check_tree_host(np.array(bad, np.int32))
+
+
+def test_status_strings(D):
+    lib = D.lib()
+    for s in (0, -1, -2, -3, -4):
+        assert lib.dreams_status_string(s).decode().startswith("DREAMS_")
+    assert b"unknown" in lib.dreams_status_string(42)

@@ -1,0 +1,279 @@
+"""GPU parity of dreams_tree_verify_attn against the fp64 CPU oracle, on the same seeded inputs.
+
+Bars: the contract (max-abs <= 2e-2 for bf16 in / fp32 accumulate; 1e-5 for the fp32 path) and a tighter
+bound derived from the bf16 path's arithmetic.  The probabilities are rounded to bf16 once before the value
+product and the output is rounded to bf16 once, everything else is fp32, so per element
+    |out - ref| <= 2^-9 * (sum_j p_j |v_j| / sum_j p_j + |ref|)     (+ fp32 noise),
+and the first term is exactly the oracle's output on |V|.  The tests allow 1.5x that.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import ATTN_TOL_BF16, ATTN_TOL_F32, LSE_TOL, attn_errors, device, f32, layer_tensors, note, to_dev
+from paper_2606_00535_amd import dreams
+from paper_2606_00535_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+
+def oracle_layer(batch, li, abs_v=False, parent=None, mask=None):
+    v = f32(batch.v_cache[li])
+    return oracle.tree_attn(f32(batch.q[li]), f32(batch.k_cache[li]), np.abs(v) if abs_v else v, batch.kv_len,
+                            batch.parent if parent is None and mask is None else parent, batch.scale,
+                            batch.wl.num_kv_heads, tree_mask=mask)
+
+
+def check_bf16(out, lse, batch, li, label, ref=None, absref=None, mask=None):
+    if ref is None:
+        ref = oracle_layer(batch, li, mask=mask)
+    if absref is None:
+        absref = oracle_layer(batch, li, abs_v=True, mask=mask)[0]
+    o_ref, l_ref = ref
+    mx, _, o = attn_errors(out, o_ref)
+    bound = 1.5 * 2.0 ** -9 * (absref + np.abs(o_ref)) + 1e-5
+    worst = float(np.max(np.abs(o - o_ref) / bound))
+    lerr = float(np.nanmax(np.abs(lse.cpu().numpy() - l_ref))) if lse is not None else 0.0
+    note("%s: max_abs=%.3e (contract %.0e) worst/bound=%.3f lse_err=%.2e" % (label, mx, ATTN_TOL_BF16, worst, lerr))
+    assert mx <= ATTN_TOL_BF16, label
+    assert worst <= 1.0, label
+    assert lerr <= LSE_TOL, label
+    return o
+
+
+def small_wl(**kw):
+    base = dict(name="small", batch=2, num_q_heads=4, num_kv_heads=2, head_dim=128, dtype="bf16", num_layers=1,
+                kv_len=300, image_tokens=0, num_nodes=16, depth=4, max_branch=3, vocab=64, agree=0.7, seed=11)
+    base.update(kw)
+    return W.Workload(**base)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    d = device()
+    dreams.lib()
+    return d
+
+
+def test_tiny_fp32(dev):
+    batch = W.make_batch(W.WORKLOADS["tiny"], with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    note("tiny fp32: B=1 Hq=4 D=64 L=640 T=16")
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par)
+    torch.cuda.synchronize()
+    ref, lref = oracle_layer(batch, 0)
+    err = float(np.abs(out.cpu().numpy() - ref).max())
+    lerr = float(np.abs(lse.cpu().numpy() - lref).max())
+    note("tiny fp32 max_abs=%.3e lse=%.3e" % (err, lerr))
+    assert err <= ATTN_TOL_F32 and lerr <= 1e-4
+
+
+@pytest.mark.parametrize("variant", ["plain", "sharp", "tree_dominant"])
+def test_tiny_fp32_variants(dev, variant):
+    batch = W.make_batch(W.WORKLOADS["tiny"], with_logits=False)
+    batch = {"plain": batch, "sharp": W.make_sharp(batch, 32.0), "tree_dominant": W.make_tree_dominant(batch)}[variant]
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    out, _ = dreams.tree_verify_attn(q, k, v, kv, par)
+    ref, _ = oracle_layer(batch, 0)
+    err = float(np.abs(out.cpu().numpy() - ref).max())
+    note("tiny fp32 %s max_abs=%.3e" % (variant, err))
+    assert err <= ATTN_TOL_F32
+
+
+CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits)
+    (128, 4, 2, 16, 4, 3, 300, 0),
+    (128, 4, 2, 16, 4, 3, 300, 1),
+    (128, 4, 2, 16, 4, 3, 300, 3),
+    (128, 2, 2, 60, 6, 4, 1000, 0),
+    (128, 2, 2, 60, 6, 4, 1000, 7),
+    (128, 3, 1, 60, 6, 4, 77, 2),      # G=3: 180 rows -> 3 row groups, ragged
+    (64, 4, 4, 16, 4, 3, 513, 0),
+    (64, 2, 1, 100, 8, 6, 130, 4),     # T > 64: second mask word
+    (128, 2, 2, 1, 0, 1, 250, 0),      # single node = decode step
+    (128, 2, 2, 33, 5, 3, 0, 0),       # empty prefix: tree keys only
+    (128, 2, 2, 33, 5, 3, 0, 2),
+    (128, 7, 1, 128, 8, 6, 700, 0),    # GQA 7 x 128 rows = 14 row groups, deepest tree
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "D%d_Hq%d_Hkv%d_T%d_L%d_S%d" % (c[0], c[1], c[2], c[3], c[6], c[7]))
+@pytest.mark.parametrize("variant", ["plain", "tree_dominant"])
+def test_bf16_parity(dev, case, variant):
+    D, Hq, Hkv, T, depth, br, L, splits = case
+    wl = small_wl(head_dim=D, num_q_heads=Hq, num_kv_heads=Hkv, num_nodes=T, depth=depth, max_branch=br, kv_len=L)
+    batch = W.make_batch(wl, with_logits=False, kv_lens=[L, max(0, L - 37)])
+    if variant == "tree_dominant":
+        batch = W.make_tree_dominant(batch)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    note("bf16 %s %s" % (variant, case))
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=splits)
+    torch.cuda.synchronize()
+    check_bf16(out, lse, batch, 0, "bf16 %s %s" % (variant, case))
+
+
+def test_split_sweep_agrees(dev):
+    wl = small_wl(num_q_heads=2, num_kv_heads=2, num_nodes=60, depth=6, max_branch=4, kv_len=1500)
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    ref = oracle_layer(batch, 0)
+    absref = oracle_layer(batch, 0, abs_v=True)[0]
+    outs = []
+    for s in (1, 2, 8, 24, 4096):
+        note("split sweep S=%d" % s)
+        out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=s)
+        torch.cuda.synchronize()
+        outs.append(check_bf16(out, lse, batch, 0, "split %d" % s, ref, absref))
+    for o in outs[1:]:
+        assert np.max(np.abs(o - outs[0])) <= 2 * 2.0 ** -8 * (np.abs(outs[0]).max() + 1)
+
+
+def test_repeat_is_bitwise_identical(dev):
+    wl = small_wl(num_q_heads=4, num_kv_heads=4, num_nodes=60, depth=6, max_branch=4, kv_len=2000)
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    first = None
+    for rep in range(5):
+        out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=8)
+        torch.cuda.synchronize()
+        cur = (out.view(torch.int16).cpu().numpy(), lse.cpu().numpy())
+        if first is None:
+            first = cur
+        else:
+            assert np.array_equal(cur[0], first[0]) and np.array_equal(cur[1], first[1]), rep
+
+
+def test_workspace_left_zero(dev):
+    wl = small_wl(num_nodes=60, depth=6, max_branch=4, kv_len=900)
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    desc = dreams.attn_desc(q, k, num_splits=5)
+    n = dreams.tree_verify_attn_workspace_size(desc)
+    ws = torch.zeros(n, dtype=torch.uint8, device=dev)
+    for _ in range(3):
+        dreams.tree_verify_attn(q, k, v, kv, par, num_splits=5, workspace=ws)
+    torch.cuda.synchronize()
+    sets = 2 * 2 * 1
+    cnt = ws[n - ((sets * 4 + 255) // 256 * 256):].cpu().numpy()
+    assert not cnt.any()
+
+
+def test_nonancestor_perturbation_bitwise(dev):
+    wl = small_wl(num_q_heads=2, num_kv_heads=2, num_nodes=60, depth=6, max_branch=4, kv_len=700, batch=1)
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=3)
+    parent = batch.parent[0]
+    anc = [set() for _ in range(60)]
+    for i in range(60):
+        j = i
+        while j >= 0:
+            anc[i].add(j)
+            j = parent[j]
+    rng = np.random.default_rng(5)
+    for i in rng.choice(60, size=6, replace=False):
+        k2, v2 = k.clone(), v.clone()
+        others = [j for j in range(60) if j not in anc[i]]
+        idx = torch.tensor([700 + j for j in others], device=dev)
+        k2[0][:, idx] = torch.randn_like(k2[0][:, idx]) * 3
+        v2[0][:, idx] = torch.randn_like(v2[0][:, idx]) * 3
+        out2, lse2 = dreams.tree_verify_attn(q, k2, v2, kv, par, num_splits=3)
+        torch.cuda.synchronize()
+        assert torch.equal(out2[0, :, i].view(torch.int16), out[0, :, i].view(torch.int16)), int(i)
+        assert torch.equal(lse2[0, :, i], lse[0, :, i]), int(i)
+
+
+def test_mask_input_matches_parent_and_empty_rows(dev):
+    from pins import ancestor_closure, mask_bits_from_closure
+    wl = small_wl(num_q_heads=2, num_kv_heads=1, num_nodes=100, depth=8, max_branch=6, kv_len=400)
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    bits = np.stack([mask_bits_from_closure(ancestor_closure(batch.parent[b])) for b in range(2)])
+    mask = to_dev(bits.view(np.int64), dev)
+    o1, l1 = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=2)
+    o2, l2 = dreams.tree_verify_attn(q, k, v, kv, None, tree_mask=mask, num_splits=2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+    # empty prefix and an all-zero mask row: nothing visible -> zeros and lse = -inf, like the oracle
+    bits2 = bits.copy()
+    bits2[:, 5] = 0
+    kv0 = torch.zeros(2, dtype=torch.int32, device=dev)
+    o3, l3 = dreams.tree_verify_attn(q, k, v, kv0, None, tree_mask=to_dev(bits2.view(np.int64), dev), num_splits=2)
+    torch.cuda.synchronize()
+    assert torch.all(o3[:, :, 5] == 0) and torch.all(torch.isneginf(l3[:, :, 5]))
+    ref, lref = oracle.tree_attn(f32(batch.q[0]), f32(batch.k_cache[0]), f32(batch.v_cache[0]),
+                                 np.zeros(2, np.int32), None, batch.scale, 1, tree_mask=bits2)
+    o3n = o3.float().cpu().numpy()
+    ok = np.isfinite(lref)
+    assert np.max(np.abs(o3n - ref)) <= ATTN_TOL_BF16 and np.max(np.abs(l3.cpu().numpy()[ok] - lref[ok])) <= LSE_TOL
+
+
+def test_kv_len_clamped_into_cache(dev):
+    # a prefix length past the capacity is clamped to S_cap - T: same result as that length, no stray access
+    wl = small_wl(num_nodes=16, kv_len=300)
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    S = batch.k_cache.shape[3]
+    big = torch.tensor([S + 1000, 10 ** 9], dtype=torch.int32, device=dev)
+    clamp = torch.tensor([S - 16, S - 16], dtype=torch.int32, device=dev)
+    o1, _ = dreams.tree_verify_attn(q, k, v, big, par, num_splits=2)
+    o2, _ = dreams.tree_verify_attn(q, k, v, clamp, par, num_splits=2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+
+
+def test_batch_zero_is_noop(dev):
+    q = torch.empty((0, 2, 4, 128), dtype=torch.bfloat16, device=dev)
+    k = torch.empty((0, 2, 64, 128), dtype=torch.bfloat16, device=dev)
+    kv = torch.empty(0, dtype=torch.int32, device=dev)
+    par = torch.empty((0, 4), dtype=torch.int32, device=dev)
+    out, lse = dreams.tree_verify_attn(q, k, k, kv, par)
+    torch.cuda.synchronize()
+    assert out.shape == q.shape
+
+
+# ------------------------------------------------------------------------- full-size shapes
+def test_llava7b_layer_full_parity(dev):
+    batch = W.make_batch(W.WORKLOADS["llava7b_layer"], with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    note("llava7b_layer: B=1 Hq=32 D=128 L=3136 T=60 (auto splits)")
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par)
+    torch.cuda.synchronize()
+    check_bf16(out, lse, batch, 0, "llava7b_layer")
+    bdom = W.make_tree_dominant(batch)
+    q, k, v, kv, par = layer_tensors(bdom, 0, dev)
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par)
+    torch.cuda.synchronize()
+    check_bf16(out, lse, bdom, 0, "llava7b_layer tree_dominant")
+
+
+def sampled_rows(rng, B, Hq, T, n):
+    rows = np.stack([rng.integers(0, B, n), rng.integers(0, Hq, n), rng.integers(0, T, n)], axis=1).astype(np.int32)
+    rows[:4] = [[0, 0, 0], [B - 1, Hq - 1, T - 1], [0, Hq - 1, T // 2], [B - 1, 0, 1 % T]]
+    return rows
+
+
+@pytest.mark.parametrize("name,layers", [("llava7b_full", [0, 15, 31]), ("llava13b_layer", [0]), ("gqa_long", [0])])
+def test_full_size_sampled_rows(dev, name, layers):
+    wl = W.WORKLOADS[name]
+    batch = W.make_batch(wl, layers=layers, with_logits=False)
+    rng = np.random.default_rng(3)
+    for li, layer in enumerate(layers):
+        q, k, v, kv, par = layer_tensors(batch, li, dev)
+        note("%s layer %d: sampled rows (auto splits)" % (name, layer))
+        out, lse = dreams.tree_verify_attn(q, k, v, kv, par, max_kv_len=wl.max_kv_len)
+        torch.cuda.synchronize()
+        rows = sampled_rows(rng, wl.batch, wl.num_q_heads, wl.num_nodes, 96)
+        args = (f32(batch.q[li]), f32(batch.k_cache[li]))
+        ref, lref = oracle.tree_attn_rows(*args, f32(batch.v_cache[li]), batch.kv_len, batch.parent, batch.scale,
+                                          wl.num_kv_heads, rows)
+        absref, _ = oracle.tree_attn_rows(*args, np.abs(f32(batch.v_cache[li])), batch.kv_len, batch.parent,
+                                          batch.scale, wl.num_kv_heads, rows)
+        o = out.float().cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]].astype(np.float64)
+        l = lse.cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
+        mx = float(np.abs(o - ref).max())
+        worst = float(np.max(np.abs(o - ref) / (1.5 * 2.0 ** -9 * (absref + np.abs(ref)) + 1e-5)))
+        note("  max_abs=%.3e worst/bound=%.3f lse=%.2e" % (mx, worst, float(np.abs(l - lref).max())))
+        assert mx <= ATTN_TOL_BF16 and worst <= 1.0 and float(np.abs(l - lref).max()) <= LSE_TOL
+        # property at any size: every output row is a convex combination of V rows -> bounded by max |V|
+        assert float(out.float().abs().max()) <= float(v.float().abs().max()) * (1 + 2 ** -7)
