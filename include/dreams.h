@@ -46,6 +46,16 @@ typedef enum {
 typedef enum { DREAMS_F32 = 0, DREAMS_BF16 = 1 } dreams_dtype_t;
 
 /*
+ * Workspaces.  Every workspace (of either verb that takes one) begins with DREAMS_WORKSPACE_COUNTER_BYTES
+ * bytes of arrival counters.  Zero-fill that region once, before the workspace is first used (zeroing the
+ * whole buffer after allocating it does this).  Every call, of any shape, leaves the region zero again when it
+ * completes, so one workspace of sufficient size can serve calls of different shapes and of both verbs one
+ * after another.  Calls that overlap in time on one workspace (different streams without synchronisation)
+ * race and give unspecified results.  Workspaces must be 256-byte aligned.
+ */
+#define DREAMS_WORKSPACE_COUNTER_BYTES 65536
+
+/*
  * Shape of one tree-verification attention call.
  *   batch            B >= 0 sequences
  *   num_q_heads      Hq >= 1 query heads
@@ -74,7 +84,9 @@ typedef struct {
   float scale;
 } dreams_attn_desc_t;
 
-/* Bytes of workspace dreams_tree_verify_attn needs for `desc` on the current device (may be 0). */
+/* Bytes of workspace dreams_tree_verify_attn needs for `desc` on the current device (0 if none: then the
+ * call accepts a NULL workspace).  DREAMS_ERR_UNSUPPORTED if the work plan needs more than
+ * DREAMS_WORKSPACE_COUNTER_BYTES / 4 counters (batch * num_kv_heads * row groups of 64 query rows). */
 dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t* desc, size_t* bytes);
 
 /*
@@ -101,8 +113,8 @@ dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t*
  *                                         node i.  Takes precedence over parent.
  *   out        device [B, Hq, T, D]      same dtype as q
  *   lse        device [B, Hq, T] float, or NULL
- *   workspace  device, >= dreams_tree_verify_attn_workspace_size bytes.  Must be zero-filled before its
- *              first use; every call leaves the part it relies on zero again when it completes.
+ *   workspace  device, >= dreams_tree_verify_attn_workspace_size bytes (see "Workspaces" above), or NULL
+ *              when that size is 0.
  * Arithmetic: bf16 products accumulated in fp32 on the matrix cores, softmax statistics in fp32, one
  * rounding of the probabilities to bf16 before the value product; output rounded to the nearest bf16.
  */
@@ -111,7 +123,7 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
                                         const uint64_t* tree_mask, void* out, float* lse, void* workspace,
                                         size_t workspace_bytes, hipStream_t stream);
 
-/* Bytes of workspace dreams_tree_accept needs (may be 0). */
+/* Bytes of workspace dreams_tree_accept needs (never 0; batch <= DREAMS_WORKSPACE_COUNTER_BYTES / 4). */
 dreams_status_t dreams_tree_accept_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
                                                   size_t* bytes);
 
@@ -135,8 +147,7 @@ dreams_status_t dreams_tree_accept_workspace_size(int32_t batch, int32_t num_nod
  *   accept_path    device [B, T] int32 (out)
  *   next_token     device [B] int32 (out)
  *   target_argmax  device [B, T] int32 (out) or NULL: tgt[i] for every node
- *   workspace      device, >= dreams_tree_accept_workspace_size bytes, zero-filled before first use; every
- *                  call leaves it zero again.
+ *   workspace      device, >= dreams_tree_accept_workspace_size bytes (see "Workspaces" above).
  * Bit-exact: integer results only; every comparison is an fp32 comparison of the caller's logits.
  */
 dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t vocab, const float* target_logits,

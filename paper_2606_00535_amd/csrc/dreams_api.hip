@@ -61,9 +61,16 @@ dreams_status_t device_cus(int* cus) {
 }
 
 // ------------------------------------------------------------------------------------------ attention
+// Every workspace starts with a fixed region of arrival counters, whatever the verb and shape, so a
+// workspace left zero by one call is valid for any other call.
+constexpr size_t kCounterBytes = DREAMS_WORKSPACE_COUNTER_BYTES;
+constexpr size_t kMaxCounters = kCounterBytes / sizeof(uint32_t);
+
 struct AttnPlan {
   int G, rows_total, row_groups, units, splits, key_tile;
-  size_t acc_off, ml_off, cnt_off, bytes;
+  int rows_per_wg;   // query rows one workgroup owns
+  bool stream;       // bandwidth-bound kernel (waves split keys) rather than the shared-tile kernel
+  size_t acc_off, ml_off, bytes;
 };
 
 constexpr int kMaxSplitsRequest = 4096;
@@ -100,7 +107,9 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   *p = AttnPlan{};
   p->G = d->num_q_heads / d->num_kv_heads;
   p->rows_total = p->G * d->num_nodes;
-  p->row_groups = (p->rows_total + kAttnRows - 1) / kAttnRows;
+  p->stream = d->dtype == DREAMS_BF16 && p->rows_total <= kStreamMaxRows;
+  p->rows_per_wg = p->stream ? kStreamRows : kAttnRows;
+  p->row_groups = (p->rows_total + p->rows_per_wg - 1) / p->rows_per_wg;
   p->units = d->batch * d->num_kv_heads;
   p->key_tile = 64;
   p->splits = 1;
@@ -111,23 +120,29 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   const int max_splits = (n_keys + p->key_tile - 1) / p->key_tile;
   int splits = d->num_splits;
   if (splits == 0) {
+    // enough workgroups to give every compute unit two (stream kernel) or one (shared-tile kernel)
     int cus = 0;
     st = device_cus(&cus);
     if (st != DREAMS_OK) return st;
+    const long long target = (long long)cus * (p->stream ? 2 : 1);
     const long long wgs = (long long)p->units * p->row_groups;
-    splits = (int)((cus + wgs - 1) / wgs);
+    splits = (int)((target + wgs / 2) / wgs);
   }
-  splits = splits < 1 ? 1 : (splits > max_splits ? max_splits : splits);
+  if (splits > max_splits) splits = max_splits;
+  if (splits > kAttnMaxSplits) splits = kAttnMaxSplits;
+  if (splits < 1) splits = 1;
   p->splits = splits;
   const long long grid = 8LL * ((p->units + 7) / 8) * splits * p->row_groups;
   if (grid > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large: %lld workgroups", grid);
   if (splits > 1) {
     const size_t sets = (size_t)p->units * p->row_groups;
-    const size_t rows = sets * splits * kAttnRows;
-    p->acc_off = 0;
-    p->ml_off = align_up(rows * d->head_dim * sizeof(float), 256);
-    p->cnt_off = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
-    p->bytes = p->cnt_off + align_up(sets * sizeof(uint32_t), 256);
+    if (sets > kMaxCounters)
+      return fail(DREAMS_ERR_UNSUPPORTED, "%zu (sequence, KV head, row group) sets exceed the %zu arrival counters",
+                  sets, kMaxCounters);
+    const size_t rows = sets * splits * p->rows_per_wg;
+    p->acc_off = kCounterBytes;
+    p->ml_off = p->acc_off + align_up(rows * d->head_dim * sizeof(float), 256);
+    p->bytes = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
   }
   return DREAMS_OK;
 }
@@ -135,7 +150,7 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
 // ----------------------------------------------------------------------------------------- acceptance
 struct AcceptPlan {
   int chunks, chunk;
-  size_t val_off, idx_off, cnt_off, bytes;
+  size_t val_off, idx_off, bytes;
 };
 
 constexpr int kAcceptTargetWgs = 2048;
@@ -151,6 +166,7 @@ dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
   long long chunks = (kAcceptTargetWgs + rows - 1) / rows;
   const long long max_chunks = (V + kAcceptMinPiece - 1) / kAcceptMinPiece;
   if (chunks > max_chunks) chunks = max_chunks;
+  if (chunks * T > kAcceptMaxParts) chunks = kAcceptMaxParts / T;
   if (chunks < 1) chunks = 1;
   long long chunk = (V + chunks - 1) / chunks;
   chunk = (chunk + 3) / 4 * 4;
@@ -158,11 +174,12 @@ dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
   if (rows * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
   p->chunks = (int)chunks;
   p->chunk = (int)chunk;
+  if ((size_t)B > kMaxCounters)
+    return fail(DREAMS_ERR_UNSUPPORTED, "batch = %d exceeds the %zu arrival counters", B, kMaxCounters);
   const size_t parts = (size_t)rows * chunks;
-  p->val_off = 0;
-  p->idx_off = align_up(parts * sizeof(float), 256);
-  p->cnt_off = p->idx_off + align_up(parts * sizeof(int32_t), 256);
-  p->bytes = p->cnt_off + align_up((size_t)B * sizeof(uint32_t), 256);
+  p->val_off = kCounterBytes;
+  p->idx_off = p->val_off + align_up(parts * sizeof(float), 256);
+  p->bytes = p->idx_off + align_up(parts * sizeof(int32_t), 256);
   return DREAMS_OK;
 }
 
@@ -224,7 +241,7 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   char* ws = (char*)workspace;
   a.part_acc = p.bytes ? (float*)(ws + p.acc_off) : nullptr;
   a.part_ml = p.bytes ? (float*)(ws + p.ml_off) : nullptr;
-  a.counters = p.bytes ? (uint32_t*)(ws + p.cnt_off) : nullptr;
+  a.counters = p.bytes ? (uint32_t*)ws : nullptr;
   a.B = desc->batch;
   a.Hq = desc->num_q_heads;
   a.Hkv = desc->num_kv_heads;
@@ -235,9 +252,12 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   a.units = p.units;
   a.row_groups = p.row_groups;
   a.splits = p.splits;
+  a.max_keys = (desc->max_kv_len > 0 ? desc->max_kv_len : desc->cache_capacity - desc->num_nodes) + desc->num_nodes;
   a.key_tile = p.key_tile;
   a.scale_log2 = desc->scale * 1.4426950408889634f;
-  hipError_t e = desc->dtype == DREAMS_BF16 ? launch_tree_attn_bf16(a, stream) : launch_tree_attn_f32(a, stream);
+  hipError_t e = desc->dtype == DREAMS_F32 ? launch_tree_attn_f32(a, stream)
+                 : p.stream               ? launch_tree_attn_stream(a, stream)
+                                          : launch_tree_attn_bf16(a, stream);
   if (e != hipSuccess) return hip_fail(e, "tree attention launch");
   return ok();
 }
@@ -281,7 +301,7 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
   char* ws = (char*)workspace;
   a.part_val = (float*)(ws + p.val_off);
   a.part_idx = (int32_t*)(ws + p.idx_off);
-  a.counters = (uint32_t*)(ws + p.cnt_off);
+  a.counters = (uint32_t*)ws;
   a.B = batch;
   a.T = num_nodes;
   a.V = vocab;

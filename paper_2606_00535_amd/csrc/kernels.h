@@ -6,6 +6,34 @@
 
 namespace dreams {
 
+// ------------------------------------------------------------------ cross-workgroup publication
+// Workgroups hand partial results to the last of them to finish through device-scope ("sc1") stores and
+// loads, which write through / read past the per-XCD L2 for exactly those words, plus a relaxed device-scope
+// atomic counter issued after an explicit wait for the stores.  Release/acquire fences would instead write
+// back and invalidate the whole L2 of the issuing XCD on every call.
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_coherent(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t load_coherent(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Wait until every vector-memory operation this thread issued has completed (gfx9 s_waitcnt encoding:
+// vmcnt = 0, expcnt and lgkmcnt left at their maxima).
+__device__ __forceinline__ void wait_vector_memory() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+// Arrival counter: returns true in exactly one workgroup, the one whose increment completes the count.
+__device__ __forceinline__ bool arrive_last(uint32_t* counter, uint32_t expected) {
+  return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == expected - 1;
+}
+__device__ __forceinline__ void reset_counter(uint32_t* counter) {
+  __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ------------------------------------------------------------------------------------ tree attention
 // Matrix-core (bf16) path: one workgroup = 4 waves, each wave owns 16 query rows of one KV head, so a
 // workgroup covers kAttnRows rows; the key axis of every (sequence, KV head) is cut into `splits` pieces.
@@ -13,6 +41,8 @@ constexpr int kAttnWaves = 4;
 constexpr int kAttnRows = 16 * kAttnWaves;
 constexpr int kAttnThreads = 64 * kAttnWaves;
 constexpr int kMaxNodes = 128;
+// The merge stages every piece's (m, l) for 64 rows in the K/V tile buffers: at most 32 pieces.
+constexpr int kAttnMaxSplits = 32;
 
 struct AttnArgs {
   const void* q;          // [B, Hq, T, D]
@@ -30,6 +60,7 @@ struct AttnArgs {
   int units;              // B * Hkv
   int row_groups;         // ceil(G*T / kAttnRows)
   int splits;
+  int max_keys;           // host-side bound on L_b + T over the batch (plans the pieces of the key axis)
   int key_tile;           // keys per LDS tile (64 or 128)
   float scale_log2;       // scale * log2(e)
 };
@@ -37,10 +68,19 @@ struct AttnArgs {
 // Grid size (in workgroups) of the bf16 kernel for this plan.
 int tree_attn_bf16_grid(const AttnArgs& a);
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream);
+
+// Bandwidth-bound bf16 path (few query rows per KV head): a workgroup of kStreamWaves waves owns kStreamRows
+// rows and one piece of the key axis; its waves split the piece's keys.  Used while G*T <= kStreamMaxRows.
+constexpr int kStreamRows = 32;
+constexpr int kStreamWaves = 4;
+constexpr int kStreamMaxRows = 128;
+hipError_t launch_tree_attn_stream(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------------------------------- acceptance
 constexpr int kAcceptThreads = 256;
+// Pieces (node x vocabulary chunk) of one sequence, staged in LDS by the path scan.
+constexpr int kAcceptMaxParts = 2304;
 
 struct AcceptArgs {
   const float* logits;    // [B, T, V]

@@ -7,7 +7,8 @@
 //      B*T*V*4 bytes).  Ties go to the smallest index: every thread visits its elements in increasing order
 //      and replaces its candidate only on a strictly larger value, and every merge prefers the smaller index
 //      on equal values (fp32 comparison, so -0.0 and +0.0 are equal).
-//   2. Path scan, by the last workgroup of the sequence to finish (arrival counter): per node, merge the
+//   2. Path scan, by the last workgroup of the sequence to finish (arrival counter; pieces travel through
+//      device-scope stores and loads): per node, merge the
 //      pieces in index order, then every node walks its own ancestor chain (at most depth steps, no
 //      barriers) to decide whether each draft on it equals the target token at its parent.  The deepest
 //      consistent node (smallest index among equals) is found with one block-wide max over the key
@@ -96,30 +97,36 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
   if (tid == 0) {
     for (int w = 1; w < NW; ++w)
       if (better(red_v[w], red_i[w], best.v, best.i)) { best.v = red_v[w]; best.i = red_i[w]; }
-    a.part_val[n] = best.v;
-    a.part_idx[n] = best.i;
-    __threadfence();
-    const uint32_t prev = atomicAdd(&a.counters[b], 1u);
-    last_flag = prev == (uint32_t)(a.T * a.chunks - 1);
+    store_coherent(a.part_val + n, best.v);
+    store_coherent(a.part_idx + n, best.i);
+    wait_vector_memory();
+    last_flag = arrive_last(&a.counters[b], (uint32_t)(a.T * a.chunks));
   }
   __syncthreads();
   if (!last_flag) return;
-  __threadfence();
 
-  // ---- phase 2: the sequence's path scan
+  // ---- phase 2: the sequence's path scan.  One parallel round trip stages all of the sequence's pieces.
   const int T = a.T;
+  __shared__ float pv_s[kAcceptMaxParts];
+  __shared__ int pi_s[kAcceptMaxParts];
+  const int parts = T * a.chunks;
+  const size_t p0 = (size_t)b * parts;
+  for (int e = tid; e < parts; e += NT) {
+    pv_s[e] = load_coherent(a.part_val + p0 + e);
+    pi_s[e] = load_coherent(a.part_idx + p0 + e);
+  }
   if (tid < T) {
-    const size_t p0 = ((size_t)b * T + tid) * a.chunks;
-    float bv = a.part_val[p0];
-    int bx = a.part_idx[p0];
-    for (int cc = 1; cc < a.chunks; ++cc) {
-      const float v = a.part_val[p0 + cc];
-      const int x = a.part_idx[p0 + cc];
-      if (better(v, x, bv, bx)) { bv = v; bx = x; }
-    }
-    am_s[tid] = bx;
     tok_s[tid] = a.tokens[(size_t)b * T + tid];
     par_s[tid] = a.parent[(size_t)b * T + tid];
+  }
+  __syncthreads();
+  if (tid < T) {
+    const int q0 = tid * a.chunks;
+    float bv = pv_s[q0];
+    int bx = pi_s[q0];
+    for (int cc = 1; cc < a.chunks; ++cc)
+      if (better(pv_s[q0 + cc], pi_s[q0 + cc], bv, bx)) { bv = pv_s[q0 + cc]; bx = pi_s[q0 + cc]; }
+    am_s[tid] = bx;
   }
   __syncthreads();
 
@@ -149,7 +156,7 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
     a.next_token[b] = am_s[last];
     int j = last;
     for (int k = alen; k >= 0; --k) { path[k] = j; j = par_s[j]; }
-    a.counters[b] = 0u;  // ready for the next call
+    reset_counter(&a.counters[b]);  // ready for the next call
   }
   if (tid > alen && tid < T) path[tid] = -1;
   if (a.target_argmax && tid < T) a.target_argmax[(size_t)b * T + tid] = am_s[tid];

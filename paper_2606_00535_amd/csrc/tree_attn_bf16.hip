@@ -15,8 +15,10 @@
 //     counter) merges them with the log-sum-exp identity in fixed split order, so results are reproducible
 //     bit for bit whichever workgroup arrives last.
 //   * Workgroup ids are remapped so that every workgroup of one (sequence, KV head) runs on the same XCD
-//     (the dispatcher deals consecutive ids round-robin over the 8 XCDs): the pieces' partial results are
-//     then merged from that XCD's L2, and row groups that read the same K/V tile share it there.
+//     (the dispatcher deals consecutive ids round-robin over the 8 XCDs): row groups that read the same K/V
+//     tile share it in that XCD's L2.  Partial results travel through device-scope stores and loads.
+//   * This kernel serves shapes with many query rows per KV head (grouped-query heads x tree nodes); shapes
+//     with few rows go to the streaming kernel, whose waves split the keys instead of the rows.
 //
 // Per key tile (KT keys): the whole workgroup streams K and V rows with 16-byte coalesced loads into LDS
 // (register double-buffered: the next tile's loads are in flight while this one is computed).  Each wave
@@ -79,8 +81,12 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_bf16_kernel(AttnArgs a
   constexpr int LPT = KT * CPR / NT;  // chunks of K (and of V) each thread moves per tile
   static_assert(LPT * NT == KT * CPR, "tile must split evenly over the workgroup");
 
-  __shared__ __attribute__((aligned(16))) __bf16 k_lds[KT * KS];
-  __shared__ __attribute__((aligned(16))) __bf16 v_lds[KT * VS];
+  // K tile, then V tile; after the main loop the same bytes hold the merge's staging (see below)
+  __shared__ __attribute__((aligned(16))) __bf16 tiles[KT * KS + KT * VS];
+  __bf16* const k_lds = tiles;
+  __bf16* const v_lds = tiles + KT * KS;
+  static_assert(kAttnMaxSplits * kAttnRows * 8 + 2 * kAttnRows * 4 <= (KT * KS + KT * VS) * 2,
+                "merge staging must fit in the tile buffers");
   __shared__ uint64_t anc_lds[2 * kMaxNodes];
   __shared__ int last_flag;
 
@@ -281,51 +287,90 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_bf16_kernel(AttnArgs a
   {
     float* pa = a.part_acc + pbase * D + quad * 4;
 #pragma unroll
-    for (int d = 0; d < DB; ++d) *(f32x4*)(pa + d * 16) = o[d];
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) store_coherent(pa + d * 16 + e, o[d][e]);
     if (quad == 0) {
-      a.part_ml[2 * pbase] = m_run;
-      a.part_ml[2 * pbase + 1] = l_run;
+      store_coherent(a.part_ml + 2 * pbase, m_run);
+      store_coherent(a.part_ml + 2 * pbase + 1, l_run);
     }
   }
-  __threadfence();
+  wait_vector_memory();
   __syncthreads();
-  if (tid == 0) {
-    const uint32_t prev = atomicAdd(&a.counters[pset], 1u);
-    last_flag = prev == (uint32_t)(a.splits - 1);
-  }
+  if (tid == 0) last_flag = arrive_last(&a.counters[pset], (uint32_t)a.splits);
   __syncthreads();
   if (!last_flag) return;
-  __threadfence();
-  if (tid == 0) a.counters[pset] = 0u;  // ready for the next call
+  if (tid == 0) reset_counter(&a.counters[pset]);
 
-  const int rows_here = min(kAttnRows, rows_total - rg * kAttnRows);
-  constexpr int D4 = D / 4;
-  for (int item = tid; item < rows_here * D4; item += NT) {
-    const int rl = item / D4, d4 = item - rl * D4;
+  // Merge.  (1) one round trip stages every piece's (m, l) for the 64 rows in LDS (the K/V tile buffers are
+  // free now); (2) one thread per row turns them into weights 2^(m_s - M) and 1/sum; (3) every thread owns
+  // one 4-column slice of several rows and streams the pieces' accumulators with many loads in flight.
+  float2* ml = (float2*)tiles;                       // [splits][kAttnRows]
+  float* inv_l = (float*)(ml + kAttnMaxSplits * kAttnRows);  // [kAttnRows]
+  float* row_m = inv_l + kAttnRows;                  // [kAttnRows]
+  const int S = a.splits;
+  const size_t pset_rows = pset * S * kAttnRows;
+  for (int e = tid; e < S * kAttnRows; e += NT)
+    ml[e] = make_float2(load_coherent(a.part_ml + 2 * (pset_rows + e)), load_coherent(a.part_ml + 2 * (pset_rows + e) + 1));
+  __syncthreads();
+  if (tid < kAttnRows) {
     float M = -INFINITY;
-    for (int sp = 0; sp < a.splits; ++sp)
-      M = fmaxf(M, a.part_ml[2 * ((pset * a.splits + sp) * kAttnRows + rl)]);
+    for (int sp = 0; sp < S; ++sp) M = fmaxf(M, ml[sp * kAttnRows + tid].x);
     float lsum = 0.f;
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (M != -INFINITY) {
-      for (int sp = 0; sp < a.splits; ++sp) {
-        const size_t pr = (pset * a.splits + sp) * kAttnRows + rl;
-        const float ms = a.part_ml[2 * pr];
-        if (ms == -INFINITY) continue;  // empty or fully masked piece
-        const float w = fast_exp2(ms - M);
-        lsum += w * a.part_ml[2 * pr + 1];
-        acc += w * *(const f32x4*)(a.part_acc + pr * D + d4 * 4);
-      }
+    for (int sp = 0; sp < S; ++sp) {
+      const float2 v = ml[sp * kAttnRows + tid];
+      const float w = v.x == -INFINITY ? 0.f : fast_exp2(v.x - M);
+      lsum += w * v.y;
+      ml[sp * kAttnRows + tid].x = w;
     }
+    inv_l[tid] = lsum > 0.f ? 1.0f / lsum : 0.f;
+    row_m[tid] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+  }
+  __syncthreads();
+
+  constexpr int D4 = D / 4;                          // 4-column slices per row
+  constexpr int RSTEP = NT / D4;                     // rows covered by one pass of the workgroup
+  constexpr int RPT = kAttnRows / RSTEP;             // rows per thread
+  const int d4 = tid % D4, r0 = tid / D4;
+  f32x4 acc[RPT];
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const float* pacc = a.part_acc + pset_rows * D + d4 * 4;
+  auto load4 = [&](size_t idx) {
+    const float* p = pacc + idx * D;
+    return f32x4{load_coherent(p), load_coherent(p + 1), load_coherent(p + 2), load_coherent(p + 3)};
+  };
+  int sp = 0;
+  for (; sp + 1 < S; sp += 2) {                      // two pieces x RPT rows of loads in flight
+    f32x4 x0[RPT], x1[RPT];
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+      x0[j] = load4((size_t)sp * kAttnRows + r0 + j * RSTEP);
+      x1[j] = load4((size_t)(sp + 1) * kAttnRows + r0 + j * RSTEP);
+    }
+#pragma unroll
+    for (int j = 0; j < RPT; ++j)
+      acc[j] += ml[sp * kAttnRows + r0 + j * RSTEP].x * x0[j] + ml[(sp + 1) * kAttnRows + r0 + j * RSTEP].x * x1[j];
+  }
+  if (sp < S) {
+#pragma unroll
+    for (int j = 0; j < RPT; ++j)
+      acc[j] += ml[sp * kAttnRows + r0 + j * RSTEP].x * load4((size_t)sp * kAttnRows + r0 + j * RSTEP);
+  }
+  const int rows_here = min(kAttnRows, rows_total - rg * kAttnRows);
+#pragma unroll
+  for (int j = 0; j < RPT; ++j) {
+    const int rl = r0 + j * RSTEP;
+    if (rl >= rows_here) continue;
     const int r = rg * kAttnRows + rl;
     const int hg = r / T, nd = r - hg * T;
     const size_t orow = ((size_t)b * a.Hq + g * a.G + hg) * T + nd;
-    const float inv = lsum > 0.f ? 1.0f / lsum : 0.f;
+    const float inv = inv_l[rl];
     bf16x4 res;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) res[e] = (__bf16)(acc[e] * inv);
+    for (int e = 0; e < 4; ++e) res[e] = (__bf16)(acc[j][e] * inv);
     *(bf16x4*)((__bf16*)a.out + orow * D + d4 * 4) = res;
-    if (a.lse && d4 == 0) a.lse[orow] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+    if (a.lse && d4 == 0) a.lse[orow] = row_m[rl];
   }
 }
 

@@ -80,12 +80,13 @@ def test_attn_workspace_size_formula(D):
     assert st == 0
     rows = 32 * 1 * 8 * 64
     up = lambda x: (x + 255) // 256 * 256
-    assert n == up(rows * 128 * 4) + up(rows * 2 * 4) + up(32 * 4)
+    assert n == 65536 + up(rows * 128 * 4) + up(rows * 2 * 4)     # counters, accumulators, (m, l)
     assert D.lib().dreams_last_error_message().decode() == ""
     assert _ws(D, _desc(D, num_splits=1))[1] == 0
     assert _ws(D, _desc(D, dtype=D.DREAMS_F32, num_splits=4))[1] == 0
-    # a request above the number of 64-key tiles is reduced to it: 3200 slots -> 50 tiles
-    assert _ws(D, _desc(D, num_splits=4000)) == _ws(D, _desc(D, num_splits=50))
+    # a request above the number of 64-key tiles (3200 slots -> 50) or above 32 pieces is reduced
+    assert _ws(D, _desc(D, num_splits=4000)) == _ws(D, _desc(D, num_splits=32))
+    assert _ws(D, _desc(D, num_splits=20, cache_capacity=640)) == _ws(D, _desc(D, num_splits=10, cache_capacity=640))
 
 
 def test_attn_call_rejections(D):
@@ -115,7 +116,7 @@ def test_attn_call_rejections(D):
 def test_accept_rejections_and_sizes(D):
     lib = D.lib()
     n = ctypes.c_size_t(0)
-    assert lib.dreams_tree_accept_workspace_size(1, 60, 32000, ctypes.byref(n)) == 0 and n.value > 0
+    assert lib.dreams_tree_accept_workspace_size(1, 60, 32000, ctypes.byref(n)) == 0 and n.value > 65536
     assert lib.dreams_tree_accept_workspace_size(1, 0, 32000, ctypes.byref(n)) == -1
     assert lib.dreams_tree_accept_workspace_size(1, 129, 32000, ctypes.byref(n)) == -1
     assert lib.dreams_tree_accept_workspace_size(1, 60, 0, ctypes.byref(n)) == -1

@@ -82,6 +82,24 @@ def test_extreme_cases(dev):
     run_and_compare(dev, logits[:, :1], agree[:, :1], one, "single node")
 
 
+def test_one_workspace_serves_every_shape(dev):
+    """Calls of different shapes (and both verbs) one after another on a single workspace."""
+    n = max(dreams.tree_accept_workspace_size(16, 128, 152064), 1 << 22)
+    ws = torch.zeros(n, dtype=torch.uint8, device=dev)
+    rng = np.random.default_rng(12)
+    for B, T, V in [(16, 128, 5000), (3, 7, 11), (1, 60, 32000), (8, 20, 4099), (2, 128, 3)]:
+        parent = np.stack([W.random_tree(rng, T, min(T - 1, 6), 6) for _ in range(B)])
+        logits = rng.standard_normal((B, T, V)).astype(np.float32)
+        tokens = rng.integers(0, V, (B, T)).astype(np.int32)
+        alen, path, nxt, am = dreams.tree_accept(to_dev(logits, dev), to_dev(tokens, dev), to_dev(parent, dev),
+                                                 want_target_argmax=True, workspace=ws)
+        torch.cuda.synchronize()
+        ra, rp, rn, ram = oracle.tree_accept(logits, tokens, parent)
+        assert np.array_equal(am.cpu().numpy(), ram) and np.array_equal(path.cpu().numpy(), rp), (B, T, V)
+        assert np.array_equal(alen.cpu().numpy(), ra) and np.array_equal(nxt.cpu().numpy(), rn), (B, T, V)
+    assert not ws[:65536].any()
+
+
 def test_workspace_reuse_and_repeat(dev):
     wl = W.WORKLOADS["llava7b_layer"].replace(batch=4)
     batch = W.make_batch(wl, layers=[], with_logits=True)
@@ -90,7 +108,7 @@ def test_workspace_reuse_and_repeat(dev):
     ws = torch.zeros(n, dtype=torch.uint8, device=dev)
     outs = [dreams.tree_accept(lg, tk, pr, want_target_argmax=True, workspace=ws) for _ in range(4)]
     torch.cuda.synchronize()
-    assert not ws[n - 256:].any()        # the arrival counters are back to zero
+    assert not ws[:65536].any()          # the arrival counters are back to zero
     for o in outs[1:]:
         for x, y in zip(o, outs[0]):
             assert torch.equal(x, y)

@@ -2,9 +2,10 @@
 
 Bars: the contract (max-abs <= 2e-2 for bf16 in / fp32 accumulate; 1e-5 for the fp32 path) and a tighter
 bound derived from the bf16 path's arithmetic.  The probabilities are rounded to bf16 once before the value
-product and the output is rounded to bf16 once, everything else is fp32, so per element
-    |out - ref| <= 2^-9 * (sum_j p_j |v_j| / sum_j p_j + |ref|)     (+ fp32 noise),
-and the first term is exactly the oracle's output on |V|.  The tests allow 1.5x that.
+product and the output is rounded to bf16 once (unit roundoff u = 2^-8: bf16 keeps 8 significant bits),
+everything else is fp32, so per element
+    |out - ref| <= u * (sum_j p_j |v_j| / sum_j p_j + |ref|)     (+ fp32 noise),
+and the first term is exactly the oracle's output on |V|.  The tests allow 1.02x that plus 1e-6.
 """
 import numpy as np
 import pytest
@@ -16,6 +17,10 @@ from paper_2606_00535_amd import dreams
 from paper_2606_00535_amd import workload as W
 
 pytestmark = pytest.mark.gpu
+
+
+def bf16_bound(absref, ref):
+    return 1.02 * 2.0 ** -8 * (absref + np.abs(ref)) + 1e-6
 
 
 def oracle_layer(batch, li, abs_v=False, parent=None, mask=None):
@@ -32,7 +37,7 @@ def check_bf16(out, lse, batch, li, label, ref=None, absref=None, mask=None):
         absref = oracle_layer(batch, li, abs_v=True, mask=mask)[0]
     o_ref, l_ref = ref
     mx, _, o = attn_errors(out, o_ref)
-    bound = 1.5 * 2.0 ** -9 * (absref + np.abs(o_ref)) + 1e-5
+    bound = bf16_bound(absref, o_ref)
     worst = float(np.max(np.abs(o - o_ref) / bound))
     lerr = float(np.nanmax(np.abs(lse.cpu().numpy() - l_ref))) if lse is not None else 0.0
     note("%s: max_abs=%.3e (contract %.0e) worst/bound=%.3f lse_err=%.2e" % (label, mx, ATTN_TOL_BF16, worst, lerr))
@@ -119,7 +124,7 @@ def test_split_sweep_agrees(dev):
     ref = oracle_layer(batch, 0)
     absref = oracle_layer(batch, 0, abs_v=True)[0]
     outs = []
-    for s in (1, 2, 8, 24, 4096):
+    for s in (1, 2, 8, 24, 32, 4096):
         note("split sweep S=%d" % s)
         out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=s)
         torch.cuda.synchronize()
@@ -153,8 +158,7 @@ def test_workspace_left_zero(dev):
     for _ in range(3):
         dreams.tree_verify_attn(q, k, v, kv, par, num_splits=5, workspace=ws)
     torch.cuda.synchronize()
-    sets = 2 * 2 * 1
-    cnt = ws[n - ((sets * 4 + 255) // 256 * 256):].cpu().numpy()
+    cnt = ws[:65536].cpu().numpy()          # the arrival counters open every workspace
     assert not cnt.any()
 
 
@@ -272,7 +276,7 @@ def test_full_size_sampled_rows(dev, name, layers):
         o = out.float().cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]].astype(np.float64)
         l = lse.cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
         mx = float(np.abs(o - ref).max())
-        worst = float(np.max(np.abs(o - ref) / (1.5 * 2.0 ** -9 * (absref + np.abs(ref)) + 1e-5)))
+        worst = float(np.max(np.abs(o - ref) / bf16_bound(absref, ref)))
         note("  max_abs=%.3e worst/bound=%.3f lse=%.2e" % (mx, worst, float(np.abs(l - lref).max())))
         assert mx <= ATTN_TOL_BF16 and worst <= 1.0 and float(np.abs(l - lref).max()) <= LSE_TOL
         # property at any size: every output row is a convex combination of V rows -> bounded by max |V|
