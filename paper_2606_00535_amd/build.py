@@ -23,6 +23,9 @@ CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
     # the packed-fp32 VALU forms are kept out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the attention loop also scales them with vector ALU
+    # instructions, and AGPR accumulators would be copied out and back on every iteration
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I" + INCLUDE, "-I" + CSRC,
 ]
 

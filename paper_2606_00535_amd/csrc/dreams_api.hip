@@ -67,11 +67,12 @@ constexpr size_t kCounterBytes = DREAMS_WORKSPACE_COUNTER_BYTES;
 constexpr size_t kMaxCounters = kCounterBytes / sizeof(uint32_t);
 
 struct AttnPlan {
-  int G, rows_total, row_groups, units, splits, key_tile;
+  int G, rows_total, row_groups, units, splits;
   int rows_per_wg;   // query rows one workgroup owns
-  bool stream;       // bandwidth-bound kernel (waves split keys) rather than the shared-tile kernel
   size_t acc_off, ml_off, bytes;
 };
+
+constexpr int kPieceMinKeys = 128;   // keys per piece of the key axis, at least
 
 constexpr int kMaxSplitsRequest = 4096;
 
@@ -107,26 +108,23 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   *p = AttnPlan{};
   p->G = d->num_q_heads / d->num_kv_heads;
   p->rows_total = p->G * d->num_nodes;
-  p->stream = d->dtype == DREAMS_BF16 && p->rows_total <= kStreamMaxRows;
-  p->rows_per_wg = p->stream ? kStreamRows : kAttnRows;
+  p->rows_per_wg = tree_attn_bf16_rows_per_wg(p->rows_total);
   p->row_groups = (p->rows_total + p->rows_per_wg - 1) / p->rows_per_wg;
   p->units = d->batch * d->num_kv_heads;
-  p->key_tile = 64;
   p->splits = 1;
   if (d->dtype == DREAMS_F32 || p->units == 0) return DREAMS_OK;
 
   const int max_len = d->max_kv_len > 0 ? d->max_kv_len : d->cache_capacity - d->num_nodes;
   const int n_keys = max_len + d->num_nodes;
-  const int max_splits = (n_keys + p->key_tile - 1) / p->key_tile;
+  const int max_splits = (n_keys + kPieceMinKeys - 1) / kPieceMinKeys;
   int splits = d->num_splits;
   if (splits == 0) {
-    // enough workgroups to give every compute unit two (stream kernel) or one (shared-tile kernel)
+    // about one workgroup per compute unit (a workgroup holds most of a compute unit's LDS)
     int cus = 0;
     st = device_cus(&cus);
     if (st != DREAMS_OK) return st;
-    const long long target = (long long)cus * (p->stream ? 2 : 1);
     const long long wgs = (long long)p->units * p->row_groups;
-    splits = (int)((target + wgs / 2) / wgs);
+    splits = (int)((cus + wgs / 2) / wgs);
   }
   if (splits > max_splits) splits = max_splits;
   if (splits > kAttnMaxSplits) splits = kAttnMaxSplits;
@@ -135,11 +133,8 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   const long long grid = 8LL * ((p->units + 7) / 8) * splits * p->row_groups;
   if (grid > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large: %lld workgroups", grid);
   if (splits > 1) {
-    const size_t sets = (size_t)p->units * p->row_groups;
-    if (sets > kMaxCounters)
-      return fail(DREAMS_ERR_UNSUPPORTED, "%zu (sequence, KV head, row group) sets exceed the %zu arrival counters",
-                  sets, kMaxCounters);
-    const size_t rows = sets * splits * p->rows_per_wg;
+    // partial results of the pieces, after the counter region every workspace starts with
+    const size_t rows = (size_t)p->units * p->row_groups * splits * p->rows_per_wg;
     p->acc_off = kCounterBytes;
     p->ml_off = p->acc_off + align_up(rows * d->head_dim * sizeof(float), 256);
     p->bytes = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
@@ -241,7 +236,6 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   char* ws = (char*)workspace;
   a.part_acc = p.bytes ? (float*)(ws + p.acc_off) : nullptr;
   a.part_ml = p.bytes ? (float*)(ws + p.ml_off) : nullptr;
-  a.counters = p.bytes ? (uint32_t*)ws : nullptr;
   a.B = desc->batch;
   a.Hq = desc->num_q_heads;
   a.Hkv = desc->num_kv_heads;
@@ -250,14 +244,12 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   a.D = desc->head_dim;
   a.S_cap = desc->cache_capacity;
   a.units = p.units;
+  a.rows_per_wg = p.rows_per_wg;
   a.row_groups = p.row_groups;
   a.splits = p.splits;
   a.max_keys = (desc->max_kv_len > 0 ? desc->max_kv_len : desc->cache_capacity - desc->num_nodes) + desc->num_nodes;
-  a.key_tile = p.key_tile;
   a.scale_log2 = desc->scale * 1.4426950408889634f;
-  hipError_t e = desc->dtype == DREAMS_F32 ? launch_tree_attn_f32(a, stream)
-                 : p.stream               ? launch_tree_attn_stream(a, stream)
-                                          : launch_tree_attn_bf16(a, stream);
+  hipError_t e = desc->dtype == DREAMS_F32 ? launch_tree_attn_f32(a, stream) : launch_tree_attn_bf16(a, stream);
   if (e != hipSuccess) return hip_fail(e, "tree attention launch");
   return ok();
 }

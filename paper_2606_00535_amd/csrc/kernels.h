@@ -35,13 +35,10 @@ __device__ __forceinline__ void reset_counter(uint32_t* counter) {
 }
 
 // ------------------------------------------------------------------------------------ tree attention
-// Matrix-core (bf16) path: one workgroup = 4 waves, each wave owns 16 query rows of one KV head, so a
-// workgroup covers kAttnRows rows; the key axis of every (sequence, KV head) is cut into `splits` pieces.
-constexpr int kAttnWaves = 4;
-constexpr int kAttnRows = 16 * kAttnWaves;
-constexpr int kAttnThreads = 64 * kAttnWaves;
+// Matrix-core (bf16) path: one workgroup = 4 waves, each wave owning 16 (narrow) or 32 (wide) query rows of
+// one KV head for a whole piece of that head's key axis; the key axis of every (sequence, KV head, row
+// group) is cut into `splits` pieces.
 constexpr int kMaxNodes = 128;
-// The merge stages every piece's (m, l) for 64 rows in the K/V tile buffers: at most 32 pieces.
 constexpr int kAttnMaxSplits = 32;
 
 struct AttnArgs {
@@ -53,28 +50,20 @@ struct AttnArgs {
   const uint64_t* mask;   // [B, T, ceil(T/64)] or nullptr
   void* out;              // [B, Hq, T, D]
   float* lse;             // [B, Hq, T] or nullptr
-  float* part_acc;        // [units * row_groups, splits, kAttnRows, D]   (splits > 1 only)
-  float* part_ml;         // [units * row_groups, splits, kAttnRows, 2]
-  uint32_t* counters;     // [units * row_groups], zero between calls
+  float* part_acc;        // [units * row_groups, splits, rows_per_wg, D]   (splits > 1 only)
+  float* part_ml;         // [units * row_groups, splits, rows_per_wg, 2]
   int B, Hq, Hkv, G, T, D, S_cap;
   int units;              // B * Hkv
-  int row_groups;         // ceil(G*T / kAttnRows)
+  int rows_per_wg;        // query rows of one workgroup (64 or 128)
+  int row_groups;         // ceil(G*T / rows_per_wg)
   int splits;
   int max_keys;           // host-side bound on L_b + T over the batch (plans the pieces of the key axis)
-  int key_tile;           // keys per LDS tile (64 or 128)
   float scale_log2;       // scale * log2(e)
 };
 
-// Grid size (in workgroups) of the bf16 kernel for this plan.
-int tree_attn_bf16_grid(const AttnArgs& a);
+// Query rows per workgroup the bf16 kernel uses for G*T rows per KV head.
+int tree_attn_bf16_rows_per_wg(int rows_total);
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream);
-
-// Bandwidth-bound bf16 path (few query rows per KV head): a workgroup of kStreamWaves waves owns kStreamRows
-// rows and one piece of the key axis; its waves split the piece's keys.  Used while G*T <= kStreamMaxRows.
-constexpr int kStreamRows = 32;
-constexpr int kStreamWaves = 4;
-constexpr int kStreamMaxRows = 128;
-hipError_t launch_tree_attn_stream(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------------------------------- acceptance

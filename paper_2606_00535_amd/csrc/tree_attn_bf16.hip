@@ -1,32 +1,37 @@
-// Tree-masked verification attention on the gfx950 matrix cores (bf16 inputs, fp32 accumulation).
+// Tree-masked verification attention, bf16 inputs, fp32 accumulation on the matrix cores.
 //
-// What is computed (the paper's Section 3.2 attention matrix, applied to the target's verification pass of
+// What is computed (the paper's Section 3.2 attention mask applied to the target's verification pass of
 // Section 2): for every tree node i of every query head, softmax(scale * q_i . k_j) v_j over the committed
-// prefix slots and the slots of node i's ancestors-or-self.  A row's visible set is "all prefix slots" plus
-// at most depth+1 tree slots, so the mask is only evaluated on key tiles that reach the tree part.
+// prefix slots and the slots of node i's ancestors-or-self.
 //
 // Work decomposition
-//   * A workgroup (4 waves) owns kAttnRows = 64 query rows of one KV head.  With grouped-query attention
-//     the rows of all G query heads that share the KV head are packed together (row r -> head r / T, node
-//     r % T), so every K/V tile read from HBM is used by all of them.
-//   * The key axis of a (sequence, KV head) is cut into `splits` contiguous pieces, one per workgroup, so a
-//     single-sequence shape still fills all compute units.  Each piece keeps an online softmax (running max
-//     m, running sum l, unnormalised accumulator); the last workgroup of a piece set to finish (arrival
-//     counter) merges them with the log-sum-exp identity in fixed split order, so results are reproducible
-//     bit for bit whichever workgroup arrives last.
-//   * Workgroup ids are remapped so that every workgroup of one (sequence, KV head) runs on the same XCD
-//     (the dispatcher deals consecutive ids round-robin over the 8 XCDs): row groups that read the same K/V
-//     tile share it in that XCD's L2.  Partial results travel through device-scope stores and loads.
-//   * This kernel serves shapes with many query rows per KV head (grouped-query heads x tree nodes); shapes
-//     with few rows go to the streaming kernel, whose waves split the keys instead of the rows.
-//
-// Per key tile (KT keys): the whole workgroup streams K and V rows with 16-byte coalesced loads into LDS
-// (register double-buffered: the next tile's loads are in flight while this one is computed).  Each wave
-// then computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (K rows as the A operand, read straight from LDS
-// in operand layout; the wave's 16 query rows stay in registers as the B operand).  Producing S^T rather
-// than S leaves each lane holding one query row's scores, which is exactly the B-operand layout of the next
-// product, O^T += V^T P^T, so the probabilities never leave registers; only V needs a transposed read from
-// LDS.  All row statistics are lane-local up to a 4-way cross-lane reduction.
+//   * A workgroup of 4 waves owns R = 64*RB query rows of one KV head (the rows of the G query heads sharing
+//     it are packed: row r -> head r / T, node r % T, which is also their order in memory) and one piece of
+//     that head's key axis.  Wave w owns rows [16*RB*w, 16*RB*(w+1)) for every key of the piece, so there
+//     is no merge between waves, and every K/V byte the workgroup reads serves all of its rows.
+//   * K/V stream through a ring of NST step slots in LDS (a step = 32 keys: 32 K rows then 32 V rows).  The
+//     four waves each copy a quarter of every step straight from global memory into LDS
+//     (global_load_lds_dwordx4: no registers in between), NST-1 steps ahead, so up to NST-1 steps per
+//     compute unit are in flight.  One barrier per step hands a landed step to all waves and frees the slot
+//     of the previous step for the next copy.  The copies are issued with inline assembly and waited for by
+//     exact count; nothing else in the kernel loads through the vector memory path before the epilogue, so
+//     the compiler never inserts a wait that would drain the ring.
+//   * Each lane fetches the source chunk that lands where an XOR-swizzled row layout wants it, which makes
+//     both operand reads below bank-conflict free:
+//       S^T = K Q^T        v_mfma_f32_16x16x32_bf16, K rows as the A operand (16-byte LDS reads)
+//       online softmax     per query row; each lane holds one row's scores, 4-way cross-lane reductions
+//       O^T += V^T P^T     A operand read with ds_read_b64_tr_b16 (a 4 x 16 transposing LDS read); the
+//                          probabilities are already in B-operand layout, so they never leave registers.
+//   * Waves are arranged as KW key groups of 4/KW waves: the groups take alternate steps (group k the steps
+//     k, k+KW, ...) and each wave owns 16*RB rows, so a wave's operand reads serve as many rows as possible;
+//     the groups' (max, sum, accumulator) states are merged through LDS at the end.
+//   * With several pieces per (sequence, KV head, row group), each workgroup writes its rows' (max, sum,
+//     accumulator) to the workspace and a second, small kernel merges the pieces in piece order (so the
+//     result does not depend on scheduling); the kernel boundary is what makes the partial results visible
+//     across XCDs, with no device-scope stores, fences or counters on the streaming kernel's path.
+//   * Workgroup ids are remapped so that all workgroups of one (sequence, KV head) run on the same XCD
+//     (consecutive ids are dealt round-robin over the 8 XCDs): row groups reading the same keys share them
+//     in that XCD's L2.
 #include "kernels.h"
 
 #include <math.h>
@@ -36,61 +41,105 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
+constexpr int kStep = 32;          // keys per step
+constexpr float kLazyLog2 = 8.0f;  // slack of the running maximum, log2 units
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Ancestor-or-self bit sets of every tree node of sequence b, into LDS (2 x 64 bits per node).
-__device__ __forceinline__ void build_ancestors(const AttnArgs& a, int b, uint64_t* anc, int tid) {
-  const int T = a.T;
-  if (tid < T) {
-    uint64_t m0 = 0, m1 = 0;
-    if (a.mask) {
-      const int W = (T + 63) / 64;
-      const uint64_t* mr = a.mask + ((size_t)b * T + tid) * W;
-      m0 = mr[0];
-      m1 = W > 1 ? mr[1] : 0;
-    } else {
-      const int32_t* par = a.parent + (size_t)b * T;
-      int j = tid;
-      for (int step = 0; step <= T && j >= 0; ++step) {
-        if (j < 64) m0 |= 1ull << j; else m1 |= 1ull << (j - 64);
-        const int p = par[j];
-        if (p >= j) break;  // not a valid parent: the walk ends here
-        j = p;              // -1 at the root ends the walk
-      }
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_void*)p; }
+
+// Wave-wide copies from global memory into LDS.  m0 (wave-uniform) is the LDS byte address of lane 0's
+// data; lane l's data lands at m0 + 16*l (dwordx4) or m0 + 4*l (dword).
+__device__ __forceinline__ void copy16_to_lds(uint32_t m0, const void* src) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0), "v"(src) : "memory");
+}
+// Same, addressed as a wave-uniform base plus a per-lane 32-bit byte offset.
+__device__ __forceinline__ void copy16_to_lds(uint32_t m0, const void* sbase, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(sbase)
+               : "memory");
+}
+__device__ __forceinline__ void copy4_to_lds(uint32_t m0, const void* src) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off" ::"s"(m0), "v"(src) : "memory");
+}
+// At most N of this wave's vector-memory operations still outstanding (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// wait_vm<PER * k> for a run-time k in [0, K]
+template <int PER, int K>
+__device__ __forceinline__ void wait_vm_steps(int k) {
+  if constexpr (K > 0) {
+    if (k >= K) {
+      wait_vm<PER * K>();
+      return;
     }
-    anc[2 * tid] = m0;
-    anc[2 * tid + 1] = m1;
+    wait_vm_steps<PER, K - 1>(k);
+  } else {
+    wait_vm<0>();
   }
 }
+// Workgroup barrier after this wave's LDS reads and writes have completed; outstanding copies stay in
+// flight (a __syncthreads() would also wait for them).
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int D, int KT>
-__global__ __launch_bounds__(kAttnThreads) void tree_attn_bf16_kernel(AttnArgs a) {
-  constexpr int NT = kAttnThreads;
+// Device-scope 8-byte store / load of two floats (see store_coherent).
+__device__ __forceinline__ void store_coherent2(float* p, float x, float y) {
+  const uint64_t v = (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32);
+  __hip_atomic_store((uint64_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_coherent2(const float* p) {
+  const uint64_t v = __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
+// Row layout in LDS: rows of D bf16, unpadded; the 16-byte chunk c of row r sits at position c ^ swz(r),
+// which spreads the 16 rows one operand read touches over distinct banks.  The swizzle repeats every 16
+// rows.  A step slot holds 32 K rows then 32 V rows; the query rows use the same layout.
+template <int D>
+struct Rows {
+  static constexpr int ROW = D * 2;           // bytes per row
+  static constexpr int CPR = D / 8;           // 16-byte chunks per row
+  static constexpr int RPL = 256 / ROW;       // rows per 256-byte bank line
+  static constexpr int HALF = kStep * ROW;    // bytes of the K (or V) part of a step
+  static constexpr int SLOT = 2 * HALF;       // bytes of a step
+  static constexpr int C16 = 16 * ROW / 1024; // wave-wide 1 KB copies per 16 rows
+  __device__ static __forceinline__ int swz(int r) { return (r / RPL) % CPR; }
+  __device__ static __forceinline__ int off(int r, int c) { return r * ROW + ((c ^ swz(r)) << 4); }
+};
+
+template <int D, int RB, int KW, int NST>
+__global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
+  constexpr int W = 4;
+  constexpr int WR = W / KW;          // waves per key group; each owns a different slice of the rows
+  constexpr int RW = 16 * RB;         // query rows per wave
+  constexpr int R = WR * RW;          // query rows per workgroup
   constexpr int DS = D / 32;          // k-steps of S^T = K Q^T
   constexpr int DB = D / 16;          // 16-column blocks of O^T
-  constexpr int KB = KT / 16;         // 16-key blocks per tile
-  constexpr int KC = KT / 32;         // 32-key chunks per tile (one O^T MFMA each)
-  constexpr int KS = D + 8;           // LDS row stride of K (elements): conflict-free 16-byte operand reads
-  constexpr int VS = D + 16;          // LDS row stride of V: conflict-free transposed 2-byte reads
-  constexpr int CPR = D / 8;          // 16-byte chunks per key row
-  constexpr int LPT = KT * CPR / NT;  // chunks of K (and of V) each thread moves per tile
-  static_assert(LPT * NT == KT * CPR, "tile must split evenly over the workgroup");
+  using L = Rows<D>;
+  constexpr int C16 = L::C16;         // wave-wide copies per 16 rows
+  constexpr int NSS = NST / KW;       // ring slots in super-steps (KW consecutive steps, one per key group)
+  constexpr int QSLOTS = (R * L::ROW + L::SLOT - 1) / L::SLOT;   // step slots the query rows occupy
+  constexpr int QSS = (QSLOTS + KW - 1) / KW;                      // ... in super-steps
+  constexpr int CPS = KW * C16;       // copies per wave per super-step (KW blocks of 16 rows)
+  constexpr int QB = R / 16;          // 16-row blocks of query rows, dealt to the waves round-robin
+  static_assert(W % KW == 0 && (NST & (NST - 1)) == 0 && NSS > QSS && NSS >= 2, "ring layout");
+  static_assert(16 * L::ROW == C16 * 1024 && (16 / L::RPL) % L::CPR == 0, "swizzle repeats every 16 rows");
+  static_assert((NSS - 1) * CPS + ((QB + W - 1) / W) * C16 + 8 <= 63, "outstanding copies fit the counter");
+  static_assert((size_t)(KW - 1) * R * (D + 2) * 4 <= (size_t)NST * L::SLOT, "group states fit the ring");
 
-  // K tile, then V tile; after the main loop the same bytes hold the merge's staging (see below)
-  __shared__ __attribute__((aligned(16))) __bf16 tiles[KT * KS + KT * VS];
-  __bf16* const k_lds = tiles;
-  __bf16* const v_lds = tiles + KT * KS;
-  static_assert(kAttnMaxSplits * kAttnRows * 8 + 2 * kAttnRows * 4 <= (KT * KS + KT * VS) * 2,
-                "merge staging must fit in the tile buffers");
+  extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots
   __shared__ uint64_t anc_lds[2 * kMaxNodes];
-  __shared__ int last_flag;
+  __shared__ uint32_t meta_lds[4 * kMaxNodes];   // the sequence's parents or tree mask rows, as copied
 
-  // ---- which (unit = sequence x KV head, split, row group) this workgroup owns
+  // ---- work item
   const int n = blockIdx.x;
   const int xcd = n & 7, slot = n >> 3;
   const int per_unit = a.splits * a.row_groups;
@@ -100,296 +149,453 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_bf16_kernel(AttnArgs a
   const int split = within / a.row_groups;
   const int rg = within - split * a.row_groups;
   const int b = u / a.Hkv, g = u - b * a.Hkv;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, quad = lane >> 4, col = lane & 15;
+  const int tid = threadIdx.x, lane = tid & 63, quad = lane >> 4, col = lane & 15;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kw = wave / WR, rh = wave - kw * WR;   // key group; row slice [rh*RW, rh*RW + RW)
   const int T = a.T;
-  int L = a.kv_len[b];
-  L = L < 0 ? 0 : (L > a.S_cap - T ? a.S_cap - T : L);
-  const int N = L + T;
-  int piece = (N + a.splits - 1) / a.splits;
-  piece = (piece + KT - 1) / KT * KT;
-  const int k_begin = split * piece;
-  const int k_end = min(N, k_begin + piece);
-
-  build_ancestors(a, b, anc_lds, tid);
-  __syncthreads();
-
-  // ---- this lane's query row (B operand of S^T and of O^T): row = col within the wave's 16 rows
   const int rows_total = a.G * T;
-  const int row_local = wave * 16 + col;
-  const int row = rg * kAttnRows + row_local;
-  const bool row_ok = row < rows_total;
-  const int head_in_group = row_ok ? row / T : 0;
-  const int node = row_ok ? row - head_in_group * T : 0;
-  const int h = g * a.G + head_in_group;
-  const uint64_t anc0 = anc_lds[2 * node], anc1 = anc_lds[2 * node + 1];
+  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(ring));
+  const int kv_len_b = a.kv_len[b];   // issued before the copies below, ahead of their traffic
 
-  bf16x8 qf[DS];
-  {
-    const __bf16* qrow = (const __bf16*)a.q + (((size_t)b * a.Hq + h) * T + node) * D;
+  // ---- this workgroup's piece of the key axis, planned from the host's bound on the key count
+  int piece = (a.max_keys + a.splits - 1) / a.splits;
+  piece = (piece + kStep - 1) / kStep * kStep;
+  const int k_begin = split * piece;
+  const int k_end_plan = split == a.splits - 1 ? a.max_keys : min(a.max_keys, k_begin + piece);
+  const int nplan = k_end_plan > k_begin ? (k_end_plan - k_begin + kStep - 1) / kStep : 0;
+  const int nsp = (nplan + KW - 1) / KW;
+  const unsigned char* kbase = (const unsigned char*)a.k + (size_t)u * a.S_cap * L::ROW;
+  const unsigned char* vbase = (const unsigned char*)a.v + (size_t)u * a.S_cap * L::ROW;
+
+  // Per-lane byte offsets of the copies of 16 consecutive rows: copy j, lane l brings row r = (j*1024 +
+  // 16*l) / ROW, position p = l % CPR, i.e. the global chunk p ^ swz(r) of that row.
+  uint32_t coff[C16];
 #pragma unroll
-    for (int s = 0; s < DS; ++s) {
-      if (row_ok) {
-        qf[s] = *(const bf16x8*)(qrow + s * 32 + quad * 8);
-      } else {
+  for (int j = 0; j < C16; ++j) {
+    const int e = j * 64 + lane;
+    const int r = e / L::CPR, p = e - r * L::CPR;
+    coff[j] = (uint32_t)(r * L::ROW + ((p ^ L::swz(r)) << 4));
+  }
+  // A super-step is KW steps x (32 K rows + 32 V rows) = 4*KW blocks of 16 rows; wave w copies blocks
+  // w*KW .. w*KW + KW - 1 (block bi: step bi/4 of the super-step, K or V part (bi/2)%2, rows 16*(bi%2)..).
+  auto issue_super = [&](int jj) {
+    const uint32_t sbase = ring_lds + (jj & (NSS - 1)) * KW * L::SLOT;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qf[s][e] = (__bf16)0.0f;
+    for (int t = 0; t < KW; ++t) {
+      const int bi = wave * KW + t;
+      const int sis = bi >> 2, part = (bi >> 1) & 1, half = bi & 1;
+      const int key0 = k_begin + (jj * KW + sis) * kStep + 16 * half;
+      const unsigned char* pbase = part ? vbase : kbase;
+      const uint32_t dst = sbase + sis * L::SLOT + part * L::HALF + half * C16 * 1024;
+      if (key0 + 16 <= a.S_cap) {
+        const unsigned char* src = pbase + (size_t)key0 * L::ROW;
+#pragma unroll
+        for (int j = 0; j < C16; ++j) copy16_to_lds(dst + j * 1024, src, coff[j]);
+      } else {  // rows past the cache capacity repeat its last row
+#pragma unroll
+        for (int j = 0; j < C16; ++j) {
+          const int r = (j * 64 + lane) / L::CPR;
+          const int key = min(key0 + r, a.S_cap - 1);
+          copy16_to_lds(dst + j * 1024, pbase + (size_t)key * L::ROW + (coff[j] - r * L::ROW));
+        }
       }
+    }
+  };
+
+  // ---- first copies: the query rows (into the last step slots), the tree (wave 0), then the ring
+  const size_t qrow0 = ((size_t)b * a.Hq + (size_t)g * a.G) * T;   // row 0 of this KV head's query rows
+  const unsigned char* qslab = ring + (NST - QSLOTS) * L::SLOT;
+#pragma unroll
+  for (int qb = wave; qb < QB; qb += W) {
+#pragma unroll
+    for (int j = 0; j < C16; ++j) {
+      const int r = (j * 64 + lane) / L::CPR;
+      const int row = min(rg * R + qb * 16 + r, rows_total - 1);
+      copy16_to_lds(lds_addr(qslab) + (qb * C16 + j) * 1024,
+                    (const unsigned char*)a.q + (qrow0 + row) * L::ROW + (coff[j] - r * L::ROW));
     }
   }
+  const int Wm = (T + 63) / 64;
+  if (wave == 0) {
+    const uint32_t mdst = lds_addr(meta_lds);
+    if (a.mask) {
+      const int nd = 2 * T * Wm;   // dwords of this sequence's mask rows
+      const uint32_t* src = (const uint32_t*)(a.mask + (size_t)b * T * Wm);
+      for (int c = 0; c * 64 < nd; ++c) copy4_to_lds(mdst + c * 256, src + min(c * 64 + lane, nd - 1));
+    } else {
+      const int32_t* src = a.parent + (size_t)b * T;
+      for (int c = 0; c * 64 < T; ++c) copy4_to_lds(mdst + c * 256, src + min(c * 64 + lane, T - 1));
+    }
+  }
+  const int fa = min(NSS - QSS, nsp);
+  for (int j = 0; j < fa; ++j) issue_super(j);
 
-  f32x4 o[DB];
-#pragma unroll
-  for (int d = 0; d < DB; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  // ---- prologue: prefix length, ancestor sets, queries (all overlapping the copies above)
+  int Lp = kv_len_b;
+  Lp = Lp < 0 ? 0 : (Lp > a.S_cap - T ? a.S_cap - T : Lp);
+  const int N = Lp + T;
+  // the last piece runs to this sequence's true end, whatever the host's bound said
+  const int k_end = split == a.splits - 1 ? N : min(N, k_begin + piece);
+  const int nact = k_end > k_begin ? (k_end - k_begin + kStep - 1) / kStep : 0;
+  const int nsa = (nact + KW - 1) / KW;
 
-  const __bf16* kbase = (const __bf16*)a.k + (size_t)u * a.S_cap * D;
-  const __bf16* vbase = (const __bf16*)a.v + (size_t)u * a.S_cap * D;
-
-  u32x4 kreg[LPT], vreg[LPT];
-  auto load_tile = [&](int t0) {
-#pragma unroll
-    for (int j = 0; j < LPT; ++j) {
-      const int c = tid + j * NT;
-      const int key = c / CPR, cc = c - key * CPR;
-      const int s = t0 + key;
-      if (s < k_end) {
-        kreg[j] = *(const u32x4*)(kbase + (size_t)s * D + cc * 8);
-        vreg[j] = *(const u32x4*)(vbase + (size_t)s * D + cc * 8);
-      } else {  // past this piece: zeros, so masked keys can never inject NaN/Inf through V
-        kreg[j] = u32x4{0u, 0u, 0u, 0u};
-        vreg[j] = u32x4{0u, 0u, 0u, 0u};
+  wait_vm_steps<CPS, NSS - QSS>(fa);   // this wave's query rows and the tree have landed
+  barrier_lds();
+  if (tid < T) {
+    uint64_t m0 = 0, m1 = 0;
+    if (a.mask) {
+      const uint64_t* mr = (const uint64_t*)meta_lds + tid * Wm;
+      m0 = mr[0];
+      m1 = Wm > 1 ? mr[1] : 0;
+    } else {
+      const int* par = (const int*)meta_lds;
+      int j = tid;
+      for (int st = 0; st <= T && j >= 0; ++st) {
+        if (j < 64) m0 |= 1ull << j; else m1 |= 1ull << (j - 64);
+        const int p = par[j];
+        if (p >= j) break;  // not a valid parent: the walk ends here
+        j = p;
       }
     }
-  };
-  auto store_tile = [&]() {
+    anc_lds[2 * tid] = m0;
+    anc_lds[2 * tid + 1] = m1;
+  }
+  bf16x8 qf[RB][DS];
 #pragma unroll
-    for (int j = 0; j < LPT; ++j) {
-      const int c = tid + j * NT;
-      const int key = c / CPR, cc = c - key * CPR;
-      *(u32x4*)(k_lds + key * KS + cc * 8) = kreg[j];
-      *(u32x4*)(v_lds + key * VS + cc * 8) = vreg[j];
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) qf[rb][ds] = *(const bf16x8*)(qslab + L::off(rh * RW + rb * 16 + col, ds * 4 + quad));
+  barrier_lds();   // ancestor sets written; every wave's query reads returned (their slots are reused next)
+  uint64_t anc0[RB], anc1[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = min(rg * R + rh * RW + rb * 16 + col, rows_total - 1);
+    const int node = row % T;
+    anc0[rb] = anc_lds[2 * node];
+    anc1[rb] = anc_lds[2 * node + 1];
+  }
+  const int fb = max(fa, min(NSS - 1, nsa));
+  for (int j = fa; j < fb; ++j) issue_super(j);
+
+  f32x4 o[RB][DB];
+  float m_run[RB], l_run[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int d = 0; d < DB; ++d) o[rb][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run[rb] = -INFINITY;
+    l_run[rb] = 0.f;
+  }
+
+  const int ka_row = (col & 3) * 4 + (col >> 2);       // A row m holds key kb*16 + (m%4)*4 + m/4
+  const int tr_row = (col >> 2) * 4 + quad;            // transposed read: 4 keys j*4+quad, 16 columns
+  const int tr_c = (col & 3) >> 1, tr_half = (col & 1) * 8;
+
+  for (int js = 0; js < nsa; ++js) {
+    // this wave's copies of super-step js have landed once only later super-steps' copies are outstanding
+    wait_vm_steps<CPS, NSS - 2>(max(fa, min(js + NSS - 1, nsa)) - 1 - js);
+    unsigned char* sslot = ring + (js & (NSS - 1)) * KW * L::SLOT;
+    // value rows at or past the sequence end hold whatever the cache had there: the waves that copied them
+    // zero them, so that no bit pattern can reach the value product (their keys are masked below)
+#pragma unroll
+    for (int t = 0; t < KW; ++t) {
+      const int bi = wave * KW + t;
+      const int sis = bi >> 2, part = (bi >> 1) & 1, half = bi & 1;
+      const int key0 = k_begin + (js * KW + sis) * kStep;
+      if (part == 1 && key0 + kStep > N) {
+        const int r = 16 * half + (lane >> 2);
+        if (key0 + r >= N) {
+          constexpr int PER = L::CPR / 4;
+          unsigned char* vrow = sslot + sis * L::SLOT + L::HALF + r * L::ROW;
+#pragma unroll
+          for (int c = 0; c < PER; ++c) *(u32x4*)(vrow + ((lane & 3) * PER + c) * 16) = u32x4{0u, 0u, 0u, 0u};
+        }
+      }
     }
-  };
+    barrier_lds();   // super-step js complete in LDS for every wave; the slots of super-step js-1 are free
+    if (js + NSS - 1 < nsa) issue_super(js + NSS - 1);
 
-  if (k_begin < k_end) {
-    load_tile(k_begin);
-    for (int t0 = k_begin; t0 < k_end; t0 += KT) {
-      __syncthreads();  // every wave is done reading the previous tile
-      store_tile();
-      __syncthreads();
-      if (t0 + KT < k_end) load_tile(t0 + KT);
+    const int step = js * KW + kw;   // this wave's step
+    if (step >= nact) continue;
+    const int key0 = k_begin + step * kStep;
+    const unsigned char* tile = sslot + kw * L::SLOT;
+    const unsigned char* vt = tile + L::HALF;
 
-      // S^T block kb: A-operand row m holds key kb*16 + (m%4)*4 + m/4, so that accumulator element e of a
-      // lane in quad q is key kb*16 + e*4 + q (see the V read below for why).
-      f32x4 s[KB];
-      {
-        const int keyA = (col & 3) * 4 + (col >> 2);
+    // All of the step's operand reads are issued before any product, so their LDS latencies overlap:
+    // K fragments (A operand of S^T: A row m holds key kb*16 + (m%4)*4 + m/4) and V^T fragments (A operand of
+    // O^T, transposing reads: lo = keys j*4+quad, hi = keys 16+j*4+quad, matching the probabilities' slots).
+    bf16x8 kf[2][DS];
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          const __bf16* kr = k_lds + (kb * 16 + keyA) * KS + quad * 8;
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int ds = 0; ds < DS; ++ds)
-            s[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)(kr + ds * 32), qf[ds], s[kb], 0, 0, 0);
-        }
-      }
+      for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = *(const bf16x8*)(tile + L::off(kb * 16 + ka_row, ds * 4 + quad));
+    s16x4 vlo[DB], vhi[DB];
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+      const int c = d * 2 + tr_c;
+      vlo[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vt + L::off(tr_row, c) + tr_half));
+      vhi[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vt + L::off(16 + tr_row, c) + tr_half));
+    }
+    __builtin_amdgcn_sched_barrier(0);
 
-      // scale into log2 units, mask, tile row-max
-      float tmax = -INFINITY;
-      const bool tree_tile = t0 + KT > L;
+    // S^T blocks kb = 0, 1: element e of a lane in quad q is key kb*16 + e*4 + q, row col
+    f32x4 s[RB][2];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
+    for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = t0 + kb * 16 + e * 4 + quad;
-          float x = s[kb][e] * a.scale_log2;
-          bool vis = key < k_end;
-          if (tree_tile && key >= L) {
-            const int j = key - L;
-            vis = vis && (((j < 64 ? anc0 >> j : anc1 >> (j - 64)) & 1ull) != 0);
-          }
-          x = vis ? x : -INFINITY;
-          s[kb][e] = x;
-          tmax = fmaxf(tmax, x);
-        }
-      }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float m_new = fmaxf(m_run, tmax);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
-      m_run = m_new;
-      float psum = 0.f;
+    for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float p = fast_exp2(s[kb][e] - m_use);
-          s[kb][e] = p;
-          psum += p;
-        }
-      }
-      l_run = l_run * alpha + psum;
-#pragma unroll
-      for (int d = 0; d < DB; ++d) o[d] *= alpha;
+        for (int rb = 0; rb < RB; ++rb) s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][ds], qf[rb][ds], s[rb][kb], 0, 0, 0);
 
-      // O^T[d][row] += sum over 32 keys V[key][d] * P[row][key].  k-slot 0..3 of quad q = keys e*4+q of the
-      // even 16-key block, k-slots 4..7 = the same of the odd block: exactly what this lane holds in s[].
+    // scale to log2 units; only steps that reach the tree slots or the piece end need the mask
 #pragma unroll
-      for (int c = 0; c < KC; ++c) {
-        bf16x8 pb;
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          pb[e] = (__bf16)s[2 * c][e];
-          pb[4 + e] = (__bf16)s[2 * c + 1][e];
-        }
-        const __bf16* vr0 = v_lds + (c * 32 + quad) * VS + col;
-        const __bf16* vr1 = vr0 + 16 * VS;
+      for (int kb = 0; kb < 2; ++kb) s[rb][kb] *= a.scale_log2;
+    if (key0 + kStep > Lp || key0 + kStep > k_end) {
 #pragma unroll
-        for (int d = 0; d < DB; ++d) {
-          bf16x8 va;
+      for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            va[e] = vr0[e * 4 * VS + d * 16];
-            va[4 + e] = vr1[e * 4 * VS + d * 16];
+            const int key = key0 + kb * 16 + e * 4 + quad;
+            const int j = key - Lp;                      // tree node of a key past the prefix
+            const uint64_t word = j < 64 ? anc0[rb] : anc1[rb];
+            const bool anc = ((word >> (j & 63)) & 1ull) != 0;
+            const bool vis = (key < k_end) & ((key < Lp) | anc);
+            s[rb][kb][e] = vis ? s[rb][kb][e] : -INFINITY;
           }
-          o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, o[d], 0, 0, 0);
+        }
+      }
+    }
+    bf16x8 pb[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float lmax = fmaxf(fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3])),
+                         fmaxf(fmaxf(s[rb][1][0], s[rb][1][1]), fmaxf(s[rb][1][2], s[rb][1][3])));
+      // The reference maximum m only moves when some score exceeds it by more than 2^8 (the exponentials
+      // then stay <= 256, and softmax does not depend on the reference), which after the first steps is
+      // rare: in the common case no cross-lane reduction and no rescale happen at all.
+      if (__any(lmax > m_run[rb] + kLazyLog2)) {
+        float tmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+        if (tmax > m_run[rb] + kLazyLog2) {
+          const float alpha = m_run[rb] == -INFINITY ? 0.f : fast_exp2(m_run[rb] - tmax);
+          m_run[rb] = tmax;
+          l_run[rb] *= alpha;
+#pragma unroll
+          for (int d = 0; d < DB; ++d) o[rb][d] *= alpha;
+        }
+      }
+      const float m_use = m_run[rb] == -INFINITY ? 0.f : m_run[rb];
+      float psum = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p = fast_exp2(s[rb][kb][e] - m_use);
+          psum += p;
+          pb[rb][kb * 4 + e] = (__bf16)p;
+        }
+      }
+      l_run[rb] += psum;
+    }
+
+    // O^T[d][row] += sum over the 32 keys of V[key][d] P[row][key]
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+      bf16x8 va;
+      const bf16x4 lo_b = __builtin_bit_cast(bf16x4, vlo[d]), hi_b = __builtin_bit_cast(bf16x4, vhi[d]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        va[e] = lo_b[e];
+        va[4 + e] = hi_b[e];
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) o[rb][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[rb], o[rb][d], 0, 0, 0);
+    }
+  }
+  wait_vm<0>();   // copies planned past a sequence's own end land before LDS is reused
+
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    l_run[rb] += __shfl_xor(l_run[rb], 16);
+    l_run[rb] += __shfl_xor(l_run[rb], 32);
+  }
+
+  // ---- key groups 1.. hand their states to group 0 through LDS (merged in group order)
+  if constexpr (KW > 1) {
+    barrier_lds();   // every wave is done with the ring
+    float* st_o = (float*)ring;                          // [KW-1][R][D]
+    float2* st_ml = (float2*)(st_o + (KW - 1) * R * D);  // [KW-1][R]
+    if (kw > 0) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int row = (kw - 1) * R + rh * RW + rb * 16 + col;
+#pragma unroll
+        for (int d = 0; d < DB; ++d) *(f32x4*)(st_o + (size_t)row * D + d * 16 + quad * 4) = o[rb][d];
+        if (quad == 0) st_ml[row] = make_float2(m_run[rb], l_run[rb]);
+      }
+    }
+    barrier_lds();
+    if (kw == 0) {
+#pragma unroll
+      for (int k = 1; k < KW; ++k) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const int row = (k - 1) * R + rh * RW + rb * 16 + col;
+          const float2 ml = st_ml[row];
+          const float M = fmaxf(m_run[rb], ml.x);
+          const float w0 = m_run[rb] == -INFINITY ? 0.f : fast_exp2(m_run[rb] - M);
+          const float w1 = ml.x == -INFINITY ? 0.f : fast_exp2(ml.x - M);
+          m_run[rb] = M;
+          l_run[rb] = l_run[rb] * w0 + ml.y * w1;
+#pragma unroll
+          for (int d = 0; d < DB; ++d) o[rb][d] = o[rb][d] * w0 + *(const f32x4*)(st_o + (size_t)row * D + d * 16 + quad * 4) * w1;
         }
       }
     }
   }
+  const bool owner = kw == 0;   // the waves that now hold the workgroup's final states
 
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
-
-  // lane holds O[row][d*16 + quad*4 + e] for e = 0..3
+  // ---- a single piece: normalise and write.  Rows of one KV head are consecutive in memory.
   if (a.splits == 1) {
-    if (row_ok) {
-      const size_t orow = (((size_t)b * a.Hq + h) * T + node);
-      const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
-      __bf16* op = (__bf16*)a.out + orow * D + quad * 4;
+    if (!owner) return;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = rg * R + rh * RW + rb * 16 + col;
+      if (row >= rows_total) continue;
+      const size_t orow = qrow0 + row;
+      const float inv = l_run[rb] > 0.f ? 1.0f / l_run[rb] : 0.f;
 #pragma unroll
       for (int d = 0; d < DB; ++d) {
-        bf16x4 r;
+        bf16x4 res;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) r[e] = (__bf16)(o[d][e] * inv);
-        *(bf16x4*)(op + d * 16) = r;
+        for (int e = 0; e < 4; ++e) res[e] = (__bf16)(o[rb][d][e] * inv);
+        *(bf16x4*)((__bf16*)a.out + orow * D + d * 16 + quad * 4) = res;
       }
-      if (a.lse && quad == 0) a.lse[orow] = l_run > 0.f ? (m_run + __log2f(l_run)) * kLn2 : -INFINITY;
+      if (a.lse && quad == 0)
+        a.lse[orow] = l_run[rb] > 0.f ? (m_run[rb] + __log2f(l_run[rb])) * kLn2 : -INFINITY;
     }
     return;
   }
 
-  // ---- several pieces: publish this piece's partial result, the last arrival merges
+  // ---- several pieces: write this piece's unnormalised rows and (max, sum) for the merge kernel (plain
+  // stores: the kernel boundary makes them visible to it)
+  if (!owner) return;
   const size_t pset = (size_t)u * a.row_groups + rg;
-  const size_t pbase = (pset * a.splits + split) * kAttnRows + row_local;
-  {
-    float* pa = a.part_acc + pbase * D + quad * 4;
 #pragma unroll
-    for (int d = 0; d < DB; ++d)
+  for (int rb = 0; rb < RB; ++rb) {
+    const size_t pr = (pset * a.splits + split) * R + rh * RW + rb * 16 + col;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) store_coherent(pa + d * 16 + e, o[d][e]);
-    if (quad == 0) {
-      store_coherent(a.part_ml + 2 * pbase, m_run);
-      store_coherent(a.part_ml + 2 * pbase + 1, l_run);
-    }
-  }
-  wait_vector_memory();
-  __syncthreads();
-  if (tid == 0) last_flag = arrive_last(&a.counters[pset], (uint32_t)a.splits);
-  __syncthreads();
-  if (!last_flag) return;
-  if (tid == 0) reset_counter(&a.counters[pset]);
-
-  // Merge.  (1) one round trip stages every piece's (m, l) for the 64 rows in LDS (the K/V tile buffers are
-  // free now); (2) one thread per row turns them into weights 2^(m_s - M) and 1/sum; (3) every thread owns
-  // one 4-column slice of several rows and streams the pieces' accumulators with many loads in flight.
-  float2* ml = (float2*)tiles;                       // [splits][kAttnRows]
-  float* inv_l = (float*)(ml + kAttnMaxSplits * kAttnRows);  // [kAttnRows]
-  float* row_m = inv_l + kAttnRows;                  // [kAttnRows]
-  const int S = a.splits;
-  const size_t pset_rows = pset * S * kAttnRows;
-  for (int e = tid; e < S * kAttnRows; e += NT)
-    ml[e] = make_float2(load_coherent(a.part_ml + 2 * (pset_rows + e)), load_coherent(a.part_ml + 2 * (pset_rows + e) + 1));
-  __syncthreads();
-  if (tid < kAttnRows) {
-    float M = -INFINITY;
-    for (int sp = 0; sp < S; ++sp) M = fmaxf(M, ml[sp * kAttnRows + tid].x);
-    float lsum = 0.f;
-    for (int sp = 0; sp < S; ++sp) {
-      const float2 v = ml[sp * kAttnRows + tid];
-      const float w = v.x == -INFINITY ? 0.f : fast_exp2(v.x - M);
-      lsum += w * v.y;
-      ml[sp * kAttnRows + tid].x = w;
-    }
-    inv_l[tid] = lsum > 0.f ? 1.0f / lsum : 0.f;
-    row_m[tid] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
-  }
-  __syncthreads();
-
-  constexpr int D4 = D / 4;                          // 4-column slices per row
-  constexpr int RSTEP = NT / D4;                     // rows covered by one pass of the workgroup
-  constexpr int RPT = kAttnRows / RSTEP;             // rows per thread
-  const int d4 = tid % D4, r0 = tid / D4;
-  f32x4 acc[RPT];
-#pragma unroll
-  for (int j = 0; j < RPT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const float* pacc = a.part_acc + pset_rows * D + d4 * 4;
-  auto load4 = [&](size_t idx) {
-    const float* p = pacc + idx * D;
-    return f32x4{load_coherent(p), load_coherent(p + 1), load_coherent(p + 2), load_coherent(p + 3)};
-  };
-  int sp = 0;
-  for (; sp + 1 < S; sp += 2) {                      // two pieces x RPT rows of loads in flight
-    f32x4 x0[RPT], x1[RPT];
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      x0[j] = load4((size_t)sp * kAttnRows + r0 + j * RSTEP);
-      x1[j] = load4((size_t)(sp + 1) * kAttnRows + r0 + j * RSTEP);
-    }
-#pragma unroll
-    for (int j = 0; j < RPT; ++j)
-      acc[j] += ml[sp * kAttnRows + r0 + j * RSTEP].x * x0[j] + ml[(sp + 1) * kAttnRows + r0 + j * RSTEP].x * x1[j];
-  }
-  if (sp < S) {
-#pragma unroll
-    for (int j = 0; j < RPT; ++j)
-      acc[j] += ml[sp * kAttnRows + r0 + j * RSTEP].x * load4((size_t)sp * kAttnRows + r0 + j * RSTEP);
-  }
-  const int rows_here = min(kAttnRows, rows_total - rg * kAttnRows);
-#pragma unroll
-  for (int j = 0; j < RPT; ++j) {
-    const int rl = r0 + j * RSTEP;
-    if (rl >= rows_here) continue;
-    const int r = rg * kAttnRows + rl;
-    const int hg = r / T, nd = r - hg * T;
-    const size_t orow = ((size_t)b * a.Hq + g * a.G + hg) * T + nd;
-    const float inv = inv_l[rl];
-    bf16x4 res;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) res[e] = (__bf16)(acc[j][e] * inv);
-    *(bf16x4*)((__bf16*)a.out + orow * D + d4 * 4) = res;
-    if (a.lse && d4 == 0) a.lse[orow] = row_m[rl];
+    for (int d = 0; d < DB; ++d) *(f32x4*)(a.part_acc + pr * D + d * 16 + quad * 4) = o[rb][d];
+    if (quad == 0) *(float2*)(a.part_ml + 2 * pr) = make_float2(m_run[rb], l_run[rb]);
   }
 }
 
-template <int D, int KT>
+// Merge of the key-axis pieces: out = sum_s w_s acc_s / sum_s w_s l_s with w_s = 2^(m_s - max_s m_s), in
+// piece order.  A workgroup merges 16 rows of one (sequence, KV head, row group); thread t handles row t/16
+// and the 8 columns (t%16)*8 .. +8 (D = 128) or 4 columns (D = 64) of it.  All loads of a chunk of 8 pieces
+// are issued before any is used.
+template <int D>
+__global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
+  constexpr int CPT = D / 16;           // columns per thread
+  constexpr int CH = 8;                 // pieces per batch of loads
+  typedef float fv __attribute__((ext_vector_type(CPT)));
+  const int R = a.rows_per_wg;
+  const int blocks = R / 16;
+  const int n = blockIdx.x;
+  const int pset = n / blocks, rblk = n - pset * blocks;
+  const int u = pset / a.row_groups, rg = pset - u * a.row_groups;
+  const int b = u / a.Hkv, g = u - b * a.Hkv;
+  const int t = threadIdx.x, r = rblk * 16 + t / 16, c0 = (t % 16) * CPT;
+  const int row = rg * R + r;                     // row within the KV head's G*T rows
+  const int S = a.splits;
+  const size_t prow0 = (size_t)pset * S * R + r;  // this row in piece 0; piece s adds s * R
+
+  float M = -INFINITY, lsum = 0.f;
+  fv acc = {};
+  for (int s0 = 0; s0 < S; s0 += CH) {
+    float2 ml[CH];
+    fv x[CH];
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const size_t pr = prow0 + (size_t)min(s0 + k, S - 1) * R;
+      ml[k] = *(const float2*)(a.part_ml + 2 * pr);
+      x[k] = *(const fv*)(a.part_acc + pr * D + c0);
+    }
+    float Mn = M;
+#pragma unroll
+    for (int k = 0; k < CH; ++k)
+      if (s0 + k < S) Mn = fmaxf(Mn, ml[k].x);
+    const float scale_old = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
+    lsum *= scale_old;
+    acc *= scale_old;
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const float w = (s0 + k >= S || ml[k].x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml[k].x - Mn);
+      lsum += w * ml[k].y;
+      acc += w * x[k];
+    }
+    M = Mn;
+  }
+  if (row >= a.G * a.T) return;
+  const size_t orow = ((size_t)b * a.Hq + (size_t)g * a.G) * a.T + row;
+  const float inv = lsum > 0.f ? 1.0f / lsum : 0.f;
+  __bf16 res[CPT];
+#pragma unroll
+  for (int e = 0; e < CPT; ++e) res[e] = (__bf16)(acc[e] * inv);
+  __builtin_memcpy((__bf16*)a.out + orow * D + c0, res, sizeof(res));
+  if (a.lse && c0 == 0) a.lse[orow] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+}
+
+template <int D, int RB, int KW, int NST>
 hipError_t launch(const AttnArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((tree_attn_bf16_kernel<D, KT>), dim3(tree_attn_bf16_grid(a)), dim3(kAttnThreads), 0, stream, a);
+  constexpr size_t lds = (size_t)NST * Rows<D>::SLOT;
+  static_assert(lds + 2 * kMaxNodes * 8 + 4 * kMaxNodes * 4 + 64 <= 160 * 1024, "LDS budget");
+  auto kern = tree_attn_bf16_kernel<D, RB, KW, NST>;
+  static bool configured = false;
+  if (!configured) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  if (a.rows_per_wg != 16 * RB * (4 / KW)) return hipErrorInvalidValue;
+  const unsigned units_rounded = (a.units + 7) / 8 * 8;
+  const unsigned grid = units_rounded * (unsigned)(a.splits * a.row_groups);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  const unsigned mgrid = (unsigned)a.units * a.row_groups * (a.rows_per_wg / 16);
+  hipLaunchKernelGGL(tree_attn_merge_kernel<D>, dim3(mgrid), dim3(256), 0, stream, a);
   return hipGetLastError();
+}
+
+template <int D, int NST>
+hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
+  switch (a.rows_per_wg) {
+    case 16: return launch<D, 1, 4, NST>(a, stream);
+    case 32: return launch<D, 2, 4, NST>(a, stream);
+    case 64: return launch<D, 2, 2, NST>(a, stream);
+    case 128: return launch<D, 2, 1, NST>(a, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-int tree_attn_bf16_grid(const AttnArgs& a) {
-  const int unit_rounds = (a.units + 7) / 8;
-  return 8 * unit_rounds * a.splits * a.row_groups;
+// Rows per workgroup: the narrowest of 16, 32, 64 rows (waves in 4, 4, 2 key groups) that holds every row
+// of a KV head, else 128 (all four waves on the same keys, 32 rows each, several row groups).
+int tree_attn_bf16_rows_per_wg(int rows_total) {
+  return rows_total <= 16 ? 16 : rows_total <= 32 ? 32 : rows_total <= 64 ? 64 : 128;
 }
 
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream) {
-  if (a.D == 128) return a.key_tile == 128 ? launch<128, 128>(a, stream) : launch<128, 64>(a, stream);
-  if (a.D == 64) return a.key_tile == 128 ? launch<64, 128>(a, stream) : launch<64, 64>(a, stream);
+  if (a.D == 128) return launch_for_rows<128, 8>(a, stream);
+  if (a.D == 64) return launch_for_rows<64, 16>(a, stream);
   return hipErrorInvalidValue;
 }
 

@@ -84,7 +84,7 @@ def test_attn_workspace_size_formula(D):
     assert D.lib().dreams_last_error_message().decode() == ""
     assert _ws(D, _desc(D, num_splits=1))[1] == 0
     assert _ws(D, _desc(D, dtype=D.DREAMS_F32, num_splits=4))[1] == 0
-    # a request above the number of 64-key tiles (3200 slots -> 50) or above 32 pieces is reduced
+    # a request above one piece per 128 keys (3200 slots -> 25) or above 32 pieces is reduced
     assert _ws(D, _desc(D, num_splits=4000)) == _ws(D, _desc(D, num_splits=32))
     assert _ws(D, _desc(D, num_splits=20, cache_capacity=640)) == _ws(D, _desc(D, num_splits=10, cache_capacity=640))
 
