@@ -85,8 +85,8 @@ typedef struct {
 } dreams_attn_desc_t;
 
 /* Bytes of workspace dreams_tree_verify_attn needs for `desc` on the current device (0 if none: then the
- * call accepts a NULL workspace).  DREAMS_ERR_UNSUPPORTED if the work plan needs more than
- * DREAMS_WORKSPACE_COUNTER_BYTES / 4 counters (batch * num_kv_heads * row groups of 64 query rows). */
+ * call accepts a NULL workspace).  Non-zero when the key axis is cut into pieces: the pieces' partial
+ * results live there, after the counter region every workspace starts with. */
 dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t* desc, size_t* bytes);
 
 /*
@@ -123,7 +123,9 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
                                         const uint64_t* tree_mask, void* out, float* lse, void* workspace,
                                         size_t workspace_bytes, hipStream_t stream);
 
-/* Bytes of workspace dreams_tree_accept needs (never 0; batch <= DREAMS_WORKSPACE_COUNTER_BYTES / 4). */
+/* Bytes of workspace dreams_tree_accept needs (never 0).  DREAMS_ERR_UNSUPPORTED if batch exceeds
+ * DREAMS_WORKSPACE_COUNTER_BYTES / 4 (one arrival counter per sequence; rows of long vocabularies are cut
+ * into pieces with one more counter per row while batch * (num_nodes + 1) counters fit). */
 dreams_status_t dreams_tree_accept_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
                                                   size_t* bytes);
 

@@ -145,11 +145,10 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
 // ----------------------------------------------------------------------------------------- acceptance
 struct AcceptPlan {
   int chunks, chunk;
-  size_t val_off, idx_off, bytes;
+  size_t val_off, idx_off, am_off, bytes;
 };
 
-constexpr int kAcceptTargetWgs = 2048;
-constexpr int kAcceptMinPiece = 2048;
+constexpr int kAcceptPieceElems = 8192;   // logits per workgroup (32 KiB), all in flight at once
 
 dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
   if (B < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", B);
@@ -157,24 +156,23 @@ dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
   if (V < 1) return fail(DREAMS_ERR_INVALID_ARG, "vocab = %d < 1", V);
   *p = AcceptPlan{};
   const long long rows = (long long)B * T;
-  if (rows == 0) return DREAMS_OK;
-  long long chunks = (kAcceptTargetWgs + rows - 1) / rows;
-  const long long max_chunks = (V + kAcceptMinPiece - 1) / kAcceptMinPiece;
-  if (chunks > max_chunks) chunks = max_chunks;
-  if (chunks * T > kAcceptMaxParts) chunks = kAcceptMaxParts / T;
-  if (chunks < 1) chunks = 1;
+  long long chunks = (V + kAcceptPieceElems - 1) / kAcceptPieceElems;
+  if (chunks > kAcceptMaxChunks) chunks = kAcceptMaxChunks;
+  // counters: one per sequence, plus one per row when rows are cut into pieces
+  if (chunks > 1 && (size_t)(B + rows) > kMaxCounters) chunks = 1;
+  if ((size_t)B > kMaxCounters)
+    return fail(DREAMS_ERR_UNSUPPORTED, "batch = %d exceeds the %zu arrival counters", B, kMaxCounters);
   long long chunk = (V + chunks - 1) / chunks;
   chunk = (chunk + 3) / 4 * 4;
   chunks = (V + chunk - 1) / chunk;
   if (rows * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
   p->chunks = (int)chunks;
   p->chunk = (int)chunk;
-  if ((size_t)B > kMaxCounters)
-    return fail(DREAMS_ERR_UNSUPPORTED, "batch = %d exceeds the %zu arrival counters", B, kMaxCounters);
   const size_t parts = (size_t)rows * chunks;
   p->val_off = kCounterBytes;
   p->idx_off = p->val_off + align_up(parts * sizeof(float), 256);
-  p->bytes = p->idx_off + align_up(parts * sizeof(int32_t), 256);
+  p->am_off = p->idx_off + align_up(parts * sizeof(int32_t), 256);
+  p->bytes = p->am_off + align_up((size_t)rows * sizeof(int32_t), 256);
   return DREAMS_OK;
 }
 
@@ -293,6 +291,7 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
   char* ws = (char*)workspace;
   a.part_val = (float*)(ws + p.val_off);
   a.part_idx = (int32_t*)(ws + p.idx_off);
+  a.row_am = (int32_t*)(ws + p.am_off);
   a.counters = (uint32_t*)ws;
   a.B = batch;
   a.T = num_nodes;

@@ -68,8 +68,7 @@ hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------------------------------- acceptance
 constexpr int kAcceptThreads = 256;
-// Pieces (node x vocabulary chunk) of one sequence, staged in LDS by the path scan.
-constexpr int kAcceptMaxParts = 2304;
+constexpr int kAcceptMaxChunks = kAcceptThreads;   // pieces per row (merged one per thread)
 
 struct AcceptArgs {
   const float* logits;    // [B, T, V]
@@ -81,7 +80,8 @@ struct AcceptArgs {
   int32_t* target_argmax; // [B, T] or nullptr
   float* part_val;        // [B, T, chunks]
   int32_t* part_idx;      // [B, T, chunks]
-  uint32_t* counters;     // [B], zero between calls
+  int32_t* row_am;        // [B, T] argmax of each row
+  uint32_t* counters;     // [B] per sequence, then [B, T] per row (chunks > 1); zero between calls
   int B, T, V;
   int chunks;             // vocabulary pieces per row
   int chunk;              // elements per piece (multiple of 4 when vectorised)

@@ -1,18 +1,19 @@
 // Greedy tree acceptance (the paper's Section 2, "Speculative decoding": drafts are kept while they equal the
 // target's own token at their position; at the first mismatch the target's token replaces the draft).
 //
-// One kernel, two phases:
+// One kernel, three levels, each finished by the last workgroup to arrive at an arrival counter (pieces
+// travel through device-scope stores and loads, see kernels.h):
 //   1. Row argmax of the target logits.  Each (sequence, node) row of V logits is cut into `chunks` pieces,
-//      one 256-thread workgroup per piece, streamed with 16-byte loads (the logits are the only large input:
-//      B*T*V*4 bytes).  Ties go to the smallest index: every thread visits its elements in increasing order
-//      and replaces its candidate only on a strictly larger value, and every merge prefers the smaller index
-//      on equal values (fp32 comparison, so -0.0 and +0.0 are equal).
-//   2. Path scan, by the last workgroup of the sequence to finish (arrival counter; pieces travel through
-//      device-scope stores and loads): per node, merge the
-//      pieces in index order, then every node walks its own ancestor chain (at most depth steps, no
-//      barriers) to decide whether each draft on it equals the target token at its parent.  The deepest
-//      consistent node (smallest index among equals) is found with one block-wide max over the key
-//      depth*256 + (255 - node).
+//      one 256-thread workgroup per piece, every thread keeping up to 8 16-byte loads in flight (the logits
+//      are the only large input: B*T*V*4 bytes).  Ties go to the smallest index: every thread visits its
+//      elements in increasing order and replaces its candidate only on a strictly larger value, and every
+//      merge prefers the smaller index on equal values (fp32 comparison, so -0.0 and +0.0 are equal).
+//   2. The last piece of a row to finish merges the row's pieces (one counter per row, so at most `chunks`
+//      workgroups ever touch the same counter) and publishes the row's argmax.
+//   3. The last row of a sequence to finish runs the path scan: every node walks its own ancestor chain (at
+//      most depth steps, no barriers) to decide whether each draft on it equals the target token at its
+//      parent; the deepest consistent node (smallest index among equals) comes out of one block-wide max
+//      over the key depth*256 + (255 - node).
 #include "kernels.h"
 
 #include <limits.h>
@@ -23,24 +24,29 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-struct Cand {
-  float v;
-  int i;
-};
-
 // true iff (v2, i2) beats (v1, i1): larger value, or equal value and smaller index
 __device__ __forceinline__ bool better(float v2, int i2, float v1, int i1) {
   return v2 > v1 || (v2 == v1 && i2 < i1);
 }
 
-__device__ __forceinline__ Cand wave_best(Cand c) {
+// Block-wide best (value, index); the result is valid in every thread.
+__device__ __forceinline__ void block_best(float& v, int& i, float* red_v, int* red_i) {
+  constexpr int NW = kAcceptThreads / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
-    const float v2 = __shfl_xor(c.v, off);
-    const int i2 = __shfl_xor(c.i, off);
-    if (better(v2, i2, c.v, c.i)) { c.v = v2; c.i = i2; }
+    const float v2 = __shfl_xor(v, off);
+    const int i2 = __shfl_xor(i, off);
+    if (better(v2, i2, v, i)) { v = v2; i = i2; }
   }
-  return c;
+  __syncthreads();   // earlier readers of red_v / red_i are done
+  if (lane == 0) { red_v[wave] = v; red_i[wave] = i; }
+  __syncthreads();
+  v = red_v[0];
+  i = red_i[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w)
+    if (better(red_v[w], red_i[w], v, i)) { v = red_v[w]; i = red_i[w]; }
 }
 
 __device__ __forceinline__ int wave_max(int x) {
@@ -52,10 +58,12 @@ __device__ __forceinline__ int wave_max(int x) {
 template <bool VEC>
 __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs a) {
   constexpr int NT = kAcceptThreads, NW = NT / 64;
+  constexpr int UNROLL = 8;   // loads in flight per thread
   __shared__ float red_v[NW];
   __shared__ int red_i[NW];
-  __shared__ int last_flag;
+  __shared__ int flag;
   __shared__ int am_s[kMaxNodes], tok_s[kMaxNodes], par_s[kMaxNodes];
+  __shared__ int red_k[NW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = blockIdx.x;                 // ((b * T) + i) * chunks + c
@@ -64,69 +72,78 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
   const float* row = a.logits + (size_t)bi * a.V;
   const int x0 = c * a.chunk, x1 = min(a.V, x0 + a.chunk);
 
-  // ---- phase 1: best (value, index) of this piece
-  Cand best{-INFINITY, INT_MAX};
+  // ---- level 1: best (value, index) of this piece
+  float bv = -INFINITY;
+  int bx = INT_MAX;
   if (VEC) {
     constexpr int STEP = NT * 4;
-    int x = x0 + tid * 4;
-    for (; x + 3 * STEP < x1; x += 4 * STEP) {  // four independent 16-byte loads in flight
-      f32x4 r[4];
+    for (int xb = x0 + tid * 4; xb < x1; xb += UNROLL * STEP) {
+      f32x4 r[UNROLL];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) r[u] = *(const f32x4*)(row + x + u * STEP);
+      for (int u = 0; u < UNROLL; ++u) {   // unconditional loads (clamped) so that all are in flight together
+        const int x = min(xb + u * STEP, x1 - 4);
+        r[u] = *(const f32x4*)(row + x);
+      }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < UNROLL; ++u) {
+        const int x = xb + u * STEP;
+        if (x < x1) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (r[u][e] > best.v || best.i == INT_MAX) { best.v = r[u][e]; best.i = x + u * STEP + e; }
-    }
-    for (; x < x1; x += STEP) {
-      const f32x4 r = *(const f32x4*)(row + x);
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (r[e] > best.v || best.i == INT_MAX) { best.v = r[e]; best.i = x + e; }
+          for (int e = 0; e < 4; ++e)
+            if (r[u][e] > bv || bx == INT_MAX) { bv = r[u][e]; bx = x + e; }
+        }
+      }
     }
   } else {
-    for (int x = x0 + tid; x < x1; x += NT) {
-      const float r = row[x];
-      if (r > best.v || best.i == INT_MAX) { best.v = r; best.i = x; }
+    for (int xb = x0 + tid; xb < x1; xb += UNROLL * NT) {
+      float r[UNROLL];
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) r[u] = row[min(xb + u * NT, x1 - 1)];
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        const int x = xb + u * NT;
+        if (x < x1 && (r[u] > bv || bx == INT_MAX)) { bv = r[u]; bx = x; }
+      }
     }
   }
-  best = wave_best(best);
-  if (lane == 0) { red_v[wave] = best.v; red_i[wave] = best.i; }
-  __syncthreads();
-  if (tid == 0) {
-    for (int w = 1; w < NW; ++w)
-      if (better(red_v[w], red_i[w], best.v, best.i)) { best.v = red_v[w]; best.i = red_i[w]; }
-    store_coherent(a.part_val + n, best.v);
-    store_coherent(a.part_idx + n, best.i);
-    wait_vector_memory();
-    last_flag = arrive_last(&a.counters[b], (uint32_t)(a.T * a.chunks));
-  }
-  __syncthreads();
-  if (!last_flag) return;
+  block_best(bv, bx, red_v, red_i);
 
-  // ---- phase 2: the sequence's path scan.  One parallel round trip stages all of the sequence's pieces.
-  const int T = a.T;
-  __shared__ float pv_s[kAcceptMaxParts];
-  __shared__ int pi_s[kAcceptMaxParts];
-  const int parts = T * a.chunks;
-  const size_t p0 = (size_t)b * parts;
-  for (int e = tid; e < parts; e += NT) {
-    pv_s[e] = load_coherent(a.part_val + p0 + e);
-    pi_s[e] = load_coherent(a.part_idx + p0 + e);
+  // ---- level 2: the row's pieces (skipped when a row is one piece)
+  uint32_t* seq_counter = a.counters + b;
+  if (a.chunks > 1) {
+    uint32_t* row_counter = a.counters + a.B + bi;
+    if (tid == 0) {
+      store_coherent(a.part_val + n, bv);
+      store_coherent(a.part_idx + n, bx);
+      wait_vector_memory();
+      flag = arrive_last(row_counter, (uint32_t)a.chunks);
+    }
+    __syncthreads();
+    if (!flag) return;
+    float v = -INFINITY;
+    int x = INT_MAX;
+    if (tid < a.chunks) {
+      v = load_coherent(a.part_val + (size_t)bi * a.chunks + tid);
+      x = load_coherent(a.part_idx + (size_t)bi * a.chunks + tid);
+    }
+    block_best(v, x, red_v, red_i);
+    bx = x;
+    if (tid == 0) reset_counter(row_counter);
   }
+  if (tid == 0) {
+    store_coherent(a.row_am + bi, bx);
+    wait_vector_memory();
+    flag = arrive_last(seq_counter, (uint32_t)a.T);
+  }
+  __syncthreads();
+  if (!flag) return;
+
+  // ---- level 3: the sequence's path scan
+  const int T = a.T;
   if (tid < T) {
+    am_s[tid] = load_coherent(a.row_am + (size_t)b * T + tid);
     tok_s[tid] = a.tokens[(size_t)b * T + tid];
     par_s[tid] = a.parent[(size_t)b * T + tid];
-  }
-  __syncthreads();
-  if (tid < T) {
-    const int q0 = tid * a.chunks;
-    float bv = pv_s[q0];
-    int bx = pi_s[q0];
-    for (int cc = 1; cc < a.chunks; ++cc)
-      if (better(pv_s[q0 + cc], pi_s[q0 + cc], bv, bx)) { bv = pv_s[q0 + cc]; bx = pi_s[q0 + cc]; }
-    am_s[tid] = bx;
   }
   __syncthreads();
 
@@ -143,10 +160,10 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
     if (ok) key = depth * 256 + (255 - tid);
   }
   key = wave_max(key);
-  __shared__ int red_k[NW];
   if (lane == 0) red_k[wave] = key;
   __syncthreads();
   key = red_k[0];
+#pragma unroll
   for (int w = 1; w < NW; ++w) key = max(key, red_k[w]);
 
   const int last = 255 - (key & 255), alen = key >> 8;   // the root is always consistent: key >= 255
@@ -156,7 +173,7 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
     a.next_token[b] = am_s[last];
     int j = last;
     for (int k = alen; k >= 0; --k) { path[k] = j; j = par_s[j]; }
-    reset_counter(&a.counters[b]);  // ready for the next call
+    reset_counter(seq_counter);  // ready for the next call
   }
   if (tid > alen && tid < T) path[tid] = -1;
   if (a.target_argmax && tid < T) a.target_argmax[(size_t)b * T + tid] = am_s[tid];

@@ -90,16 +90,6 @@ __device__ __forceinline__ void wait_vm_steps(int k) {
 // flight (a __syncthreads() would also wait for them).
 __device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// Device-scope 8-byte store / load of two floats (see store_coherent).
-__device__ __forceinline__ void store_coherent2(float* p, float x, float y) {
-  const uint64_t v = (uint64_t)__float_as_uint(x) | ((uint64_t)__float_as_uint(y) << 32);
-  __hip_atomic_store((uint64_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 load_coherent2(const float* p) {
-  const uint64_t v = __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
-}
-
 // Row layout in LDS: rows of D bf16, unpadded; the 16-byte chunk c of row r sits at position c ^ swz(r),
 // which spreads the 16 rows one operand read touches over distinct banks.  The swizzle repeats every 16
 // rows.  A step slot holds 32 K rows then 32 V rows; the query rows use the same layout.
@@ -115,9 +105,8 @@ struct Rows {
   __device__ static __forceinline__ int off(int r, int c) { return r * ROW + ((c ^ swz(r)) << 4); }
 };
 
-template <int D, int RB, int KW, int NST>
-__global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
-  constexpr int W = 4;
+template <int D, int RB, int KW, int W, int NST>
+__global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   constexpr int WR = W / KW;          // waves per key group; each owns a different slice of the rows
   constexpr int RW = 16 * RB;         // query rows per wave
   constexpr int R = WR * RW;          // query rows per workgroup
@@ -128,9 +117,10 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
   constexpr int NSS = NST / KW;       // ring slots in super-steps (KW consecutive steps, one per key group)
   constexpr int QSLOTS = (R * L::ROW + L::SLOT - 1) / L::SLOT;   // step slots the query rows occupy
   constexpr int QSS = (QSLOTS + KW - 1) / KW;                      // ... in super-steps
-  constexpr int CPS = KW * C16;       // copies per wave per super-step (KW blocks of 16 rows)
+  constexpr int CPS = 4 * KW * C16 / W;   // copies per wave per super-step (4*KW blocks of 16 rows)
   constexpr int QB = R / 16;          // 16-row blocks of query rows, dealt to the waves round-robin
   static_assert(W % KW == 0 && (NST & (NST - 1)) == 0 && NSS > QSS && NSS >= 2, "ring layout");
+  static_assert(CPS * W == 4 * KW * C16 && CPS >= 1 && (C16 % CPS == 0 || CPS % C16 == 0), "copy split");
   static_assert(16 * L::ROW == C16 * 1024 && (16 / L::RPL) % L::CPR == 0, "swizzle repeats every 16 rows");
   static_assert((NSS - 1) * CPS + ((QB + W - 1) / W) * C16 + 8 <= 63, "outstanding copies fit the counter");
   static_assert((size_t)(KW - 1) * R * (D + 2) * 4 <= (size_t)NST * L::SLOT, "group states fit the ring");
@@ -176,30 +166,36 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
     const int r = e / L::CPR, p = e - r * L::CPR;
     coff[j] = (uint32_t)(r * L::ROW + ((p ^ L::swz(r)) << 4));
   }
-  // A super-step is KW steps x (32 K rows + 32 V rows) = 4*KW blocks of 16 rows; wave w copies blocks
-  // w*KW .. w*KW + KW - 1 (block bi: step bi/4 of the super-step, K or V part (bi/2)%2, rows 16*(bi%2)..).
-  auto issue_super = [&](int jj) {
+  // A super-step is KW steps x (32 K rows + 32 V rows) = 4*KW blocks of 16 rows = 4*KW*C16 wave-wide 1 KB
+  // copies; wave w issues copies w*CPS .. w*CPS + CPS - 1 (copy ci: block bi = ci / C16 -- step bi/4 of the
+  // super-step, K or V part (bi/2)%2, rows 16*(bi%2).. -- and copy ci % C16 of that block), in groups of
+  // GRP = min(CPS, C16) copies that share a block.
+  constexpr int GRP = CPS < C16 ? CPS : C16;
+  constexpr int NGRP = CPS / GRP;
+  auto issue_group = [&](int jj, int t) {
     const uint32_t sbase = ring_lds + (jj & (NSS - 1)) * KW * L::SLOT;
+    const int ci0 = wave * CPS + t * GRP;
+    const int bi = ci0 / C16, j0 = ci0 - bi * C16;
+    const int sis = bi >> 2, part = (bi >> 1) & 1, half = bi & 1;
+    const int key0 = k_begin + (jj * KW + sis) * kStep + 16 * half;
+    const unsigned char* pbase = part ? vbase : kbase;
+    const uint32_t dst = sbase + sis * L::SLOT + part * L::HALF + half * C16 * 1024;
+    if (key0 + 16 <= a.S_cap) {
+      const unsigned char* src = pbase + (size_t)key0 * L::ROW;
 #pragma unroll
-    for (int t = 0; t < KW; ++t) {
-      const int bi = wave * KW + t;
-      const int sis = bi >> 2, part = (bi >> 1) & 1, half = bi & 1;
-      const int key0 = k_begin + (jj * KW + sis) * kStep + 16 * half;
-      const unsigned char* pbase = part ? vbase : kbase;
-      const uint32_t dst = sbase + sis * L::SLOT + part * L::HALF + half * C16 * 1024;
-      if (key0 + 16 <= a.S_cap) {
-        const unsigned char* src = pbase + (size_t)key0 * L::ROW;
+      for (int j = 0; j < GRP; ++j) copy16_to_lds(dst + (j0 + j) * 1024, src, coff[j0 + j]);
+    } else {  // rows past the cache capacity repeat its last row
 #pragma unroll
-        for (int j = 0; j < C16; ++j) copy16_to_lds(dst + j * 1024, src, coff[j]);
-      } else {  // rows past the cache capacity repeat its last row
-#pragma unroll
-        for (int j = 0; j < C16; ++j) {
-          const int r = (j * 64 + lane) / L::CPR;
-          const int key = min(key0 + r, a.S_cap - 1);
-          copy16_to_lds(dst + j * 1024, pbase + (size_t)key * L::ROW + (coff[j] - r * L::ROW));
-        }
+      for (int j = 0; j < GRP; ++j) {
+        const int r = ((j0 + j) * 64 + lane) / L::CPR;
+        const int key = min(key0 + r, a.S_cap - 1);
+        copy16_to_lds(dst + (j0 + j) * 1024, pbase + (size_t)key * L::ROW + (coff[j0 + j] - r * L::ROW));
       }
     }
+  };
+  auto issue_super = [&](int jj) {
+#pragma unroll
+    for (int t = 0; t < NGRP; ++t) issue_group(jj, t);
   };
 
   // ---- first copies: the query rows (into the last step slots), the tree (wave 0), then the ring
@@ -241,7 +237,10 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
 
   wait_vm_steps<CPS, NSS - QSS>(fa);   // this wave's query rows and the tree have landed
   barrier_lds();
-  if (tid < T) {
+  // Only a piece that reaches the tree slots consults ancestor sets (a step before them has key < L_b
+  // everywhere, and a masked step past k_end hides its keys whatever the sets say).
+  const bool need_anc = k_end > Lp;
+  if (need_anc && tid < T) {
     uint64_t m0 = 0, m1 = 0;
     if (a.mask) {
       const uint64_t* mr = (const uint64_t*)meta_lds + tid * Wm;
@@ -265,14 +264,23 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) qf[rb][ds] = *(const bf16x8*)(qslab + L::off(rh * RW + rb * 16 + col, ds * 4 + quad));
+  // Scores are scaled by c = |scale| log2(e) > 0 inside the exponent (one fma per score); a negative scale
+  // flips the sign of the queries instead (exact in bf16), a zero scale becomes the smallest normal float.
+  const float c_scale = fmaxf(fabsf(a.scale_log2), 1.17549435e-38f);
+  if (a.scale_log2 < 0.f) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) qf[rb][ds] = __builtin_bit_cast(bf16x8, __builtin_bit_cast(u32x4, qf[rb][ds]) ^ 0x80008000u);
+  }
   barrier_lds();   // ancestor sets written; every wave's query reads returned (their slots are reused next)
   uint64_t anc0[RB], anc1[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const int row = min(rg * R + rh * RW + rb * 16 + col, rows_total - 1);
     const int node = row % T;
-    anc0[rb] = anc_lds[2 * node];
-    anc1[rb] = anc_lds[2 * node + 1];
+    anc0[rb] = need_anc ? anc_lds[2 * node] : 0;
+    anc1[rb] = need_anc ? anc_lds[2 * node + 1] : 0;
   }
   const int fb = max(fa, min(NSS - 1, nsa));
   for (int j = fa; j < fb; ++j) issue_super(j);
@@ -298,25 +306,36 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
     // value rows at or past the sequence end hold whatever the cache had there: the waves that copied them
     // zero them, so that no bit pattern can reach the value product (their keys are masked below)
 #pragma unroll
-    for (int t = 0; t < KW; ++t) {
-      const int bi = wave * KW + t;
+    for (int t = 0; t < NGRP; ++t) {
+      const int ci0 = wave * CPS + t * GRP;
+      const int bi = ci0 / C16, j0 = ci0 - bi * C16;
       const int sis = bi >> 2, part = (bi >> 1) & 1, half = bi & 1;
       const int key0 = k_begin + (js * KW + sis) * kStep;
       if (part == 1 && key0 + kStep > N) {
-        const int r = 16 * half + (lane >> 2);
+        // the rows this wave's copies brought: 64*GRP lanes' worth of 16-byte chunks, rows j0*1024/ROW ..
+        constexpr int RPG = GRP * 1024 / L::ROW;   // rows per group of copies
+        constexpr int LPR = 64 / RPG;              // lanes per row
+        constexpr int PER = L::CPR / LPR;          // chunks per lane
+        const int r = 16 * half + j0 * 1024 / L::ROW + lane / LPR;
         if (key0 + r >= N) {
-          constexpr int PER = L::CPR / 4;
           unsigned char* vrow = sslot + sis * L::SLOT + L::HALF + r * L::ROW;
 #pragma unroll
-          for (int c = 0; c < PER; ++c) *(u32x4*)(vrow + ((lane & 3) * PER + c) * 16) = u32x4{0u, 0u, 0u, 0u};
+          for (int c = 0; c < PER; ++c) *(u32x4*)(vrow + ((lane % LPR) * PER + c) * 16) = u32x4{0u, 0u, 0u, 0u};
         }
       }
     }
     barrier_lds();   // super-step js complete in LDS for every wave; the slots of super-step js-1 are free
-    if (js + NSS - 1 < nsa) issue_super(js + NSS - 1);
+    // the refill of the freed slots is spread over the step: block 0 now, the others after the products
+    const bool refill = js + NSS - 1 < nsa;
+    if (refill) issue_group(js + NSS - 1, 0);
 
     const int step = js * KW + kw;   // this wave's step
-    if (step >= nact) continue;
+    if (step >= nact) {
+      if (refill)
+#pragma unroll
+        for (int t = 1; t < NGRP; ++t) issue_group(js + NSS - 1, t);
+      continue;
+    }
     const int key0 = k_begin + step * kStep;
     const unsigned char* tile = sslot + kw * L::SLOT;
     const unsigned char* vt = tile + L::HALF;
@@ -348,12 +367,11 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][ds], qf[rb][ds], s[rb][kb], 0, 0, 0);
+    if (refill)
+#pragma unroll
+      for (int t = 1; t < NGRP; ++t) issue_group(js + NSS - 1, t);
 
-    // scale to log2 units; only steps that reach the tree slots or the piece end need the mask
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) s[rb][kb] *= a.scale_log2;
+    // only steps that reach the tree slots or the piece end need the mask
     if (key0 + kStep > Lp || key0 + kStep > k_end) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
@@ -374,8 +392,9 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
     bf16x8 pb[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      float lmax = fmaxf(fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3])),
-                         fmaxf(fmaxf(s[rb][1][0], s[rb][1][1]), fmaxf(s[rb][1][2], s[rb][1][3])));
+      // this lane's maximum over its 8 keys of the row, in scaled log2 units (c > 0 keeps the order)
+      const float lmax = c_scale * fmaxf(fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3])),
+                                         fmaxf(fmaxf(s[rb][1][0], s[rb][1][1]), fmaxf(s[rb][1][2], s[rb][1][3])));
       // The reference maximum m only moves when some score exceeds it by more than 2^8 (the exponentials
       // then stay <= 256, and softmax does not depend on the reference), which after the first steps is
       // rare: in the common case no cross-lane reduction and no rescale happen at all.
@@ -396,7 +415,7 @@ __global__ __launch_bounds__(256) void tree_attn_bf16_kernel(AttnArgs a) {
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p = fast_exp2(s[rb][kb][e] - m_use);
+          const float p = fast_exp2(fmaf(s[rb][kb][e], c_scale, -m_use));
           psum += p;
           pb[rb][kb * 4 + e] = (__bf16)p;
         }
@@ -552,21 +571,21 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
   if (a.lse && c0 == 0) a.lse[orow] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
 }
 
-template <int D, int RB, int KW, int NST>
+template <int D, int RB, int KW, int W, int NST>
 hipError_t launch(const AttnArgs& a, hipStream_t stream) {
   constexpr size_t lds = (size_t)NST * Rows<D>::SLOT;
   static_assert(lds + 2 * kMaxNodes * 8 + 4 * kMaxNodes * 4 + 64 <= 160 * 1024, "LDS budget");
-  auto kern = tree_attn_bf16_kernel<D, RB, KW, NST>;
+  auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST>;
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     configured = true;
   }
-  if (a.rows_per_wg != 16 * RB * (4 / KW)) return hipErrorInvalidValue;
+  if (a.rows_per_wg != 16 * RB * (W / KW)) return hipErrorInvalidValue;
   const unsigned units_rounded = (a.units + 7) / 8 * 8;
   const unsigned grid = units_rounded * (unsigned)(a.splits * a.row_groups);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, stream, a);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * W), lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   const unsigned mgrid = (unsigned)a.units * a.row_groups * (a.rows_per_wg / 16);
@@ -577,18 +596,19 @@ hipError_t launch(const AttnArgs& a, hipStream_t stream) {
 template <int D, int NST>
 hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
   switch (a.rows_per_wg) {
-    case 16: return launch<D, 1, 4, NST>(a, stream);
-    case 32: return launch<D, 2, 4, NST>(a, stream);
-    case 64: return launch<D, 2, 2, NST>(a, stream);
-    case 128: return launch<D, 2, 1, NST>(a, stream);
+    case 16: return launch<D, 1, 4, 4, NST>(a, stream);
+    case 32: return launch<D, 1, 4, 8, NST>(a, stream);
+    case 64: return launch<D, 1, 2, 8, NST>(a, stream);
+    case 128: return launch<D, 1, 1, 8, NST>(a, stream);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-// Rows per workgroup: the narrowest of 16, 32, 64 rows (waves in 4, 4, 2 key groups) that holds every row
-// of a KV head, else 128 (all four waves on the same keys, 32 rows each, several row groups).
+// Rows per workgroup: the narrowest of 16, 32, 64 rows (4 waves in 4 key groups; 8 waves in 4 or 2 key
+// groups) that holds every row of a KV head, else 128 (all 8 waves on the same keys, several row groups).
+// Every wave owns 16 rows; 8 waves put two on each SIMD, so one's softmax overlaps the other's products.
 int tree_attn_bf16_rows_per_wg(int rows_total) {
   return rows_total <= 16 ? 16 : rows_total <= 32 ? 32 : rows_total <= 64 ? 64 : 128;
 }

@@ -98,7 +98,10 @@ CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits)
     (128, 2, 2, 1, 0, 1, 250, 0),      # single node = decode step
     (128, 2, 2, 33, 5, 3, 0, 0),       # empty prefix: tree keys only
     (128, 2, 2, 33, 5, 3, 0, 2),
-    (128, 7, 1, 128, 8, 6, 700, 0),    # GQA 7 x 128 rows = 14 row groups, deepest tree
+    (128, 7, 1, 128, 8, 6, 700, 0),    # GQA 7 x 128 rows = 7 row groups of 128, deepest tree
+    (128, 2, 2, 9, 3, 3, 400, 3),      # 9 rows: 16-row workgroups, four key groups
+    (64, 4, 2, 16, 4, 3, 333, 2),      # 32 rows, head_dim 64
+    (64, 2, 2, 60, 6, 4, 900, 0),      # 64 rows, head_dim 64
 ]
 
 
@@ -115,6 +118,22 @@ def test_bf16_parity(dev, case, variant):
     out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=splits)
     torch.cuda.synchronize()
     check_bf16(out, lse, batch, 0, "bf16 %s %s" % (variant, case))
+
+
+@pytest.mark.parametrize("scale", [-0.07, 0.0, 0.31])
+def test_scale_sign_and_zero(dev, scale):
+    # the kernel folds |scale| into the exponent and flips the queries' sign for a negative scale
+    wl = small_wl(num_nodes=60, depth=6, max_branch=4, kv_len=500)
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    note("scale %g" % scale)
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par, scale=scale, num_splits=2)
+    torch.cuda.synchronize()
+    v32 = f32(batch.v_cache[0])
+    args = (f32(batch.q[0]), f32(batch.k_cache[0]))
+    ref = oracle.tree_attn(*args, v32, batch.kv_len, batch.parent, scale, wl.num_kv_heads)
+    absref = oracle.tree_attn(*args, np.abs(v32), batch.kv_len, batch.parent, scale, wl.num_kv_heads)[0]
+    check_bf16(out, lse, batch, 0, "scale %g" % scale, ref, absref)
 
 
 def test_split_sweep_agrees(dev):
