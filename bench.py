@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true", help="skip the CPU baseline and the parity spot check")
+    ap.add_argument("--traffic-calibration", action="store_true",
+                    help="for rocprofv3 --pmc runs: a plain device copy of known size, then attention launches; "
+                         "prints what each launch should move and exits")
     return ap.parse_args()
 
 
@@ -159,6 +162,9 @@ def main():
             dreams.kv_commit(st["k"], st["v"], st["kv"], st["path"], st["alen"], kv_len_out=st["kv_out"])
 
     # ---- warm-up (eager), then capture R steps (one per input set) and the remainder into HIP graphs
+    if args.traffic_calibration:
+        calibrate_traffic(torch, dev, sets, attention, R, wl, host)
+        return
     for i in range(max(1, args.warmup)):
         step(sets[i % R])
     torch.cuda.synchronize()
@@ -269,6 +275,25 @@ def main():
     if not (args.no_cpu_baseline or args.profile_only):
         result["cpu_baseline"], result["parity_spot_check"] = cpu_baseline(wl, sets[0], host, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def calibrate_traffic(torch, dev, sets, attention, R, wl, host):
+    """Launches for the HBM-traffic counters: 5 copies of a 512 MiB buffer (reads 512 MiB, writes 512 MiB per
+    launch: the reference that turns FETCH_SIZE / WRITE_SIZE into bytes), then 2 * R attention calls over
+    the rotated input sets.  Eager launches, one stream; the counters are read per dispatch."""
+    n = 512 << 20
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    for i in range(2 * R):
+        attention(sets[i % R])
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copy_launches": 5,
+                      "attention_calls": 2 * R, "attention_algorithmic_bytes_per_call":
+                      attn_bytes_per_layer(wl, host.kv_len), "workload": wl.name}), flush=True)
 
 
 def cpu_baseline(wl, st, host, seconds):

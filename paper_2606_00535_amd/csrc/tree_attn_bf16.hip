@@ -516,21 +516,22 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 }
 
 // Merge of the key-axis pieces: out = sum_s w_s acc_s / sum_s w_s l_s with w_s = 2^(m_s - max_s m_s), in
-// piece order.  A workgroup merges 16 rows of one (sequence, KV head, row group); thread t handles row t/16
-// and the 8 columns (t%16)*8 .. +8 (D = 128) or 4 columns (D = 64) of it.  All loads of a chunk of 8 pieces
-// are issued before any is used.
+// piece order.  A one-wave workgroup merges kMergeRows rows of one (sequence, KV head, row group), so that
+// the merge spreads over many compute units; thread t handles row t/16 and the 8 columns (t%16)*8 .. +8
+// (D = 128) or 4 columns (D = 64) of it.  All loads of a chunk of 8 pieces are issued before any is used.
+constexpr int kMergeRows = 4;
 template <int D>
-__global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64) void tree_attn_merge_kernel(AttnArgs a) {
   constexpr int CPT = D / 16;           // columns per thread
   constexpr int CH = 8;                 // pieces per batch of loads
   typedef float fv __attribute__((ext_vector_type(CPT)));
   const int R = a.rows_per_wg;
-  const int blocks = R / 16;
+  const int blocks = R / kMergeRows;
   const int n = blockIdx.x;
   const int pset = n / blocks, rblk = n - pset * blocks;
   const int u = pset / a.row_groups, rg = pset - u * a.row_groups;
   const int b = u / a.Hkv, g = u - b * a.Hkv;
-  const int t = threadIdx.x, r = rblk * 16 + t / 16, c0 = (t % 16) * CPT;
+  const int t = threadIdx.x, r = rblk * kMergeRows + t / 16, c0 = (t % 16) * CPT;
   const int row = rg * R + r;                     // row within the KV head's G*T rows
   const int S = a.splits;
   const size_t prow0 = (size_t)pset * S * R + r;  // this row in piece 0; piece s adds s * R
@@ -588,8 +589,8 @@ hipError_t launch(const AttnArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * W), lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  const unsigned mgrid = (unsigned)a.units * a.row_groups * (a.rows_per_wg / 16);
-  hipLaunchKernelGGL(tree_attn_merge_kernel<D>, dim3(mgrid), dim3(256), 0, stream, a);
+  const unsigned mgrid = (unsigned)a.units * a.row_groups * (a.rows_per_wg / kMergeRows);
+  hipLaunchKernelGGL(tree_attn_merge_kernel<D>, dim3(mgrid), dim3(64), 0, stream, a);
   return hipGetLastError();
 }
 
