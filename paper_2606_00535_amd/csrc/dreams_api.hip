@@ -148,7 +148,10 @@ struct AcceptPlan {
   size_t val_off, idx_off, am_off, bytes;
 };
 
-constexpr int kAcceptPieceElems = 8192;   // logits per workgroup (32 KiB), all in flight at once
+// Pieces of a row: 8192 logits (8 16-byte loads per thread) while the batch has fewer rows than about two
+// workgroups per compute unit, so that the logits spread over the whole chip; otherwise up to 32768 logits
+// (32 loads per thread) per piece, so that most rows are one piece and need no second merge level.
+constexpr int kAcceptSmallPiece = 8192, kAcceptLargePiece = 32768, kAcceptTargetWgs = 512;
 
 dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
   if (B < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", B);
@@ -156,7 +159,14 @@ dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
   if (V < 1) return fail(DREAMS_ERR_INVALID_ARG, "vocab = %d < 1", V);
   *p = AcceptPlan{};
   const long long rows = (long long)B * T;
-  long long chunks = (V + kAcceptPieceElems - 1) / kAcceptPieceElems;
+  if (rows == 0) return DREAMS_OK;   // nothing to do, no workspace needed
+  long long chunks = (V + kAcceptLargePiece - 1) / kAcceptLargePiece;
+  if (rows < kAcceptTargetWgs) {
+    const long long want = (kAcceptTargetWgs + rows - 1) / rows;
+    const long long small = (V + kAcceptSmallPiece - 1) / kAcceptSmallPiece;
+    chunks = want < small ? want : small;
+    if (chunks < 1) chunks = 1;
+  }
   if (chunks > kAcceptMaxChunks) chunks = kAcceptMaxChunks;
   // counters: one per sequence, plus one per row when rows are cut into pieces
   if (chunks > 1 && (size_t)(B + rows) > kMaxCounters) chunks = 1;

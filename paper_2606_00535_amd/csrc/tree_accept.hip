@@ -4,8 +4,8 @@
 // One kernel, three levels, each finished by the last workgroup to arrive at an arrival counter (pieces
 // travel through device-scope stores and loads, see kernels.h):
 //   1. Row argmax of the target logits.  Each (sequence, node) row of V logits is cut into `chunks` pieces,
-//      one 256-thread workgroup per piece, every thread keeping up to 8 16-byte loads in flight (the logits
-//      are the only large input: B*T*V*4 bytes).  Ties go to the smallest index: every thread visits its
+//      one 256-thread workgroup per piece, every thread issuing its piece's 16-byte loads UNROLL at a time
+//      (8, 16 or 32, from the piece size; the logits are the only large input: B*T*V*4 bytes).  Ties go to the smallest index: every thread visits its
 //      elements in increasing order and replaces its candidate only on a strictly larger value, and every
 //      merge prefers the smaller index on equal values (fp32 comparison, so -0.0 and +0.0 are equal).
 //   2. The last piece of a row to finish merges the row's pieces (one counter per row, so at most `chunks`
@@ -55,10 +55,9 @@ __device__ __forceinline__ int wave_max(int x) {
   return x;
 }
 
-template <bool VEC>
+template <bool VEC, int UNROLL>
 __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs a) {
   constexpr int NT = kAcceptThreads, NW = NT / 64;
-  constexpr int UNROLL = 8;   // loads in flight per thread
   __shared__ float red_v[NW];
   __shared__ int red_i[NW];
   __shared__ int flag;
@@ -183,10 +182,19 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
 
 hipError_t launch_tree_accept(const AcceptArgs& a, hipStream_t stream) {
   const int grid = a.B * a.T * a.chunks;
-  if (a.vec4)
-    hipLaunchKernelGGL(tree_accept_kernel<true>, dim3(grid), dim3(kAcceptThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(tree_accept_kernel<false>, dim3(grid), dim3(kAcceptThreads), 0, stream, a);
+  // the piece's loads in one batch per thread where they fit 8, 16 or 32 per thread
+  const int per_batch = kAcceptThreads * (a.vec4 ? 4 : 1);
+  const int u = a.chunk <= 8 * per_batch ? 8 : a.chunk <= 16 * per_batch ? 16 : 32;
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3(grid), dim3(kAcceptThreads), 0, stream, a); };
+  if (a.vec4) {
+    if (u == 8) go(tree_accept_kernel<true, 8>);
+    else if (u == 16) go(tree_accept_kernel<true, 16>);
+    else go(tree_accept_kernel<true, 32>);
+  } else {
+    if (u == 8) go(tree_accept_kernel<false, 8>);
+    else if (u == 16) go(tree_accept_kernel<false, 16>);
+    else go(tree_accept_kernel<false, 32>);
+  }
   return hipGetLastError();
 }
 
