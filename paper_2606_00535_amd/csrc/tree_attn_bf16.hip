@@ -601,6 +601,7 @@ hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
     case 32: return launch<D, 1, 4, 8, NST>(a, stream);
     case 64: return launch<D, 1, 2, 8, NST>(a, stream);
     case 128: return launch<D, 1, 1, 8, NST>(a, stream);
+    case 256: return launch<D, 2, 1, 8, NST>(a, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -611,7 +612,7 @@ hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
 // groups) that holds every row of a KV head, else 128 (all 8 waves on the same keys, several row groups).
 // Every wave owns 16 rows; 8 waves put two on each SIMD, so one's softmax overlaps the other's products.
 int tree_attn_bf16_rows_per_wg(int rows_total) {
-  return rows_total <= 16 ? 16 : rows_total <= 32 ? 32 : rows_total <= 64 ? 64 : 128;
+  return rows_total <= 16 ? 16 : rows_total <= 32 ? 32 : rows_total <= 64 ? 64 : rows_total <= 128 ? 128 : 256;
 }
 
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream) {
