@@ -516,22 +516,27 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 }
 
 // Merge of the key-axis pieces: out = sum_s w_s acc_s / sum_s w_s l_s with w_s = 2^(m_s - max_s m_s), in
-// piece order.  A one-wave workgroup merges kMergeRows rows of one (sequence, KV head, row group), so that
-// the merge spreads over many compute units; thread t handles row t/16 and the 8 columns (t%16)*8 .. +8
-// (D = 128) or 4 columns (D = 64) of it.  All loads of a chunk of 8 pieces are issued before any is used.
-constexpr int kMergeRows = 4;
+// piece order.  A one-wave workgroup merges the 64 / (D/4) rows (2 for D = 128, 4 for D = 64) of one
+// (sequence, KV head, row group) that its lanes cover at 4 columns (one 16-byte load per piece) each, so the
+// merge spreads over many compute units with many requests in flight.  All loads of a chunk of 8 pieces are
+// issued before any is used.
+template <int D>
+constexpr int merge_rows() { return 64 / (D / 4); }
 template <int D>
 __global__ __launch_bounds__(64) void tree_attn_merge_kernel(AttnArgs a) {
-  constexpr int CPT = D / 16;           // columns per thread
+  constexpr int CPT = 4;                // columns per thread
+  constexpr int TPR = D / CPT;          // threads per row
+  constexpr int MR = merge_rows<D>();   // rows per workgroup
+  static_assert(TPR * MR == 64, "one wave per workgroup");
   constexpr int CH = 8;                 // pieces per batch of loads
   typedef float fv __attribute__((ext_vector_type(CPT)));
   const int R = a.rows_per_wg;
-  const int blocks = R / kMergeRows;
+  const int blocks = R / MR;
   const int n = blockIdx.x;
   const int pset = n / blocks, rblk = n - pset * blocks;
   const int u = pset / a.row_groups, rg = pset - u * a.row_groups;
   const int b = u / a.Hkv, g = u - b * a.Hkv;
-  const int t = threadIdx.x, r = rblk * kMergeRows + t / 16, c0 = (t % 16) * CPT;
+  const int t = threadIdx.x, r = rblk * MR + t / TPR, c0 = (t % TPR) * CPT;
   const int row = rg * R + r;                     // row within the KV head's G*T rows
   const int S = a.splits;
   const size_t prow0 = (size_t)pset * S * R + r;  // this row in piece 0; piece s adds s * R
@@ -589,7 +594,7 @@ hipError_t launch(const AttnArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * W), lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  const unsigned mgrid = (unsigned)a.units * a.row_groups * (a.rows_per_wg / kMergeRows);
+  const unsigned mgrid = (unsigned)a.units * a.row_groups * (a.rows_per_wg / merge_rows<D>());
   hipLaunchKernelGGL(tree_attn_merge_kernel<D>, dim3(mgrid), dim3(64), 0, stream, a);
   return hipGetLastError();
 }
