@@ -87,8 +87,15 @@ __device__ __forceinline__ void wait_vm_steps(int k) {
   }
 }
 // Workgroup barrier after this wave's LDS reads and writes have completed; outstanding copies stay in
-// flight (a __syncthreads() would also wait for them).
-__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// flight (a __syncthreads() would also wait for them).  The wait is the compiler's own instruction
+// (vmcnt and expcnt at their maxima, lgkmcnt 0), so its wait-count bookkeeping knows that every LDS read
+// issued before the barrier has returned.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // Row layout in LDS: rows of D bf16, unpadded; the 16-byte chunk c of row r sits at position c ^ swz(r),
 // which spreads the 16 rows one operand read touches over distinct banks.  The swizzle repeats every 16
@@ -105,7 +112,7 @@ struct Rows {
   __device__ static __forceinline__ int off(int r, int c) { return r * ROW + ((c ^ swz(r)) << 4); }
 };
 
-template <int D, int RB, int KW, int W, int NST>
+template <int D, int RB, int KW, int W, int NST, bool PIPE>
 __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   constexpr int WR = W / KW;          // waves per key group; each owns a different slice of the rows
   constexpr int RW = 16 * RB;         // query rows per wave
@@ -122,7 +129,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   static_assert(W % KW == 0 && (NST & (NST - 1)) == 0 && NSS > QSS && NSS >= 2, "ring layout");
   static_assert(CPS * W == 4 * KW * C16 && CPS >= 1 && (C16 % CPS == 0 || CPS % C16 == 0), "copy split");
   static_assert(16 * L::ROW == C16 * 1024 && (16 / L::RPL) % L::CPR == 0, "swizzle repeats every 16 rows");
-  static_assert((NSS - 1) * CPS + ((QB + W - 1) / W) * C16 + 8 <= 63, "outstanding copies fit the counter");
+  static_assert(NSS * CPS + ((QB + W - 1) / W) * C16 + 8 <= 63, "outstanding copies fit the counter");
   static_assert((size_t)(KW - 1) * R * (D + 2) * 4 <= (size_t)NST * L::SLOT, "group states fit the ring");
 
   extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots
@@ -282,8 +289,13 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     anc0[rb] = need_anc ? anc_lds[2 * node] : 0;
     anc1[rb] = need_anc ? anc_lds[2 * node + 1] : 0;
   }
-  const int fb = max(fa, min(NSS - 1, nsa));
+  // Ring depth: the pipelined loop frees a super-step's slots at the barrier that follows its operand reads,
+  // so every slot can hold a copy in flight; the plain loop keeps one slot for the super-step being read.
+  constexpr int AHEAD = PIPE ? NSS : NSS - 1;
+  const int fb = max(fa, min(AHEAD, nsa));
   for (int j = fa; j < fb; ++j) issue_super(j);
+  // super-steps issued by this wave once the refill of iteration js - 1 is out
+  auto issued_by = [&](int js) { return max(fa, min(js + AHEAD, nsa)); };
 
   f32x4 o[RB][DB];
   float m_run[RB], l_run[RB];
@@ -299,79 +311,61 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   const int tr_row = (col >> 2) * 4 + quad;            // transposed read: 4 keys j*4+quad, 16 columns
   const int tr_c = (col & 3) >> 1, tr_half = (col & 1) * 8;
 
-  for (int js = 0; js < nsa; ++js) {
-    // this wave's copies of super-step js have landed once only later super-steps' copies are outstanding
-    wait_vm_steps<CPS, NSS - 2>(max(fa, min(js + NSS - 1, nsa)) - 1 - js);
-    unsigned char* sslot = ring + (js & (NSS - 1)) * KW * L::SLOT;
-    // value rows at or past the sequence end hold whatever the cache had there: the waves that copied them
-    // zero them, so that no bit pattern can reach the value product (their keys are masked below)
+  // Key and value rows at or past the sequence end hold whatever the cache had there: the waves that copied
+  // them zero them once their own copies have landed, so that no bit pattern (an infinity, a NaN) can reach
+  // the products; their scores are then exactly the mask's -inf.
+  auto zero_tail = [&](int jj) {
+    unsigned char* sslot = ring + (jj & (NSS - 1)) * KW * L::SLOT;
 #pragma unroll
     for (int t = 0; t < NGRP; ++t) {
       const int ci0 = wave * CPS + t * GRP;
       const int bi = ci0 / C16, j0 = ci0 - bi * C16;
       const int sis = bi >> 2, part = (bi >> 1) & 1, half = bi & 1;
-      const int key0 = k_begin + (js * KW + sis) * kStep;
-      if (part == 1 && key0 + kStep > N) {
+      const int key0 = k_begin + (jj * KW + sis) * kStep;
+      if (key0 + kStep > N) {
         // the rows this wave's copies brought: 64*GRP lanes' worth of 16-byte chunks, rows j0*1024/ROW ..
         constexpr int RPG = GRP * 1024 / L::ROW;   // rows per group of copies
         constexpr int LPR = 64 / RPG;              // lanes per row
         constexpr int PER = L::CPR / LPR;          // chunks per lane
         const int r = 16 * half + j0 * 1024 / L::ROW + lane / LPR;
         if (key0 + r >= N) {
-          unsigned char* vrow = sslot + sis * L::SLOT + L::HALF + r * L::ROW;
+          unsigned char* vrow = sslot + sis * L::SLOT + part * L::HALF + r * L::ROW;
 #pragma unroll
           for (int c = 0; c < PER; ++c) *(u32x4*)(vrow + ((lane % LPR) * PER + c) * 16) = u32x4{0u, 0u, 0u, 0u};
         }
       }
     }
-    barrier_lds();   // super-step js complete in LDS for every wave; the slots of super-step js-1 are free
-    // the refill of the freed slots is spread over the step: block 0 now, the others after the products
-    const bool refill = js + NSS - 1 < nsa;
-    if (refill) issue_group(js + NSS - 1, 0);
+  };
 
-    const int step = js * KW + kw;   // this wave's step
-    if (step >= nact) {
-      if (refill)
-#pragma unroll
-        for (int t = 1; t < NGRP; ++t) issue_group(js + NSS - 1, t);
-      continue;
-    }
-    const int key0 = k_begin + step * kStep;
-    const unsigned char* tile = sslot + kw * L::SLOT;
-    const unsigned char* vt = tile + L::HALF;
-
-    // All of the step's operand reads are issued before any product, so their LDS latencies overlap:
-    // K fragments (A operand of S^T: A row m holds key kb*16 + (m%4)*4 + m/4) and V^T fragments (A operand of
-    // O^T, transposing reads: lo = keys j*4+quad, hi = keys 16+j*4+quad, matching the probabilities' slots).
+  // A step's operands: K fragments (A operand of S^T: A row m holds key kb*16 + (m%4)*4 + m/4) and V^T
+  // fragments (A operand of O^T, transposing reads: lo = keys j*4+quad, hi = keys 16+j*4+quad, matching the
+  // probabilities' slots).  All are issued together, so their LDS latencies overlap.
+  struct Ops {
     bf16x8 kf[2][DS];
+    s16x4 vlo[DB], vhi[DB];
+  };
+  auto read_ops = [&](Ops& op, int jj) {
+    const unsigned char* tile = ring + (jj & (NSS - 1)) * KW * L::SLOT + kw * L::SLOT;
+    const unsigned char* vt = tile + L::HALF;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) kf[kb][ds] = *(const bf16x8*)(tile + L::off(kb * 16 + ka_row, ds * 4 + quad));
-    s16x4 vlo[DB], vhi[DB];
+      for (int ds = 0; ds < DS; ++ds) op.kf[kb][ds] = *(const bf16x8*)(tile + L::off(kb * 16 + ka_row, ds * 4 + quad));
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
       const int c = d * 2 + tr_c;
-      vlo[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vt + L::off(tr_row, c) + tr_half));
-      vhi[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vt + L::off(16 + tr_row, c) + tr_half));
+      op.vlo[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vt + L::off(tr_row, c) + tr_half));
+      op.vhi[d] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vt + L::off(16 + tr_row, c) + tr_half));
     }
-    __builtin_amdgcn_sched_barrier(0);
+  };
 
-    // S^T blocks kb = 0, 1: element e of a lane in quad q is key kb*16 + e*4 + q, row col
+  // One step (32 keys) of this wave's rows: scores, mask, online softmax, value product.
+  auto compute = [&](const Ops& op, int step) {
+    const int key0 = k_begin + step * kStep;
+    // S^T blocks kb = 0, 1: element e of a lane in quad q is key kb*16 + e*4 + q, row col.  The mask enters
+    // as the products' starting value (0 or -inf), so nothing rewrites the scores after the matrix cores
+    // have written them; only steps that reach the tree slots or the piece end need it.
     f32x4 s[RB][2];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][ds], qf[rb][ds], s[rb][kb], 0, 0, 0);
-    if (refill)
-#pragma unroll
-      for (int t = 1; t < NGRP; ++t) issue_group(js + NSS - 1, t);
-
-    // only steps that reach the tree slots or the piece end need the mask
     if (key0 + kStep > Lp || key0 + kStep > k_end) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
@@ -384,11 +378,21 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
             const uint64_t word = j < 64 ? anc0[rb] : anc1[rb];
             const bool anc = ((word >> (j & 63)) & 1ull) != 0;
             const bool vis = (key < k_end) & ((key < Lp) | anc);
-            s[rb][kb][e] = vis ? s[rb][kb][e] : -INFINITY;
+            s[rb][kb][e] = vis ? 0.f : -INFINITY;
           }
         }
       }
+    } else {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op.kf[kb][ds], qf[rb][ds], s[rb][kb], 0, 0, 0);
+
     bf16x8 pb[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
@@ -427,7 +431,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
       bf16x8 va;
-      const bf16x4 lo_b = __builtin_bit_cast(bf16x4, vlo[d]), hi_b = __builtin_bit_cast(bf16x4, vhi[d]);
+      const bf16x4 lo_b = __builtin_bit_cast(bf16x4, op.vlo[d]), hi_b = __builtin_bit_cast(bf16x4, op.vhi[d]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         va[e] = lo_b[e];
@@ -435,6 +439,53 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
       }
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) o[rb][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[rb], o[rb][d], 0, 0, 0);
+    }
+  };
+
+  if constexpr (PIPE) {
+    // Software-pipelined: after the barrier that hands over super-step js+1, a wave issues that super-step's
+    // operand reads and then computes super-step js from registers, so the LDS reads of one step overlap the
+    // products and softmax of the previous one on every wave.
+    Ops op[2];
+    if (nsa > 0) {
+      wait_vm_steps<CPS, NSS - 1>(issued_by(0) - 1);   // this wave's copies of super-step 0 have landed
+      zero_tail(0);
+      barrier_lds();
+      if (kw < nact) read_ops(op[0], 0);
+    }
+    auto half_step = [&](int js, const Ops& cur, Ops& nxt) {
+      const bool more = js + 1 < nsa;
+      if (more) {
+        wait_vm_steps<CPS, NSS - 2>(issued_by(js) - 2 - js);   // ... and of super-step js+1
+        zero_tail(js + 1);
+      }
+      // super-step js+1 complete in LDS for every wave; every wave's reads of super-step js have returned,
+      // so its slots take the copies of super-step js+NSS.  (Also taken after the last super-step, so that
+      // on every path the operands of super-step js are known to have landed in registers.)
+      barrier_lds();
+      if (more) {
+        if (js + NSS < nsa) issue_super(js + NSS);
+        if ((js + 1) * KW + kw < nact) read_ops(nxt, js + 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (js * KW + kw < nact) compute(cur, js * KW + kw);
+    };
+    for (int js = 0; js < nsa; js += 2) {
+      half_step(js, op[0], op[1]);
+      if (js + 1 < nsa) half_step(js + 1, op[1], op[0]);
+    }
+  } else {
+    for (int js = 0; js < nsa; ++js) {
+      wait_vm_steps<CPS, NSS - 2>(issued_by(js) - 1 - js);   // this wave's copies of super-step js have landed
+      zero_tail(js);
+      barrier_lds();   // super-step js complete in LDS for every wave; the slots of super-step js-1 are free
+      if (js + NSS - 1 < nsa) issue_super(js + NSS - 1);
+      const int step = js * KW + kw;   // this wave's step
+      if (step >= nact) continue;
+      Ops op;
+      read_ops(op, js);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(op, step);
     }
   }
   wait_vm<0>();   // copies planned past a sequence's own end land before LDS is reused
@@ -448,14 +499,16 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   // ---- key groups 1.. hand their states to group 0 through LDS (merged in group order)
   if constexpr (KW > 1) {
     barrier_lds();   // every wave is done with the ring
-    float* st_o = (float*)ring;                          // [KW-1][R][D]
-    float2* st_ml = (float2*)(st_o + (KW - 1) * R * D);  // [KW-1][R]
+    // accumulators as [KW-1][D/4][R] 16-byte chunks: the 16 lanes of a quad touch 256 consecutive bytes,
+    // so neither the writes nor the reads below conflict on banks
+    f32x4* st_o = (f32x4*)ring;
+    float2* st_ml = (float2*)(st_o + (KW - 1) * R * (D / 4));  // [KW-1][R]
     if (kw > 0) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         const int row = (kw - 1) * R + rh * RW + rb * 16 + col;
 #pragma unroll
-        for (int d = 0; d < DB; ++d) *(f32x4*)(st_o + (size_t)row * D + d * 16 + quad * 4) = o[rb][d];
+        for (int d = 0; d < DB; ++d) st_o[((kw - 1) * (D / 4) + d * 4 + quad) * R + rh * RW + rb * 16 + col] = o[rb][d];
         if (quad == 0) st_ml[row] = make_float2(m_run[rb], l_run[rb]);
       }
     }
@@ -473,7 +526,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
           m_run[rb] = M;
           l_run[rb] = l_run[rb] * w0 + ml.y * w1;
 #pragma unroll
-          for (int d = 0; d < DB; ++d) o[rb][d] = o[rb][d] * w0 + *(const f32x4*)(st_o + (size_t)row * D + d * 16 + quad * 4) * w1;
+          for (int d = 0; d < DB; ++d) o[rb][d] = o[rb][d] * w0 + st_o[((k - 1) * (D / 4) + d * 4 + quad) * R + rh * RW + rb * 16 + col] * w1;
         }
       }
     }
@@ -532,9 +585,16 @@ __global__ __launch_bounds__(64) void tree_attn_merge_kernel(AttnArgs a) {
   typedef float fv __attribute__((ext_vector_type(CPT)));
   const int R = a.rows_per_wg;
   const int blocks = R / MR;
+  // same XCD as the streaming kernel's workgroups of this (sequence, KV head): ids dealt round-robin over
+  // the 8 XCDs, unit u on XCD u % 8
   const int n = blockIdx.x;
-  const int pset = n / blocks, rblk = n - pset * blocks;
-  const int u = pset / a.row_groups, rg = pset - u * a.row_groups;
+  const int xcd = n & 7, slot = n >> 3;
+  const int per_unit = a.row_groups * blocks;
+  const int u = xcd + 8 * (slot / per_unit);
+  if (u >= a.units) return;
+  const int within = slot - (slot / per_unit) * per_unit;
+  const int rg = within / blocks, rblk = within - rg * blocks;
+  const int pset = u * a.row_groups + rg;
   const int b = u / a.Hkv, g = u - b * a.Hkv;
   const int t = threadIdx.x, r = rblk * MR + t / TPR, c0 = (t % TPR) * CPT;
   const int row = rg * R + r;                     // row within the KV head's G*T rows
@@ -581,7 +641,8 @@ template <int D, int RB, int KW, int W, int NST>
 hipError_t launch(const AttnArgs& a, hipStream_t stream) {
   constexpr size_t lds = (size_t)NST * Rows<D>::SLOT;
   static_assert(lds + 2 * kMaxNodes * 8 + 4 * kMaxNodes * 4 + 64 <= 160 * 1024, "LDS budget");
-  auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST>;
+  // two sets of operand registers fit beside one 16-row block's state, not beside two
+  auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST, RB == 1>;
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -594,7 +655,7 @@ hipError_t launch(const AttnArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * W), lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  const unsigned mgrid = (unsigned)a.units * a.row_groups * (a.rows_per_wg / merge_rows<D>());
+  const unsigned mgrid = units_rounded * a.row_groups * (a.rows_per_wg / merge_rows<D>());
   hipLaunchKernelGGL(tree_attn_merge_kernel<D>, dim3(mgrid), dim3(64), 0, stream, a);
   return hipGetLastError();
 }

@@ -102,6 +102,14 @@ CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits)
     (128, 2, 2, 9, 3, 3, 400, 3),      # 9 rows: 16-row workgroups, four key groups
     (64, 4, 2, 16, 4, 3, 333, 2),      # 32 rows, head_dim 64
     (64, 2, 2, 60, 6, 4, 900, 0),      # 64 rows, head_dim 64
+    # long pieces: the ring wraps several times in every row configuration
+    (128, 2, 2, 9, 3, 3, 2100, 1),     # 16 rows
+    (128, 4, 2, 16, 4, 3, 2100, 1),    # 32 rows
+    (128, 2, 2, 60, 6, 4, 3000, 2),    # 64 rows
+    (128, 4, 2, 60, 6, 4, 2000, 1),    # 128 rows
+    (128, 3, 1, 60, 6, 4, 2000, 1),    # 256 rows (180)
+    (64, 2, 2, 60, 6, 4, 3000, 1),     # 64 rows, head_dim 64
+    (64, 4, 2, 60, 6, 4, 2000, 1),     # 128 rows, head_dim 64
 ]
 
 
@@ -204,6 +212,28 @@ def test_nonancestor_perturbation_bitwise(dev):
         torch.cuda.synchronize()
         assert torch.equal(out2[0, :, i].view(torch.int16), out[0, :, i].view(torch.int16)), int(i)
         assert torch.equal(lse2[0, :, i], lse[0, :, i]), int(i)
+
+
+@pytest.mark.parametrize("hq,hkv,t", [(2, 2, 60), (4, 2, 60), (3, 1, 60), (4, 2, 16)],
+                         ids=["64rows", "128rows", "256rows", "32rows"])
+def test_garbage_past_sequence_end_bitwise(dev, hq, hkv, t):
+    # cache slots at or past L_b + T are not part of the problem: infinities and NaNs there change nothing
+    wl = small_wl(num_q_heads=hq, num_kv_heads=hkv, num_nodes=t, depth=4, max_branch=4, kv_len=500)
+    batch = W.make_batch(wl, with_logits=False, kv_lens=[500, 437])
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    note("garbage past end %s" % ((hq, hkv, t),))
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=2, max_kv_len=500)
+    k2, v2 = k.clone(), v.clone()
+    for b, L in enumerate(batch.kv_len):
+        n = int(L) + t
+        k2[b, :, n:] = float("nan")
+        v2[b, :, n:] = float("inf")
+        k2[b, :, n + 1::3] = float("-inf")
+        v2[b, :, n + 1::3] = float("nan")
+    out2, lse2 = dreams.tree_verify_attn(q, k2, v2, kv, par, num_splits=2, max_kv_len=500)
+    torch.cuda.synchronize()
+    assert torch.equal(out2.view(torch.int16), out.view(torch.int16))
+    assert torch.equal(lse2, lse)
 
 
 def test_mask_input_matches_parent_and_empty_rows(dev):
