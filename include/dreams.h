@@ -123,9 +123,10 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
                                         const uint64_t* tree_mask, void* out, float* lse, void* workspace,
                                         size_t workspace_bytes, hipStream_t stream);
 
-/* Bytes of workspace dreams_tree_accept needs (never 0).  DREAMS_ERR_UNSUPPORTED if batch exceeds
- * DREAMS_WORKSPACE_COUNTER_BYTES / 4 (one arrival counter per sequence; rows of long vocabularies are cut
- * into pieces with one more counter per row while batch * (num_nodes + 1) counters fit). */
+/* Bytes of workspace dreams_tree_accept needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if batch
+ * exceeds DREAMS_WORKSPACE_COUNTER_BYTES / 4 (one arrival counter per sequence, plus up to 8 group counters
+ * per sequence while batch * 9 counters fit).  After the counters: one (value, index) pair per piece of each
+ * row (rows of long vocabularies are cut into pieces). */
 dreams_status_t dreams_tree_accept_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
                                                   size_t* bytes);
 

@@ -144,14 +144,15 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
 
 // ----------------------------------------------------------------------------------------- acceptance
 struct AcceptPlan {
-  int chunks, chunk;
-  size_t val_off, idx_off, am_off, bytes;
+  int chunks, chunk, groups, group_base, group_stride;
+  size_t val_off, idx_off, bytes;
 };
 
 // Pieces of a row: 8192 logits (8 16-byte loads per thread) while the batch has fewer rows than about two
 // workgroups per compute unit, so that the logits spread over the whole chip; otherwise up to 32768 logits
 // (32 loads per thread) per piece, so that most rows are one piece and need no second merge level.
 constexpr int kAcceptSmallPiece = 8192, kAcceptLargePiece = 32768, kAcceptTargetWgs = 512;
+constexpr int kAcceptGroups = 8;   // group counters per sequence (see tree_accept.hip)
 
 dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
   if (B < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", B);
@@ -168,21 +169,36 @@ dreams_status_t plan_accept(int32_t B, int32_t T, int32_t V, AcceptPlan* p) {
     if (chunks < 1) chunks = 1;
   }
   if (chunks > kAcceptMaxChunks) chunks = kAcceptMaxChunks;
-  // counters: one per sequence, plus one per row when rows are cut into pieces
-  if (chunks > 1 && (size_t)(B + rows) > kMaxCounters) chunks = 1;
-  if ((size_t)B > kMaxCounters)
-    return fail(DREAMS_ERR_UNSUPPORTED, "batch = %d exceeds the %zu arrival counters", B, kMaxCounters);
   long long chunk = (V + chunks - 1) / chunks;
   chunk = (chunk + 3) / 4 * 4;
   chunks = (V + chunk - 1) / chunk;
   if (rows * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  // counters: one per sequence, then up to 8 group counters per sequence while they fit
+  if ((size_t)B > kMaxCounters)
+    return fail(DREAMS_ERR_UNSUPPORTED, "batch = %d exceeds the %zu arrival counters", B, kMaxCounters);
+  const long long per_seq = (long long)T * chunks;
+  // group counters after the sequence counters, a 128-byte line apart where they fit (else closer); with
+  // no room for them the sequence counter serves as the one group counter (its last arrival resets it and
+  // arrives again, alone)
+  const long long groups = per_seq < kAcceptGroups ? per_seq : kAcceptGroups;
+  const size_t base = ((size_t)B + 31) / 32 * 32;
+  size_t stride = 32;
+  while (stride > 1 && base + (size_t)B * groups * stride > kMaxCounters) stride /= 2;
   p->chunks = (int)chunks;
   p->chunk = (int)chunk;
+  if (base + (size_t)B * groups * stride <= kMaxCounters) {
+    p->groups = (int)groups;
+    p->group_base = (int)base;
+    p->group_stride = (int)stride;
+  } else {
+    p->groups = 1;
+    p->group_base = 0;
+    p->group_stride = 1;
+  }
   const size_t parts = (size_t)rows * chunks;
   p->val_off = kCounterBytes;
   p->idx_off = p->val_off + align_up(parts * sizeof(float), 256);
-  p->am_off = p->idx_off + align_up(parts * sizeof(int32_t), 256);
-  p->bytes = p->am_off + align_up((size_t)rows * sizeof(int32_t), 256);
+  p->bytes = p->idx_off + align_up(parts * sizeof(int32_t), 256);
   return DREAMS_OK;
 }
 
@@ -301,11 +317,13 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
   char* ws = (char*)workspace;
   a.part_val = (float*)(ws + p.val_off);
   a.part_idx = (int32_t*)(ws + p.idx_off);
-  a.row_am = (int32_t*)(ws + p.am_off);
   a.counters = (uint32_t*)ws;
   a.B = batch;
   a.T = num_nodes;
   a.V = vocab;
+  a.groups = p.groups;
+  a.group_base = p.group_base;
+  a.group_stride = p.group_stride;
   a.chunks = p.chunks;
   a.chunk = p.chunk;
   a.vec4 = (vocab % 4 == 0) && aligned(target_logits, 16);

@@ -68,7 +68,7 @@ hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
 
 // ---------------------------------------------------------------------------------------- acceptance
 constexpr int kAcceptThreads = 256;
-constexpr int kAcceptMaxChunks = kAcceptThreads;   // pieces per row (merged one per thread)
+constexpr int kAcceptMaxChunks = kAcceptThreads;   // pieces per row, at most
 
 struct AcceptArgs {
   const float* logits;    // [B, T, V]
@@ -78,11 +78,13 @@ struct AcceptArgs {
   int32_t* accept_path;   // [B, T]
   int32_t* next_token;    // [B]
   int32_t* target_argmax; // [B, T] or nullptr
-  float* part_val;        // [B, T, chunks]
-  int32_t* part_idx;      // [B, T, chunks]
-  int32_t* row_am;        // [B, T] argmax of each row
-  uint32_t* counters;     // [B] per sequence, then [B, T] per row (chunks > 1); zero between calls
+  float* part_val;        // [B, T, chunks] best value of each piece
+  int32_t* part_idx;      // [B, T, chunks] its index
+  uint32_t* counters;     // [B] per sequence, then group counters; zero between calls
   int B, T, V;
+  int groups;             // group counters per sequence (1..8)
+  int group_base;         // word index of the first group counter
+  int group_stride;       // words between consecutive group counters (32: a 128-byte line each)
   int chunks;             // vocabulary pieces per row
   int chunk;              // elements per piece (multiple of 4 when vectorised)
   int vec4;               // logits rows are 16-byte aligned and V % 4 == 0

@@ -1,19 +1,23 @@
 // Greedy tree acceptance (the paper's Section 2, "Speculative decoding": drafts are kept while they equal the
 // target's own token at their position; at the first mismatch the target's token replaces the draft).
 //
-// One kernel, three levels, each finished by the last workgroup to arrive at an arrival counter (pieces
-// travel through device-scope stores and loads, see kernels.h):
-//   1. Row argmax of the target logits.  Each (sequence, node) row of V logits is cut into `chunks` pieces,
-//      one 256-thread workgroup per piece, every thread issuing its piece's 16-byte loads UNROLL at a time
-//      (8, 16 or 32, from the piece size; the logits are the only large input: B*T*V*4 bytes).  Ties go to the smallest index: every thread visits its
-//      elements in increasing order and replaces its candidate only on a strictly larger value, and every
-//      merge prefers the smaller index on equal values (fp32 comparison, so -0.0 and +0.0 are equal).
-//   2. The last piece of a row to finish merges the row's pieces (one counter per row, so at most `chunks`
-//      workgroups ever touch the same counter) and publishes the row's argmax.
-//   3. The last row of a sequence to finish runs the path scan: every node walks its own ancestor chain (at
-//      most depth steps, no barriers) to decide whether each draft on it equals the target token at its
-//      parent; the deepest consistent node (smallest index among equals) comes out of one block-wide max
-//      over the key depth*256 + (255 - node).
+// One kernel.  Each (sequence, node) row of V logits is cut into `chunks` pieces, one 256-thread workgroup per
+// piece, every thread issuing its piece's 16-byte loads UNROLL at a time (8, 16 or 32, from the piece size;
+// the logits are the only large input: B*T*V*4 bytes).  A workgroup publishes its piece's best (value, index)
+// and arrives at its sequence's counters; the last workgroup of the sequence to arrive merges all of the
+// sequence's pieces and runs the path scan:
+//   * piece best: ties go to the smallest index -- every thread visits its elements in increasing order and
+//     replaces its candidate only on a strictly larger value, and every merge prefers the smaller index on
+//     equal values (fp32 comparison, so -0.0 and +0.0 are equal);
+//   * arrival: a sequence's workgroups are dealt round-robin to up to 8 group counters (each on a cache line
+//     of its own where the counter region allows), and the last arrival of each group arrives at the
+//     sequence counter, so that no counter takes more than a few dozen atomics (atomics on one line
+//     serialise);
+//   * path scan: one wave sweeps the tree from the root, one depth per round, growing the set of consistent
+//     nodes (every draft on the way equal to the target's token at its parent) by ballots; the last round's
+//     smallest new member is the deepest consistent node (smallest index among equals).
+// The pieces travel through device-scope stores and loads (see kernels.h); the tree (tokens, parents) is
+// fetched by every workgroup at entry, ahead of its logits, for whichever one ends up finishing the sequence.
 #include "kernels.h"
 
 #include <limits.h>
@@ -49,12 +53,6 @@ __device__ __forceinline__ void block_best(float& v, int& i, float* red_v, int* 
     if (better(red_v[w], red_i[w], v, i)) { v = red_v[w]; i = red_i[w]; }
 }
 
-__device__ __forceinline__ int wave_max(int x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x = max(x, __shfl_xor(x, off));
-  return x;
-}
-
 template <bool VEC, int UNROLL>
 __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs a) {
   constexpr int NT = kAcceptThreads, NW = NT / 64;
@@ -62,16 +60,22 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
   __shared__ int red_i[NW];
   __shared__ int flag;
   __shared__ int am_s[kMaxNodes], tok_s[kMaxNodes], par_s[kMaxNodes];
-  __shared__ int red_k[NW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int T = a.T;
   const int n = blockIdx.x;                 // ((b * T) + i) * chunks + c
+  const int per_seq = T * a.chunks;         // workgroups of one sequence
+  const int b = n / per_seq, local = n - b * per_seq;
   const int bi = n / a.chunks, c = n - bi * a.chunks;
-  const int b = bi / a.T;
+  int tok_r = 0, par_r = 0;
+  if (tid < T) {
+    tok_r = a.tokens[(size_t)b * T + tid];
+    par_r = a.parent[(size_t)b * T + tid];
+  }
   const float* row = a.logits + (size_t)bi * a.V;
   const int x0 = c * a.chunk, x1 = min(a.V, x0 + a.chunk);
 
-  // ---- level 1: best (value, index) of this piece
+  // ---- best (value, index) of this piece
   float bv = -INFINITY;
   int bx = INT_MAX;
   if (VEC) {
@@ -107,75 +111,101 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
   }
   block_best(bv, bx, red_v, red_i);
 
-  // ---- level 2: the row's pieces (skipped when a row is one piece)
-  uint32_t* seq_counter = a.counters + b;
-  if (a.chunks > 1) {
-    uint32_t* row_counter = a.counters + a.B + bi;
-    if (tid == 0) {
-      store_coherent(a.part_val + n, bv);
-      store_coherent(a.part_idx + n, bx);
-      wait_vector_memory();
-      flag = arrive_last(row_counter, (uint32_t)a.chunks);
-    }
-    __syncthreads();
-    if (!flag) return;
-    float v = -INFINITY;
-    int x = INT_MAX;
-    if (tid < a.chunks) {
-      v = load_coherent(a.part_val + (size_t)bi * a.chunks + tid);
-      x = load_coherent(a.part_idx + (size_t)bi * a.chunks + tid);
-    }
-    block_best(v, x, red_v, red_i);
-    bx = x;
-    if (tid == 0) reset_counter(row_counter);
-  }
+  // ---- publish it and arrive: group counter, then (last of the group) the sequence counter
   if (tid == 0) {
-    store_coherent(a.row_am + bi, bx);
+    store_coherent(a.part_val + n, bv);
+    store_coherent(a.part_idx + n, bx);
     wait_vector_memory();
-    flag = arrive_last(seq_counter, (uint32_t)a.T);
+    const int NG = a.groups;
+    const int g = local % NG;
+    uint32_t* gc = a.counters + a.group_base + ((size_t)b * NG + g) * a.group_stride;
+    bool last = arrive_last(gc, (uint32_t)((per_seq - g + NG - 1) / NG));
+    if (last) {
+      reset_counter(gc);   // every workgroup of the group has arrived: ready for the next call
+      last = arrive_last(a.counters + b, (uint32_t)NG);
+    }
+    flag = last;
   }
   __syncthreads();
   if (!flag) return;
 
-  // ---- level 3: the sequence's path scan
-  const int T = a.T;
+  // ---- the sequence's last workgroup: every row's argmax from its pieces (all loads of a batch of 8 pieces
+  // in flight together, merged in piece order), then the path scan
   if (tid < T) {
-    am_s[tid] = load_coherent(a.row_am + (size_t)b * T + tid);
-    tok_s[tid] = a.tokens[(size_t)b * T + tid];
-    par_s[tid] = a.parent[(size_t)b * T + tid];
-  }
-  __syncthreads();
-
-  int key = -1;
-  if (tid < T) {
-    int j = tid, depth = 0;
-    bool ok = true;
-    while (j != 0) {
-      const int p = par_s[j];
-      if (p < 0 || p >= j || tok_s[j] != am_s[p]) { ok = false; break; }
-      j = p;
-      ++depth;
-    }
-    if (ok) key = depth * 256 + (255 - tid);
-  }
-  key = wave_max(key);
-  if (lane == 0) red_k[wave] = key;
-  __syncthreads();
-  key = red_k[0];
+    float v = -INFINITY;
+    int x = INT_MAX;
+    const size_t p0 = ((size_t)b * T + tid) * a.chunks;
+    for (int c0 = 0; c0 < a.chunks; c0 += 8) {
+      float pv[8];
+      int px[8];
 #pragma unroll
-  for (int w = 1; w < NW; ++w) key = max(key, red_k[w]);
+      for (int k = 0; k < 8; ++k) {
+        const size_t pp = p0 + min(c0 + k, a.chunks - 1);
+        pv[k] = load_coherent(a.part_val + pp);
+        px[k] = load_coherent(a.part_idx + pp);
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (c0 + k < a.chunks && better(pv[k], px[k], v, x)) { v = pv[k]; x = px[k]; }
+    }
+    am_s[tid] = x;
+    tok_s[tid] = tok_r;
+    par_s[tid] = par_r;
+  }
+  if (tid == 0) reset_counter(a.counters + b);   // ready for the next call
+  __syncthreads();
+  if (a.target_argmax && tid < T) a.target_argmax[(size_t)b * T + tid] = am_s[tid];
+  if (wave != 0) return;
 
-  const int last = 255 - (key & 255), alen = key >> 8;   // the root is always consistent: key >= 255
+  // Path scan, by wave 0 alone (lane l holds nodes l and l + 64): a sweep from the root, one depth per round.
+  // A node joins the consistent set when its draft equals the target's token at its parent and the parent
+  // joined the round before; the set lives in two 64-bit wave-uniform masks grown by ballots.  The last
+  // non-empty round holds the deepest consistent nodes: the smallest index among them is `last`, the number
+  // of rounds its depth.
+  int par_h[2];
+  bool ok_h[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = lane + 64 * h;
+    const int p = i < T ? par_s[i] : -1;
+    par_h[h] = p;
+    ok_h[h] = i > 0 && i < T && p >= 0 && p < i && tok_s[i] == am_s[p];
+  }
+  auto in_set = [](uint64_t s0, uint64_t s1, int x) {
+    return (((x < 64 ? s0 : s1) >> (x & 63)) & 1ull) != 0;
+  };
+  uint64_t c0 = 1, c1 = 0;      // the root is always consistent
+  uint64_t l0 = 1, l1 = 0;      // the last round's new members
+  int depth = 0;
+  while (true) {
+    const bool j0 = ok_h[0] && !in_set(c0, c1, lane) && in_set(c0, c1, par_h[0]);
+    const bool j1 = ok_h[1] && !in_set(c0, c1, lane + 64) && in_set(c0, c1, par_h[1]);
+    const uint64_t n0 = __ballot(j0), n1 = __ballot(j1);
+    if ((n0 | n1) == 0) break;
+    c0 |= n0;
+    c1 |= n1;
+    l0 = n0;
+    l1 = n1;
+    ++depth;
+  }
+  const int last = l0 ? __builtin_ctzll(l0) : 64 + __builtin_ctzll(l1);
+  const int alen = depth;
   int32_t* path = a.accept_path + (size_t)b * T;
-  if (tid == 0) {
+  if (lane == 0) {
     a.accept_len[b] = alen;
     a.next_token[b] = am_s[last];
-    int j = last;
-    for (int k = alen; k >= 0; --k) { path[k] = j; j = par_s[j]; }
-    reset_counter(seq_counter);  // ready for the next call
   }
-  if (tid > alen && tid < T) path[tid] = -1;
-  if (a.target_argmax && tid < T) a.target_argmax[(size_t)b * T + tid] = am_s[tid];
+  // the path from the root to `last`, read off the parents held in the lanes (uniform steps, no LDS)
+  int j = last;
+  for (int k = alen; k >= 0; --k) {
+    if (lane == 0) path[k] = j;
+    j = j < 64 ? __builtin_amdgcn_readlane(par_h[0], j) : __builtin_amdgcn_readlane(par_h[1], j - 64);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = lane + 64 * h;
+    if (i > alen && i < T) path[i] = -1;
+  }
 }
 
 }  // namespace
