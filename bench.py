@@ -231,6 +231,8 @@ def main():
     torch.cuda.synchronize()
     acc_us = a0.elapsed_time(a1) * 1e3 / (reps * R)
 
+    stream = stream_peak(torch, dev)
+
     kv_len = host.kv_len
     a_bytes = attn_bytes_per_layer(wl, kv_len)
     acc_b = accept_bytes(wl)
@@ -270,11 +272,41 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic)},
+        "stream_peak": dict(stream, attention_frac_of_read=round(attn_gbps / stream["read_GBps"], 4)),
     }
 
     if not (args.no_cpu_baseline or args.profile_only):
         result["cpu_baseline"], result["parity_spot_check"] = cpu_baseline(wl, sets[0], host, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def stream_peak(torch, dev):
+    """This box's plain streaming rates: the library's read-stream helper over 1 GiB (reads 1 GiB) and a 1 GiB
+    device copy (reads and writes 1 GiB), each the median of 10 launches timed with HIP events.  The reference
+    for the share of the measured peak that the attention call reaches, beside its share of the 8 TB/s figure."""
+    from paper_2606_00535_amd import dreams
+    n = 1 << 28
+    x = torch.ones(n, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    sink = torch.empty(dreams.STREAM_READ_SINK_WORDS, dtype=torch.int32, device=dev)
+    out = {}
+    for name, fn, nbytes in (("read_GBps", lambda: dreams.stream_read(x, sink), 4 * n),
+                             ("copy_GBps", lambda: y.copy_(x), 8 * n)):
+        fn()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(10):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        times.sort()
+        out[name] = round(nbytes / (times[len(times) // 2] * 1e-3) / 1e9, 1)
+    del x, y
+    torch.cuda.empty_cache()
+    return out
 
 
 def calibrate_traffic(torch, dev, sets, attention, R, wl, host):

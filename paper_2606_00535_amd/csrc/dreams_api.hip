@@ -332,6 +332,17 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
   return ok();
 }
 
+dreams_status_t dreams_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream) {
+  if (!src || !sink) return fail(DREAMS_ERR_INVALID_ARG, "src and sink must not be NULL");
+  if (!aligned(src, 16) || bytes % 16 != 0)
+    return fail(DREAMS_ERR_INVALID_ARG, "src must be 16-byte aligned and bytes a multiple of 16 (bytes = %zu)", bytes);
+  if (!aligned(sink, 4)) return fail(DREAMS_ERR_INVALID_ARG, "sink must be 4-byte aligned");
+  if (bytes == 0) return ok();
+  hipError_t e = launch_stream_read(src, bytes, sink, stream);
+  if (e != hipSuccess) return hip_fail(e, "stream read launch");
+  return ok();
+}
+
 dreams_status_t dreams_kv_commit(int32_t num_layers, int64_t layer_stride_elems, int32_t batch,
                                  int32_t num_kv_heads, int32_t head_dim, int32_t cache_capacity,
                                  dreams_dtype_t dtype, void* k_cache, void* v_cache, const int32_t* kv_len_in,

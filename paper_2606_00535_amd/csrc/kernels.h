@@ -111,4 +111,7 @@ struct CommitArgs {
 
 hipError_t launch_kv_commit(const CommitArgs& a, hipStream_t stream);
 
+// ------------------------------------------------------------------------------- stream read (measurement)
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream);
+
 }  // namespace dreams

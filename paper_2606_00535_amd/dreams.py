@@ -23,7 +23,7 @@ DREAMS_F32, DREAMS_BF16 = 0, 1
 EXPORTS = (
     "dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn", "dreams_tree_accept_workspace_size",
     "dreams_tree_accept", "dreams_kv_commit", "dreams_status_string", "dreams_last_error_message",
-    "dreams_check_tree_host",
+    "dreams_check_tree_host", "dreams_stream_read",
 )
 
 
@@ -69,9 +69,10 @@ def lib():
                 L.dreams_last_error_message.argtypes = []
                 L.dreams_last_error_message.restype = ctypes.c_char_p
                 L.dreams_check_tree_host.argtypes = [P, I32]
+                L.dreams_stream_read.argtypes = [P, SZ, P, P]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
-                          "dreams_check_tree_host"):
+                          "dreams_check_tree_host", "dreams_stream_read"):
                     getattr(L, f).restype = ctypes.c_int
                 _lib = L
     return _lib
@@ -270,3 +271,17 @@ def check_tree_host(parent) -> None:
     import numpy as np
     p = np.ascontiguousarray(parent, dtype=np.int32)
     _check(lib().dreams_check_tree_host(p.ctypes.data_as(ctypes.c_void_p), int(p.shape[0])))
+
+
+STREAM_READ_SINK_WORDS = 16384
+
+
+def stream_read(src: torch.Tensor, sink: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """dreams_stream_read: one plain read of every byte of `src` (a contiguous device tensor whose size is a
+    multiple of 16 bytes), for measuring read bandwidth.  Returns the sink words."""
+    if not src.is_contiguous():
+        raise ValueError("src must be contiguous")
+    if sink is None:
+        sink = torch.empty(STREAM_READ_SINK_WORDS, dtype=torch.int32, device=src.device)
+    _check(lib().dreams_stream_read(_ptr(src), src.numel() * src.element_size(), _ptr(sink), _stream(stream)))
+    return sink

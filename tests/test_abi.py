@@ -162,3 +162,11 @@ def test_status_strings(D):
     for s in (0, -1, -2, -3, -4):
         assert lib.dreams_status_string(s).decode().startswith("DREAMS_")
     assert b"unknown" in lib.dreams_status_string(42)
+
+
+def test_stream_read_rejects_bad_arguments(D):
+    lib = D.lib()
+    fake = ctypes.c_void_p(4096)   # never dereferenced: validation fails before any launch
+    assert lib.dreams_stream_read(fake, 17, fake, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_stream_read(ctypes.c_void_p(4100), 64, fake, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_stream_read(None, 64, fake, None) == D.DREAMS_ERR_INVALID_ARG

@@ -100,3 +100,16 @@ def test_full_step_llava7b_full_layers(dev):
             ot, lt = outs[li][0][b, :, last].float(), outs[li][1][b, :, last]
             assert float((od[0, :, 0].float() - ot).abs().max()) <= ATTN_TOL_BF16
             assert float((ld[0, :, 0] - lt).abs().max()) <= LSE_TOL
+
+
+@pytest.mark.gpu
+def test_stream_read_touches_every_word_once(dev):
+    # the XOR of the sink words is the XOR of every word read: each 16-byte piece is read exactly once
+    g = torch.Generator().manual_seed(3)
+    for n_words in (4, 4 * 1000, 4 * (1 << 20) + 4 * 77):
+        x = torch.randint(-2 ** 31, 2 ** 31 - 1, (n_words,), generator=g, dtype=torch.int64).to(torch.int32)
+        sink = dreams.stream_read(x.to(dev))
+        torch.cuda.synchronize()
+        want = int(np.bitwise_xor.reduce(x.numpy().view(np.uint32)))
+        got = int(np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32)))
+        assert got == want, n_words
