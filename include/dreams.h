@@ -190,14 +190,15 @@ const char* dreams_last_error_message(void);
 dreams_status_t dreams_check_tree_host(const int32_t* parent, int32_t num_nodes);
 
 /*
- * Measurement helper, not part of the method: reads `bytes` bytes at `src` once, with plain 16-byte loads spread
- * over every compute unit, and writes one word per wave to `sink` (DREAMS_STREAM_READ_SINK_WORDS words) so
+ * Measurement helper, not part of the method: reads `bytes` bytes at `src` once, with non-temporal 16-byte loads,
+ * one contiguous chunk per workgroup over every compute unit, and writes one word per wave to `sink`
+ * (DREAMS_STREAM_READ_SINK_WORDS words) so
  * that the loads cannot be elided.  Timed around, it gives the device's plain read bandwidth, the reference for
  * the share of the measured peak that the kernels above reach.
  *   src    device, 16-byte aligned; bytes a multiple of 16 (DREAMS_ERR_INVALID_ARG otherwise)
  *   sink   device, DREAMS_STREAM_READ_SINK_WORDS uint32 words (contents unspecified afterwards)
  */
-#define DREAMS_STREAM_READ_SINK_WORDS 16384
+#define DREAMS_STREAM_READ_SINK_WORDS 2048
 dreams_status_t dreams_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream);
 
 #ifdef __cplusplus

@@ -55,13 +55,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_void*)p; }
 
 // Wave-wide copies from global memory into LDS.  m0 (wave-uniform) is the LDS byte address of lane 0's
-// data; lane l's data lands at m0 + 16*l (dwordx4) or m0 + 4*l (dword).
+// data; lane l's data lands at m0 + 16*l (dwordx4) or m0 + 4*l (dword).  The 16-byte copies move data that
+// is read exactly once (queries, keys, values) and carry the non-temporal hint.
 __device__ __forceinline__ void copy16_to_lds(uint32_t m0, const void* src) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0), "v"(src) : "memory");
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(m0), "v"(src) : "memory");
 }
 // Same, addressed as a wave-uniform base plus a per-lane 32-bit byte offset.
 __device__ __forceinline__ void copy16_to_lds(uint32_t m0, const void* sbase, uint32_t voff) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(voff), "s"(sbase)
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(m0), "v"(voff), "s"(sbase)
                : "memory");
 }
 __device__ __forceinline__ void copy4_to_lds(uint32_t m0, const void* src) {

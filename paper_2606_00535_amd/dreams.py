@@ -273,7 +273,7 @@ def check_tree_host(parent) -> None:
     _check(lib().dreams_check_tree_host(p.ctypes.data_as(ctypes.c_void_p), int(p.shape[0])))
 
 
-STREAM_READ_SINK_WORDS = 16384
+STREAM_READ_SINK_WORDS = 2048
 
 
 def stream_read(src: torch.Tensor, sink: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
