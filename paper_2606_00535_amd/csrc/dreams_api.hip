@@ -69,6 +69,7 @@ constexpr size_t kMaxCounters = kCounterBytes / sizeof(uint32_t);
 struct AttnPlan {
   int G, rows_total, row_groups, units, splits;
   int rows_per_wg;   // query rows one workgroup owns
+  int merge_stride;  // words between the merge counters in the counter region; 0: separate merge kernel
   size_t acc_off, ml_off, bytes;
 };
 
@@ -102,7 +103,8 @@ dreams_status_t check_attn_desc(const dreams_attn_desc_t* d) {
   return DREAMS_OK;
 }
 
-dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
+// `launching`: also decide how the pieces are merged (which needs the device; the workspace size does not)
+dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p, bool launching) {
   dreams_status_t st = check_attn_desc(d);
   if (st != DREAMS_OK) return st;
   *p = AttnPlan{};
@@ -117,14 +119,20 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   const int max_len = d->max_kv_len > 0 ? d->max_kv_len : d->cache_capacity - d->num_nodes;
   const int n_keys = max_len + d->num_nodes;
   const int max_splits = (n_keys + kPieceMinKeys - 1) / kPieceMinKeys;
+  int cus = 0;
   int splits = d->num_splits;
   if (splits == 0) {
     // about one workgroup per compute unit (a workgroup holds most of a compute unit's LDS)
-    int cus = 0;
     st = device_cus(&cus);
     if (st != DREAMS_OK) return st;
     const long long wgs = (long long)p->units * p->row_groups;
     splits = (int)((cus + wgs / 2) / wgs);
+    // More workgroups than compute units: a last round of workgroups that fills less than half of the chip
+    // cannot keep the memory busy, so cut the key axis until it does (or the rounds come out whole).
+    if (wgs >= cus) {
+      splits = 1;
+      while (splits < 4 && (wgs * splits) % cus != 0 && (wgs * splits) % cus < cus / 2) ++splits;
+    }
   }
   if (splits > max_splits) splits = max_splits;
   if (splits > kAttnMaxSplits) splits = kAttnMaxSplits;
@@ -135,6 +143,21 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   if (splits > 1) {
     // partial results of the pieces, after the counter region every workspace starts with
     const size_t rows = (size_t)p->units * p->row_groups * splits * p->rows_per_wg;
+    // With more streaming workgroups than compute units, the pieces are merged in the same launch, where the
+    // merging overlaps the last round of streaming; with one round, a separate merge kernel is faster (its
+    // launch costs less than making every piece wait for its device-scope stores).  The merge in the launch
+    // takes two counters per (sequence, KV head, row group) in the counter region, each on a cache line of
+    // its own where there is room (atomics on one line serialise).
+    if (launching) {
+      if (cus == 0) {
+        st = device_cus(&cus);
+        if (st != DREAMS_OK) return st;
+      }
+      const long long sets = (long long)p->units * p->row_groups;
+      int stride = 32;
+      while (stride > 1 && 2 * sets * stride > (long long)kMaxCounters) stride >>= 1;
+      p->merge_stride = grid > cus && 2 * sets * stride <= (long long)kMaxCounters ? stride : 0;
+    }
     p->acc_off = kCounterBytes;
     p->ml_off = p->acc_off + align_up(rows * d->head_dim * sizeof(float), 256);
     p->bytes = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
@@ -215,7 +238,7 @@ extern "C" {
 dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t* desc, size_t* bytes) {
   if (!bytes) return fail(DREAMS_ERR_INVALID_ARG, "bytes is NULL");
   AttnPlan p;
-  dreams_status_t st = plan_attn(desc, &p);
+  dreams_status_t st = plan_attn(desc, &p, false);
   if (st != DREAMS_OK) return st;
   *bytes = p.bytes;
   return ok();
@@ -237,7 +260,7 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
       (tree_mask && !aligned(tree_mask, 8)))
     return fail(DREAMS_ERR_INVALID_ARG, "kv_len, parent, lse or tree_mask is misaligned");
   AttnPlan p;
-  st = plan_attn(desc, &p);
+  st = plan_attn(desc, &p, false);
   if (st != DREAMS_OK) return st;
   if (p.bytes > 0) {
     if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", p.bytes);
@@ -247,6 +270,8 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   }
   if (desc->dtype == DREAMS_F32 && (long long)desc->batch * desc->num_q_heads * desc->num_nodes > 0x7fffffffLL)
     return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  st = plan_attn(desc, &p, true);   // the same plan, plus how the pieces are merged
+  if (st != DREAMS_OK) return st;
 
   AttnArgs a{};
   a.q = q;
@@ -260,6 +285,8 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   char* ws = (char*)workspace;
   a.part_acc = p.bytes ? (float*)(ws + p.acc_off) : nullptr;
   a.part_ml = p.bytes ? (float*)(ws + p.ml_off) : nullptr;
+  a.merge_ctr = p.bytes && p.merge_stride ? (uint32_t*)ws : nullptr;
+  a.merge_stride = p.merge_stride;
   a.B = desc->batch;
   a.Hq = desc->num_q_heads;
   a.Hkv = desc->num_kv_heads;

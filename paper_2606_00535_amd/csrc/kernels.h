@@ -52,6 +52,12 @@ struct AttnArgs {
   float* lse;             // [B, Hq, T] or nullptr
   float* part_acc;        // [units * row_groups, splits, rows_per_wg, D]   (splits > 1 only)
   float* part_ml;         // [units * row_groups, splits, rows_per_wg, 2]
+  // Merge in the same launch (splits > 1): the workgroups past the first `stream_wgs` merge the pieces of a
+  // (sequence, KV head, row group) once its pieces have arrived at merge_ctr[set * merge_stride]; their own
+  // arrivals are counted at merge_ctr[(sets + set) * merge_stride].  nullptr: a separate merge kernel.
+  uint32_t* merge_ctr;
+  int merge_stride;       // words between consecutive counters
+  int stream_wgs;         // set by the launcher
   int B, Hq, Hkv, G, T, D, S_cap;
   int units;              // B * Hkv
   int rows_per_wg;        // query rows of one workgroup (64 or 128)

@@ -26,9 +26,12 @@
 //     k, k+KW, ...) and each wave owns 16*RB rows, so a wave's operand reads serve as many rows as possible;
 //     the groups' (max, sum, accumulator) states are merged through LDS at the end.
 //   * With several pieces per (sequence, KV head, row group), each workgroup writes its rows' (max, sum,
-//     accumulator) to the workspace and a second, small kernel merges the pieces in piece order (so the
-//     result does not depend on scheduling); the kernel boundary is what makes the partial results visible
-//     across XCDs, with no device-scope stores, fences or counters on the streaming kernel's path.
+//     accumulator) to the workspace and the pieces are merged in piece order (so the result does not depend
+//     on scheduling), in one of two ways:
+//       - one round of workgroups: a second, small kernel; the kernel boundary makes the partial results
+//         visible across XCDs, with no device-scope stores, fences or counters on the streaming path;
+//       - several rounds: extra workgroups at the end of the same launch, which wait for their set's pieces
+//         (device-scope stores, then one arrival per piece) and merge them while the last round streams.
 //   * Workgroup ids are remapped so that all workgroups of one (sequence, KV head) run on the same XCD
 //     (consecutive ids are dealt round-robin over the 8 XCDs): row groups reading the same keys share them
 //     in that XCD's L2.
@@ -98,6 +101,20 @@ __device__ __forceinline__ void barrier_lds() {
   asm volatile("" ::: "memory");
 }
 
+// Device-scope (sc1) accesses through a buffer resource over [base, base + bytes): coherent across the
+// XCDs' L2s, which the pieces' partial results need when the merge runs in the same launch.
+// (the buffer builtins take and return plain `vector_size` vectors: values cross to and from them by bit_cast
+// only, never by assignment)
+typedef uint32_t buf_b128 __attribute__((vector_size(16)));
+typedef uint32_t buf_b64 __attribute__((vector_size(8)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+constexpr int kDeviceScope = 16;   // sc1 bit of the buffer instructions' cache-policy operand
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// Bound on a merging workgroup's wait for the pieces (100 MHz real-time ticks): 0.2 s, far beyond any call.
+constexpr uint64_t kMergeWaitTicks = 20000000;
+
 // Row layout in LDS: rows of D bf16, unpadded; the 16-byte chunk c of row r sits at position c ^ swz(r),
 // which spreads the 16 rows one operand read touches over distinct banks.  The swizzle repeats every 16
 // rows.  A step slot holds 32 K rows then 32 V rows; the query rows use the same layout.
@@ -112,6 +129,98 @@ struct Rows {
   __device__ static __forceinline__ int swz(int r) { return (r / RPL) % CPR; }
   __device__ static __forceinline__ int off(int r, int c) { return r * ROW + ((c ^ swz(r)) << 4); }
 };
+
+// Merge of a set's pieces by workgroups of the streaming launch (the ones past a.stream_wgs), laid out like
+// the merge kernel below: each wave covers 64 / (D/4) rows at 4 columns per lane; a set takes
+// ceil(R / (W * those rows)) workgroups.  They are dispatched after every streaming workgroup, so the pieces
+// they wait for are already running or done and never wait themselves: the wait ends.  The pieces' rows are
+// read with device-scope loads after their arrival count is complete; the last merging workgroup of the set
+// clears both counters for the next call.
+template <int D, int W>
+__device__ __forceinline__ void merge_in_launch(const AttnArgs& a, int m) {
+  constexpr int CPT = 4;                // columns per lane
+  constexpr int TPR = D / CPT;          // lanes per row
+  constexpr int MR = 64 / TPR;          // rows per wave
+  constexpr int CH = 8;                 // pieces per batch of loads
+  const int R = a.rows_per_wg, S = a.splits;
+  const int MB = (R + W * MR - 1) / (W * MR);
+  const int sets = a.units * a.row_groups;
+  const int pset = m / MB, mb = m - pset * MB;
+  const int wave = threadIdx.x >> 6, t = threadIdx.x & 63;
+  const int r = (mb * W + wave) * MR + t / TPR, c0 = (t % TPR) * CPT;
+  uint32_t* arrive = a.merge_ctr + (size_t)pset * a.merge_stride;
+  uint32_t* done = a.merge_ctr + (size_t)(sets + pset) * a.merge_stride;
+
+  // wave 0 waits for the set's pieces; the others wait for wave 0
+  __shared__ int in_time_lds;
+  if (wave == 0) {
+    bool in_time = true;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    while (__hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)S) {
+      if (__builtin_amdgcn_s_memrealtime() - t0 > kMergeWaitTicks) {
+        in_time = false;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    if (t == 0) in_time_lds = in_time;
+  }
+  __syncthreads();
+  const bool in_time = in_time_lds != 0;
+  // This workgroup is done with the arrival counter: count it as done now, so that the atomic's round trip
+  // overlaps the loads below; the last workgroup of the set clears both counters at its end.
+  uint32_t done_before = 0;
+  if (threadIdx.x == 0) done_before = __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  if (r < R) {
+    const size_t row0 = (size_t)pset * S * R;   // the set's piece 0, row 0
+    const auto racc = buffer_rsrc(a.part_acc + row0 * D, (uint32_t)S * R * D * 4);
+    const auto rml = buffer_rsrc(a.part_ml + row0 * 2, (uint32_t)S * R * 8);
+    float M = -INFINITY, lsum = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < S; s0 += CH) {
+      float2 ml[CH];
+      f32x4 x[CH];
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        const int pr = min(s0 + k, S - 1) * R + r;
+        const f32x2 mlv = __builtin_bit_cast(f32x2, __builtin_amdgcn_raw_buffer_load_b64(rml, pr * 8, 0, kDeviceScope));
+        ml[k] = make_float2(mlv.x, mlv.y);
+        x[k] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(racc, (pr * D + c0) * 4, 0, kDeviceScope));
+      }
+      float Mn = M;
+#pragma unroll
+      for (int k = 0; k < CH; ++k)
+        if (s0 + k < S) Mn = fmaxf(Mn, ml[k].x);
+      const float scale_old = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
+      lsum *= scale_old;
+      acc *= scale_old;
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        const float w = (s0 + k >= S || ml[k].x == -INFINITY) ? 0.f : fast_exp2(ml[k].x - Mn);
+        lsum += w * ml[k].y;
+        acc += w * x[k];
+      }
+      M = Mn;
+    }
+    const int rg = pset % a.row_groups, u = pset / a.row_groups;
+    const int b = u / a.Hkv, g = u - b * a.Hkv;
+    const int row = rg * R + r;   // row within the KV head's G*T rows
+    if (row < a.G * a.T) {
+      const size_t orow = ((size_t)b * a.Hq + (size_t)g * a.G) * a.T + row;
+      const float inv = !in_time ? NAN : lsum > 0.f ? 1.0f / lsum : 0.f;
+      bf16x4 res;
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) res[e] = (__bf16)(acc[e] * inv);
+      *(bf16x4*)((__bf16*)a.out + orow * D + c0) = res;
+      if (a.lse && c0 == 0) a.lse[orow] = !in_time ? NAN : lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+    }
+  }
+  if (threadIdx.x == 0 && done_before == (uint32_t)MB - 1) {
+    reset_counter(done);
+    reset_counter(arrive);
+  }
+}
 
 template <int D, int RB, int KW, int W, int NST, bool PIPE>
 __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
@@ -136,6 +245,12 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots
   __shared__ uint64_t anc_lds[2 * kMaxNodes];
   __shared__ uint32_t meta_lds[4 * kMaxNodes];   // the sequence's parents or tree mask rows, as copied
+  __shared__ uint32_t stored_lds;                 // owner waves whose partial rows are stored (merge in launch)
+
+  if (a.merge_ctr && (int)blockIdx.x >= a.stream_wgs) {
+    merge_in_launch<D, W>(a, (int)blockIdx.x - a.stream_wgs);
+    return;
+  }
 
   // ---- work item
   const int n = blockIdx.x;
@@ -154,6 +269,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   const int rows_total = a.G * T;
   const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(ring));
   const int kv_len_b = a.kv_len[b];   // issued before the copies below, ahead of their traffic
+  if (tid == 0) stored_lds = 0;       // (published by the prologue's barriers)
 
   // ---- this workgroup's piece of the key axis, planned from the host's bound on the key count
   int piece = (a.max_keys + a.splits - 1) / a.splits;
@@ -556,10 +672,34 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     return;
   }
 
-  // ---- several pieces: write this piece's unnormalised rows and (max, sum) for the merge kernel (plain
-  // stores: the kernel boundary makes them visible to it)
+  // ---- several pieces: write this piece's unnormalised rows and (max, sum) for the merge
   if (!owner) return;
   const size_t pset = (size_t)u * a.row_groups + rg;
+  if (a.merge_ctr) {
+    // merged in this launch: device-scope stores, then one arrival per workgroup once every owner wave's
+    // stores have completed
+    const size_t row0 = pset * a.splits * R;
+    const auto racc = buffer_rsrc(a.part_acc + row0 * D, (uint32_t)a.splits * R * D * 4);
+    const auto rml = buffer_rsrc(a.part_ml + row0 * 2, (uint32_t)a.splits * R * 8);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int pr = split * R + rh * RW + rb * 16 + col;   // row within the set's pieces
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(buf_b128, o[rb][d]), racc, (pr * D + d * 16 + quad * 4) * 4, 0,
+                                               kDeviceScope);
+      if (quad == 0) {
+        const f32x2 mlv = {m_run[rb], l_run[rb]};
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(buf_b64, mlv), rml, pr * 8, 0, kDeviceScope);
+      }
+    }
+    wait_vector_memory();
+    if (lane == 0 &&
+        __hip_atomic_fetch_add(&stored_lds, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == (uint32_t)WR - 1)
+      __hip_atomic_fetch_add(a.merge_ctr + pset * a.merge_stride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  // separate merge kernel: plain stores, which the kernel boundary makes visible to it
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     const size_t pr = (pset * a.splits + split) * R + rh * RW + rb * 16 + col;
@@ -653,6 +793,15 @@ hipError_t launch(const AttnArgs& a, hipStream_t stream) {
   if (a.rows_per_wg != 16 * RB * (W / KW)) return hipErrorInvalidValue;
   const unsigned units_rounded = (a.units + 7) / 8 * 8;
   const unsigned grid = units_rounded * (unsigned)(a.splits * a.row_groups);
+  if (a.splits > 1 && a.merge_ctr) {
+    // the merging workgroups follow the streaming ones in the same launch
+    constexpr int MRW = W * merge_rows<D>();
+    const unsigned merge_wgs = (unsigned)(a.units * a.row_groups) * ((a.rows_per_wg + MRW - 1) / MRW);
+    AttnArgs b = a;
+    b.stream_wgs = (int)grid;
+    hipLaunchKernelGGL(kern, dim3(grid + merge_wgs), dim3(64 * W), lds, stream, b);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * W), lds, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;

@@ -128,6 +128,40 @@ def test_bf16_parity(dev, case, variant):
     check_bf16(out, lse, batch, 0, "bf16 %s %s" % (variant, case))
 
 
+# More streaming workgroups than the 256 compute units with several pieces each: the pieces are merged by
+# workgroups of the same launch (every row configuration that reaches that path at these sizes).
+FUSED_CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits): grid = 8*ceil(2*Hkv/8) * splits * row_groups
+    (128, 64, 64, 16, 4, 3, 400, 4),   # 16-row workgroups (4 waves): 512 workgroups
+    (64, 48, 48, 60, 6, 4, 700, 3),    # 64 rows, head_dim 64: 288
+    (128, 64, 32, 60, 6, 4, 600, 5),   # G=2, 128 rows: 320
+    (128, 84, 12, 128, 8, 6, 500, 3),  # G=7, 256-row workgroups, 4 row groups: 288
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=lambda c: "D%d_Hq%d_Hkv%d_T%d_L%d_S%d" % (c[0], c[1], c[2], c[3], c[6], c[7]))
+def test_merge_in_launch(dev, case):
+    D, Hq, Hkv, T, depth, br, L, splits = case
+    wl = small_wl(head_dim=D, num_q_heads=Hq, num_kv_heads=Hkv, num_nodes=T, depth=depth, max_branch=br, kv_len=L)
+    batch = W.make_batch(wl, with_logits=False, kv_lens=[L, max(0, L - 37)])
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    desc = dreams.attn_desc(q, k, num_splits=splits)
+    ws = torch.zeros(dreams.tree_verify_attn_workspace_size(desc), dtype=torch.uint8, device=dev)
+    note("merge in launch %s" % (case,))
+    ref = oracle_layer(batch, 0)
+    absref = oracle_layer(batch, 0, abs_v=True)[0]
+    first = None
+    for rep in range(3):
+        out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=splits, workspace=ws)
+        torch.cuda.synchronize()
+        cur = out.view(torch.int16).cpu().numpy()
+        if first is None:
+            check_bf16(out, lse, batch, 0, "merge in launch %s" % (case,), ref, absref)
+            first = cur
+        else:
+            assert np.array_equal(cur, first), rep   # same result on every call
+    assert not ws[:65536].cpu().numpy().any()       # counters left zero
+
+
 @pytest.mark.parametrize("scale", [-0.07, 0.0, 0.31])
 def test_scale_sign_and_zero(dev, scale):
     # the kernel folds |scale| into the exponent and flips the queries' sign for a negative scale
