@@ -65,7 +65,9 @@ class Oracle:
         lib.oracle_tree_attn_rows.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, P, I, P, P, P]
         lib.oracle_tree_accept.argtypes = [I, I, I, P, P, P, P, P, P, P]
         lib.oracle_kv_commit.argtypes = [I, ctypes.c_int64, I, I, I, I, I, P, P, P, P, P, I, P]
-        for f in (lib.oracle_tree_attn, lib.oracle_tree_attn_rows, lib.oracle_tree_accept, lib.oracle_kv_commit):
+        lib.oracle_tree_attn_entropy.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, P]
+        for f in (lib.oracle_tree_attn, lib.oracle_tree_attn_rows, lib.oracle_tree_accept, lib.oracle_kv_commit,
+                  lib.oracle_tree_attn_entropy):
             f.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
@@ -114,6 +116,21 @@ class Oracle:
                                             rows.shape[0], _p(rows), _p(out), _p(lse))
         _check(rc, "oracle_tree_attn_rows")
         return out, lse
+
+    def tree_attn_entropy(self, q, k_cache, kv_len, parent, scale: float, num_kv_heads: int, tree_mask=None):
+        """Attention entropy (nats) of every row, [B,Hq,T] float64: -sum_j A_ij log A_ij over the row's visible
+        slots (the per-row term of the paper's average attention entropy AE, Section 3.2)."""
+        q = _c(q, np.float32)
+        k_cache = _c(k_cache, np.float32)
+        B, Hq, T, D = q.shape
+        S_cap = k_cache.shape[2]
+        assert k_cache.shape == (B, num_kv_heads, S_cap, D)
+        ent = np.empty((B, Hq, T), dtype=np.float64)
+        rc = self.lib.oracle_tree_attn_entropy(B, Hq, num_kv_heads, T, D, S_cap, float(scale), _p(q), _p(k_cache),
+                                               _p(_c(kv_len, np.int32)), _p(_c(parent, np.int32)),
+                                               _p(_c(tree_mask, np.uint64)), _p(ent))
+        _check(rc, "oracle_tree_attn_entropy")
+        return ent
 
     def tree_accept(self, logits, tokens, parent):
         """Returns (accept_len [B], accept_path [B,T], next_token [B], target_argmax [B,T]), all int32."""
@@ -174,3 +191,31 @@ def tree_accept(*a, **kw):
 
 def kv_commit(*a, **kw):
     return default().kv_commit(*a, **kw)
+
+
+def tree_attn_entropy(*a, **kw):
+    return default().tree_attn_entropy(*a, **kw)
+
+
+def attn_entropy_mean(entropy) -> float:
+    """AE of one layer (Section 3.2): the mean of its rows' attention entropies (rows of every head and
+    sequence alike), summed in fp64."""
+    e = np.asarray(entropy, dtype=np.float64).ravel()
+    if e.size == 0:
+        raise OracleError("attn_entropy_mean of no rows")
+    return float(e.sum() / e.size)
+
+
+def attn_entropy_select(ae) -> int:
+    """The distillation layer of Section 3.2: the layer l minimising AE(l) + |AE(l) - AE(l-1)|.  Only layers
+    with a predecessor are candidates (the change is undefined for the first), so l runs over 1..NL-1; the
+    scores are formed in fp32 from fp32 AE values and ties go to the smallest l."""
+    ae = np.asarray(ae, dtype=np.float32).ravel()
+    if ae.size < 2:
+        raise OracleError("attn_entropy_select needs at least two layers")
+    best, best_score = -1, None
+    for l in range(1, ae.size):
+        score = np.float32(ae[l] + np.float32(abs(np.float32(ae[l] - ae[l - 1]))))
+        if best_score is None or score < best_score:
+            best, best_score = l, score
+    return best

@@ -30,6 +30,12 @@
  *  oracle_kv_commit
  *      Keeps the root and the accepted nodes' K/V as the next contiguous cache slots, in path order.
  *
+ *  oracle_tree_attn_entropy
+ *      Attention entropy of every verification row: -sum_j A_ij log A_ij over the row's attention
+ *      probabilities, the per-row quantity whose mean over rows and heads is the average attention entropy
+ *      AE of a layer (Section 3.2, "Adaptive Intermediate Feature Distillation").  Same masking and scores as
+ *      oracle_tree_attn; natural logarithm; a row with nothing visible has entropy 0.
+ *
  * Return value of every entry point: 0 on success, negative on invalid input (nothing written then).
  */
 #include <math.h>
@@ -160,6 +166,64 @@ int oracle_tree_attn_rows(int B, int Hq, int Hkv, int T, int D, int S_cap, doubl
                rows[3 * r + 2], out_rows + (size_t)r * D, &lse_r, visible, score);
       if (lse_rows) lse_rows[r] = lse_r;
     }
+    free(visible);
+    free(score);
+  }
+  return 0;
+}
+
+/* Entropy of one row (b, h, i): softmax of the visible scores (two passes), then -sum p log p. */
+static double entropy_row(int Hq, int Hkv, int T, int D, int S_cap, double scale, const float* q, const float* k,
+                          const int32_t* kv_len, const int32_t* parent, const uint64_t* tree_mask, int b, int h,
+                          int i, unsigned char* visible, double* score) {
+  const int G = Hq / Hkv;
+  const int g = h / G;
+  const int L = kv_len[b];
+  const int W = (T + 63) / 64;
+  const float* qi = q + (((size_t)b * Hq + h) * T + i) * D;
+  const float* kb = k + ((size_t)b * Hkv + g) * (size_t)S_cap * D;
+  visible_nodes(parent ? parent + (size_t)b * T : NULL,
+                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);
+  const int n = L + T;
+  double m = -INFINITY;
+  for (int s = 0; s < n; ++s) {
+    if (s >= L && !visible[s - L]) continue;
+    double dot = 0.0;
+    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];
+    score[s] = scale * dot;
+    if (score[s] > m) m = score[s];
+  }
+  if (m == -INFINITY) return 0.0;
+  double l = 0.0;
+  for (int s = 0; s < n; ++s) {
+    if (s >= L && !visible[s - L]) continue;
+    l += exp(score[s] - m);
+  }
+  double H = 0.0;
+  for (int s = 0; s < n; ++s) {
+    if (s >= L && !visible[s - L]) continue;
+    const double p = exp(score[s] - m) / l;   /* the row's attention probability of slot s */
+    if (p > 0.0) H -= p * log(p);
+  }
+  return H;
+}
+
+/* Layouts as for oracle_tree_attn (v is not needed); entropy [B,Hq,T]. */
+int oracle_tree_attn_entropy(int B, int Hq, int Hkv, int T, int D, int S_cap, double scale, const float* q,
+                             const float* k, const int32_t* kv_len, const int32_t* parent,
+                             const uint64_t* tree_mask, double* entropy) {
+  int rc = attn_args_ok(B, Hq, Hkv, T, D, S_cap, kv_len, parent, tree_mask);
+  if (rc) return rc;
+#pragma omp parallel
+  {
+    unsigned char* visible = (unsigned char*)malloc((size_t)T);
+    double* score = (double*)malloc(sizeof(double) * (size_t)(S_cap + 1));
+#pragma omp for collapse(2) schedule(dynamic)
+    for (int b = 0; b < B; ++b)
+      for (int h = 0; h < Hq; ++h)
+        for (int i = 0; i < T; ++i)
+          entropy[((size_t)b * Hq + h) * T + i] =
+              entropy_row(Hq, Hkv, T, D, S_cap, scale, q, k, kv_len, parent, tree_mask, b, h, i, visible, score);
     free(visible);
     free(score);
   }

@@ -495,4 +495,121 @@ def pin_commit_composition(orc):
 
 
 COMMIT_PINS = [pin_commit_gather, pin_commit_composition]
-ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS
+
+
+# ------------------------------------------------------------------------------------- attention entropy
+def _visible_counts(parent, L):
+    """Number of slots each node sees: the L prefix slots plus its ancestors-or-self."""
+    C = ancestor_closure(parent)
+    return L + C.sum(axis=1)
+
+
+def pin_entropy_uniform_is_log_count(orc):
+    """Equal keys make every visible score equal, so a row's attention is uniform over its n visible slots and
+    its entropy is exactly ln n (the maximum); prefix-free rows of a chain see depth+1 slots."""
+    rng = np.random.default_rng(41)
+    for L, T in ((0, 1), (0, 9), (13, 12), (40, 33)):
+        parent = W.random_tree(rng, T, max(1, min(5, T - 1)), 3)[None] if T > 1 else np.array([[-1]], np.int32)
+        q, k, _ = random_inputs(rng, 1, 4, 2, T, 8, L)
+        kc = np.broadcast_to(k[:, :, :1], k.shape).copy()
+        ent = orc.tree_attn_entropy(q, kc, np.array([L], np.int32), parent, 0.3, 2)
+        n = _visible_counts(parent[0], L)
+        for h in range(4):
+            assert np.max(np.abs(ent[0, h] - np.log(n))) <= 1e-12, (L, T, h)
+
+
+def pin_entropy_two_slots_closed_form(orc):
+    """A single node over one prefix slot sees two keys with score gap d: the binary entropy
+    H = ln(1 + e^-d) + d e^-d / (1 + e^-d) (written for d >= 0 by symmetry)."""
+    rng = np.random.default_rng(42)
+    for trial in range(20):
+        D = 8
+        q, k, _ = random_inputs(rng, 1, 1, 1, 1, D, 1)
+        q *= rng.uniform(0.1, 3.0)
+        scale = 0.5
+        ent = orc.tree_attn_entropy(q, k, np.array([1], np.int32), np.array([[-1]], np.int32), scale, 1)
+        qd, kd = q[0, 0, 0].astype(np.float64), k[0, 0].astype(np.float64)
+        d = abs(scale * (qd @ kd[1] - qd @ kd[0]))
+        H = np.log1p(np.exp(-d)) + d * np.exp(-d) / (1.0 + np.exp(-d))
+        assert abs(ent[0, 0, 0] - H) <= 1e-12, trial
+
+
+def pin_entropy_one_slot_is_zero(orc):
+    """A root with an empty prefix sees only itself: its attention is one-hot, entropy 0; a one-hot row also
+    results when one score dominates all others by far."""
+    rng = np.random.default_rng(43)
+    q, k, _ = random_inputs(rng, 2, 2, 1, 5, 8, 0)
+    parent = np.array([[-1, 0, 1, 2, 3]] * 2, np.int32)
+    ent = orc.tree_attn_entropy(q, k, np.array([0, 0], np.int32), parent, 0.25, 1)
+    assert np.all(ent[:, :, 0] == 0.0)
+    kb = k.copy()
+    kb[:, :, 3] = q[:, 0:1, 3] * 1000.0   # node 3's own key dominates its row
+    ent = orc.tree_attn_entropy(q[:, :1], kb, np.array([0, 0], np.int32), parent, 1.0, 1)
+    assert np.all(ent[:, 0, 3] <= 1e-200)
+
+
+def pin_entropy_bruteforce_and_bounds(orc):
+    """Dense masked softmax (closure-built mask, scipy logsumexp) then -sum p log p agrees to 1e-11; every
+    entropy lies in [0, ln n]; the values V play no part."""
+    rng = np.random.default_rng(44)
+    for trial in range(4):
+        B, Hq, Hkv, T, D = 2, 4, 2, int(rng.integers(1, 18)), 8
+        Ls = [int(rng.integers(0, 30)), int(rng.integers(0, 30))]
+        S = max(Ls) + T
+        q = rng.standard_normal((B, Hq, T, D)).astype(np.float32)
+        k = rng.standard_normal((B, Hkv, S, D)).astype(np.float32)
+        parent = np.stack([random_parent(rng, T) for _ in range(B)])
+        kv = np.array(Ls, np.int32)
+        ent = orc.tree_attn_entropy(q, k, kv, parent, 0.45, Hkv)
+        for b in range(B):
+            L = Ls[b]
+            C = ancestor_closure(parent[b])
+            vis = np.concatenate([np.ones((T, L), dtype=bool), C], axis=1)
+            n = vis.sum(axis=1)
+            for h in range(Hq):
+                sc = 0.45 * (q[b, h].astype(np.float64) @ k[b, h // (Hq // Hkv), :L + T].astype(np.float64).T)
+                sc[~vis] = -np.inf
+                logp = sc - logsumexp(sc, axis=1)[:, None]
+                H = -np.sum(np.where(vis, np.exp(logp) * np.where(vis, logp, 0.0), 0.0), axis=1)
+                assert np.max(np.abs(ent[b, h] - H)) <= 1e-11, (trial, b, h)
+                assert np.all(ent[b, h] >= -1e-15) and np.all(ent[b, h] <= np.log(n) + 1e-12)
+
+
+def pin_entropy_nonancestor_invariance(orc):
+    """A row's entropy ignores every key it cannot see: changing a non-ancestor tree key leaves it bitwise
+    unchanged, while changing an ancestor's key moves it."""
+    rng = np.random.default_rng(45)
+    L, T, D = 9, 15, 8
+    q, k, _ = random_inputs(rng, 1, 2, 2, T, D, L)
+    parent = W.random_tree(rng, T, 4, 3)[None]
+    kv = np.array([L], np.int32)
+    ent = orc.tree_attn_entropy(q, k, kv, parent, 0.5, 2)
+    C = ancestor_closure(parent[0])
+    for j in range(1, T):
+        k2 = k.copy()
+        k2[0, :, L + j] += 0.75
+        ent2 = orc.tree_attn_entropy(q, k2, kv, parent, 0.5, 2)
+        for i in range(T):
+            if C[i, j]:
+                assert np.all(ent2[0, :, i] != ent[0, :, i]), (i, j)
+            else:
+                assert np.array_equal(ent2[0, :, i], ent[0, :, i]), (i, j)
+
+
+def pin_entropy_layer_choice(orc):
+    """AE is the plain mean of the rows' entropies; the distillation layer minimises AE(l) + |AE(l) - AE(l-1)|
+    over the layers that have a predecessor, the first such layer on ties (hand-worked cases)."""
+    import oracle as O
+    assert O.attn_entropy_mean([[1.0, 2.0], [3.0, 6.0]]) == 3.0
+    # scores for l = 1..4: 4+1, 4.5+0.5, 1+3.5, 1.5+0.5 -> layer 4
+    assert O.attn_entropy_select([5.0, 4.0, 4.5, 1.0, 1.5]) == 4
+    # a flat profile: every score equals AE, the first candidate wins
+    assert O.attn_entropy_select([2.0, 2.0, 2.0]) == 1
+    # low entropy but a jump: layer 2 scores 0.5 + 3.5 = 4, layer 1 scores 4 + 0 = 4, tie -> 1
+    assert O.attn_entropy_select([4.0, 4.0, 0.5]) == 1
+    assert O.attn_entropy_select([3.0, 2.0]) == 1
+
+
+ENTROPY_PINS = [pin_entropy_uniform_is_log_count, pin_entropy_two_slots_closed_form, pin_entropy_one_slot_is_zero,
+                pin_entropy_bruteforce_and_bounds, pin_entropy_nonancestor_invariance, pin_entropy_layer_choice]
+ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS
