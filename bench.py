@@ -231,6 +231,29 @@ def main():
     torch.cuda.synchronize()
     acc_us = a0.elapsed_time(a1) * 1e3 / (reps * R)
 
+    # the attention call with every row's attention entropy as well (the layer-selection statistic), same method
+    ents = [torch.empty((B, Hq, T), dtype=torch.float32, device=dev) for _ in range(NL)]
+
+    def attention_entropy(st):
+        for l in range(NL):
+            dreams.tree_verify_attn_entropy(st["q"][l], st["k"][l], st["v"][l], st["kv"], st["par"],
+                                            out=st["out"][l], with_lse=False, entropy=ents[l],
+                                            max_kv_len=wl.max_kv_len, num_splits=args.num_splits,
+                                            workspace=ws_attn)
+
+    g_ent = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_ent):
+        for r in range(R):
+            attention_entropy(sets[r])
+    g_ent.replay()
+    torch.cuda.synchronize()
+    a0.record()
+    for _ in range(reps):
+        g_ent.replay()
+    a1.record()
+    torch.cuda.synchronize()
+    ent_us = a0.elapsed_time(a1) * 1e3 / (reps * R * NL)
+
     stream = stream_peak(torch, dev)
 
     kv_len = host.kv_len
@@ -269,6 +292,8 @@ def main():
                       "GBps": round(attn_gbps, 1), "splits": "auto" if splits_used == 0 else splits_used},
         "accept": {"us_per_launch": round(acc_us, 3), "bytes_per_launch": acc_b,
                    "GBps": round(acc_b / (acc_us * 1e-6) / 1e9, 1)},
+        "attention_entropy": {"us_per_launch": round(ent_us, 3), "bytes_per_launch": a_bytes + B * Hq * T * 4,
+                              "GBps": round((a_bytes + B * Hq * T * 4) / (ent_us * 1e-6) / 1e9, 1)},
         "roofline": {"bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic)},

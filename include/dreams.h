@@ -123,6 +123,39 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
                                         const uint64_t* tree_mask, void* out, float* lse, void* workspace,
                                         size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * dreams_tree_verify_attn_entropy -- dreams_tree_verify_attn, plus the attention entropy of every row: the
+ * per-row term of the average attention entropy AE(l) by which the paper's Section 3.2 ("Adaptive
+ * Intermediate Feature Distillation") ranks target layers.
+ *
+ *   entropy[b,h,i] = - sum_j A[j] ln A[j]   over the slots row (b,h,i) sees, A = its attention probabilities
+ *                    (natural log; 0 for a row with no visible slot)
+ *
+ * Arguments, layouts, workspace and errors as dreams_tree_verify_attn; entropy is device [B, Hq, T] float
+ * (required, 4-byte aligned).  The entropy is computed in the same pass over the keys as out and lse (one
+ * more fp32 sum per row next to the softmax denominator), from the fp32 probabilities before their bf16
+ * rounding.
+ */
+dreams_status_t dreams_tree_verify_attn_entropy(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                                const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                                const uint64_t* tree_mask, void* out, float* lse, float* entropy,
+                                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * dreams_attn_entropy_mean -- AE of one layer (Section 3.2): the mean of `count` >= 1 row entropies, e.g. the
+ * B*Hq*T values one dreams_tree_verify_attn_entropy call wrote (every head and sequence counts alike).
+ * entropy: device [count] float; ae: device, one float (out).  Summed in fp64 in a fixed order.
+ */
+dreams_status_t dreams_attn_entropy_mean(int64_t count, const float* entropy, float* ae, hipStream_t stream);
+
+/*
+ * dreams_attn_entropy_select -- the distillation layer of Section 3.2: the layer l minimising
+ * AE(l) + |AE(l) - AE(l-1)| (entropy plus its change from the layer below).  The change needs a
+ * predecessor, so the candidates are l = 1 .. num_layers-1 (num_layers >= 2); scores are fp32 and ties go to
+ * the smaller l.  ae: device [num_layers] float; best: device, one int32 (out).
+ */
+dreams_status_t dreams_attn_entropy_select(int32_t num_layers, const float* ae, int32_t* best, hipStream_t stream);
+
 /* Bytes of workspace dreams_tree_accept needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if batch
  * exceeds DREAMS_WORKSPACE_COUNTER_BYTES / 4 (one arrival counter per sequence, plus up to 8 group counters
  * per sequence while batch * 9 counters fit).  After the counters: one (value, index) pair per piece of each

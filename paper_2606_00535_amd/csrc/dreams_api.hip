@@ -70,7 +70,7 @@ struct AttnPlan {
   int G, rows_total, row_groups, units, splits;
   int rows_per_wg;   // query rows one workgroup owns
   int merge_stride;  // words between the merge counters in the counter region; 0: separate merge kernel
-  size_t acc_off, ml_off, bytes;
+  size_t acc_off, ml_off, e_off, bytes;
 };
 
 constexpr int kPieceMinKeys = 128;   // keys per piece of the key axis, at least
@@ -160,7 +160,8 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p, bool launchi
     }
     p->acc_off = kCounterBytes;
     p->ml_off = p->acc_off + align_up(rows * d->head_dim * sizeof(float), 256);
-    p->bytes = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
+    p->e_off = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
+    p->bytes = p->e_off + align_up(rows * sizeof(float), 256);
   }
   return DREAMS_OK;
 }
@@ -244,10 +245,14 @@ dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t*
   return ok();
 }
 
-dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
-                                        const void* v_cache, const int32_t* kv_len, const int32_t* parent,
-                                        const uint64_t* tree_mask, void* out, float* lse, void* workspace,
-                                        size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache, const void* v_cache,
+                            const int32_t* kv_len, const int32_t* parent, const uint64_t* tree_mask, void* out,
+                            float* lse, float* entropy, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
   dreams_status_t st = check_attn_desc(desc);
   if (st != DREAMS_OK) return st;
   if (desc->batch == 0) return ok();
@@ -282,9 +287,11 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   a.mask = tree_mask;
   a.out = out;
   a.lse = lse;
+  a.entropy = entropy;
   char* ws = (char*)workspace;
   a.part_acc = p.bytes ? (float*)(ws + p.acc_off) : nullptr;
   a.part_ml = p.bytes ? (float*)(ws + p.ml_off) : nullptr;
+  a.part_e = p.bytes ? (float*)(ws + p.e_off) : nullptr;
   a.merge_ctr = p.bytes && p.merge_stride ? (uint32_t*)ws : nullptr;
   a.merge_stride = p.merge_stride;
   a.B = desc->batch;
@@ -302,6 +309,46 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
   a.scale_log2 = desc->scale * 1.4426950408889634f;
   hipError_t e = desc->dtype == DREAMS_F32 ? launch_tree_attn_f32(a, stream) : launch_tree_attn_bf16(a, stream);
   if (e != hipSuccess) return hip_fail(e, "tree attention launch");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                        const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                        const uint64_t* tree_mask, void* out, float* lse, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  return verify_attn(desc, q, k_cache, v_cache, kv_len, parent, tree_mask, out, lse, nullptr, workspace,
+                     workspace_bytes, stream);
+}
+
+dreams_status_t dreams_tree_verify_attn_entropy(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                                const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                                const uint64_t* tree_mask, void* out, float* lse, float* entropy,
+                                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!entropy) return fail(DREAMS_ERR_INVALID_ARG, "entropy must not be NULL");
+  if (!aligned(entropy, 4)) return fail(DREAMS_ERR_INVALID_ARG, "entropy is misaligned");
+  return verify_attn(desc, q, k_cache, v_cache, kv_len, parent, tree_mask, out, lse, entropy, workspace,
+                     workspace_bytes, stream);
+}
+
+dreams_status_t dreams_attn_entropy_mean(int64_t count, const float* entropy, float* ae, hipStream_t stream) {
+  if (count < 1) return fail(DREAMS_ERR_INVALID_ARG, "count = %lld, at least 1 row is needed", (long long)count);
+  if (!entropy || !ae) return fail(DREAMS_ERR_INVALID_ARG, "entropy and ae must not be NULL");
+  if (!aligned(entropy, 4) || !aligned(ae, 4)) return fail(DREAMS_ERR_INVALID_ARG, "entropy or ae is misaligned");
+  hipError_t e = launch_attn_entropy_mean((long long)count, entropy, ae, stream);
+  if (e != hipSuccess) return hip_fail(e, "attention entropy mean launch");
+  return ok();
+}
+
+dreams_status_t dreams_attn_entropy_select(int32_t num_layers, const float* ae, int32_t* best, hipStream_t stream) {
+  if (num_layers < 2) return fail(DREAMS_ERR_INVALID_ARG, "num_layers = %d, at least 2 are needed", num_layers);
+  if (!ae || !best) return fail(DREAMS_ERR_INVALID_ARG, "ae and best must not be NULL");
+  if (!aligned(ae, 4) || !aligned(best, 4)) return fail(DREAMS_ERR_INVALID_ARG, "ae or best is misaligned");
+  hipError_t e = launch_attn_entropy_select(num_layers, ae, best, stream);
+  if (e != hipSuccess) return hip_fail(e, "attention entropy layer selection launch");
   return ok();
 }
 

@@ -50,8 +50,10 @@ struct AttnArgs {
   const uint64_t* mask;   // [B, T, ceil(T/64)] or nullptr
   void* out;              // [B, Hq, T, D]
   float* lse;             // [B, Hq, T] or nullptr
+  float* entropy;         // [B, Hq, T] attention entropy of every row (nats), or nullptr
   float* part_acc;        // [units * row_groups, splits, rows_per_wg, D]   (splits > 1 only)
   float* part_ml;         // [units * row_groups, splits, rows_per_wg, 2]
+  float* part_e;          // [units * row_groups, splits, rows_per_wg]   (entropy terms; with entropy only)
   // Merge in the same launch (splits > 1): the workgroups past the first `stream_wgs` merge the pieces of a
   // (sequence, KV head, row group) once its pieces have arrived at merge_ctr[set * merge_stride]; their own
   // arrivals are counted at merge_ctr[(sets + set) * merge_stride].  nullptr: a separate merge kernel.
@@ -71,6 +73,10 @@ struct AttnArgs {
 int tree_attn_bf16_rows_per_wg(int rows_total);
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
+
+// Layer AE: the mean of `count` row entropies; the distillation layer from per-layer AE values.
+hipError_t launch_attn_entropy_mean(long long count, const float* entropy, float* ae, hipStream_t stream);
+hipError_t launch_attn_entropy_select(int num_layers, const float* ae, int32_t* best, hipStream_t stream);
 
 // ---------------------------------------------------------------------------------------- acceptance
 constexpr int kAcceptThreads = 256;

@@ -54,6 +54,16 @@ constexpr float kLazyLog2 = 8.0f;  // slack of the running maximum, log2 units
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Attention entropy from a row's softmax state.  With scores z in log2 units, a reference m, l = sum 2^(z-m)
+// and e = sum 2^(z-m) (z-m), the row's probabilities are 2^(z-m)/l and its entropy (nats) is
+// ln2 * (log2 l - e/l).  Re-referencing a state to M (weight w = 2^(m-M)) turns e into w (e + (m-M) l).
+__device__ __forceinline__ float ent_term(float w, float e, float m, float M, float l) {
+  return w == 0.f ? 0.f : w * fmaf(m - M, l, e);
+}
+__device__ __forceinline__ float row_entropy(float l, float e) {
+  return l > 0.f ? 0.69314718055994530942f * (__log2f(l) - e / l) : 0.f;
+}
+
 typedef __attribute__((address_space(3))) void lds_void;
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_void*)p; }
 
@@ -136,7 +146,7 @@ struct Rows {
 // they wait for are already running or done and never wait themselves: the wait ends.  The pieces' rows are
 // read with device-scope loads after their arrival count is complete; the last merging workgroup of the set
 // clears both counters for the next call.
-template <int D, int W>
+template <int D, int W, bool ENT>
 __device__ __forceinline__ void merge_in_launch(const AttnArgs& a, int m) {
   constexpr int CPT = 4;                // columns per lane
   constexpr int TPR = D / CPT;          // lanes per row
@@ -176,28 +186,34 @@ __device__ __forceinline__ void merge_in_launch(const AttnArgs& a, int m) {
     const size_t row0 = (size_t)pset * S * R;   // the set's piece 0, row 0
     const auto racc = buffer_rsrc(a.part_acc + row0 * D, (uint32_t)S * R * D * 4);
     const auto rml = buffer_rsrc(a.part_ml + row0 * 2, (uint32_t)S * R * 8);
-    float M = -INFINITY, lsum = 0.f;
+    const auto re = buffer_rsrc(a.part_e + row0, (uint32_t)S * R * 4);
+    constexpr bool ent = ENT;
+    float M = -INFINITY, lsum = 0.f, esum = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s0 = 0; s0 < S; s0 += CH) {
       float2 ml[CH];
       f32x4 x[CH];
+      float ev[CH];
 #pragma unroll
       for (int k = 0; k < CH; ++k) {
         const int pr = min(s0 + k, S - 1) * R + r;
         const f32x2 mlv = __builtin_bit_cast(f32x2, __builtin_amdgcn_raw_buffer_load_b64(rml, pr * 8, 0, kDeviceScope));
         ml[k] = make_float2(mlv.x, mlv.y);
         x[k] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(racc, (pr * D + c0) * 4, 0, kDeviceScope));
+        ev[k] = ent ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(re, pr * 4, 0, kDeviceScope)) : 0.f;
       }
       float Mn = M;
 #pragma unroll
       for (int k = 0; k < CH; ++k)
         if (s0 + k < S) Mn = fmaxf(Mn, ml[k].x);
       const float scale_old = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
+      esum = ent_term(scale_old, esum, M, Mn, lsum);
       lsum *= scale_old;
       acc *= scale_old;
 #pragma unroll
       for (int k = 0; k < CH; ++k) {
         const float w = (s0 + k >= S || ml[k].x == -INFINITY) ? 0.f : fast_exp2(ml[k].x - Mn);
+        esum += ent_term(w, ev[k], ml[k].x, Mn, ml[k].y);
         lsum += w * ml[k].y;
         acc += w * x[k];
       }
@@ -214,6 +230,7 @@ __device__ __forceinline__ void merge_in_launch(const AttnArgs& a, int m) {
       for (int e = 0; e < CPT; ++e) res[e] = (__bf16)(acc[e] * inv);
       *(bf16x4*)((__bf16*)a.out + orow * D + c0) = res;
       if (a.lse && c0 == 0) a.lse[orow] = !in_time ? NAN : lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+      if (ent && c0 == 0) a.entropy[orow] = !in_time ? NAN : row_entropy(lsum, esum);
     }
   }
   if (threadIdx.x == 0 && done_before == (uint32_t)MB - 1) {
@@ -222,7 +239,7 @@ __device__ __forceinline__ void merge_in_launch(const AttnArgs& a, int m) {
   }
 }
 
-template <int D, int RB, int KW, int W, int NST, bool PIPE>
+template <int D, int RB, int KW, int W, int NST, bool PIPE, bool ENT>
 __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   constexpr int WR = W / KW;          // waves per key group; each owns a different slice of the rows
   constexpr int RW = 16 * RB;         // query rows per wave
@@ -240,7 +257,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   static_assert(CPS * W == 4 * KW * C16 && CPS >= 1 && (C16 % CPS == 0 || CPS % C16 == 0), "copy split");
   static_assert(16 * L::ROW == C16 * 1024 && (16 / L::RPL) % L::CPR == 0, "swizzle repeats every 16 rows");
   static_assert(NSS * CPS + ((QB + W - 1) / W) * C16 + 8 <= 63, "outstanding copies fit the counter");
-  static_assert((size_t)(KW - 1) * R * (D + 2) * 4 <= (size_t)NST * L::SLOT, "group states fit the ring");
+  static_assert((size_t)(KW - 1) * R * (D + 3) * 4 <= (size_t)NST * L::SLOT, "group states fit the ring");
 
   extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots
   __shared__ uint64_t anc_lds[2 * kMaxNodes];
@@ -248,7 +265,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   __shared__ uint32_t stored_lds;                 // owner waves whose partial rows are stored (merge in launch)
 
   if (a.merge_ctr && (int)blockIdx.x >= a.stream_wgs) {
-    merge_in_launch<D, W>(a, (int)blockIdx.x - a.stream_wgs);
+    merge_in_launch<D, W, ENT>(a, (int)blockIdx.x - a.stream_wgs);
     return;
   }
 
@@ -416,12 +433,14 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 
   f32x4 o[RB][DB];
   float m_run[RB], l_run[RB];
+  float e_run[RB];   // entropy term: sum of p * (z - m) over the keys so far (ENT only)
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
 #pragma unroll
     for (int d = 0; d < DB; ++d) o[rb][d] = f32x4{0.f, 0.f, 0.f, 0.f};
     m_run[rb] = -INFINITY;
     l_run[rb] = 0.f;
+    e_run[rb] = 0.f;
   }
 
   const int ka_row = (col & 3) * 4 + (col >> 2);       // A row m holds key kb*16 + (m%4)*4 + m/4
@@ -510,38 +529,54 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op.kf[kb][ds], qf[rb][ds], s[rb][kb], 0, 0, 0);
 
-    bf16x8 pb[RB];
+    // this lane's maximum over its 8 keys of each row, in scaled log2 units (c > 0 keeps the order)
+    float lmax[RB];
+    bool grow = false;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      // this lane's maximum over its 8 keys of the row, in scaled log2 units (c > 0 keeps the order)
-      const float lmax = c_scale * fmaxf(fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3])),
-                                         fmaxf(fmaxf(s[rb][1][0], s[rb][1][1]), fmaxf(s[rb][1][2], s[rb][1][3])));
-      // The reference maximum m only moves when some score exceeds it by more than 2^8 (the exponentials
-      // then stay <= 256, and softmax does not depend on the reference), which after the first steps is
-      // rare: in the common case no cross-lane reduction and no rescale happen at all.
-      if (__any(lmax > m_run[rb] + kLazyLog2)) {
-        float tmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+      lmax[rb] = c_scale * fmaxf(fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3])),
+                                 fmaxf(fmaxf(s[rb][1][0], s[rb][1][1]), fmaxf(s[rb][1][2], s[rb][1][3])));
+      grow |= lmax[rb] > m_run[rb] + kLazyLog2;
+    }
+    // The reference maximum m only moves when some score exceeds it by more than 2^8 (the exponentials then
+    // stay <= 256, and softmax does not depend on the reference), which after the first steps is rare: in
+    // the common case no cross-lane reduction and no rescale happen at all, and one branch covers every
+    // row block, so the exponentials and value products of all of them form one scheduling region.
+    if (__any(grow)) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        float tmax = fmaxf(lmax[rb], __shfl_xor(lmax[rb], 16));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
         if (tmax > m_run[rb] + kLazyLog2) {
           const float alpha = m_run[rb] == -INFINITY ? 0.f : fast_exp2(m_run[rb] - tmax);
+          // p * (z - m) with the new reference: each old term gains (m_old - m_new) before the rescale
+          if (ENT) e_run[rb] = alpha == 0.f ? 0.f : alpha * fmaf(m_run[rb] - tmax, l_run[rb], e_run[rb]);
           m_run[rb] = tmax;
           l_run[rb] *= alpha;
 #pragma unroll
           for (int d = 0; d < DB; ++d) o[rb][d] *= alpha;
         }
       }
+    }
+    bf16x8 pb[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
       const float m_use = m_run[rb] == -INFINITY ? 0.f : m_run[rb];
-      float psum = 0.f;
+      float psum = 0.f, esum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p = fast_exp2(fmaf(s[rb][kb][e], c_scale, -m_use));
+          const float t = fmaf(s[rb][kb][e], c_scale, -m_use);
+          const float p = fast_exp2(t);
           psum += p;
+          // (a masked key has t = -inf and p = 0; the clamp keeps its term 0 rather than NaN)
+          if (ENT) esum = fmaf(p, fmaxf(t, -1.0e4f), esum);
           pb[rb][kb * 4 + e] = (__bf16)p;
         }
       }
       l_run[rb] += psum;
+      if (ENT) e_run[rb] += esum;
     }
 
     // O^T[d][row] += sum over the 32 keys of V[key][d] P[row][key]
@@ -611,6 +646,10 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   for (int rb = 0; rb < RB; ++rb) {
     l_run[rb] += __shfl_xor(l_run[rb], 16);
     l_run[rb] += __shfl_xor(l_run[rb], 32);
+    if (ENT) {
+      e_run[rb] += __shfl_xor(e_run[rb], 16);
+      e_run[rb] += __shfl_xor(e_run[rb], 32);
+    }
   }
 
   // ---- key groups 1.. hand their states to group 0 through LDS (merged in group order)
@@ -620,13 +659,17 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     // so neither the writes nor the reads below conflict on banks
     f32x4* st_o = (f32x4*)ring;
     float2* st_ml = (float2*)(st_o + (KW - 1) * R * (D / 4));  // [KW-1][R]
+    float* st_e = (float*)(st_ml + (KW - 1) * R);                // [KW-1][R]
     if (kw > 0) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         const int row = (kw - 1) * R + rh * RW + rb * 16 + col;
 #pragma unroll
         for (int d = 0; d < DB; ++d) st_o[((kw - 1) * (D / 4) + d * 4 + quad) * R + rh * RW + rb * 16 + col] = o[rb][d];
-        if (quad == 0) st_ml[row] = make_float2(m_run[rb], l_run[rb]);
+        if (quad == 0) {
+          st_ml[row] = make_float2(m_run[rb], l_run[rb]);
+          if (ENT) st_e[row] = e_run[rb];
+        }
       }
     }
     barrier_lds();
@@ -640,6 +683,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
           const float M = fmaxf(m_run[rb], ml.x);
           const float w0 = m_run[rb] == -INFINITY ? 0.f : fast_exp2(m_run[rb] - M);
           const float w1 = ml.x == -INFINITY ? 0.f : fast_exp2(ml.x - M);
+          if (ENT) e_run[rb] = ent_term(w0, e_run[rb], m_run[rb], M, l_run[rb]) + ent_term(w1, st_e[row], ml.x, M, ml.y);
           m_run[rb] = M;
           l_run[rb] = l_run[rb] * w0 + ml.y * w1;
 #pragma unroll
@@ -668,6 +712,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
       }
       if (a.lse && quad == 0)
         a.lse[orow] = l_run[rb] > 0.f ? (m_run[rb] + __log2f(l_run[rb])) * kLn2 : -INFINITY;
+      if (ENT && quad == 0) a.entropy[orow] = row_entropy(l_run[rb], e_run[rb]);
     }
     return;
   }
@@ -681,6 +726,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     const size_t row0 = pset * a.splits * R;
     const auto racc = buffer_rsrc(a.part_acc + row0 * D, (uint32_t)a.splits * R * D * 4);
     const auto rml = buffer_rsrc(a.part_ml + row0 * 2, (uint32_t)a.splits * R * 8);
+    const auto re = buffer_rsrc(a.part_e + row0, (uint32_t)a.splits * R * 4);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int pr = split * R + rh * RW + rb * 16 + col;   // row within the set's pieces
@@ -691,6 +737,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
       if (quad == 0) {
         const f32x2 mlv = {m_run[rb], l_run[rb]};
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(buf_b64, mlv), rml, pr * 8, 0, kDeviceScope);
+        if (ENT) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, e_run[rb]), re, pr * 4, 0, kDeviceScope);
       }
     }
     wait_vector_memory();
@@ -705,7 +752,10 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     const size_t pr = (pset * a.splits + split) * R + rh * RW + rb * 16 + col;
 #pragma unroll
     for (int d = 0; d < DB; ++d) *(f32x4*)(a.part_acc + pr * D + d * 16 + quad * 4) = o[rb][d];
-    if (quad == 0) *(float2*)(a.part_ml + 2 * pr) = make_float2(m_run[rb], l_run[rb]);
+    if (quad == 0) {
+      *(float2*)(a.part_ml + 2 * pr) = make_float2(m_run[rb], l_run[rb]);
+      if (ENT) a.part_e[pr] = e_run[rb];
+    }
   }
 }
 
@@ -716,7 +766,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 // issued before any is used.
 template <int D>
 constexpr int merge_rows() { return 64 / (D / 4); }
-template <int D>
+template <int D, bool ENT>
 __global__ __launch_bounds__(64) void tree_attn_merge_kernel(AttnArgs a) {
   constexpr int CPT = 4;                // columns per thread
   constexpr int TPR = D / CPT;          // threads per row
@@ -742,27 +792,32 @@ __global__ __launch_bounds__(64) void tree_attn_merge_kernel(AttnArgs a) {
   const int S = a.splits;
   const size_t prow0 = (size_t)pset * S * R + r;  // this row in piece 0; piece s adds s * R
 
-  float M = -INFINITY, lsum = 0.f;
+  constexpr bool ent = ENT;
+  float M = -INFINITY, lsum = 0.f, esum = 0.f;
   fv acc = {};
   for (int s0 = 0; s0 < S; s0 += CH) {
     float2 ml[CH];
     fv x[CH];
+    float ev[CH];
 #pragma unroll
     for (int k = 0; k < CH; ++k) {
       const size_t pr = prow0 + (size_t)min(s0 + k, S - 1) * R;
       ml[k] = *(const float2*)(a.part_ml + 2 * pr);
       x[k] = *(const fv*)(a.part_acc + pr * D + c0);
+      ev[k] = ent ? a.part_e[pr] : 0.f;
     }
     float Mn = M;
 #pragma unroll
     for (int k = 0; k < CH; ++k)
       if (s0 + k < S) Mn = fmaxf(Mn, ml[k].x);
     const float scale_old = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
+    esum = ent_term(scale_old, esum, M, Mn, lsum);
     lsum *= scale_old;
     acc *= scale_old;
 #pragma unroll
     for (int k = 0; k < CH; ++k) {
       const float w = (s0 + k >= S || ml[k].x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml[k].x - Mn);
+      esum += ent_term(w, ev[k], ml[k].x, Mn, ml[k].y);
       lsum += w * ml[k].y;
       acc += w * x[k];
     }
@@ -776,14 +831,15 @@ __global__ __launch_bounds__(64) void tree_attn_merge_kernel(AttnArgs a) {
   for (int e = 0; e < CPT; ++e) res[e] = (__bf16)(acc[e] * inv);
   __builtin_memcpy((__bf16*)a.out + orow * D + c0, res, sizeof(res));
   if (a.lse && c0 == 0) a.lse[orow] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+  if (ent && c0 == 0) a.entropy[orow] = row_entropy(lsum, esum);
 }
 
-template <int D, int RB, int KW, int W, int NST>
-hipError_t launch(const AttnArgs& a, hipStream_t stream) {
+template <int D, int RB, int KW, int W, int NST, bool ENT>
+hipError_t launch_streaming(const AttnArgs& a, hipStream_t stream) {
   constexpr size_t lds = (size_t)NST * Rows<D>::SLOT;
   static_assert(lds + 2 * kMaxNodes * 8 + 4 * kMaxNodes * 4 + 64 <= 160 * 1024, "LDS budget");
   // two sets of operand registers fit beside one 16-row block's state, not beside two
-  auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST, RB == 1>;
+  auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST, RB == 1, ENT>;
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -806,8 +862,16 @@ hipError_t launch(const AttnArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   const unsigned mgrid = units_rounded * a.row_groups * (a.rows_per_wg / merge_rows<D>());
-  hipLaunchKernelGGL(tree_attn_merge_kernel<D>, dim3(mgrid), dim3(64), 0, stream, a);
+  auto merge = tree_attn_merge_kernel<D, ENT>;
+  hipLaunchKernelGGL(merge, dim3(mgrid), dim3(64), 0, stream, a);
   return hipGetLastError();
+}
+
+// Every configuration in two builds: with the entropy term (a.entropy given) and without (no extra work).
+template <int D, int RB, int KW, int W, int NST>
+hipError_t launch(const AttnArgs& a, hipStream_t stream) {
+  return a.entropy ? launch_streaming<D, RB, KW, W, NST, true>(a, stream)
+                   : launch_streaming<D, RB, KW, W, NST, false>(a, stream);
 }
 
 template <int D, int NST>

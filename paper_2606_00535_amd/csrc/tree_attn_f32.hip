@@ -3,7 +3,9 @@
 // One wave per output row (sequence b, query head h, node i).  Lane t visits keys t, t+64, ... of the
 // visible set, keeping its own online softmax (running max, running sum, D-wide accumulator) in fp32; the 64
 // per-lane states are then merged pairwise with the log-sum-exp identity (butterfly over lanes), so the
-// merge order is fixed and results are reproducible.
+// merge order is fixed and results are reproducible.  With an entropy output, each state also carries
+// e = sum 2^(x-m) (x-m) (scores x in log2 units), from which the row's attention entropy follows as
+// ln2 * (log2 l - e/l); re-referencing a state to M with weight w = 2^(m-M) turns e into w (e + (m-M) l).
 #include "kernels.h"
 
 #include <math.h>
@@ -12,6 +14,10 @@ namespace dreams {
 namespace {
 
 constexpr float kLn2 = 0.69314718055994530942f;
+
+__device__ __forceinline__ float ent_term(float w, float e, float m, float M, float l) {
+  return w == 0.f ? 0.f : w * fmaf(m - M, l, e);
+}
 
 template <int D>
 __global__ __launch_bounds__(64) void tree_attn_f32_kernel(AttnArgs a) {
@@ -50,7 +56,8 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(AttnArgs a) {
 
   const float* kb = (const float*)a.k + ((size_t)b * a.Hkv + g) * a.S_cap * D;
   const float* vb = (const float*)a.v + ((size_t)b * a.Hkv + g) * a.S_cap * D;
-  float m = -INFINITY, l = 0.f;
+  const bool ent = a.entropy != nullptr;
+  float m = -INFINITY, l = 0.f, e = 0.f;
   float acc[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) acc[d] = 0.f;
@@ -68,6 +75,7 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(AttnArgs a) {
     const float m_new = fmaxf(m, x);
     const float alpha = exp2f(m - m_new);
     const float p = exp2f(x - m_new);
+    if (ent) e = ent_term(l == 0.f ? 0.f : alpha, e, m, m_new, l) + p * (x - m_new);
     l = l * alpha + p;
     const float* vr = vb + (size_t)s * D;
 #pragma unroll
@@ -78,6 +86,7 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(AttnArgs a) {
   for (int off = 32; off >= 1; off >>= 1) {
     const float mo = __shfl_xor(m, off);
     const float lo = __shfl_xor(l, off);
+    const float eo = __shfl_xor(e, off);
     const float M = fmaxf(m, mo);
     const float w = M == -INFINITY ? 0.f : exp2f(m - M);
     const float wo = M == -INFINITY ? 0.f : exp2f(mo - M);
@@ -86,6 +95,7 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(AttnArgs a) {
       const float ao = __shfl_xor(acc[d], off);
       acc[d] = acc[d] * w + ao * wo;
     }
+    if (ent) e = ent_term(w, e, m, M, l) + ent_term(wo, eo, mo, M, lo);
     l = l * w + lo * wo;
     m = M;
   }
@@ -96,6 +106,7 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(AttnArgs a) {
   for (int d = 0; d < D; ++d)
     if ((d & 63) == lane) orow[d] = acc[d] * inv;
   if (a.lse && lane == 0) a.lse[r] = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
+  if (ent && lane == 0) a.entropy[r] = l > 0.f ? kLn2 * (log2f(l) - e / l) : 0.f;
 }
 
 }  // namespace

@@ -23,7 +23,8 @@ DREAMS_F32, DREAMS_BF16 = 0, 1
 EXPORTS = (
     "dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn", "dreams_tree_accept_workspace_size",
     "dreams_tree_accept", "dreams_kv_commit", "dreams_status_string", "dreams_last_error_message",
-    "dreams_check_tree_host", "dreams_stream_read",
+    "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy", "dreams_attn_entropy_mean",
+    "dreams_attn_entropy_select",
 )
 
 
@@ -70,9 +71,14 @@ def lib():
                 L.dreams_last_error_message.restype = ctypes.c_char_p
                 L.dreams_check_tree_host.argtypes = [P, I32]
                 L.dreams_stream_read.argtypes = [P, SZ, P, P]
+                L.dreams_tree_verify_attn_entropy.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, P, P, P, P, P, P,
+                                                              SZ, P]
+                L.dreams_attn_entropy_mean.argtypes = [ctypes.c_int64, P, P, P]
+                L.dreams_attn_entropy_select.argtypes = [I32, P, P, P]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
-                          "dreams_check_tree_host", "dreams_stream_read"):
+                          "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy",
+                          "dreams_attn_entropy_mean", "dreams_attn_entropy_select"):
                     getattr(L, f).restype = ctypes.c_int
                 _lib = L
     return _lib
@@ -150,6 +156,50 @@ def tree_verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     """dreams_tree_verify_attn.  q [B,Hq,T,D]; k_cache/v_cache [B,Hkv,S_cap,D] (bf16 or fp32, same as q);
     kv_len [B] int32; parent [B,T] int32 or tree_mask [B,T,ceil(T/64)] int64 (bit patterns).
     Returns (out [B,Hq,T,D], lse [B,Hq,T] float32 or None)."""
+    out, lse, _ = _verify_attn(q, k_cache, v_cache, kv_len, parent, tree_mask, scale, out, lse, with_lse,
+                               max_kv_len, num_splits, workspace, stream, None)
+    return out, lse
+
+
+def tree_verify_attn_entropy(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor,
+                             parent: Optional[torch.Tensor] = None, tree_mask: Optional[torch.Tensor] = None,
+                             scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                             lse: Optional[torch.Tensor] = None, with_lse: bool = True,
+                             entropy: Optional[torch.Tensor] = None, max_kv_len: int = 0, num_splits: int = 0,
+                             workspace: Optional[torch.Tensor] = None, stream=None):
+    """dreams_tree_verify_attn_entropy: as tree_verify_attn, plus every row's attention entropy (nats).
+    Returns (out, lse or None, entropy [B,Hq,T] float32)."""
+    B, Hq, T, _ = q.shape
+    if entropy is None:
+        entropy = torch.empty((B, Hq, T), dtype=torch.float32, device=q.device)
+    else:
+        _need(entropy, "entropy", torch.float32, q.device)
+        if tuple(entropy.shape) != (B, Hq, T):
+            raise ValueError("entropy must be [B, Hq, T]")
+    return _verify_attn(q, k_cache, v_cache, kv_len, parent, tree_mask, scale, out, lse, with_lse, max_kv_len,
+                        num_splits, workspace, stream, entropy)
+
+
+def attn_entropy_mean(entropy: torch.Tensor, ae: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """dreams_attn_entropy_mean: AE of one layer from its row entropies (any shape).  Returns a [1] float32."""
+    _need(entropy, "entropy", torch.float32, entropy.device)
+    if ae is None:
+        ae = torch.empty(1, dtype=torch.float32, device=entropy.device)
+    _check(lib().dreams_attn_entropy_mean(entropy.numel(), _ptr(entropy), _ptr(ae), _stream(stream)))
+    return ae
+
+
+def attn_entropy_select(ae: torch.Tensor, best: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """dreams_attn_entropy_select: the distillation layer from per-layer AE [NL].  Returns a [1] int32."""
+    _need(ae, "ae", torch.float32, ae.device, 1)
+    if best is None:
+        best = torch.empty(1, dtype=torch.int32, device=ae.device)
+    _check(lib().dreams_attn_entropy_select(ae.numel(), _ptr(ae), _ptr(best), _stream(stream)))
+    return best
+
+
+def _verify_attn(q, k_cache, v_cache, kv_len, parent, tree_mask, scale, out, lse, with_lse, max_kv_len, num_splits,
+                 workspace, stream, entropy):
     dt = q.dtype
     if dt not in (torch.bfloat16, torch.float32):
         raise TypeError("q must be bfloat16 or float32")
@@ -188,11 +238,16 @@ def tree_verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     nbytes = tree_verify_attn_workspace_size(desc)
     if workspace is None:
         workspace = _workspace("attn", nbytes, dev, st)
-    _check(lib().dreams_tree_verify_attn(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_len),
-                                         _ptr(parent), _ptr(tree_mask), _ptr(out), _ptr(lse), _ptr(workspace),
-                                         0 if workspace is None else workspace.numel() * workspace.element_size(),
-                                         st))
-    return out, lse
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if entropy is None:
+        _check(lib().dreams_tree_verify_attn(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kv_len),
+                                             _ptr(parent), _ptr(tree_mask), _ptr(out), _ptr(lse), _ptr(workspace),
+                                             ws_bytes, st))
+    else:
+        _check(lib().dreams_tree_verify_attn_entropy(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                                     _ptr(kv_len), _ptr(parent), _ptr(tree_mask), _ptr(out), _ptr(lse),
+                                                     _ptr(entropy), _ptr(workspace), ws_bytes, st))
+    return out, lse, entropy
 
 
 def tree_accept_workspace_size(batch: int, num_nodes: int, vocab: int) -> int:

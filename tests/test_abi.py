@@ -74,13 +74,14 @@ def test_attn_desc_rejected(D, kw, status):
 
 
 def test_attn_workspace_size_formula(D):
-    # explicit split count: no device query needed; partial accumulators + (m, l) + counters, 256-aligned
+    # explicit split count: no device query needed; counters, partial accumulators, (m, l) and the entropy
+    # terms, each 256-aligned
     desc = _desc(D, num_splits=8)
     st, n = _ws(D, desc)
     assert st == 0
     rows = 32 * 1 * 8 * 64
     up = lambda x: (x + 255) // 256 * 256
-    assert n == 65536 + up(rows * 128 * 4) + up(rows * 2 * 4)     # counters, accumulators, (m, l)
+    assert n == 65536 + up(rows * 128 * 4) + up(rows * 2 * 4) + up(rows * 4)
     assert D.lib().dreams_last_error_message().decode() == ""
     assert _ws(D, _desc(D, num_splits=1))[1] == 0
     assert _ws(D, _desc(D, dtype=D.DREAMS_F32, num_splits=4))[1] == 0
@@ -170,3 +171,20 @@ def test_stream_read_rejects_bad_arguments(D):
     assert lib.dreams_stream_read(fake, 17, fake, None) == D.DREAMS_ERR_INVALID_ARG
     assert lib.dreams_stream_read(ctypes.c_void_p(4100), 64, fake, None) == D.DREAMS_ERR_INVALID_ARG
     assert lib.dreams_stream_read(None, 64, fake, None) == D.DREAMS_ERR_INVALID_ARG
+
+
+def test_entropy_entry_points_reject_bad_arguments(D):
+    lib = D.lib()
+    fake = ctypes.c_void_p(0x100000)
+    desc = _desc(D, num_splits=1)
+    # the entropy output is required (before anything else is looked at)
+    assert lib.dreams_tree_verify_attn_entropy(ctypes.byref(desc), fake, fake, fake, fake, fake, None, fake, None,
+                                               None, None, 0, None) == D.DREAMS_ERR_INVALID_ARG
+    assert "entropy" in lib.dreams_last_error_message().decode()
+    assert lib.dreams_tree_verify_attn_entropy(ctypes.byref(desc), fake, fake, fake, fake, fake, None, fake, None,
+                                               ctypes.c_void_p(0x100002), None, 0, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_attn_entropy_mean(0, fake, fake, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_attn_entropy_mean(10, None, fake, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_attn_entropy_select(1, fake, fake, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_attn_entropy_select(4, fake, None, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_attn_entropy_select(4, ctypes.c_void_p(0x100001), fake, None) == D.DREAMS_ERR_INVALID_ARG
