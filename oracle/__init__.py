@@ -66,8 +66,12 @@ class Oracle:
         lib.oracle_tree_accept.argtypes = [I, I, I, P, P, P, P, P, P, P]
         lib.oracle_kv_commit.argtypes = [I, ctypes.c_int64, I, I, I, I, I, P, P, P, P, P, I, P]
         lib.oracle_tree_attn_entropy.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, P]
+        lib.oracle_visual_importance.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, I, I, P]
+        lib.oracle_visual_topk.argtypes = [I, I, I, P, P]
+        lib.oracle_visual_gather.argtypes = [I, I, I, I, I, P, P, I, P, I, P, P]
         for f in (lib.oracle_tree_attn, lib.oracle_tree_attn_rows, lib.oracle_tree_accept, lib.oracle_kv_commit,
-                  lib.oracle_tree_attn_entropy):
+                  lib.oracle_tree_attn_entropy, lib.oracle_visual_importance, lib.oracle_visual_topk,
+                  lib.oracle_visual_gather):
             f.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
@@ -132,6 +136,41 @@ class Oracle:
         _check(rc, "oracle_tree_attn_entropy")
         return ent
 
+    def visual_importance(self, q, k_cache, kv_len, parent, scale: float, num_kv_heads: int, vis_begin: int,
+                          vis_count: int, tree_mask=None):
+        """Importance of visual tokens vis_begin.. (Eq. 2, Section 3.1): [B, vis_count] float64."""
+        q = _c(q, np.float32)
+        k_cache = _c(k_cache, np.float32)
+        B, Hq, T, D = q.shape
+        S_cap = k_cache.shape[2]
+        assert k_cache.shape == (B, num_kv_heads, S_cap, D)
+        imp = np.empty((B, vis_count), dtype=np.float64)
+        rc = self.lib.oracle_visual_importance(B, Hq, num_kv_heads, T, D, S_cap, float(scale), _p(q), _p(k_cache),
+                                               _p(_c(kv_len, np.int32)), _p(_c(parent, np.int32)),
+                                               _p(_c(tree_mask, np.uint64)), int(vis_begin), int(vis_count), _p(imp))
+        _check(rc, "oracle_visual_importance")
+        return imp
+
+    def visual_topk(self, importance, r: int):
+        """Indices of the r most important tokens per sequence (ties: smaller index), increasing: [B, r]."""
+        imp = _c(importance, np.float32)
+        B, n = imp.shape
+        keep = np.empty((B, r), dtype=np.int32)
+        _check(self.lib.oracle_visual_topk(B, n, int(r), _p(imp), _p(keep)), "oracle_visual_topk")
+        return keep
+
+    def visual_gather(self, k_cache, v_cache, vis_begin: int, keep):
+        """k_cache/v_cache [B, Hkv, S_cap, D] (uint16 bf16 bits or float32) -> (k_out, v_out) [B, Hkv, r, D]."""
+        assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous and k_cache.shape == v_cache.shape
+        B, Hkv, S_cap, D = k_cache.shape
+        keep = _c(keep, np.int32)
+        r = keep.shape[1]
+        ko = np.empty((B, Hkv, r, D), dtype=k_cache.dtype)
+        vo = np.empty_like(ko)
+        _check(self.lib.oracle_visual_gather(B, Hkv, D, S_cap, k_cache.dtype.itemsize, _p(k_cache), _p(v_cache),
+                                             int(vis_begin), _p(keep), r, _p(ko), _p(vo)), "oracle_visual_gather")
+        return ko, vo
+
     def tree_accept(self, logits, tokens, parent):
         """Returns (accept_len [B], accept_path [B,T], next_token [B], target_argmax [B,T]), all int32."""
         logits = _c(logits, np.float32)
@@ -195,6 +234,18 @@ def kv_commit(*a, **kw):
 
 def tree_attn_entropy(*a, **kw):
     return default().tree_attn_entropy(*a, **kw)
+
+
+def visual_importance(*a, **kw):
+    return default().visual_importance(*a, **kw)
+
+
+def visual_topk(*a, **kw):
+    return default().visual_topk(*a, **kw)
+
+
+def visual_gather(*a, **kw):
+    return default().visual_gather(*a, **kw)
 
 
 def attn_entropy_mean(entropy) -> float:

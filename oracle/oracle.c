@@ -30,6 +30,12 @@
  *  oracle_kv_commit
  *      Keeps the root and the accepted nodes' K/V as the next contiguous cache slots, in path order.
  *
+ *  oracle_visual_importance / oracle_visual_topk / oracle_visual_gather
+ *      Target-aware visual-token selection (Section 3.1, "Visual Token Compression", Eq. 2): the importance of
+ *      visual token j is its attention weight averaged over every head and every query row of the call,
+ *      I_j = (1/(H*Q)) sum_h sum_i A[h,i,j]; the r most important tokens are kept (ties to the smaller
+ *      index), listed in increasing token order, and their K/V rows gathered into a compact cache.
+ *
  *  oracle_tree_attn_entropy
  *      Attention entropy of every verification row: -sum_j A_ij log A_ij over the row's attention
  *      probabilities, the per-row quantity whose mean over rows and heads is the average attention entropy
@@ -227,6 +233,105 @@ int oracle_tree_attn_entropy(int B, int Hq, int Hkv, int T, int D, int S_cap, do
     free(visible);
     free(score);
   }
+  return 0;
+}
+
+/*
+ * Visual-token importance.  The visual tokens are prefix slots vis_begin .. vis_begin+vis_count-1.  For every
+ * sequence b, query head h and row i, A[h,i,.] is that row's attention (the same visible slots and scores as
+ * oracle_tree_attn, softmax in two passes); importance[b][j] = sum over h, i of A[h,i,vis_begin+j], divided
+ * by Hq*T.  A visual slot outside sequence b's committed prefix (>= kv_len[b]) has importance 0.
+ */
+int oracle_visual_importance(int B, int Hq, int Hkv, int T, int D, int S_cap, double scale, const float* q,
+                             const float* k, const int32_t* kv_len, const int32_t* parent,
+                             const uint64_t* tree_mask, int vis_begin, int vis_count, double* importance) {
+  int rc = attn_args_ok(B, Hq, Hkv, T, D, S_cap, kv_len, parent, tree_mask);
+  if (rc) return rc;
+  if (vis_begin < 0 || vis_count < 1 || vis_begin + vis_count > S_cap) return ORACLE_BAD_ARG;
+  const int G = Hq / Hkv;
+  const int W = (T + 63) / 64;
+#pragma omp parallel for schedule(dynamic)
+  for (int b = 0; b < B; ++b) {
+    unsigned char* visible = (unsigned char*)malloc((size_t)T);
+    double* score = (double*)malloc(sizeof(double) * (size_t)(S_cap + 1));
+    double* imp = importance + (size_t)b * vis_count;
+    for (int j = 0; j < vis_count; ++j) imp[j] = 0.0;
+    const int L = kv_len[b];
+    const int n = L + T;
+    for (int h = 0; h < Hq; ++h) {
+      const int g = h / G;
+      const float* kb = k + ((size_t)b * Hkv + g) * (size_t)S_cap * D;
+      for (int i = 0; i < T; ++i) {
+        const float* qi = q + (((size_t)b * Hq + h) * T + i) * D;
+        visible_nodes(parent ? parent + (size_t)b * T : NULL,
+                      tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);
+        double m = -INFINITY;
+        for (int s = 0; s < n; ++s) {
+          if (s >= L && !visible[s - L]) continue;
+          double dot = 0.0;
+          for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];
+          score[s] = scale * dot;
+          if (score[s] > m) m = score[s];
+        }
+        if (m == -INFINITY) continue;   /* a row that sees nothing attends to no visual token */
+        double l = 0.0;
+        for (int s = 0; s < n; ++s) {
+          if (s >= L && !visible[s - L]) continue;
+          l += exp(score[s] - m);
+        }
+        for (int j = 0; j < vis_count; ++j) {
+          const int s = vis_begin + j;
+          if (s < L) imp[j] += exp(score[s] - m) / l;   /* A[h,i,s]; prefix slots are visible to every row */
+        }
+      }
+    }
+    for (int j = 0; j < vis_count; ++j) imp[j] /= (double)Hq * T;
+    free(visible);
+    free(score);
+  }
+  return 0;
+}
+
+/* The r largest of each sequence's vis_count importances (ties: the smaller index first), as token indices in
+ * increasing order: keep [B, r].  A plain selection by repeated maximum. */
+int oracle_visual_topk(int B, int vis_count, int r, const float* importance, int32_t* keep) {
+  if (B < 0 || vis_count < 1 || r < 1 || r > vis_count) return ORACLE_BAD_ARG;
+  unsigned char* taken = (unsigned char*)malloc((size_t)vis_count);
+  for (int b = 0; b < B; ++b) {
+    const float* v = importance + (size_t)b * vis_count;
+    memset(taken, 0, (size_t)vis_count);
+    for (int t = 0; t < r; ++t) {
+      int best = -1;
+      for (int j = 0; j < vis_count; ++j)
+        if (!taken[j] && (best < 0 || v[j] > v[best])) best = j;   /* first index among equal maxima */
+      taken[best] = 1;
+    }
+    int m = 0;
+    for (int j = 0; j < vis_count; ++j)
+      if (taken[j]) keep[(size_t)b * r + m++] = j;
+  }
+  free(taken);
+  return 0;
+}
+
+/* k_out/v_out [B, Hkv, r, D] (elem_bytes per element) receive the K/V rows of slots vis_begin + keep[b][m]. */
+int oracle_visual_gather(int B, int Hkv, int D, int S_cap, int elem_bytes, const void* k_cache, const void* v_cache,
+                         int vis_begin, const int32_t* keep, int r, void* k_out, void* v_out) {
+  if (B < 0 || Hkv < 1 || D < 1 || r < 1 || elem_bytes < 1) return ORACLE_BAD_ARG;
+  const size_t row = (size_t)D * elem_bytes;
+  for (int b = 0; b < B; ++b)
+    for (int m = 0; m < r; ++m) {
+      const int s = vis_begin + keep[(size_t)b * r + m];
+      if (s < 0 || s >= S_cap) return ORACLE_BAD_ARG;
+    }
+  for (int b = 0; b < B; ++b)
+    for (int g = 0; g < Hkv; ++g)
+      for (int m = 0; m < r; ++m) {
+        const size_t src = (((size_t)b * Hkv + g) * S_cap + vis_begin + keep[(size_t)b * r + m]) * row;
+        const size_t dst = (((size_t)b * Hkv + g) * r + m) * row;
+        memcpy((char*)k_out + dst, (const char*)k_cache + src, row);
+        memcpy((char*)v_out + dst, (const char*)v_cache + src, row);
+      }
   return 0;
 }
 

@@ -612,4 +612,93 @@ def pin_entropy_layer_choice(orc):
 
 ENTROPY_PINS = [pin_entropy_uniform_is_log_count, pin_entropy_two_slots_closed_form, pin_entropy_one_slot_is_zero,
                 pin_entropy_bruteforce_and_bounds, pin_entropy_nonancestor_invariance, pin_entropy_layer_choice]
-ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS
+
+
+# ---------------------------------------------------------------------------------- visual-token selection
+def pin_visual_bruteforce(orc):
+    """Column means of the dense masked softmax (closure-built mask, scipy logsumexp) over every head and row
+    agree to 1e-13 for any visual range, including one that runs past a sequence's prefix (those are 0)."""
+    rng = np.random.default_rng(51)
+    for trial in range(4):
+        B, Hq, Hkv, T, D = 2, 6, 3, int(rng.integers(1, 20)), 8
+        Ls = [int(rng.integers(5, 40)), int(rng.integers(5, 40))]
+        S = max(Ls) + T
+        q = rng.standard_normal((B, Hq, T, D)).astype(np.float32)
+        k = rng.standard_normal((B, Hkv, S, D)).astype(np.float32)
+        parent = np.stack([random_parent(rng, T) for _ in range(B)])
+        kv = np.array(Ls, np.int32)
+        v0 = int(rng.integers(0, 5))
+        nv = int(rng.integers(1, S - v0))
+        imp = orc.visual_importance(q, k, kv, parent, 0.6, Hkv, v0, nv)
+        for b in range(B):
+            L = Ls[b]
+            C = ancestor_closure(parent[b])
+            vis = np.concatenate([np.ones((T, L), dtype=bool), C], axis=1)
+            colsum = np.zeros(L + T)
+            for h in range(Hq):
+                sc = 0.6 * (q[b, h].astype(np.float64) @ k[b, h // (Hq // Hkv), :L + T].astype(np.float64).T)
+                sc[~vis] = -np.inf
+                colsum += np.exp(sc - logsumexp(sc, axis=1)[:, None]).sum(axis=0)
+            ref = np.zeros(nv)
+            for j in range(nv):
+                if v0 + j < L:
+                    ref[j] = colsum[v0 + j] / (Hq * T)
+            assert np.max(np.abs(imp[b] - ref)) <= 1e-13, (trial, b)
+
+
+def pin_visual_uniform_closed_form(orc):
+    """Equal keys: row i of every head spreads 1/n_i over its n_i visible slots, so a prefix token's
+    importance is the mean of 1/n_i over the rows (and 0 past the prefix)."""
+    rng = np.random.default_rng(52)
+    L, T = 30, 11
+    parent = W.random_tree(rng, T, 4, 3)[None]
+    q, k, _ = random_inputs(rng, 1, 4, 2, T, 8, L)
+    kc = np.broadcast_to(k[:, :, :1], k.shape).copy()
+    imp = orc.visual_importance(q, kc, np.array([L], np.int32), parent, 0.3, 2, 0, L + 5)
+    n = L + ancestor_closure(parent[0]).sum(axis=1)
+    assert np.max(np.abs(imp[0, :L] - np.mean(1.0 / n))) <= 1e-15
+    assert np.all(imp[0, L:] == 0.0)
+
+
+def pin_visual_mass_balance(orc):
+    """Over the whole prefix, the importances sum to one minus the mean attention mass on tree slots; that mass
+    is the attention output for values that are 1 on tree slots and 0 on prefix slots (the attention oracle,
+    an independent route)."""
+    rng = np.random.default_rng(53)
+    B, Hq, Hkv, T, D, L = 2, 4, 2, 13, 8, 17
+    q, k, _ = random_inputs(rng, B, Hq, Hkv, T, D, L)
+    q *= 2.0
+    parent = np.stack([W.random_tree(rng, T, 5, 3) for _ in range(B)])
+    kv = np.array([L, L], np.int32)
+    imp = orc.visual_importance(q, k, kv, parent, 0.5, Hkv, 0, L)
+    ind = np.zeros((B, Hkv, L + T, D), np.float32)
+    ind[:, :, L:] = 1.0
+    tree_mass, _ = orc.tree_attn(q, k, ind, kv, parent, 0.5, Hkv)
+    for b in range(B):
+        assert abs(imp[b].sum() - (1.0 - tree_mass[b, :, :, 0].mean())) <= 1e-13
+
+
+def pin_visual_topk_and_gather(orc):
+    """Top-r against a lexicographic sort (value descending, index ascending) on values with many exact ties,
+    r from 1 to all; the gather against numpy fancy indexing, bit for bit."""
+    rng = np.random.default_rng(54)
+    for trial in range(20):
+        B, n = 3, int(rng.integers(1, 60))
+        vals = (rng.integers(0, 6, size=(B, n)) / 4.0).astype(np.float32)
+        for r in sorted({1, n, int(rng.integers(1, n + 1))}):
+            keep = orc.visual_topk(vals, r)
+            for b in range(B):
+                order = np.lexsort((np.arange(n), -vals[b].astype(np.float64)))
+                assert np.array_equal(keep[b], np.sort(order[:r])), (trial, b, r)
+    B, Hkv, S, D, v0 = 2, 3, 40, 16, 4
+    kc = rng.integers(0, 65536, size=(B, Hkv, S, D), dtype=np.uint16)
+    vc = rng.integers(0, 65536, size=(B, Hkv, S, D), dtype=np.uint16)
+    keep = np.sort(np.stack([rng.choice(S - v0, 9, replace=False) for _ in range(B)]), axis=1).astype(np.int32)
+    ko, vo = orc.visual_gather(kc, vc, v0, keep)
+    for b in range(B):
+        assert np.array_equal(ko[b], kc[b][:, v0 + keep[b]]) and np.array_equal(vo[b], vc[b][:, v0 + keep[b]])
+
+
+VISUAL_PINS = [pin_visual_bruteforce, pin_visual_uniform_closed_form, pin_visual_mass_balance,
+               pin_visual_topk_and_gather]
+ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS + VISUAL_PINS

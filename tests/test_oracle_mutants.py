@@ -8,7 +8,7 @@ import pytest
 import oracle
 import pins
 
-ATTN, ACC, COM, ENT = "attn", "accept", "commit", "entropy"
+ATTN, ACC, COM, ENT, VIS = "attn", "accept", "commit", "entropy", "visual"
 MUTANTS = [
     ("drop_scale", ATTN, "score[s] = scale * dot;", "score[s] = dot;"),
     ("wrong_kv_head", ATTN, "const int g = h / G;", "const int g = h % Hkv;"),
@@ -40,6 +40,18 @@ MUTANTS = [
     ("commit_skips_v", COM, "memmove(vc + (size_t)(L + k) * row, vc + (size_t)(L + path[k]) * row, row);", ""),
     ("commit_drops_last", COM, "for (int k = 0; k <= accept_len[b]; ++k) {",
      "for (int k = 0; k < accept_len[b]; ++k) {"),
+    ("importance_no_row_norm", VIS, "if (s < L) imp[j] += exp(score[s] - m) / l;", "if (s < L) imp[j] += exp(score[s] - m);"),
+    ("importance_mean_over_heads_only", VIS, "for (int j = 0; j < vis_count; ++j) imp[j] /= (double)Hq * T;",
+     "for (int j = 0; j < vis_count; ++j) imp[j] /= (double)Hq;"),
+    ("importance_offset_ignored", VIS, "const int s = vis_begin + j;", "const int s = j;"),
+    ("importance_past_prefix", VIS, "if (s < L) imp[j] += exp(score[s] - m) / l;",
+     "if (s < n && (s < L || visible[s - L])) imp[j] += exp(score[s] - m) / l;"),
+    ("topk_ties_high", VIS, "if (!taken[j] && (best < 0 || v[j] > v[best])) best = j;",
+     "if (!taken[j] && (best < 0 || v[j] >= v[best])) best = j;"),
+    ("topk_smallest", VIS, "if (!taken[j] && (best < 0 || v[j] > v[best])) best = j;",
+     "if (!taken[j] && (best < 0 || v[j] < v[best])) best = j;"),
+    ("gather_without_offset", VIS, "const size_t src = (((size_t)b * Hkv + g) * S_cap + vis_begin + keep[(size_t)b * r + m]) * row;",
+     "const size_t src = (((size_t)b * Hkv + g) * S_cap + keep[(size_t)b * r + m]) * row;"),
     ("entropy_log2", ENT, "if (p > 0.0) H -= p * log(p);", "if (p > 0.0) H -= p * log2(p);"),
     ("entropy_unnormalised", ENT, "const double p = exp(score[s] - m) / l;", "const double p = exp(score[s] - m);"),
     ("entropy_sign", ENT, "if (p > 0.0) H -= p * log(p);", "if (p > 0.0) H += p * log(p);"),
@@ -48,7 +60,8 @@ MUTANTS = [
     ("entropy_self_hidden", ENT, "  visible_nodes(parent ? parent + (size_t)b * T : NULL,\n                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);\n  const int n = L + T;\n  double m = -INFINITY;\n  for (int s = 0; s < n; ++s) {\n    if (s >= L && !visible[s - L]) continue;\n    double dot = 0.0;\n    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];\n    score[s] = scale * dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;",
      "  visible_nodes(parent ? parent + (size_t)b * T : NULL,\n                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);\n  visible[i] = 0;\n  const int n = L + T;\n  double m = -INFINITY;\n  for (int s = 0; s < n; ++s) {\n    if (s >= L && !visible[s - L]) continue;\n    double dot = 0.0;\n    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];\n    score[s] = scale * dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;"),
 ]
-GROUPS = {ATTN: pins.ATTN_PINS, ACC: pins.ACCEPT_PINS, COM: pins.COMMIT_PINS, ENT: pins.ENTROPY_PINS}
+GROUPS = {ATTN: pins.ATTN_PINS, ACC: pins.ACCEPT_PINS, COM: pins.COMMIT_PINS, ENT: pins.ENTROPY_PINS,
+          VIS: pins.VISUAL_PINS}
 
 
 @pytest.mark.parametrize("name,group,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
