@@ -254,6 +254,50 @@ def main():
     torch.cuda.synchronize()
     ent_us = a0.elapsed_time(a1) * 1e3 / (reps * R * NL)
 
+    # target-aware visual-token selection on the same rows (Eq. 2 importance over the image tokens, keep one
+    # in five, gather their K/V): each verb alone, same method; the rows' lse comes from an attention call
+    vis = None
+    if wl.image_tokens > 0 and tdt == torch.bfloat16:
+        n_img, keep_r = wl.image_tokens, max(1, wl.image_tokens // 5)
+        for st in sets:
+            st["lse0"] = dreams.tree_verify_attn(st["q"][0], st["k"][0], st["v"][0], st["kv"], st["par"],
+                                                 max_kv_len=wl.max_kv_len, workspace=ws_attn)[1]
+            st["imp"] = torch.empty((B, n_img), dtype=torch.float32, device=dev)
+            st["keep"] = torch.empty((B, keep_r), dtype=torch.int32, device=dev)
+            st["ko"] = torch.empty((B, Hkv, keep_r, D), dtype=tdt, device=dev)
+            st["vo"] = torch.empty((B, Hkv, keep_r, D), dtype=tdt, device=dev)
+        vis_ws = torch.zeros(dreams.visual_importance_workspace_size(B, Hkv, n_img), dtype=torch.uint8, device=dev)
+        verbs = {
+            "importance": lambda st: dreams.visual_importance(st["q"][0], st["k"][0], st["kv"], st["lse0"], 0, n_img,
+                                                              importance=st["imp"], workspace=vis_ws),
+            "topk": lambda st: dreams.visual_topk(st["imp"], keep_r, keep=st["keep"]),
+            "gather": lambda st: dreams.visual_gather(st["k"][0], st["v"][0], 0, st["keep"], k_out=st["ko"],
+                                                      v_out=st["vo"]),
+        }
+        vis = {"image_tokens": n_img, "keep": keep_r}
+        for name in ("importance", "topk", "gather"):
+            for st in sets:
+                verbs[name](st)
+            torch.cuda.synchronize()
+            g_v = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_v):
+                for r in range(R):
+                    verbs[name](sets[r])
+            g_v.replay()
+            torch.cuda.synchronize()
+            a0.record()
+            for _ in range(reps):
+                g_v.replay()
+            a1.record()
+            torch.cuda.synchronize()
+            vis[name + "_us"] = round(a0.elapsed_time(a1) * 1e3 / (reps * R), 3)
+        # importance: the image tokens' keys, every query row and lse, the importances out
+        imp_bytes = B * Hkv * n_img * D * 2 + B * Hq * T * (D * 2 + 4) + B * n_img * 4
+        vis["importance_bytes"] = imp_bytes
+        vis["importance_GBps"] = round(imp_bytes / (vis["importance_us"] * 1e-6) / 1e9, 1)
+        gat_bytes = 2 * 2 * B * Hkv * keep_r * D * 2
+        vis["gather_GBps"] = round(gat_bytes / (vis["gather_us"] * 1e-6) / 1e9, 1)
+
     stream = stream_peak(torch, dev)
 
     kv_len = host.kv_len
@@ -292,6 +336,7 @@ def main():
                       "GBps": round(attn_gbps, 1), "splits": "auto" if splits_used == 0 else splits_used},
         "accept": {"us_per_launch": round(acc_us, 3), "bytes_per_launch": acc_b,
                    "GBps": round(acc_b / (acc_us * 1e-6) / 1e9, 1)},
+        "visual_select": vis,
         "attention_entropy": {"us_per_launch": round(ent_us, 3), "bytes_per_launch": a_bytes + B * Hq * T * 4,
                               "GBps": round((a_bytes + B * Hq * T * 4) / (ent_us * 1e-6) / 1e9, 1)},
         "roofline": {"bound": "hbm", "achieved": round(attn_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",

@@ -156,6 +156,50 @@ dreams_status_t dreams_attn_entropy_mean(int64_t count, const float* entropy, fl
  */
 dreams_status_t dreams_attn_entropy_select(int32_t num_layers, const float* ae, int32_t* best, hipStream_t stream);
 
+/*
+ * Target-aware visual-token selection (the paper's Section 3.1, "Visual Token Compression", Eq. 2).
+ *
+ * dreams_visual_importance -- the importance of visual token j (cache slot vis_begin + j of every sequence):
+ *   importance[b,j] = (1 / (Hq*T)) * sum over query heads h and rows i of A[b,h,i,vis_begin+j]
+ * where A[b,h,i,.] is row (b,h,i)'s attention as dreams_tree_verify_attn defines it (same desc, q, k_cache and
+ * kv_len; lse = that call's log-sum-exp output, [B, Hq, T]).  A visual slot at or past a sequence's prefix
+ * length has importance 0; a row whose lse is -inf contributes nothing.  bf16 only (DREAMS_ERR_UNSUPPORTED
+ * otherwise).  importance: device [B, vis_count] float (out).  Requires vis_begin >= 0, vis_count >= 1,
+ * vis_begin + vis_count <= cache_capacity and B * ceil(vis_count / 256) <= DREAMS_WORKSPACE_COUNTER_BYTES / 4
+ * (DREAMS_ERR_UNSUPPORTED otherwise).  workspace: device, 256-byte aligned, >=
+ * dreams_visual_importance_workspace_size bytes: the arrival-counter region every workspace starts with (see
+ * "Workspaces" above), then B*Hkv*vis_count floats of per-KV-head partial sums.  Arithmetic: bf16 products, fp32
+ * sums; the heads are summed in head order, so results are reproducible.
+ */
+dreams_status_t dreams_visual_importance_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t vis_count,
+                                                        size_t* bytes);
+dreams_status_t dreams_visual_importance(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                         const int32_t* kv_len, const float* lse, int32_t vis_begin,
+                                         int32_t vis_count, float* importance, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * dreams_visual_topk -- the keep_count most important visual tokens of every sequence: keep[b] lists them in
+ * increasing token order.  Ranking: larger importance first, the smaller token index among equal values
+ * (exact fp32 comparisons; importance must not hold NaN).  importance device [B, vis_count] float, with
+ * 1 <= vis_count <= DREAMS_VISUAL_MAX_TOKENS and 1 <= keep_count <= vis_count; keep device [B, keep_count] int32.
+ */
+#define DREAMS_VISUAL_MAX_TOKENS 8192
+dreams_status_t dreams_visual_topk(int32_t batch, int32_t vis_count, int32_t keep_count, const float* importance,
+                                   int32_t* keep, hipStream_t stream);
+
+/*
+ * dreams_visual_gather -- the kept tokens' K/V rows, for a cache that holds only them:
+ *   k_out[b,g,m,:] = k_cache[b,g,vis_begin + keep[b,m],:]   (same for v), bit for bit
+ * k_cache, v_cache device [B, Hkv, S_cap, D] of dtype; keep device [B, keep_count] int32 (as dreams_visual_topk
+ * writes it); k_out, v_out device [B, Hkv, keep_count, D].  head_dim * element size must be a multiple of 16.
+ * A kept token whose slot falls outside the cache leaves its output rows unwritten.
+ */
+dreams_status_t dreams_visual_gather(int32_t batch, int32_t num_kv_heads, int32_t head_dim, int32_t cache_capacity,
+                                     dreams_dtype_t dtype, const void* k_cache, const void* v_cache,
+                                     int32_t vis_begin, const int32_t* keep, int32_t keep_count, void* k_out,
+                                     void* v_out, hipStream_t stream);
+
 /* Bytes of workspace dreams_tree_accept needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if batch
  * exceeds DREAMS_WORKSPACE_COUNTER_BYTES / 4 (one arrival counter per sequence, plus up to 8 group counters
  * per sequence while batch * 9 counters fit).  After the counters: one (value, index) pair per piece of each

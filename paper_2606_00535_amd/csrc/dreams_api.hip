@@ -417,6 +417,134 @@ dreams_status_t dreams_stream_read(const void* src, size_t bytes, uint32_t* sink
   return ok();
 }
 
+static_assert(kVisualMaxTokens == DREAMS_VISUAL_MAX_TOKENS, "top-r capacity");
+
+// visual importance workspace: the fixed counter region every workspace starts with (one arrival counter per
+// (sequence, 256 tokens), on a cache line of its own where the region allows), then the per-KV-head partial
+// sums.  The region's size does not depend on the shape, so a workspace left zero by any call serves any other.
+size_t visual_workspace_bytes(int batch, int num_kv_heads, int vis_count) {
+  return kCounterBytes + (size_t)batch * num_kv_heads * vis_count * sizeof(float);
+}
+int visual_counter_stride(int batch, int vis_count) {   // 0: the counters do not fit
+  const long long n = (long long)batch * ((vis_count + 255) / 256);
+  int stride = kCounterStride;
+  while (stride > 1 && n * stride > (long long)kMaxCounters) stride >>= 1;
+  return n * stride <= (long long)kMaxCounters ? stride : 0;
+}
+
+dreams_status_t dreams_visual_importance_workspace_size(int32_t batch, int32_t num_kv_heads, int32_t vis_count,
+                                                        size_t* bytes) {
+  if (!bytes) return fail(DREAMS_ERR_INVALID_ARG, "bytes is NULL");
+  if (batch < 0 || num_kv_heads < 1 || vis_count < 1)
+    return fail(DREAMS_ERR_INVALID_ARG, "batch = %d, num_kv_heads = %d, vis_count = %d", batch, num_kv_heads,
+                vis_count);
+  *bytes = visual_workspace_bytes(batch, num_kv_heads, vis_count);
+  return ok();
+}
+
+dreams_status_t dreams_visual_importance(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                         const int32_t* kv_len, const float* lse, int32_t vis_begin,
+                                         int32_t vis_count, float* importance, void* workspace,
+                                         size_t workspace_bytes, hipStream_t stream) {
+  dreams_status_t st = check_attn_desc(desc);
+  if (st != DREAMS_OK) return st;
+  if (desc->dtype != DREAMS_BF16) return fail(DREAMS_ERR_UNSUPPORTED, "visual importance takes bf16 q and k_cache");
+  if (vis_begin < 0 || vis_count < 1 || (long long)vis_begin + vis_count > desc->cache_capacity)
+    return fail(DREAMS_ERR_INVALID_ARG, "visual tokens [%d, %d + %d) are not inside the cache (capacity %d)",
+                vis_begin, vis_begin, vis_count, desc->cache_capacity);
+  const size_t need = visual_workspace_bytes(desc->batch, desc->num_kv_heads, vis_count);
+  if (desc->batch == 0) return ok();
+  if (!q || !k_cache || !kv_len || !lse || !importance)
+    return fail(DREAMS_ERR_INVALID_ARG, "q, k_cache, kv_len, lse and importance must not be NULL");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(kv_len, 4) || !aligned(lse, 4) || !aligned(importance, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "q and k_cache must be 16-byte aligned, kv_len, lse and importance 4-byte");
+  if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+  if (workspace_bytes < need)
+    return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, need);
+  if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if ((long long)desc->batch * desc->num_kv_heads * ((vis_count + 63) / 64) > 0x7fffffffLL)
+    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  const int stride = visual_counter_stride(desc->batch, vis_count);
+  if (stride == 0)
+    return fail(DREAMS_ERR_UNSUPPORTED, "batch * ceil(vis_count / 256) = %lld exceeds %zu arrival counters",
+                (long long)desc->batch * ((vis_count + 255) / 256), kMaxCounters);
+  VisualArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.kv_len = kv_len;
+  a.lse = lse;
+  a.counters = (uint32_t*)workspace;
+  a.counter_stride = stride;
+  a.partial = (float*)((char*)workspace + kCounterBytes);
+  a.importance = importance;
+  a.B = desc->batch;
+  a.Hq = desc->num_q_heads;
+  a.Hkv = desc->num_kv_heads;
+  a.G = desc->num_q_heads / desc->num_kv_heads;
+  a.T = desc->num_nodes;
+  a.D = desc->head_dim;
+  a.S_cap = desc->cache_capacity;
+  a.vis_begin = vis_begin;
+  a.vis_count = vis_count;
+  a.scale_log2 = desc->scale * 1.4426950408889634f;
+  hipError_t e = launch_visual_importance(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "visual importance launch");
+  return ok();
+}
+
+dreams_status_t dreams_visual_topk(int32_t batch, int32_t vis_count, int32_t keep_count, const float* importance,
+                                   int32_t* keep, hipStream_t stream) {
+  if (batch < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", batch);
+  if (vis_count < 1 || vis_count > kVisualMaxTokens)
+    return fail(DREAMS_ERR_UNSUPPORTED, "vis_count = %d outside [1, %d]", vis_count, kVisualMaxTokens);
+  if (keep_count < 1 || keep_count > vis_count)
+    return fail(DREAMS_ERR_INVALID_ARG, "keep_count = %d outside [1, vis_count = %d]", keep_count, vis_count);
+  if (batch == 0) return ok();
+  if (!importance || !keep) return fail(DREAMS_ERR_INVALID_ARG, "importance and keep must not be NULL");
+  if (!aligned(importance, 4) || !aligned(keep, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "importance and keep must be 4-byte aligned");
+  hipError_t e = launch_visual_topk(batch, vis_count, keep_count, importance, keep, stream);
+  if (e != hipSuccess) return hip_fail(e, "visual top-r launch");
+  return ok();
+}
+
+dreams_status_t dreams_visual_gather(int32_t batch, int32_t num_kv_heads, int32_t head_dim, int32_t cache_capacity,
+                                     dreams_dtype_t dtype, const void* k_cache, const void* v_cache,
+                                     int32_t vis_begin, const int32_t* keep, int32_t keep_count, void* k_out,
+                                     void* v_out, hipStream_t stream) {
+  if (batch < 0 || num_kv_heads < 1 || head_dim < 1 || cache_capacity < 1 || keep_count < 1 || vis_begin < 0)
+    return fail(DREAMS_ERR_INVALID_ARG, "batch >= 0, num_kv_heads, head_dim, cache_capacity, keep_count >= 1 and "
+                                        "vis_begin >= 0 are required");
+  if (dtype != DREAMS_BF16 && dtype != DREAMS_F32)
+    return fail(DREAMS_ERR_INVALID_ARG, "dtype = %d is not DREAMS_BF16 or DREAMS_F32", (int)dtype);
+  const long long row_bytes = (long long)head_dim * (dtype == DREAMS_BF16 ? 2 : 4);
+  if (row_bytes % 16 != 0 || row_bytes > (1 << 20))
+    return fail(DREAMS_ERR_UNSUPPORTED, "head_dim * element size = %lld bytes (must be a multiple of 16)", row_bytes);
+  if (batch == 0) return ok();
+  if (!k_cache || !v_cache || !keep || !k_out || !v_out)
+    return fail(DREAMS_ERR_INVALID_ARG, "cache, keep and output pointers must not be NULL");
+  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(k_out, 16) || !aligned(v_out, 16) ||
+      !aligned(keep, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "caches and outputs must be 16-byte aligned, keep 4-byte");
+  if ((long long)batch * num_kv_heads > 0x7fffffffLL || (long long)keep_count * (row_bytes / 16) / 256 > 65535)
+    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  VisualGatherArgs a{};
+  a.k = k_cache;
+  a.v = v_cache;
+  a.keep = keep;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.B = batch;
+  a.Hkv = num_kv_heads;
+  a.S_cap = cache_capacity;
+  a.r = keep_count;
+  a.vis_begin = vis_begin;
+  a.row_bytes = (int)row_bytes;
+  hipError_t e = launch_visual_gather(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "visual gather launch");
+  return ok();
+}
+
 dreams_status_t dreams_kv_commit(int32_t num_layers, int64_t layer_stride_elems, int32_t batch,
                                  int32_t num_kv_heads, int32_t head_dim, int32_t cache_capacity,
                                  dreams_dtype_t dtype, void* k_cache, void* v_cache, const int32_t* kv_len_in,

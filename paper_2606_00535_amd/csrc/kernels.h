@@ -74,6 +74,36 @@ int tree_attn_bf16_rows_per_wg(int rows_total);
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
 
+// ------------------------------------------------------------------------------- visual-token selection
+constexpr int kCounterStride = 32;   // words between arrival counters that many workgroups hit (own cache line)
+constexpr int kVisualMaxTokens = 8192;   // visual tokens per sequence the top-r sort holds (LDS)
+
+struct VisualArgs {
+  const void* q;          // [B, Hq, T, D] bf16
+  const void* k;          // [B, Hkv, S_cap, D] bf16
+  const int32_t* kv_len;  // [B]
+  const float* lse;       // [B, Hq, T] natural log-sum-exp of every row (from the attention call)
+  float* partial;         // [B, Hkv, vis_count] workspace
+  uint32_t* counters;     // [B, ceil(vis_count / 256)] arrival counters, counter_stride words apart (zero)
+  int counter_stride;
+  float* importance;      // [B, vis_count]
+  int B, Hq, Hkv, G, T, D, S_cap;
+  int vis_begin, vis_count;
+  float scale_log2;       // scale * log2(e)
+};
+struct VisualGatherArgs {
+  const void* k;
+  const void* v;          // [B, Hkv, S_cap, D]
+  const int32_t* keep;    // [B, r]
+  void* k_out;
+  void* v_out;            // [B, Hkv, r, D]
+  int B, Hkv, S_cap, r, vis_begin;
+  int row_bytes;          // D * element size, a multiple of 16
+};
+hipError_t launch_visual_importance(const VisualArgs& a, hipStream_t stream);
+hipError_t launch_visual_topk(int B, int n, int r, const float* importance, int32_t* keep, hipStream_t stream);
+hipError_t launch_visual_gather(const VisualGatherArgs& a, hipStream_t stream);
+
 // Layer AE: the mean of `count` row entropies; the distillation layer from per-layer AE values.
 hipError_t launch_attn_entropy_mean(long long count, const float* entropy, float* ae, hipStream_t stream);
 hipError_t launch_attn_entropy_select(int num_layers, const float* ae, int32_t* best, hipStream_t stream);

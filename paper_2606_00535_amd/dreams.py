@@ -24,7 +24,8 @@ EXPORTS = (
     "dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn", "dreams_tree_accept_workspace_size",
     "dreams_tree_accept", "dreams_kv_commit", "dreams_status_string", "dreams_last_error_message",
     "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy", "dreams_attn_entropy_mean",
-    "dreams_attn_entropy_select",
+    "dreams_attn_entropy_select", "dreams_visual_importance_workspace_size", "dreams_visual_importance",
+    "dreams_visual_topk", "dreams_visual_gather",
 )
 
 
@@ -75,10 +76,16 @@ def lib():
                                                               SZ, P]
                 L.dreams_attn_entropy_mean.argtypes = [ctypes.c_int64, P, P, P]
                 L.dreams_attn_entropy_select.argtypes = [I32, P, P, P]
+                L.dreams_visual_importance_workspace_size.argtypes = [I32, I32, I32, ctypes.POINTER(SZ)]
+                L.dreams_visual_importance.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, I32, I32, P, P, SZ, P]
+                L.dreams_visual_topk.argtypes = [I32, I32, I32, P, P, P]
+                L.dreams_visual_gather.argtypes = [I32, I32, I32, I32, ctypes.c_int, P, P, I32, P, I32, P, P, P]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
                           "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy",
-                          "dreams_attn_entropy_mean", "dreams_attn_entropy_select"):
+                          "dreams_attn_entropy_mean", "dreams_attn_entropy_select",
+                          "dreams_visual_importance_workspace_size", "dreams_visual_importance", "dreams_visual_topk",
+                          "dreams_visual_gather"):
                     getattr(L, f).restype = ctypes.c_int
                 _lib = L
     return _lib
@@ -196,6 +203,76 @@ def attn_entropy_select(ae: torch.Tensor, best: Optional[torch.Tensor] = None, s
         best = torch.empty(1, dtype=torch.int32, device=ae.device)
     _check(lib().dreams_attn_entropy_select(ae.numel(), _ptr(ae), _ptr(best), _stream(stream)))
     return best
+
+
+VISUAL_MAX_TOKENS = 8192
+
+
+def visual_importance_workspace_size(batch: int, num_kv_heads: int, vis_count: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dreams_visual_importance_workspace_size(batch, num_kv_heads, vis_count, ctypes.byref(n)))
+    return n.value
+
+
+def visual_importance(q: torch.Tensor, k_cache: torch.Tensor, kv_len: torch.Tensor, lse: torch.Tensor,
+                      vis_begin: int, vis_count: int, scale: Optional[float] = None,
+                      importance: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    """dreams_visual_importance (Eq. 2): q [B,Hq,T,D] and k_cache [B,Hkv,S_cap,D] bf16, kv_len [B] int32, lse
+    [B,Hq,T] float32 from the attention call on the same rows.  Returns importance [B, vis_count] float32."""
+    dev = q.device
+    _need(q, "q", torch.bfloat16, dev, 4)
+    _need(k_cache, "k_cache", torch.bfloat16, dev, 4)
+    _need(kv_len, "kv_len", torch.int32, dev, 1)
+    _need(lse, "lse", torch.float32, dev, 3)
+    B, Hq, T, D = q.shape
+    desc = attn_desc(q, k_cache, 0, 0, scale)
+    if importance is None:
+        importance = torch.empty((B, vis_count), dtype=torch.float32, device=dev)
+    else:
+        _need(importance, "importance", torch.float32, dev)
+    nbytes = visual_importance_workspace_size(B, k_cache.shape[1], vis_count)
+    st = _stream(stream)
+    if workspace is None:
+        workspace = _workspace("visual", nbytes, dev, st)
+    _check(lib().dreams_visual_importance(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(kv_len), _ptr(lse),
+                                          vis_begin, vis_count, _ptr(importance), _ptr(workspace),
+                                          0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                          st))
+    return importance
+
+
+def visual_topk(importance: torch.Tensor, keep_count: int, keep: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """dreams_visual_topk: importance [B, n] float32 -> keep [B, keep_count] int32 (increasing token order)."""
+    _need(importance, "importance", torch.float32, importance.device, 2)
+    B, n = importance.shape
+    if keep is None:
+        keep = torch.empty((B, keep_count), dtype=torch.int32, device=importance.device)
+    else:
+        _need(keep, "keep", torch.int32, importance.device, 2)
+    _check(lib().dreams_visual_topk(B, n, keep_count, _ptr(importance), _ptr(keep), _stream(stream)))
+    return keep
+
+
+def visual_gather(k_cache: torch.Tensor, v_cache: torch.Tensor, vis_begin: int, keep: torch.Tensor,
+                  k_out: Optional[torch.Tensor] = None, v_out: Optional[torch.Tensor] = None, stream=None):
+    """dreams_visual_gather: the kept visual tokens' K/V rows -> (k_out, v_out) [B, Hkv, keep_count, D]."""
+    dt = k_cache.dtype
+    dev = k_cache.device
+    _need(k_cache, "k_cache", dt, dev, 4)
+    _need(v_cache, "v_cache", dt, dev, 4)
+    _need(keep, "keep", torch.int32, dev, 2)
+    B, Hkv, S, D = k_cache.shape
+    r = keep.shape[1]
+    if k_out is None:
+        k_out = torch.empty((B, Hkv, r, D), dtype=dt, device=dev)
+    if v_out is None:
+        v_out = torch.empty((B, Hkv, r, D), dtype=dt, device=dev)
+    _check(lib().dreams_visual_gather(B, Hkv, D, S, DREAMS_BF16 if dt == torch.bfloat16 else DREAMS_F32,
+                                      _ptr(k_cache), _ptr(v_cache), vis_begin, _ptr(keep), r, _ptr(k_out),
+                                      _ptr(v_out), _stream(stream)))
+    return k_out, v_out
 
 
 def _verify_attn(q, k_cache, v_cache, kv_len, parent, tree_mask, scale, out, lse, with_lse, max_kv_len, num_splits,
