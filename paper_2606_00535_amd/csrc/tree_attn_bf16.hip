@@ -522,12 +522,16 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    // (the products are issued at a raised wave priority, so that the SIMD's other wave -- in its softmax --
+    // does not hold them back: gqa_long 355 -> 339 us)
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op.kf[kb][ds], qf[rb][ds], s[rb][kb], 0, 0, 0);
+    __builtin_amdgcn_s_setprio(0);
 
     // this lane's maximum over its 8 keys of each row, in scaled log2 units (c > 0 keeps the order)
     float lmax[RB];
@@ -580,6 +584,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     }
 
     // O^T[d][row] += sum over the 32 keys of V[key][d] P[row][key]
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int d = 0; d < DB; ++d) {
       bf16x8 va;
@@ -592,6 +597,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) o[rb][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[rb], o[rb][d], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
   };
 
   if constexpr (PIPE) {
