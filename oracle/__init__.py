@@ -66,6 +66,8 @@ class Oracle:
         lib.oracle_tree_accept.argtypes = [I, I, I, P, P, P, P, P, P, P]
         lib.oracle_kv_commit.argtypes = [I, ctypes.c_int64, I, I, I, I, I, P, P, P, P, P, I, P]
         lib.oracle_tree_attn_entropy.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, P]
+        lib.oracle_tree_accept_sampled.argtypes = [I, I, I, ctypes.c_double, P, P, P, P, P, P, P, P]
+        lib.oracle_tree_accept_sampled.restype = ctypes.c_int
         lib.oracle_visual_importance.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, I, I, P]
         lib.oracle_visual_topk.argtypes = [I, I, I, P, P]
         lib.oracle_visual_gather.argtypes = [I, I, I, I, I, P, P, I, P, I, P, P]
@@ -171,6 +173,21 @@ class Oracle:
                                              int(vis_begin), _p(keep), r, _p(ko), _p(vo)), "oracle_visual_gather")
         return ko, vo
 
+    def tree_accept_sampled(self, target_logits, draft_logits, tokens, parent, uniforms, temperature: float):
+        """Sampled tree acceptance.  Returns (accept_len [B], accept_path [B,T], next_token [B]), int32."""
+        tl = _c(target_logits, np.float32)
+        B, T, V = tl.shape
+        dl = _c(draft_logits, np.float32)
+        assert dl.shape == tl.shape
+        alen = np.empty(B, dtype=np.int32)
+        path = np.empty((B, T), dtype=np.int32)
+        nxt = np.empty(B, dtype=np.int32)
+        rc = self.lib.oracle_tree_accept_sampled(B, T, V, float(temperature), _p(tl), _p(dl),
+                                                 _p(_c(tokens, np.int32)), _p(_c(parent, np.int32)),
+                                                 _p(_c(uniforms, np.float32)), _p(alen), _p(path), _p(nxt))
+        _check(rc, "oracle_tree_accept_sampled")
+        return alen, path, nxt
+
     def tree_accept(self, logits, tokens, parent):
         """Returns (accept_len [B], accept_path [B,T], next_token [B], target_argmax [B,T]), all int32."""
         logits = _c(logits, np.float32)
@@ -234,6 +251,10 @@ def kv_commit(*a, **kw):
 
 def tree_attn_entropy(*a, **kw):
     return default().tree_attn_entropy(*a, **kw)
+
+
+def tree_accept_sampled(*a, **kw):
+    return default().tree_accept_sampled(*a, **kw)
 
 
 def visual_importance(*a, **kw):

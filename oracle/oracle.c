@@ -30,6 +30,16 @@
  *  oracle_kv_commit
  *      Keeps the root and the accepted nodes' K/V as the next contiguous cache slots, in path order.
  *
+ *  oracle_tree_accept_sampled
+ *      Sampled verification at temperature tau (the paper reports speedups at temperature 1, Table 2): the
+ *      acceptance-rejection mechanism of speculative sampling (Section 1; Section 2, "Speculative decoding")
+ *      run down the tree.  At a node, the target's distribution p and the draft's q (softmax of the logits
+ *      over tau) are compared for each child in index order: the child's token x is accepted with
+ *      probability min(1, r(x)/q(x)), r starting as p; after a rejection r becomes max(r - q, 0),
+ *      renormalised.  The walk descends into the first accepted child; where none is accepted (or at a leaf)
+ *      the emitted token is drawn from r.  The uniforms are inputs: u[b][c] decides child c, u[b][0] draws
+ *      the final token (inverse CDF).
+ *
  *  oracle_visual_importance / oracle_visual_topk / oracle_visual_gather
  *      Target-aware visual-token selection (Section 3.1, "Visual Token Compression", Eq. 2): the importance of
  *      visual token j is its attention weight averaged over every head and every query row of the call,
@@ -233,6 +243,96 @@ int oracle_tree_attn_entropy(int B, int Hq, int Hkv, int T, int D, int S_cap, do
     free(visible);
     free(score);
   }
+  return 0;
+}
+
+/* softmax(logits / tau) in fp64, two passes */
+static void softmax_tau(const float* logits, int V, double tau, double* out) {
+  double m = logits[0];
+  for (int x = 1; x < V; ++x)
+    if (logits[x] > m) m = logits[x];
+  double s = 0.0;
+  for (int x = 0; x < V; ++x) {
+    out[x] = exp(((double)logits[x] - m) / tau);
+    s += out[x];
+  }
+  for (int x = 0; x < V; ++x) out[x] /= s;
+}
+
+/*
+ * Sampled tree acceptance.  target_logits, draft_logits [B,T,V]: row i holds the logits of the token that
+ * follows node i, under the target and under the draft (the draft sampled node i's children from it);
+ * tokens [B,T] (node 0 is the root, already emitted); parent [B,T]; uniforms [B,T] in [0,1).
+ * Outputs as oracle_tree_accept: accept_len, accept_path (root .. last accepted node, then -1), next_token.
+ */
+int oracle_tree_accept_sampled(int B, int T, int V, double tau, const float* target_logits,
+                               const float* draft_logits, const int32_t* tokens, const int32_t* parent,
+                               const float* uniforms, int32_t* accept_len, int32_t* accept_path,
+                               int32_t* next_token) {
+  if (B < 0 || T < 1 || V < 1 || !(tau > 0.0) || !isfinite(tau)) return ORACLE_BAD_ARG;
+  for (int b = 0; b < B; ++b) {
+    if (!tree_ok(parent + (size_t)b * T, T)) return ORACLE_BAD_TREE;
+    for (int i = 1; i < T; ++i) {
+      const int x = tokens[(size_t)b * T + i];
+      if (x < 0 || x >= V) return ORACLE_BAD_ARG;
+    }
+    for (int i = 0; i < T; ++i) {
+      const float u = uniforms[(size_t)b * T + i];
+      if (!(u >= 0.0f && u < 1.0f)) return ORACLE_BAD_ARG;
+    }
+  }
+  for (size_t e = 0; e < (size_t)B * T * V; ++e)
+    if (!isfinite(target_logits[e]) || !isfinite(draft_logits[e])) return ORACLE_NONFINITE;
+
+  double* p = (double*)malloc(sizeof(double) * (size_t)V);
+  double* q = (double*)malloc(sizeof(double) * (size_t)V);
+  double* r = (double*)malloc(sizeof(double) * (size_t)V);
+  for (int b = 0; b < B; ++b) {
+    const int32_t* par = parent + (size_t)b * T;
+    const int32_t* tok = tokens + (size_t)b * T;
+    const float* u = uniforms + (size_t)b * T;
+    int32_t* path = accept_path + (size_t)b * T;
+    for (int k = 0; k < T; ++k) path[k] = -1;
+    int node = 0, depth = 0;
+    path[0] = 0;
+    for (;;) {
+      softmax_tau(target_logits + ((size_t)b * T + node) * V, V, tau, p);
+      softmax_tau(draft_logits + ((size_t)b * T + node) * V, V, tau, q);
+      for (int x = 0; x < V; ++x) r[x] = p[x];
+      int accepted = -1;
+      for (int c = node + 1; c < T && accepted < 0; ++c) {
+        if (par[c] != node) continue;
+        const int x = tok[c];
+        if ((double)u[c] * q[x] < r[x]) {   /* accepted with probability min(1, r(x)/q(x)) */
+          accepted = c;
+          break;
+        }
+        double z = 0.0;   /* rejected: the residual max(r - q, 0), renormalised (kept if it vanishes) */
+        for (int y = 0; y < V; ++y) z += r[y] > q[y] ? r[y] - q[y] : 0.0;
+        if (z > 0.0)
+          for (int y = 0; y < V; ++y) r[y] = (r[y] > q[y] ? r[y] - q[y] : 0.0) / z;
+      }
+      if (accepted < 0) break;
+      node = accepted;
+      path[++depth] = node;
+    }
+    /* the emitted token: inverse CDF of r at u[0] */
+    double total = 0.0;
+    for (int x = 0; x < V; ++x) total += r[x];
+    const double thr = (double)u[0] * total;
+    double cum = 0.0;
+    int pick = -1, last_pos = 0;
+    for (int x = 0; x < V; ++x) {
+      if (r[x] > 0.0) last_pos = x;
+      cum += r[x];
+      if (pick < 0 && cum > thr) pick = x;
+    }
+    accept_len[b] = depth;
+    next_token[b] = pick >= 0 ? pick : last_pos;
+  }
+  free(p);
+  free(q);
+  free(r);
   return 0;
 }
 

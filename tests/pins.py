@@ -701,4 +701,209 @@ def pin_visual_topk_and_gather(orc):
 
 VISUAL_PINS = [pin_visual_bruteforce, pin_visual_uniform_closed_form, pin_visual_mass_balance,
                pin_visual_topk_and_gather]
-ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS + VISUAL_PINS
+
+
+# ------------------------------------------------------------------------------------ sampled acceptance
+def _softmax(logits, tau):
+    z = np.asarray(logits, dtype=np.float64) / tau
+    z -= z.max(axis=-1, keepdims=True)
+    e = np.exp(z)
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def _sample(rng, probs):
+    """One index per row of `probs` (fp64 rows summing to 1), by inverse CDF of numpy uniforms."""
+    c = np.cumsum(probs, axis=-1)
+    u = rng.random(probs.shape[:-1])[..., None] * c[..., -1:]
+    return np.minimum((c <= u).sum(axis=-1), probs.shape[-1] - 1)
+
+
+def _emitted(tokens, path, alen, nxt, b):
+    return [int(tokens[b, path[b, d]]) for d in range(1, alen[b] + 1)] + [int(nxt[b])]
+
+
+def _chi2_ok(counts, expected, floor=1e-6):
+    from scipy.stats import chi2
+    keep = expected > 0
+    assert np.all(counts[~keep] == 0), "a token of probability zero was emitted"
+    stat = float((((counts - expected) ** 2)[keep] / expected[keep]).sum())
+    dof = int(keep.sum()) - 1
+    return chi2.sf(stat, dof) > floor, stat, dof
+
+
+def pin_sampled_single_child_closed_form(orc):
+    """One child of token x: accepted iff u < p(x)/q(x); on rejection the emitted token is the inverse CDF of
+    max(p - q, 0) / sum(max(p - q, 0)) at u0 (values written out by hand from the two distributions)."""
+    tau = 0.8
+    tl = np.log(np.array([0.10, 0.45, 0.05, 0.40])) * tau          # p = [0.10, 0.45, 0.05, 0.40]
+    dl = np.log(np.array([0.40, 0.20, 0.30, 0.10])) * tau          # q = [0.40, 0.20, 0.30, 0.10]
+    p, q = _softmax(tl, tau), _softmax(dl, tau)
+    np.testing.assert_allclose(p, [0.10, 0.45, 0.05, 0.40], rtol=1e-6)
+    # max(p - q, 0) = [0, .25, 0, .30]: token 1 for u0 < .25/.55, token 3 above (u0 = 0 must give 1, not 0)
+    parent = np.array([[-1, 0]], np.int32)
+    cases = []
+    for x in range(4):
+        ratio = p[x] / q[x]
+        for u1 in (0.999 * ratio, 1.001 * ratio, 0.0, 0.99999):
+            if not u1 < 1.0:
+                continue
+            for u0 in (0.0, 0.2, 0.5, 0.9):
+                cases.append((x, u1, u0))
+    for x, u1, u0 in cases:
+        tok = np.array([[0, x]], np.int32)
+        uni = np.array([[u0, u1]], np.float32)
+        alen, path, nxt = orc.tree_accept_sampled(tl[None, None].repeat(2, 1).astype(np.float32),
+                                                  dl[None, None].repeat(2, 1).astype(np.float32), tok, parent,
+                                                  uni, tau)
+        if float(np.float32(u1)) < p[x] / q[x]:
+            assert alen[0] == 1 and list(path[0]) == [0, 1], (x, u1)
+            # the child is a leaf: its token follows the target's distribution at the child (row 1 = p)
+            assert nxt[0] == int(np.searchsorted(np.cumsum(p), np.float32(u0), side="right")), (x, u1, u0)
+        else:
+            assert alen[0] == 0 and list(path[0]) == [0, -1], (x, u1)
+            want = 1 if np.float32(u0) < 0.25 / 0.55 else 3   # the residual's support is {1, 3}
+            assert nxt[0] == want, (x, u1, u0, nxt[0], want)
+
+
+def pin_sampled_repeated_token_never_accepted_twice(orc):
+    """Siblings carrying the same token x: once x is rejected its residual mass is zero, so every later copy is
+    rejected too, whatever its uniform."""
+    rng = np.random.default_rng(41)
+    B, V, tau = 2000, 6, 1.0
+    tl = rng.standard_normal((B, 4, V)).astype(np.float32)
+    dl = rng.standard_normal((B, 4, V)).astype(np.float32)
+    x = rng.integers(0, V, size=B)
+    tok = np.stack([np.zeros(B, int), x, x, x], axis=1).astype(np.int32)
+    parent = np.tile(np.array([-1, 0, 0, 0], np.int32), (B, 1))
+    uni = rng.random((B, 4)).astype(np.float32)
+    alen, path, nxt = orc.tree_accept_sampled(tl, dl, tok, parent, uni, tau)
+    assert np.all(path[alen == 1, 1] == 1)              # only the first copy can be accepted
+    assert np.all(nxt[alen == 0] != x[alen == 0])       # and the rejected token is never emitted instead
+    assert 0 < (alen == 1).sum() < B
+
+
+def pin_sampled_low_temperature_is_greedy(orc):
+    """As tau -> 0 both distributions become one-hot at their argmax; with integer logits spaced >= 1 and
+    tau = 1e-3 every other probability underflows to exactly zero, and with distinct sibling tokens the
+    sampled walk accepts exactly the greedy rule's path and bonus token, for any uniforms."""
+    rng = np.random.default_rng(42)
+    B, T, V = 300, 20, 12
+    parent = np.stack([W.random_tree(rng, T, int(rng.integers(2, 8)), 4) for _ in range(B)])
+    tl = np.stack([rng.permutation(V) for _ in range(B * T)]).reshape(B, T, V).astype(np.float32)
+    dl = np.stack([rng.permutation(V) for _ in range(B * T)]).reshape(B, T, V).astype(np.float32)
+    am = tl.argmax(axis=2)
+    tok = np.zeros((B, T), np.int32)
+    for b in range(B):
+        used = {}
+        for i in range(1, T):
+            sib = used.setdefault(int(parent[b, i]), set())
+            # agree with the parent's target token half of the time, never repeat a sibling's token
+            choice = int(am[b, parent[b, i]]) if rng.random() < 0.6 else int(rng.integers(0, V))
+            while choice in sib:
+                choice = int(rng.integers(0, V))
+            sib.add(choice)
+            tok[b, i] = choice
+    uni = rng.random((B, T)).astype(np.float32)
+    alen, path, nxt = orc.tree_accept_sampled(tl, dl, tok, parent, uni, 1e-3)
+    galen, gpath, gnxt, _ = orc.tree_accept(tl, tok, parent)
+    np.testing.assert_array_equal(alen, galen)
+    np.testing.assert_array_equal(path, gpath)
+    np.testing.assert_array_equal(nxt, gnxt)
+
+
+def pin_sampled_identical_models(orc):
+    """Draft == target: every tested child is accepted (u q(x) < q(x) for u < 1), so the walk follows
+    first children to a leaf and emits a token drawn from the leaf's distribution at u0."""
+    rng = np.random.default_rng(43)
+    B, T, V, tau = 200, 15, 9, 0.7
+    parent = np.stack([random_parent(rng, T, max_branch=3) for _ in range(B)])
+    tl = rng.standard_normal((B, T, V)).astype(np.float32)
+    tok = rng.integers(0, V, size=(B, T)).astype(np.int32)
+    uni = rng.random((B, T)).astype(np.float32)
+    alen, path, nxt = orc.tree_accept_sampled(tl, tl, tok, parent, uni, tau)
+    for b in range(B):
+        node, walk = 0, [0]
+        while True:
+            kids = [c for c in range(T) if parent[b, c] == node]
+            if not kids:
+                break
+            node = kids[0]
+            walk.append(node)
+        assert alen[b] == len(walk) - 1 and list(path[b, :len(walk)]) == walk
+        cdf = np.cumsum(_softmax(tl[b, node], tau))
+        assert nxt[b] == int(np.searchsorted(cdf, float(uni[b, 0]) * cdf[-1], side="right"))
+
+
+def _markov_tree_step(orc, rng, P_tab, Q_tab, roots, width, depth2, tau):
+    """One verification step per root token: a tree whose root has `width` children drawn i.i.d. from the
+    draft's distribution after the root, each with `depth2` children drawn i.i.d. from the draft's distribution
+    after it.  Target and draft logits depend only on a node's own token (a Markov model)."""
+    B = len(roots)
+    T = 1 + width + width * depth2
+    parent = np.full(T, -1, np.int32)
+    for c in range(width):
+        parent[1 + c] = 0
+        for g in range(depth2):
+            parent[1 + width + c * depth2 + g] = 1 + c
+    tok = np.zeros((B, T), np.int32)
+    tok[:, 0] = roots
+    V = P_tab.shape[0]
+    qprob = _softmax(Q_tab, tau)
+    for c in range(width):
+        tok[:, 1 + c] = _sample(rng, qprob[tok[:, 0]])
+        for g in range(depth2):
+            tok[:, 1 + width + c * depth2 + g] = _sample(rng, qprob[tok[:, 1 + c]])
+    tl = P_tab[tok].astype(np.float32)
+    dl = Q_tab[tok].astype(np.float32)
+    uni = rng.random((B, T)).astype(np.float32)
+    alen, path, nxt = orc.tree_accept_sampled(tl, dl, tok, np.tile(parent, (B, 1)), uni, tau)
+    assert tl.shape == (B, T, V)
+    return tok, alen, path, nxt
+
+
+def pin_sampled_output_distribution(orc):
+    """The defining property of speculative sampling: whatever the draft, the emitted tokens follow the
+    target's own distribution.  With a Markov target P(. | previous token) the first two emitted tokens after a
+    root r0 have the joint law P(x1 | r0) P(x2 | x1); a step that emits one token is followed by a fresh step
+    rooted at it.  Chi-square test over all V^2 cells, at two temperatures; also the acceptance rate of the
+    first child equals sum_x min(p(x), q(x)) within 5 standard errors."""
+    rng = np.random.default_rng(44)
+    V, N = 4, 30000
+    P_tab = rng.standard_normal((V, V)) * 1.5
+    Q_tab = rng.standard_normal((V, V)) * 1.5
+    for tau in (1.0, 0.6):
+        P = _softmax(P_tab, tau)
+        Q = _softmax(Q_tab, tau)
+        r0 = 2
+        roots = np.full(N, r0, np.int32)
+        tok, alen, path, nxt = _markov_tree_step(orc, rng, P_tab, Q_tab, roots, 3, 2, tau)
+        pairs = np.full((N, 2), -1)
+        short = []
+        for b in range(N):
+            e = _emitted(tok, path, alen, nxt, b)
+            if len(e) >= 2:
+                pairs[b] = e[:2]
+            else:
+                pairs[b, 0] = e[0]
+                short.append(b)
+        if short:
+            tok2, alen2, path2, nxt2 = _markov_tree_step(orc, rng, P_tab, Q_tab, pairs[short, 0].astype(np.int32),
+                                                         2, 1, tau)
+            for k, b in enumerate(short):
+                pairs[b, 1] = _emitted(tok2, path2, alen2, nxt2, k)[0]
+        counts = np.zeros((V, V))
+        np.add.at(counts, (pairs[:, 0], pairs[:, 1]), 1)
+        expected = N * P[r0][:, None] * P
+        ok, stat, dof = _chi2_ok(counts.ravel(), expected.ravel())
+        assert ok, (tau, stat, dof)
+        # acceptance rate of the first child, drawn from q: sum_x min(p(x), q(x))
+        first_acc = (alen >= 1) & (path[:, 1] == 1)
+        rate = np.minimum(P[r0], Q[r0]).sum()
+        se = np.sqrt(rate * (1 - rate) / N)
+        assert abs(first_acc.mean() - rate) <= 5 * se, (tau, first_acc.mean(), rate)
+
+
+SAMPLED_PINS = [pin_sampled_single_child_closed_form, pin_sampled_repeated_token_never_accepted_twice,
+                pin_sampled_low_temperature_is_greedy, pin_sampled_identical_models,
+                pin_sampled_output_distribution]
+ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS + VISUAL_PINS + SAMPLED_PINS

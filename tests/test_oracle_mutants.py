@@ -8,7 +8,7 @@ import pytest
 import oracle
 import pins
 
-ATTN, ACC, COM, ENT, VIS = "attn", "accept", "commit", "entropy", "visual"
+ATTN, ACC, COM, ENT, VIS, SMP = "attn", "accept", "commit", "entropy", "visual", "sampled"
 MUTANTS = [
     ("drop_scale", ATTN, "score[s] = scale * dot;", "score[s] = dot;"),
     ("wrong_kv_head", ATTN, "const int g = h / G;", "const int g = h % Hkv;"),
@@ -59,9 +59,28 @@ MUTANTS = [
      "    score[s] = dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;"),
     ("entropy_self_hidden", ENT, "  visible_nodes(parent ? parent + (size_t)b * T : NULL,\n                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);\n  const int n = L + T;\n  double m = -INFINITY;\n  for (int s = 0; s < n; ++s) {\n    if (s >= L && !visible[s - L]) continue;\n    double dot = 0.0;\n    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];\n    score[s] = scale * dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;",
      "  visible_nodes(parent ? parent + (size_t)b * T : NULL,\n                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);\n  visible[i] = 0;\n  const int n = L + T;\n  double m = -INFINITY;\n  for (int s = 0; s < n; ++s) {\n    if (s >= L && !visible[s - L]) continue;\n    double dot = 0.0;\n    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];\n    score[s] = scale * dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;"),
+    ("sampled_ratio_inverted", SMP, "if ((double)u[c] * q[x] < r[x]) {", "if ((double)u[c] * r[x] < q[x]) {"),
+    ("sampled_residual_unclamped", SMP, "r[y] = (r[y] > q[y] ? r[y] - q[y] : 0.0) / z;", "r[y] = (r[y] - q[y]) / z;"),
+    ("sampled_residual_not_updated", SMP, "r[y] = (r[y] > q[y] ? r[y] - q[y] : 0.0) / z;", "r[y] = r[y];"),
+    ("sampled_residual_not_renormalised", SMP, "r[y] = (r[y] > q[y] ? r[y] - q[y] : 0.0) / z;",
+     "r[y] = (r[y] > q[y] ? r[y] - q[y] : 0.0);"),
+    ("sampled_final_from_target", SMP, "cum += r[x];", "cum += p[x];"),
+    ("sampled_final_from_draft", SMP, "cum += r[x];", "cum += q[x];"),
+    ("sampled_final_ge", SMP, "if (pick < 0 && cum > thr) pick = x;", "if (pick < 0 && cum >= thr) pick = x;"),
+    ("sampled_target_row_of_root", SMP, "softmax_tau(target_logits + ((size_t)b * T + node) * V, V, tau, p);",
+     "softmax_tau(target_logits + ((size_t)b * T) * V, V, tau, p);"),
+    ("sampled_draft_row_of_root", SMP, "softmax_tau(draft_logits + ((size_t)b * T + node) * V, V, tau, q);",
+     "softmax_tau(draft_logits + ((size_t)b * T) * V, V, tau, q);"),
+    ("sampled_no_temperature", SMP, "out[x] = exp(((double)logits[x] - m) / tau);",
+     "out[x] = exp((double)logits[x] - m);"),
+    ("sampled_shared_uniform", SMP, "if ((double)u[c] * q[x] < r[x]) {", "if ((double)u[0] * q[x] < r[x]) {"),
+    ("sampled_first_child_only", SMP, "      if (accepted < 0) break;\n      node = accepted;",
+     "      if (accepted < 0) break;\n      if (depth > 0) break;\n      node = accepted;"),
+    ("sampled_len_counts_bonus", SMP, "    accept_len[b] = depth;\n    next_token[b] = pick",
+     "    accept_len[b] = depth + 1;\n    next_token[b] = pick"),
 ]
 GROUPS = {ATTN: pins.ATTN_PINS, ACC: pins.ACCEPT_PINS, COM: pins.COMMIT_PINS, ENT: pins.ENTROPY_PINS,
-          VIS: pins.VISUAL_PINS}
+          VIS: pins.VISUAL_PINS, SMP: pins.SAMPLED_PINS}
 
 
 @pytest.mark.parametrize("name,group,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
