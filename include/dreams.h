@@ -2,9 +2,10 @@
  * dreams.h -- C ABI of libdreams.so, the MI355X (gfx950) tree-verification step of DREAM-S speculative
  * decoding for vision-language models.
  *
- * The step has three verbs, run back to back on one HIP stream:
+ * The step has three verbs (acceptance in two forms), run back to back on one HIP stream:
  *   dreams_tree_verify_attn  tree-masked attention of the draft-token tree against the KV cache
  *   dreams_tree_accept       greedy acceptance of the longest target-consistent root-to-node path
+ *   dreams_tree_accept_sampled  acceptance at temperature tau > 0 (accept-or-resample down the tree)
  *   dreams_kv_commit         compaction of the accepted path's K/V into the cache
  *
  * Conventions shared by every entry point
@@ -234,6 +235,51 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
                                    const int32_t* draft_tokens, const int32_t* parent, int32_t* accept_len,
                                    int32_t* accept_path, int32_t* next_token, int32_t* target_argmax,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace dreams_tree_accept_sampled needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if
+ * vocab exceeds 2^21 or if batch * num_nodes arrival counters (plus one per sequence and one more) do not fit
+ * in DREAMS_WORKSPACE_COUNTER_BYTES.  After the counters: per row 64 bytes of statistics plus 48 bytes per
+ * 2048-entry piece of the vocabulary. */
+dreams_status_t dreams_tree_accept_sampled_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
+                                                          size_t* bytes);
+
+/*
+ * dreams_tree_accept_sampled -- acceptance at temperature tau > 0 (the paper reports its speedups at
+ * temperature 1, Table 2): speculative sampling's accept-or-resample rule (Section 1; Section 2,
+ * "Speculative decoding"), walked down the tree.  For every sequence b:
+ *
+ *   p_i = softmax(target_logits[b,i,:] / tau), q_i = softmax(draft_logits[b,i,:] / tau): the target's and the
+ *         draft's distribution of the token that follows node i (node i's children are the draft's samples
+ *         from q_i)
+ *   walk: node = 0 (the root), r = p_node; the children c of node are tested in increasing index order:
+ *         with x = draft_tokens[b,c], c is kept iff uniforms[b,c] * q_node(x) < r(x) (probability
+ *         min(1, r(x)/q_node(x))); the walk moves to the first kept child and starts again there; after a
+ *         rejection r becomes max(r - q_node, 0) / sum(max(r - q_node, 0)) (r is kept if that sum is 0)
+ *   stop: at a node none of whose children is kept (a leaf included), with that node's residual r
+ *   accept_len[b]  = number of kept children on the walk (the step emits accept_len + 1 tokens)
+ *   accept_path[b] = node ids root .. last (accept_len + 1 entries), then -1 up to T entries
+ *   next_token[b]  = the smallest x with sum_{y <= x} r(y) > uniforms[b,0] * sum_y r(y)
+ *
+ *   temperature    tau > 0, finite
+ *   target_logits  device [B, T, V] float, finite
+ *   draft_logits   device [B, T, V] float, finite
+ *   draft_tokens   device [B, T] int32 (entry 0 = root token, not read); a token outside [0, V) is rejected
+ *   parent         device [B, T] int32, as for dreams_tree_verify_attn; a node whose parent breaks the rules
+ *                  (parent[i] outside [0, i)) is never kept
+ *   uniforms       device [B, T] float in [0, 1): entry 0 draws the emitted token, entry c decides child c
+ *   accept_len     device [B] int32 (out)
+ *   accept_path    device [B, T] int32 (out)
+ *   next_token     device [B] int32 (out)
+ *   workspace      device, >= dreams_tree_accept_sampled_workspace_size bytes (see "Workspaces" above)
+ * Probabilities are computed in fp64; the integer results equal those of the rule evaluated in fp64 except
+ * where a uniform falls within rounding (about 1e-15 relative) of a decision threshold.
+ */
+dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int32_t vocab, double temperature,
+                                           const float* target_logits, const float* draft_logits,
+                                           const int32_t* draft_tokens, const int32_t* parent,
+                                           const float* uniforms, int32_t* accept_len, int32_t* accept_path,
+                                           int32_t* next_token, void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream);
 
 /*
  * dreams_kv_commit -- keeps the accepted path in the cache: for every layer, sequence b and KV head, and

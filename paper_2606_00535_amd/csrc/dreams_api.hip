@@ -406,6 +406,110 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
   return ok();
 }
 
+// ------------------------------------------------------------------------------------- sampled acceptance
+struct SampledPlan {
+  int chunks, row_stride;
+  size_t stat_off, piece_off, mass_off, post_off, bytes;
+};
+
+dreams_status_t plan_sampled(int32_t B, int32_t T, int32_t V, SampledPlan* p) {
+  if (B < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", B);
+  if (T < 1 || T > kMaxNodes) return fail(DREAMS_ERR_INVALID_ARG, "num_nodes = %d outside [1, %d]", T, kMaxNodes);
+  if (V < 1) return fail(DREAMS_ERR_INVALID_ARG, "vocab = %d < 1", V);
+  *p = SampledPlan{};
+  if (B == 0) return DREAMS_OK;
+  const long long chunks = ((long long)V + kSampledChunk - 1) / kSampledChunk;
+  if (chunks > kSampledMaxChunks)
+    return fail(DREAMS_ERR_UNSUPPORTED, "vocab = %d exceeds %d", V, kSampledMaxChunks * kSampledChunk);
+  if ((long long)B * (2 * T - 1) * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  // counters: the ticket, one per sequence, then one per row, spread over the region as far as it allows
+  const size_t rows = (size_t)B * T, base = ((size_t)B + 1 + 31) / 32 * 32;
+  if (base + rows > kMaxCounters)
+    return fail(DREAMS_ERR_UNSUPPORTED, "batch * num_nodes = %zu exceeds the %zu arrival counters", rows,
+                kMaxCounters - base);
+  size_t stride = 32;
+  while (stride > 1 && base + rows * stride > kMaxCounters) stride >>= 1;
+  p->chunks = (int)chunks;
+  p->row_stride = (int)stride;
+  size_t off = kCounterBytes;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  p->stat_off = take(rows * 4 * sizeof(double));
+  p->piece_off = take(rows * chunks * 4 * sizeof(double));
+  p->mass_off = take(rows * 2 * chunks * sizeof(double));
+  p->post_off = take(rows * 4 * sizeof(double));
+  p->bytes = off;
+  return DREAMS_OK;
+}
+
+dreams_status_t dreams_tree_accept_sampled_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
+                                                          size_t* bytes) {
+  if (!bytes) return fail(DREAMS_ERR_INVALID_ARG, "bytes is NULL");
+  SampledPlan p;
+  dreams_status_t st = plan_sampled(batch, num_nodes, vocab, &p);
+  if (st != DREAMS_OK) return st;
+  *bytes = p.bytes;
+  return ok();
+}
+
+dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int32_t vocab, double temperature,
+                                           const float* target_logits, const float* draft_logits,
+                                           const int32_t* draft_tokens, const int32_t* parent,
+                                           const float* uniforms, int32_t* accept_len, int32_t* accept_path,
+                                           int32_t* next_token, void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream) {
+  SampledPlan p;
+  dreams_status_t st = plan_sampled(batch, num_nodes, vocab, &p);
+  if (st != DREAMS_OK) return st;
+  if (!(temperature > 0.0) || !isfinite(temperature))
+    return fail(DREAMS_ERR_INVALID_ARG, "temperature = %g is not a positive finite number", temperature);
+  if (batch == 0) return ok();
+  if (!target_logits || !draft_logits || !draft_tokens || !parent || !uniforms || !accept_len || !accept_path ||
+      !next_token)
+    return fail(DREAMS_ERR_INVALID_ARG,
+                "target_logits, draft_logits, draft_tokens, parent, uniforms, accept_len, accept_path and "
+                "next_token must not be NULL");
+  if (!aligned(target_logits, 4) || !aligned(draft_logits, 4) || !aligned(draft_tokens, 4) || !aligned(parent, 4) ||
+      !aligned(uniforms, 4) || !aligned(accept_len, 4) || !aligned(accept_path, 4) || !aligned(next_token, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "an int32/float argument is not 4-byte aligned");
+  if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", p.bytes);
+  if (workspace_bytes < p.bytes)
+    return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, p.bytes);
+  if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  SampledArgs a{};
+  a.target_logits = target_logits;
+  a.draft_logits = draft_logits;
+  a.tokens = draft_tokens;
+  a.parent = parent;
+  a.uniforms = uniforms;
+  a.accept_len = accept_len;
+  a.accept_path = accept_path;
+  a.next_token = next_token;
+  char* ws = (char*)workspace;
+  uint32_t* ctr = (uint32_t*)ws;
+  a.ticket = ctr;
+  a.seq_ctr = ctr + 1;
+  a.row_ctr = ctr + ((size_t)batch + 1 + 31) / 32 * 32;
+  a.row_stride = p.row_stride;
+  a.row_stat = (double*)(ws + p.stat_off);
+  a.piece_stat = (double*)(ws + p.piece_off);
+  a.mass = (double*)(ws + p.mass_off);
+  a.post = (double*)(ws + p.post_off);
+  a.inv_tau = 1.0 / temperature;
+  a.B = batch;
+  a.T = num_nodes;
+  a.V = vocab;
+  a.chunks = p.chunks;
+  a.vec4 = (vocab % 4 == 0) && aligned(target_logits, 16) && aligned(draft_logits, 16);
+  hipError_t e = launch_tree_accept_sampled(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "sampled tree accept launch");
+  return ok();
+}
+
 dreams_status_t dreams_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream) {
   if (!src || !sink) return fail(DREAMS_ERR_INVALID_ARG, "src and sink must not be NULL");
   if (!aligned(src, 16) || bytes % 16 != 0)

@@ -134,6 +134,42 @@ struct AcceptArgs {
 
 hipError_t launch_tree_accept(const AcceptArgs& a, hipStream_t stream);
 
+// ------------------------------------------------------------------------------- sampled acceptance
+// Every row of B * T vocabulary rows is cut into pieces of kSampledChunk entries (kSampledPerThread
+// consecutive entries per thread).  The launch's workgroups take a ticket on entry and do, in ticket order,
+// first the normaliser of every piece of every row ("stats" pieces), then for every child node c (in index
+// order, every sequence, every piece) the residual mass after c's rejection ("pass" pieces).
+constexpr int kSampledThreads = 256;
+constexpr int kSampledPerThread = 8;
+constexpr int kSampledChunk = kSampledThreads * kSampledPerThread;
+constexpr int kSampledMaxChunks = 1024;   // pieces per row, at most (vocabularies up to 2^21 entries)
+
+struct SampledArgs {
+  const float* target_logits;  // [B, T, V]
+  const float* draft_logits;   // [B, T, V]
+  const int32_t* tokens;       // [B, T]
+  const int32_t* parent;       // [B, T]
+  const float* uniforms;       // [B, T]
+  int32_t* accept_len;         // [B]
+  int32_t* accept_path;        // [B, T]
+  int32_t* next_token;         // [B]
+  uint32_t* ticket;            // one word
+  uint32_t* seq_ctr;           // [B] rows finished per sequence
+  uint32_t* row_ctr;           // [B * T] words row_stride apart: low half counts stats pieces, high half pass
+                               // pieces; a half reads chunks + 1 once the row's merged result is published
+  int row_stride;
+  double* row_stat;            // [B, T, 4]  target maximum, target normaliser, draft maximum, draft normaliser
+  double* piece_stat;          // [B, T, chunks, 4] the same per piece (maximum and sum relative to it)
+  double* mass;                // [B, 2T, chunks] slot i < T: target mass of each piece of row i;
+                               //                 slot T + c: residual mass of each piece after rejecting c
+  double* post;                // [B, T, 4]  state after rejecting child c: C, D, mass slot
+  double inv_tau;              // 1 / temperature (may be +inf)
+  int B, T, V, chunks;
+  int vec4;                    // both logits tensors 16-byte aligned and V % 4 == 0
+};
+
+hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream);
+
 // ------------------------------------------------------------------------------------------ commit
 constexpr int kCommitThreads = 256;
 constexpr int kCommitRowsPerPass = 32;

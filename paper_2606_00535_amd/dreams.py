@@ -25,7 +25,8 @@ EXPORTS = (
     "dreams_tree_accept", "dreams_kv_commit", "dreams_status_string", "dreams_last_error_message",
     "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy", "dreams_attn_entropy_mean",
     "dreams_attn_entropy_select", "dreams_visual_importance_workspace_size", "dreams_visual_importance",
-    "dreams_visual_topk", "dreams_visual_gather",
+    "dreams_visual_topk", "dreams_visual_gather", "dreams_tree_accept_sampled_workspace_size",
+    "dreams_tree_accept_sampled",
 )
 
 
@@ -79,6 +80,9 @@ def lib():
                 L.dreams_visual_importance_workspace_size.argtypes = [I32, I32, I32, ctypes.POINTER(SZ)]
                 L.dreams_visual_importance.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, I32, I32, P, P, SZ, P]
                 L.dreams_visual_topk.argtypes = [I32, I32, I32, P, P, P]
+                L.dreams_tree_accept_sampled_workspace_size.argtypes = [I32, I32, I32, ctypes.POINTER(SZ)]
+                L.dreams_tree_accept_sampled.argtypes = [I32, I32, I32, ctypes.c_double, P, P, P, P, P, P, P, P, P,
+                                                         SZ, P]
                 L.dreams_visual_gather.argtypes = [I32, I32, I32, I32, ctypes.c_int, P, P, I32, P, I32, P, P, P]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
@@ -367,6 +371,50 @@ def tree_accept(target_logits: torch.Tensor, draft_tokens: torch.Tensor, parent:
                                     _ptr(path), _ptr(nxt), _ptr(am), _ptr(workspace),
                                     0 if workspace is None else workspace.numel(), st))
     return alen, path, nxt, am
+
+
+def tree_accept_sampled_workspace_size(batch: int, num_nodes: int, vocab: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dreams_tree_accept_sampled_workspace_size(batch, num_nodes, vocab, ctypes.byref(n)))
+    return n.value
+
+
+def tree_accept_sampled(target_logits: torch.Tensor, draft_logits: torch.Tensor, draft_tokens: torch.Tensor,
+                        parent: torch.Tensor, uniforms: torch.Tensor, temperature: float = 1.0, outputs=None,
+                        workspace: Optional[torch.Tensor] = None, stream=None):
+    """dreams_tree_accept_sampled.  target_logits / draft_logits [B,T,V] float32, draft_tokens / parent [B,T]
+    int32, uniforms [B,T] float32 in [0, 1).  Returns (accept_len [B], accept_path [B,T], next_token [B]), int32.
+    `outputs` may pass preallocated (accept_len, accept_path, next_token)."""
+    dev = target_logits.device
+    _need(target_logits, "target_logits", torch.float32, dev, 3)
+    B, T, V = target_logits.shape
+    _need(draft_logits, "draft_logits", torch.float32, dev, 3)
+    if tuple(draft_logits.shape) != (B, T, V):
+        raise ValueError("draft_logits must have the shape of target_logits")
+    _need(draft_tokens, "draft_tokens", torch.int32, dev, 2)
+    _need(parent, "parent", torch.int32, dev, 2)
+    _need(uniforms, "uniforms", torch.float32, dev, 2)
+    if tuple(draft_tokens.shape) != (B, T) or tuple(parent.shape) != (B, T) or tuple(uniforms.shape) != (B, T):
+        raise ValueError("draft_tokens, parent and uniforms must be [B, T]")
+    if outputs is None:
+        alen = torch.empty(B, dtype=torch.int32, device=dev)
+        path = torch.empty((B, T), dtype=torch.int32, device=dev)
+        nxt = torch.empty(B, dtype=torch.int32, device=dev)
+    else:
+        alen, path, nxt = outputs
+        for t, nm, shp in ((alen, "accept_len", (B,)), (path, "accept_path", (B, T)), (nxt, "next_token", (B,))):
+            _need(t, nm, torch.int32, dev)
+            if tuple(t.shape) != shp:
+                raise ValueError("%s has the wrong shape" % nm)
+    st = _stream(stream)
+    nbytes = tree_accept_sampled_workspace_size(B, T, V)
+    if workspace is None:
+        workspace = _workspace("accept_sampled", nbytes, dev, st)
+    _check(lib().dreams_tree_accept_sampled(B, T, V, float(temperature), _ptr(target_logits), _ptr(draft_logits),
+                                            _ptr(draft_tokens), _ptr(parent), _ptr(uniforms), _ptr(alen),
+                                            _ptr(path), _ptr(nxt), _ptr(workspace),
+                                            0 if workspace is None else workspace.numel(), st))
+    return alen, path, nxt
 
 
 def kv_commit(k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len_in: torch.Tensor, accept_path: torch.Tensor,

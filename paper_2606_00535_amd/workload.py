@@ -4,9 +4,11 @@ This module only *draws* inputs: tree topologies, prefix lengths, queries, keys,
 draft tokens.  It contains none of the verification arithmetic (no attention, no acceptance, no commit), so
 both the HIP path and the CPU oracle can be fed from it without sharing any of the method's code.
 
-The one place where the generator looks at a logit row is when it plants draft tokens that agree with their
-parent's target argmax with a given probability (the agreement model of the synthetic workloads); it uses
-``numpy.argmax`` for that, which only shapes the *distribution* of inputs and never produces an expected value.
+The generator looks at a logit row in two places, both of which only shape the *distribution* of inputs and never
+produce an expected value: it plants draft tokens that agree with their parent's target argmax with a given
+probability (the agreement model of the greedy workloads; ``numpy.argmax``), and, for sampled acceptance, it
+draws each child's token from the draft's distribution at its parent with the Gumbel-max trick (the argmax of
+the logits over the temperature plus Gumbel noise).
 
 Shapes follow the paper's target models (LLaVA-v1.6-Vicuna-7B/13B: 32/40 heads, head_dim 128, vocabulary
 32000, 2880 "anyres" image tokens held in the KV cache beside the text tokens; the paper's Section 2,
@@ -28,6 +30,7 @@ import numpy as np
 _T_TOPOLOGY, _T_AGREE, _T_LEN, _T_LOGITS, _T_TOKENS = 0, 1, 2, 3, 4
 _T_Q, _T_KPRE, _T_VPRE, _T_KTREE, _T_VTREE = 10, 11, 12, 13, 14
 _T_VARIANT = 20
+_T_DRAFT, _T_DRAFT_TOKENS, _T_UNIFORMS = 30, 31, 32
 
 
 @dataclass(frozen=True)
@@ -294,3 +297,53 @@ def tree_depths_for_generator_checks(parent: np.ndarray) -> np.ndarray:
     for i in range(1, len(parent)):
         d[i] = d[parent[i]] + 1
     return d
+
+
+# ------------------------------------------------------------------------------------- sampled acceptance
+@dataclass
+class SampledInputs:
+    """Inputs of sampled acceptance for one verify step.
+
+    target_logits, draft_logits: [B, T, V] float32; tokens, parent: [B, T] int32; uniforms: [B, T] float32 in
+    [0, 1) (entry 0 draws the emitted token, entry c decides child c); temperature: the one both were drawn for.
+    """
+    target_logits: np.ndarray
+    draft_logits: np.ndarray
+    tokens: np.ndarray
+    parent: np.ndarray
+    uniforms: np.ndarray
+    temperature: float
+
+
+def make_sampled(wl: Workload, *, temperature: float = 1.0, draft_noise: float = 1.0,
+                 parents: Optional[np.ndarray] = None, target_logits: Optional[np.ndarray] = None) -> SampledInputs:
+    """Draw sampled-acceptance inputs for workload `wl`.
+
+    Target logits are those of make_batch (N(0, logit_std), same streams) unless given; the draft's logits are
+    the target's plus N(0, draft_noise) noise (a draft that approximates the target); every child's token is a
+    sample of softmax(draft_logits[parent] / temperature), drawn by the Gumbel-max trick; the root's token is
+    uniform.  Uniforms are float32 in [0, 1).
+    """
+    B, T, V = wl.batch, wl.num_nodes, wl.vocab
+    parent = np.empty((B, T), dtype=np.int32)
+    for b in range(B):
+        parent[b] = random_tree(rng_for(wl.seed, 0, b, _T_TOPOLOGY), T, wl.depth, wl.max_branch) \
+            if parents is None else np.asarray(parents[b], dtype=np.int32)
+    tl = np.empty((B, T, V), dtype=np.float32) if target_logits is None else np.asarray(target_logits, np.float32)
+    dl = np.empty((B, T, V), dtype=np.float32)
+    tokens = np.empty((B, T), dtype=np.int32)
+    uniforms = np.empty((B, T), dtype=np.float32)
+    for b in range(B):
+        if target_logits is None:
+            tl[b] = rng_for(wl.seed, 0, b, _T_LOGITS).standard_normal((T, V), dtype=np.float32)
+            tl[b] *= np.float32(wl.logit_std)
+        noise = rng_for(wl.seed, 0, b, _T_DRAFT).standard_normal((T, V), dtype=np.float32)
+        dl[b] = tl[b] + np.float32(draft_noise) * noise
+        r = rng_for(wl.seed, 0, b, _T_DRAFT_TOKENS)
+        tokens[b, 0] = r.integers(0, V)
+        for i in range(1, T):
+            with np.errstate(divide="ignore"):   # a uniform of exactly 0 gives -inf noise: never drawn
+                g = -np.log(-np.log(r.random(V, dtype=np.float32)))
+            tokens[b, i] = int(np.argmax(dl[b, parent[b, i]] / np.float32(temperature) + g))
+        uniforms[b] = rng_for(wl.seed, 0, b, _T_UNIFORMS).random(T, dtype=np.float32)
+    return SampledInputs(tl, dl, tokens, parent, uniforms, float(temperature))

@@ -188,3 +188,32 @@ def test_entropy_entry_points_reject_bad_arguments(D):
     assert lib.dreams_attn_entropy_select(1, fake, fake, None) == D.DREAMS_ERR_INVALID_ARG
     assert lib.dreams_attn_entropy_select(4, fake, None, None) == D.DREAMS_ERR_INVALID_ARG
     assert lib.dreams_attn_entropy_select(4, ctypes.c_void_p(0x100001), fake, None) == D.DREAMS_ERR_INVALID_ARG
+
+
+def test_sampled_accept_rejections_and_sizes(D):
+    lib = D.lib()
+    n = ctypes.c_size_t(0)
+
+    def r256(x):
+        return (x + 255) // 256 * 256
+
+    for B, T, V in [(1, 60, 32000), (16, 128, 152064), (3, 1, 1), (2, 7, 2049)]:
+        assert lib.dreams_tree_accept_sampled_workspace_size(B, T, V, ctypes.byref(n)) == 0
+        rows, chunks = B * T, (V + 2047) // 2048
+        assert n.value == 65536 + 2 * r256(rows * 32) + r256(rows * chunks * 32) + r256(rows * 2 * chunks * 8)
+    assert lib.dreams_tree_accept_sampled_workspace_size(0, 60, 32000, ctypes.byref(n)) == 0 and n.value == 0
+    assert lib.dreams_tree_accept_sampled_workspace_size(1, 0, 32000, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_sampled_workspace_size(1, 129, 32000, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, 0, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, (1 << 21) + 1, ctypes.byref(n)) == -2
+    assert lib.dreams_tree_accept_sampled_workspace_size(200, 128, 100, ctypes.byref(n)) == -2   # counters
+    assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, 10, None) == -1
+    fake = ctypes.c_void_p(0x100000)
+    f = lib.dreams_tree_accept_sampled
+    assert f(0, 60, 10, 1.0, None, None, None, None, None, None, None, None, None, 0, None) == 0
+    for tau in (0.0, -1.0, float("inf"), float("nan")):
+        assert f(1, 60, 10, tau, fake, fake, fake, fake, fake, fake, fake, fake, fake, 1 << 20, None) == -1
+        assert b"temperature" in lib.dreams_last_error_message()
+    assert f(1, 60, 10, 1.0, fake, None, fake, fake, fake, fake, fake, fake, fake, 1 << 20, None) == -1
+    assert f(1, 60, 10, 1.0, fake, fake, fake, fake, fake, fake, fake, fake, None, 0, None) == -3
+    assert f(1, 60, 10, 1.0, fake, fake, fake, fake, fake, fake, fake, fake, fake, 100, None) == -3

@@ -1,0 +1,175 @@
+"""GPU parity of dreams_tree_accept_sampled against the CPU oracle: bit-exact accepted lengths, paths and emitted
+tokens on the workloads' seeded sampled inputs (draft = target + noise, children drawn from the draft), at
+several temperatures, on ragged and misaligned vocabularies, degenerate trees, and in the limits where the rule
+reduces to something simpler (identical models; low temperature = the greedy kernel)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import device, note, to_dev
+from paper_2606_00535_amd import dreams
+from paper_2606_00535_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    d = device()
+    dreams.lib()
+    return d
+
+
+def gpu_sampled(dev, tl, dl, tok, par, uni, tau, tl_dev=None, dl_dev=None, workspace=None):
+    out = dreams.tree_accept_sampled(to_dev(tl, dev) if tl_dev is None else tl_dev,
+                                     to_dev(dl, dev) if dl_dev is None else dl_dev, to_dev(tok, dev),
+                                     to_dev(par, dev), to_dev(uni, dev), tau, workspace=workspace)
+    torch.cuda.synchronize()
+    return tuple(t.cpu().numpy() for t in out)
+
+
+def run_and_compare(dev, tl, dl, tok, par, uni, tau, label, **kw):
+    ga, gp, gn = gpu_sampled(dev, tl, dl, tok, par, uni, tau, **kw)
+    ra, rp, rn = oracle.tree_accept_sampled(tl, dl, tok, par, uni, tau)
+    note("%s: accepted mean %.3f, mismatching rows: len %d path %d next %d" % (
+        label, float(ra.mean()), int((ga != ra).sum()), int((gp != rp).any(axis=1).sum()), int((gn != rn).sum())))
+    assert np.array_equal(ga, ra) and np.array_equal(gp, rp) and np.array_equal(gn, rn), label
+    return ra
+
+
+def random_case(rng, B, T, V, depth, branch, tau=1.0, noise=1.0, std=3.0):
+    par = np.stack([W.random_tree(rng, T, depth, branch) for _ in range(B)]) if T > 1 else np.full((B, 1), -1,
+                                                                                                   np.int32)
+    tl = (rng.standard_normal((B, T, V)) * std).astype(np.float32)
+    dl = (tl + noise * rng.standard_normal((B, T, V))).astype(np.float32)
+    tok = np.zeros((B, T), np.int32)
+    for b in range(B):
+        for i in range(1, T):
+            g = -np.log(-np.log(rng.random(V)))
+            tok[b, i] = int(np.argmax(dl[b, par[b, i]] / tau + g))
+    uni = rng.random((B, T)).astype(np.float32)
+    return tl, dl, tok, par, uni
+
+
+@pytest.mark.parametrize("name", ["tiny", "llava7b_layer", "llava13b_layer", "gqa_long"])
+def test_workload_parity(dev, name):
+    wl = W.WORKLOADS[name]
+    s = W.make_sampled(wl)
+    note("%s: B=%d T=%d V=%d" % (name, wl.batch, wl.num_nodes, wl.vocab))
+    ra = run_and_compare(dev, s.target_logits, s.draft_logits, s.tokens, s.parent, s.uniforms, s.temperature, name)
+    assert np.all((ra >= 0) & (ra <= wl.depth))
+
+
+@pytest.mark.parametrize("tau", [0.25, 0.7, 1.0, 1.6])
+def test_temperatures(dev, tau):
+    rng = np.random.default_rng(int(tau * 100))
+    tl, dl, tok, par, uni = random_case(rng, 24, 40, 5000, 6, 4, tau=tau, noise=0.8)
+    run_and_compare(dev, tl, dl, tok, par, uni, tau, "tau=%g" % tau)
+
+
+@pytest.mark.parametrize("V", [1, 2, 5, 2047, 2048, 2049, 4099, 40003])
+def test_ragged_vocab(dev, V):
+    rng = np.random.default_rng(V)
+    tl, dl, tok, par, uni = random_case(rng, 16, 20, V, 5, 4, noise=1.5, std=2.0)
+    run_and_compare(dev, tl, dl, tok, par, uni, 1.0, "V=%d" % V)
+
+
+def test_misaligned_logits_scalar_path(dev):
+    rng = np.random.default_rng(9)
+    B, T, V = 3, 16, 4000
+    tl, dl, tok, par, uni = random_case(rng, B, T, V, 4, 3)
+    big_t = torch.zeros(B * T * V + 1, dtype=torch.float32, device=dev)
+    big_t[1:] = to_dev(tl.reshape(-1), dev)
+    run_and_compare(dev, tl, dl, tok, par, uni, 1.0, "misaligned", tl_dev=big_t[1:].view(B, T, V))
+
+
+def test_degenerate_trees(dev):
+    rng = np.random.default_rng(10)
+    B, V = 6, 3000
+    # single node: the emitted token is a draw from the root's target distribution
+    tl, dl, tok, par, uni = random_case(rng, B, 1, V, 0, 1)
+    run_and_compare(dev, tl, dl, tok, par, uni, 1.0, "single node")
+    # a chain, and a star whose 127 children form one long chain of residual updates
+    for label, parent in (("chain", W.chain_tree(64)), ("star", W.star_tree(128))):
+        T = len(parent)
+        par = np.tile(parent, (B, 1))
+        tl = (rng.standard_normal((B, T, V)) * 3).astype(np.float32)
+        dl = (tl + rng.standard_normal((B, T, V)) * 2).astype(np.float32)
+        tok = rng.integers(0, V, (B, T)).astype(np.int32)
+        uni = rng.random((B, T)).astype(np.float32)
+        run_and_compare(dev, tl, dl, tok, par, uni, 1.0, label)
+
+
+def test_star_rejections_reach_every_sibling(dev):
+    """Children whose tokens the target gives no mass: every sibling of the star is rejected in turn, and the
+    emitted token comes from the residual after all of them."""
+    rng = np.random.default_rng(11)
+    B, T, V = 4, 128, 2500
+    par = np.tile(W.star_tree(T), (B, 1))
+    tl = rng.standard_normal((B, T, V)).astype(np.float32)
+    tl[:, :, :1000] -= 60.0                       # tokens below 1000: target mass ~ e^-60
+    dl = rng.standard_normal((B, T, V)).astype(np.float32)
+    tok = rng.integers(0, 1000, (B, T)).astype(np.int32)
+    uni = rng.random((B, T)).astype(np.float32)
+    ra = run_and_compare(dev, tl, dl, tok, par, uni, 1.0, "star, all rejected")
+    assert np.all(ra == 0)
+
+
+def test_identical_models_follow_first_children(dev):
+    rng = np.random.default_rng(12)
+    tl, _, tok, par, uni = random_case(rng, 32, 60, 32000, 6, 4)
+    run_and_compare(dev, tl, tl, tok, par, uni, 1.0, "identical models")
+
+
+def test_low_temperature_equals_greedy_kernel(dev):
+    """Integer logits spaced >= 1 at tau = 1e-3: both distributions are exactly one-hot, and with distinct
+    sibling tokens the sampled kernel must return what the greedy kernel returns."""
+    rng = np.random.default_rng(13)
+    B, T, V = 16, 60, 300
+    par = np.stack([W.random_tree(rng, T, 6, 4) for _ in range(B)])
+    tl = np.stack([rng.permutation(V) for _ in range(B * T)]).reshape(B, T, V).astype(np.float32)
+    dl = np.stack([rng.permutation(V) for _ in range(B * T)]).reshape(B, T, V).astype(np.float32)
+    am = tl.argmax(axis=2)
+    tok = np.zeros((B, T), np.int32)
+    for b in range(B):
+        used = {}
+        for i in range(1, T):
+            sib = used.setdefault(int(par[b, i]), set())
+            x = int(am[b, par[b, i]]) if rng.random() < 0.7 else int(rng.integers(0, V))
+            while x in sib:
+                x = int(rng.integers(0, V))
+            sib.add(x)
+            tok[b, i] = x
+    uni = rng.random((B, T)).astype(np.float32)
+    ga, gp, gn = gpu_sampled(dev, tl, dl, tok, par, uni, 1e-3)
+    ka, kp, kn, _ = dreams.tree_accept(to_dev(tl, dev), to_dev(tok, dev), to_dev(par, dev))
+    torch.cuda.synchronize()
+    assert np.array_equal(ga, ka.cpu().numpy()) and np.array_equal(gp, kp.cpu().numpy())
+    assert np.array_equal(gn, kn.cpu().numpy())
+    run_and_compare(dev, tl, dl, tok, par, uni, 1e-3, "tau=1e-3")
+
+
+def test_workspace_shared_and_repeatable(dev):
+    """Calls of different shapes on one workspace, repeated: identical results, counters left zero."""
+    n = max(dreams.tree_accept_sampled_workspace_size(16, 128, 40003), 1 << 20)
+    ws = torch.zeros(n, dtype=torch.uint8, device=dev)
+    rng = np.random.default_rng(14)
+    for B, T, V in [(16, 128, 40003), (3, 7, 11), (1, 60, 32000), (8, 20, 4099)]:
+        tl, dl, tok, par, uni = random_case(rng, B, T, V, min(T - 1, 6), 6)
+        first = gpu_sampled(dev, tl, dl, tok, par, uni, 1.0, workspace=ws)
+        again = gpu_sampled(dev, tl, dl, tok, par, uni, 1.0, workspace=ws)
+        for x, y in zip(first, again):
+            assert np.array_equal(x, y), (B, T, V)
+        ra, rp, rn = oracle.tree_accept_sampled(tl, dl, tok, par, uni, 1.0)
+        assert np.array_equal(first[0], ra) and np.array_equal(first[1], rp) and np.array_equal(first[2], rn)
+    assert not ws[:65536].any()
+
+
+def test_rejected_arguments(dev):
+    z = torch.zeros((1, 2, 8), dtype=torch.float32, device=dev)
+    i2 = torch.zeros((1, 2), dtype=torch.int32, device=dev)
+    u2 = torch.zeros((1, 2), dtype=torch.float32, device=dev)
+    for tau in (0.0, -1.0, float("inf"), float("nan")):
+        with pytest.raises(dreams.DreamsError):
+            dreams.tree_accept_sampled(z, z, i2, i2, u2, tau)
