@@ -231,6 +231,41 @@ def main():
     torch.cuda.synchronize()
     acc_us = a0.elapsed_time(a1) * 1e3 / (reps * R)
 
+    # sampled acceptance at temperature 1 on the same target logits (draft = target + N(0,1) noise, children drawn
+    # from the draft), same method
+    smp = W.make_sampled(wl, target_logits=host.logits)
+    ws_smp = torch.zeros(max(1, dreams.tree_accept_sampled_workspace_size(B, T, wl.vocab)), dtype=torch.uint8,
+                         device=dev)
+    for r, st in enumerate(sets):
+        st["dlog"] = torch.from_numpy(smp.draft_logits).to(dev)
+        st["stok"] = torch.from_numpy(smp.tokens).to(dev)
+        st["uni"] = torch.from_numpy(smp.uniforms).to(dev)
+        st["salen"] = torch.empty(B, dtype=torch.int32, device=dev)
+        st["spath"] = torch.empty((B, T), dtype=torch.int32, device=dev)
+        st["snext"] = torch.empty(B, dtype=torch.int32, device=dev)
+
+    def sampled(st):
+        dreams.tree_accept_sampled(st["logits"], st["dlog"], st["stok"], st["par"], st["uni"], smp.temperature,
+                                   outputs=(st["salen"], st["spath"], st["snext"]), workspace=ws_smp)
+
+    for st in sets:
+        sampled(st)
+    torch.cuda.synchronize()
+    g_smp = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_smp):
+        for r in range(R):
+            sampled(sets[r])
+    g_smp.replay()
+    torch.cuda.synchronize()
+    a0.record()
+    for _ in range(reps):
+        g_smp.replay()
+    a1.record()
+    torch.cuda.synchronize()
+    smp_us = a0.elapsed_time(a1) * 1e3 / (reps * R)
+    smp_bytes = 2 * B * T * wl.vocab * 4 + B * T * 12
+    smp_alen = sets[0]["salen"].cpu().numpy()
+
     # the attention call with every row's attention entropy as well (the layer-selection statistic), same method
     ents = [torch.empty((B, Hq, T), dtype=torch.float32, device=dev) for _ in range(NL)]
 
@@ -336,6 +371,9 @@ def main():
                       "GBps": round(attn_gbps, 1), "splits": "auto" if splits_used == 0 else splits_used},
         "accept": {"us_per_launch": round(acc_us, 3), "bytes_per_launch": acc_b,
                    "GBps": round(acc_b / (acc_us * 1e-6) / 1e9, 1)},
+        "accept_sampled": {"us_per_launch": round(smp_us, 3), "bytes_per_launch": smp_bytes,
+                           "GBps": round(smp_bytes / (smp_us * 1e-6) / 1e9, 1), "temperature": smp.temperature,
+                           "mean_accept_len": round(float(smp_alen.mean()), 3)},
         "visual_select": vis,
         "attention_entropy": {"us_per_launch": round(ent_us, 3), "bytes_per_launch": a_bytes + B * Hq * T * 4,
                               "GBps": round((a_bytes + B * Hq * T * 4) / (ent_us * 1e-6) / 1e9, 1)},

@@ -407,9 +407,11 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
 }
 
 // ------------------------------------------------------------------------------------- sampled acceptance
+constexpr long long kSampledLargeFrom = 4096;   // stats workgroups beyond which pieces are large
+
 struct SampledPlan {
-  int chunks, row_stride;
-  size_t stat_off, piece_off, mass_off, post_off, bytes;
+  int sub_pieces, chunks, row_stride;
+  size_t row_base, piece_off, mass_off, flag_off, bytes;
 };
 
 dreams_status_t plan_sampled(int32_t B, int32_t T, int32_t V, SampledPlan* p) {
@@ -418,29 +420,38 @@ dreams_status_t plan_sampled(int32_t B, int32_t T, int32_t V, SampledPlan* p) {
   if (V < 1) return fail(DREAMS_ERR_INVALID_ARG, "vocab = %d < 1", V);
   *p = SampledPlan{};
   if (B == 0) return DREAMS_OK;
-  const long long chunks = ((long long)V + kSampledChunk - 1) / kSampledChunk;
+  // pieces of 2048 entries while there are at most about 16 statistics workgroups per compute unit (the wait
+  // chain dominates: each piece computes p and q before it waits); beyond that, pieces of 8192 entries (four
+  // times fewer workgroups, each streaming its piece after the waits)
+  const long long small = kSampledThreads * kSampledPerThread, large = small * kSampledSubLarge;
+  long long sub = 1, chunks = ((long long)V + small - 1) / small;
+  if ((long long)B * T * chunks > kSampledLargeFrom || chunks > kSampledMaxChunks) {
+    sub = kSampledSubLarge;
+    chunks = ((long long)V + large - 1) / large;
+  }
   if (chunks > kSampledMaxChunks)
-    return fail(DREAMS_ERR_UNSUPPORTED, "vocab = %d exceeds %d", V, kSampledMaxChunks * kSampledChunk);
+    return fail(DREAMS_ERR_UNSUPPORTED, "vocab = %d exceeds %lld", V, (long long)kSampledMaxChunks * large);
   if ((long long)B * (2 * T - 1) * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
-  // counters: the ticket, one per sequence, then one per row, spread over the region as far as it allows
-  const size_t rows = (size_t)B * T, base = ((size_t)B + 1 + 31) / 32 * 32;
-  if (base + rows > kMaxCounters)
-    return fail(DREAMS_ERR_UNSUPPORTED, "batch * num_nodes = %zu exceeds the %zu arrival counters", rows,
-                kMaxCounters - base);
-  size_t stride = 32;
-  while (stride > 1 && base + rows * stride > kMaxCounters) stride >>= 1;
+  // counter region: one word per sequence, then a block of 4, 8 or 16 words per row (as many as fit)
+  const size_t rows = (size_t)B * T, base = ((size_t)B + 63) / 64 * 64;
+  if (base + rows * 4 > kMaxCounters)
+    return fail(DREAMS_ERR_UNSUPPORTED, "batch * num_nodes = %zu rows exceed the arrival counters (%zu)", rows,
+                (kMaxCounters - base) / 4);
+  size_t stride = 16;
+  while (stride > 4 && base + rows * stride > kMaxCounters) stride >>= 1;
+  p->sub_pieces = (int)sub;
   p->chunks = (int)chunks;
   p->row_stride = (int)stride;
+  p->row_base = base;
   size_t off = kCounterBytes;
   auto take = [&](size_t bytes) {
     const size_t at = off;
     off += (bytes + 255) / 256 * 256;
     return at;
   };
-  p->stat_off = take(rows * 4 * sizeof(double));
   p->piece_off = take(rows * chunks * 4 * sizeof(double));
-  p->mass_off = take(rows * 2 * chunks * sizeof(double));
-  p->post_off = take(rows * 4 * sizeof(double));
+  p->mass_off = take(rows * chunks * sizeof(double));
+  p->flag_off = take(rows * 2 * sizeof(int32_t));
   p->bytes = off;
   return DREAMS_OK;
 }
@@ -491,19 +502,19 @@ dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int
   a.next_token = next_token;
   char* ws = (char*)workspace;
   uint32_t* ctr = (uint32_t*)ws;
-  a.ticket = ctr;
-  a.seq_ctr = ctr + 1;
-  a.row_ctr = ctr + ((size_t)batch + 1 + 31) / 32 * 32;
+  a.seq_ctr = ctr;
+  a.row_words = ctr + p.row_base;
   a.row_stride = p.row_stride;
-  a.row_stat = (double*)(ws + p.stat_off);
   a.piece_stat = (double*)(ws + p.piece_off);
   a.mass = (double*)(ws + p.mass_off);
-  a.post = (double*)(ws + p.post_off);
+  a.kept = (int32_t*)(ws + p.flag_off);
+  a.final_token = a.kept + (size_t)batch * num_nodes;
   a.inv_tau = 1.0 / temperature;
   a.B = batch;
   a.T = num_nodes;
   a.V = vocab;
   a.chunks = p.chunks;
+  a.sub_pieces = p.sub_pieces;
   a.vec4 = (vocab % 4 == 0) && aligned(target_logits, 16) && aligned(draft_logits, 16);
   hipError_t e = launch_tree_accept_sampled(a, stream);
   if (e != hipSuccess) return hip_fail(e, "sampled tree accept launch");

@@ -135,14 +135,14 @@ struct AcceptArgs {
 hipError_t launch_tree_accept(const AcceptArgs& a, hipStream_t stream);
 
 // ------------------------------------------------------------------------------- sampled acceptance
-// Every row of B * T vocabulary rows is cut into pieces of kSampledChunk entries (kSampledPerThread
-// consecutive entries per thread).  The launch's workgroups take a ticket on entry and do, in ticket order,
-// first the normaliser of every piece of every row ("stats" pieces), then for every child node c (in index
-// order, every sequence, every piece) the residual mass after c's rejection ("pass" pieces).
+// Every row of B * T vocabulary rows is cut into pieces of sub_pieces * 2048 entries; in each 2048-entry
+// sub-piece a thread holds kSampledPerThread consecutive entries.  The launch's workgroups are, in blockIdx order, first one per piece of
+// every row ("stats" pieces: maxima and normalisers), then one per piece of every child node c, by c ("pass"
+// pieces: the residual mass after c's rejection, and c's own accept decision).
 constexpr int kSampledThreads = 256;
 constexpr int kSampledPerThread = 8;
-constexpr int kSampledChunk = kSampledThreads * kSampledPerThread;
-constexpr int kSampledMaxChunks = 1024;   // pieces per row, at most (vocabularies up to 2^21 entries)
+constexpr int kSampledSubLarge = 4;         // sub-pieces per piece for problems of many pieces (else 1)
+constexpr int kSampledMaxChunks = 1024;     // pieces per row, at most
 
 struct SampledArgs {
   const float* target_logits;  // [B, T, V]
@@ -153,18 +153,18 @@ struct SampledArgs {
   int32_t* accept_len;         // [B]
   int32_t* accept_path;        // [B, T]
   int32_t* next_token;         // [B]
-  uint32_t* ticket;            // one word
   uint32_t* seq_ctr;           // [B] rows finished per sequence
-  uint32_t* row_ctr;           // [B * T] words row_stride apart: low half counts stats pieces, high half pass
-                               // pieces; a half reads chunks + 1 once the row's merged result is published
-  int row_stride;
-  double* row_stat;            // [B, T, 4]  target maximum, target normaliser, draft maximum, draft normaliser
-  double* piece_stat;          // [B, T, chunks, 4] the same per piece (maximum and sum relative to it)
-  double* mass;                // [B, 2T, chunks] slot i < T: target mass of each piece of row i;
-                               //                 slot T + c: residual mass of each piece after rejecting c
-  double* post;                // [B, T, 4]  state after rejecting child c: C, D, mass slot
+  uint32_t* row_words;         // [B * T] blocks of row_stride words: a 64-bit residual accumulator (arrivals in
+                               // the top 11 bits, the fixed-point mass in the low 53), then the stats arrivals
+  int row_stride;              // words per block: 4, 8 or 16
+  double* piece_stat;          // [B, T, chunks, 4] per piece: target maximum and sum of exp((l - max) / tau)
+                               // relative to it, then the same for the draft
+  double* mass;                // [B, T, chunks] residual mass of each piece after rejecting child c
+  int32_t* kept;               // [B, T] child c's decision
+  int32_t* final_token;        // [B, T] the token emitted if the walk ends at node i
   double inv_tau;              // 1 / temperature (may be +inf)
   int B, T, V, chunks;
+  int sub_pieces;              // 1 or kSampledSubLarge
   int vec4;                    // both logits tensors 16-byte aligned and V % 4 == 0
 };
 

@@ -9,29 +9,32 @@
 //
 // The residual after k rejections at a node has the closed form r_k = max(p - C_k q, 0) / D_k, with C_0 = 0,
 // D_0 = 1, and after rejecting one more child C_{k+1} = C_k + D_k, D_{k+1} = sum_x max(p - C_{k+1} q, 0) (both
-// unchanged when that sum is zero).  It does not depend on which tokens were rejected, only on how many, so
-// every child's test can be prepared before the walk: the state before child c is the state after its previous
-// sibling.  That turns the sequential walk into
-//   (1) per row and per piece of the vocabulary: maximum and sum of exp((l - max) / tau), target and draft,
-//       merged per row by the row's last piece ("stats" pieces);
-//   (2) per child c and per piece: the residual mass sum max(p - (C + D) q, 0) over the piece, where (C, D) is
-//       the state after c's previous sibling; the row's last piece sums the pieces and publishes the state
-//       after c ("pass" pieces).  Pass pieces wait for the stats of c's parent and for the previous sibling's
-//       state, a chain of waits as long as the widest sibling group;
-//   (3) the last workgroup of the sequence to finish a row: every child's test in parallel (one thread per
-//       node: u q(x) D < max(p(x) - C q(x), 0)), the walk by ballots (the first kept child of each node), and
-//       the emitted token from the final state's piece masses (prefix in piece order, then a block scan inside
-//       the chosen piece).
-// Every probability is fp64, so that the integer outcome is decided in the precision of the definition.
+// unchanged when that sum is zero).  It depends on how many siblings were rejected, not on their tokens, so
+// every child's test and every node's emitted token can be prepared before the walk:
+//   (1) "stats" pieces, one workgroup per piece of each row: maximum and sum of exp((l - max) / tau), target and
+//       draft.  Whoever needs a row's maxima and normalisers merges its pieces' statistics itself once all have
+//       arrived (the same order everywhere, so the same bits); at a leaf, the row's last piece draws the token
+//       emitted if the walk ends there.
+//   (2) "pass" pieces, one workgroup per piece of each child c of node n: the state before c follows from the
+//       residual masses of c's earlier siblings; the piece adds its part of c's residual mass
+//       sum max(p - (C + D) q, 0) and its arrival to c's 64-bit accumulator in one atomic (fixed point, units
+//       of 2^-51, so the sum does not depend on the order of arrival), and the piece holding c's token decides c
+//       (u q(x) D < max(p(x) - C q(x), 0)).  The last piece of n's last child draws the token emitted if the
+//       walk ends at n.  Pass pieces wait for n's statistics and for the accumulators of c's earlier siblings,
+//       a chain of waits as long as the widest sibling group.
+//   (3) the sequence's last row to finish walks the tree by ballots (the first kept child of each node) and
+//       emits the token prepared for the node it stops at.
+// Emitted tokens: the prefix of the piece masses in piece order finds the piece where the cumulative mass
+// first exceeds u0 * total, and a block scan of that piece finds the token.  Probabilities are fp64, so that
+// the integer outcome is decided in the precision of the definition; exp is Tang's table-driven method.
 //
-// Forward progress.  Workgroups do their work in the order of a ticket taken on entry, not in blockIdx order:
-// stats pieces first, then pass pieces by child index.  A workgroup only ever waits for results of workgroups
-// with smaller tickets, which are already running or finished, so every wait ends; waits are nevertheless
-// bounded (0.2 s), after which the results are unspecified.
+// Forward progress.  A workgroup only waits for rows whose pieces all have smaller blockIdx (stats pieces come
+// first, pass pieces are ordered by child index), and workgroups are dispatched in blockIdx order, so every
+// wait ends; waits are nevertheless bounded (0.2 s), after which the results are unspecified.
 //
 // Results cross workgroups through device-scope stores and loads, published before a relaxed device-scope
-// increment of an arrival word (see kernels.h).  Every arrival word is back at zero when the launch ends: the
-// walker of each sequence clears that sequence's words, the workgroup with the last ticket the ticket.
+// atomic on an arrival word (see kernels.h).  The walker of each sequence clears that sequence's arrival words,
+// so every one is back at zero when the launch ends.
 #include "kernels.h"
 
 #include <limits.h>
@@ -40,9 +43,12 @@
 namespace dreams {
 namespace {
 
-constexpr int NT = kSampledThreads, NW = NT / 64, EPT = kSampledPerThread, CHUNK = kSampledChunk;
-constexpr uint64_t kWaitTicks = 20000000;   // 100 MHz real-time ticks: 0.2 s
-constexpr uint32_t kStatsOne = 1u, kPassOne = 1u << 16;
+constexpr int NT = kSampledThreads, NW = NT / 64;
+constexpr uint64_t kWaitTicks = 20000000;          // 100 MHz real-time ticks: 0.2 s
+constexpr uint64_t kMassMask = (1ull << 53) - 1;   // accumulator: fixed-point mass in the low 53 bits,
+constexpr int kArrivalShift = 53;                  // arrivals above
+constexpr double kFixScale = 2251799813685248.0;   // 2^51 units per unit of mass
+constexpr double kFixUnit = 1.0 / kFixScale;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -52,26 +58,46 @@ __device__ __forceinline__ void store_d(double* p, double v) {
 __device__ __forceinline__ double load_d(const double* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint32_t add_word(uint32_t* w, uint32_t v) {
-  return __hip_atomic_fetch_add(w, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ uint64_t load_u64(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// exp(d / tau) as exp(d * (1 / tau)); d = 0 (the row maximum itself) gives exactly 1, also where 1 / tau is
-// infinite
-__device__ __forceinline__ double scaled_exp(double d, double inv_tau) { return d == 0.0 ? 1.0 : exp(d * inv_tau); }
+// exp(x) for x <= 0, by Tang's table-driven method: x = k ln2/256 + r with k = round(x 256/ln2) and
+// |r| <= ln2/512 (ln2/256 split in two so that k times the high part is exact), e^x = 2^(k/256) e^r, with
+// 2^(j/256) from a 256-entry table and e^r - 1 by its Taylor series to r^5/120 (the next term is below
+// 2^-66).  Arguments below -745.5 (past the smallest subnormal) give 0.
+__device__ __forceinline__ double exp_nonpos(double x, const double* tab) {
+  if (!(x >= -745.5)) return 0.0;
+  const double kd = rint(x * 369.3299304675746);
+  const int k = (int)kd;
+  double r = fma(-kd, 0x1.62e42fefp-9, x);
+  r = fma(-kd, 0x1.473de6af278edp-42, r);
+  const double em1 = r * fma(r, fma(r, fma(r, fma(r, 1.0 / 120.0, 1.0 / 24.0), 1.0 / 6.0), 0.5), 1.0);
+  const double t = tab[k & 255];
+  return ldexp(fma(t, em1, t), k >> 8);
+}
+// exp(d / tau) for d <= 0 as exp(d * (1 / tau)); d = 0 (the maximum itself) gives exactly 1, also where 1 / tau
+// is infinite
+__device__ __forceinline__ double scaled_exp(double d, double inv_tau, const double* tab) {
+  return d == 0.0 ? 1.0 : exp_nonpos(d * inv_tau, tab);
+}
 
 struct Shared {
-  double pm[kSampledMaxChunks];
+  double tab[256];                 // 2^(j/256)
+  double pm[kSampledMaxChunks];    // piece masses of the emitted token's distribution
+  double zs[kMaxNodes];            // residual masses of earlier siblings
   double red_d[NW];
   float red_f[NW];
   int red_i[NW];
   double scan[NW];
-  int flag;
+  int flag, nsib, last_child, depth;
   int par[kMaxNodes];
-  int acc[kMaxNodes];
+  int sib[kMaxNodes];
   int path[kMaxNodes];
-  int fin_node, fin_depth, fin_slot, fin_piece;
-  double fin_c, fin_before, fin_thr;
+  double st_c, st_d;
+  int st_slot;
+  int fin_piece;
+  double fin_before, fin_thr;
 };
 
 // Block reductions: every lane reduces its wave by a butterfly, lane 0's value is kept, waves are combined in
@@ -116,8 +142,8 @@ __device__ __forceinline__ int block_int(int v, Shared& sh) {
   for (int w = 1; w < NW; ++w) r = MAX ? max(r, sh.red_i[w]) : min(r, sh.red_i[w]);
   return r;
 }
-// Exclusive prefix of v over the threads in thread order.
-__device__ __forceinline__ double block_exclusive_scan(double v, Shared& sh) {
+// Exclusive prefix of v over the threads in thread order; `total` receives the sum over the block.
+__device__ __forceinline__ double block_exclusive_scan(double v, double& total, Shared& sh) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   double inc = v;
 #pragma unroll
@@ -130,12 +156,17 @@ __device__ __forceinline__ double block_exclusive_scan(double v, Shared& sh) {
   __syncthreads();
   double base = 0.0;
   for (int w = 0; w < wave; ++w) base += sh.scan[w];
+  total = 0.0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) total += sh.scan[w];
   return base + inc - v;
 }
 
-// Thread t holds entries x0 + t * EPT + e (e < EPT) of the piece [x0, x1); entries past x1 read as -inf.
+// A piece is SUB sub-pieces of NT * EPT entries.  In a sub-piece starting at x0, thread t holds entries
+// x0 + t * EPT + e (e < EPT); entries at or past x1 read as -inf.
+constexpr int EPT = kSampledPerThread, SUBW = NT * EPT;
 template <bool VEC>
-__device__ __forceinline__ void load_piece(const float* row, int x0, int x1, float (&v)[EPT]) {
+__device__ __forceinline__ void load_sub(const float* row, int x0, int x1, float (&v)[EPT]) {
   const int base = x0 + (int)threadIdx.x * EPT;
   if (VEC) {
 #pragma unroll
@@ -152,208 +183,235 @@ __device__ __forceinline__ void load_piece(const float* row, int x0, int x1, flo
   }
 }
 
-// Wait (one thread) until a half of an arrival word reads `target`.
-__device__ __forceinline__ void wait_half(const uint32_t* w, int shift, uint32_t target) {
-  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-  while (((__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> shift) & 0xffffu) != target) {
-    if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) break;
-    __builtin_amdgcn_s_sleep(2);
-  }
+__device__ __forceinline__ uint64_t* acc_word(const SampledArgs& a, int b, int i) {
+  return (uint64_t*)(a.row_words + ((size_t)b * a.T + i) * a.row_stride);
+}
+__device__ __forceinline__ uint32_t* stats_word(const SampledArgs& a, int b, int i) {
+  return a.row_words + ((size_t)b * a.T + i) * a.row_stride + 2;
 }
 
-__device__ __forceinline__ uint32_t* row_word(const SampledArgs& a, int b, int i) {
-  return a.row_ctr + ((size_t)b * a.T + i) * a.row_stride;
+// A row's maxima and normalisers from its pieces' statistics, merged in piece order by whichever workgroup
+// needs them (every one gets the same bits).
+struct RowStat {
+  double mt, inv_st, md, inv_sd;
+};
+__device__ RowStat merge_stats(const SampledArgs& a, size_t row, Shared& sh) {
+  const int tid = threadIdx.x;
+  const double* ps = a.piece_stat + row * a.chunks * 4;
+  float mt = -INFINITY, md = -INFINITY;
+  for (int k = tid; k < a.chunks; k += NT) {
+    mt = fmaxf(mt, (float)load_d(ps + 4 * k + 0));
+    md = fmaxf(md, (float)load_d(ps + 4 * k + 2));
+  }
+  mt = block_max(mt, sh);
+  md = block_max(md, sh);
+  double st = 0.0, sd = 0.0;
+  for (int k = tid; k < a.chunks; k += NT) {
+    st += load_d(ps + 4 * k + 1) * scaled_exp(load_d(ps + 4 * k + 0) - (double)mt, a.inv_tau, sh.tab);
+    sd += load_d(ps + 4 * k + 3) * scaled_exp(load_d(ps + 4 * k + 2) - (double)md, a.inv_tau, sh.tab);
+  }
+  st = block_sum(st, sh);
+  sd = block_sum(sd, sh);
+  return RowStat{mt, 1.0 / st, md, 1.0 / sd};
+}
+
+// The token emitted if the walk ends at node n with residual max(p - C q, 0): its piece masses are those of
+// child `src`'s residual, or, for src < 0, the target's own (from n's piece statistics).  Stored to
+// final_token by thread 0 (every thread then waits for its stores).
+template <bool VEC, int SUB>
+__device__ void final_draw(const SampledArgs& a, int b, int n, const RowStat& rs, double C, int src, Shared& sh) {
+  const int tid = threadIdx.x, T = a.T, V = a.V;
+  const size_t row = (size_t)b * T + n;
+  if (src >= 0) {
+    const double* m = a.mass + ((size_t)b * T + src) * a.chunks;
+    for (int k = tid; k < a.chunks; k += NT) sh.pm[k] = load_d(m + k);
+  } else {
+    const double* ps = a.piece_stat + row * a.chunks * 4;
+    for (int k = tid; k < a.chunks; k += NT)
+      sh.pm[k] = load_d(ps + 4 * k + 1) * scaled_exp(load_d(ps + 4 * k + 0) - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double total = 0.0;
+    for (int k = 0; k < a.chunks; ++k) total += sh.pm[k];
+    const double thr = (double)a.uniforms[(size_t)b * T] * total;
+    double cum = 0.0, before = 0.0, pos_before = 0.0;
+    int piece = -1, pos_piece = 0;
+    for (int k = 0; k < a.chunks; ++k) {
+      const double mk = sh.pm[k];
+      if (mk > 0.0) {
+        pos_piece = k;
+        pos_before = cum;
+      }
+      if (cum + mk > thr) {
+        piece = k;
+        before = cum;
+        break;
+      }
+      cum += mk;
+    }
+    if (piece < 0) {   // no crossing (an all-zero residual): the last piece of positive mass
+      piece = pos_piece;
+      before = pos_before;
+    }
+    sh.fin_piece = piece;
+    sh.fin_before = before;
+    sh.fin_thr = thr;
+  }
+  __syncthreads();
+  const int piece = sh.fin_piece;
+  const double thr = sh.fin_thr;
+  double before = sh.fin_before;
+  const float* trow = a.target_logits + row * V;
+  const float* drow = a.draft_logits + row * V;
+  int pick = INT_MAX, last_pos = -1;
+#pragma unroll 1
+  for (int sp = 0; sp < SUB && pick == INT_MAX; ++sp) {
+    const int x0 = (piece * SUB + sp) * SUBW, x1 = min(V, x0 + SUBW);
+    if (x0 >= V) break;
+    float lt[EPT], ld[EPT];
+    load_sub<VEC>(trow, x0, x1, lt);
+    load_sub<VEC>(drow, x0, x1, ld);
+    const int base = x0 + tid * EPT;
+    double r[EPT], mine = 0.0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      r[e] = 0.0;
+      if (base + e < x1) {
+        const double p = scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+        const double q = C == 0.0 ? 0.0 : scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd;
+        r[e] = fmax(p - C * q, 0.0);
+      }
+      mine += r[e];
+    }
+    double total;
+    double cum = before + block_exclusive_scan(mine, total, sh);
+    int pk = INT_MAX, lp = -1;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      cum += r[e];
+      if (pk == INT_MAX && cum > thr) pk = base + e;
+      if (r[e] > 0.0) lp = base + e;
+    }
+    pick = block_int<false>(pk, sh);
+    last_pos = max(last_pos, block_int<true>(lp, sh));
+    before += total;
+  }
+  // (rounding between the piece masses and this prefix can leave the crossing just outside the piece: then
+  // the piece's last entry of positive mass)
+  if (pick == INT_MAX) pick = last_pos >= 0 ? last_pos : min(V - 1, piece * SUB * SUBW);
+  if (tid == 0) store_coherent(a.final_token + row, pick);
+  wait_vector_memory();
 }
 
 // ---------------------------------------------------------------------------------------------------- walk
-template <bool VEC>
 __device__ void walk(const SampledArgs& a, int b, Shared& sh) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int T = a.T, V = a.V;
+  const int T = a.T;
   const size_t rb = (size_t)b * T;
-  if (tid < T) sh.par[tid] = a.parent[rb + tid];
-  __syncthreads();
-
-  // every child's test, in parallel: the state before c is the state after c's previous sibling
-  int kept = 0;
-  if (tid >= 1 && tid < T) {
-    const int n = sh.par[tid];
-    const int x = a.tokens[rb + tid];
-    if (n >= 0 && n < tid && x >= 0 && x < V) {
-      int prev = -1;
-      for (int k = tid - 1; k > n; --k)
-        if (sh.par[k] == n) { prev = k; break; }
-      double C = 0.0, D = 1.0;
-      if (prev >= 0) {
-        C = load_d(a.post + (rb + prev) * 4 + 0);
-        D = load_d(a.post + (rb + prev) * 4 + 1);
-      }
-      const double* rs = a.row_stat + (rb + n) * 4;
-      const double Mt = load_d(rs + 0), St = load_d(rs + 1), Md = load_d(rs + 2), Sd = load_d(rs + 3);
-      const double lt = a.target_logits[(rb + n) * V + x], ld = a.draft_logits[(rb + n) * V + x];
-      const double p = scaled_exp(lt - Mt, a.inv_tau) / St;
-      const double q = scaled_exp(ld - Md, a.inv_tau) / Sd;
-      const double u = a.uniforms[rb + tid];
-      kept = (u * q) * D < fmax(p - C * q, 0.0);
-    }
-  }
-  if (tid < T) sh.acc[tid] = kept;
-  __syncthreads();
-
-  // the walk (wave 0; lane l holds nodes l and l + 64): the first kept child of each node, then the state
-  // after the last node's last child
   if (wave == 0) {
-    int par_h[2], acc_h[2];
+    // lane l holds nodes l and l + 64; the first kept child of each node, from the root
+    int par_h[2], kept_h[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int i = lane + 64 * h;
-      par_h[h] = i < T ? sh.par[i] : -1;
-      acc_h[h] = i < T ? sh.acc[i] : 0;
+      par_h[h] = i < T ? a.parent[rb + i] : -1;
+      kept_h[h] = i > 0 && i < T ? load_coherent(a.kept + rb + i) : 0;
     }
     int node = 0, depth = 0;
     if (lane == 0) sh.path[0] = 0;
     while (true) {
-      const uint64_t k0 = __ballot(acc_h[0] && par_h[0] == node && lane > node);
-      const uint64_t k1 = __ballot(acc_h[1] && par_h[1] == node && lane + 64 > node);
+      const uint64_t k0 = __ballot(kept_h[0] && par_h[0] == node && lane > node);
+      const uint64_t k1 = __ballot(kept_h[1] && par_h[1] == node && lane + 64 > node);
       if ((k0 | k1) == 0) break;
       node = k0 ? __builtin_ctzll(k0) : 64 + __builtin_ctzll(k1);
       ++depth;
       if (lane == 0) sh.path[depth] = node;
     }
-    const uint64_t c0 = __ballot(par_h[0] == node && lane > node);
-    const uint64_t c1 = __ballot(par_h[1] == node && lane + 64 > node);
     if (lane == 0) {
-      double C = 0.0;
-      int slot = node;
-      if (c0 | c1) {
-        const int lc = c1 ? 127 - __builtin_clzll(c1) : 63 - __builtin_clzll(c0);
-        C = load_d(a.post + (rb + lc) * 4 + 0);
-        slot = (int)load_d(a.post + (rb + lc) * 4 + 2);
-      }
-      sh.fin_node = node;
-      sh.fin_depth = depth;
-      sh.fin_c = C;
-      sh.fin_slot = slot;
+      a.accept_len[b] = depth;
+      a.next_token[b] = load_coherent(a.final_token + rb + node);
+      reset_counter(a.seq_ctr + b);
+      sh.depth = depth;
     }
   }
   __syncthreads();
-  // the piece in which the cumulative mass (piece order) first exceeds u0 * total
-  {
-    const double* m = a.mass + ((size_t)b * 2 * T + sh.fin_slot) * a.chunks;
-    for (int k = tid; k < a.chunks; k += NT) sh.pm[k] = load_d(m + k);
-    __syncthreads();
-    if (tid == 0) {
-      double total = 0.0;
-      for (int k = 0; k < a.chunks; ++k) total += sh.pm[k];
-      const double thr = (double)a.uniforms[rb] * total;
-      double cum = 0.0, before = 0.0, pos_before = 0.0;
-      int piece = -1, pos_piece = 0;
-      for (int k = 0; k < a.chunks; ++k) {
-        const double mk = sh.pm[k];
-        if (mk > 0.0) {
-          pos_piece = k;
-          pos_before = cum;
-        }
-        if (cum + mk > thr) {
-          piece = k;
-          before = cum;
-          break;
-        }
-        cum += mk;
-      }
-      if (piece < 0) {   // no crossing (an all-zero residual): the last piece of positive mass
-        piece = pos_piece;
-        before = pos_before;
-      }
-      sh.fin_piece = piece;
-      sh.fin_before = before;
-      sh.fin_thr = thr;
-    }
+  const int depth = sh.depth;
+  if (tid < T) {
+    a.accept_path[rb + tid] = tid <= depth ? sh.path[tid] : -1;
+    __hip_atomic_store(acc_word(a, b, tid), (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    reset_counter(stats_word(a, b, tid));
   }
-  __syncthreads();
-  const int node = sh.fin_node, depth = sh.fin_depth, piece = sh.fin_piece;
-  const double C = sh.fin_c, before = sh.fin_before, thr = sh.fin_thr;
-
-  // the emitted token: prefix of max(p - C q, 0) inside the chosen piece
-  const size_t row = rb + node;
-  const double* rs = a.row_stat + row * 4;
-  const double Mt = load_d(rs + 0), St = load_d(rs + 1), Md = load_d(rs + 2), Sd = load_d(rs + 3);
-  const int x0 = piece * CHUNK, x1 = min(V, x0 + CHUNK);
-  float lt[EPT], ld[EPT];
-  load_piece<VEC>(a.target_logits + row * V, x0, x1, lt);
-  load_piece<VEC>(a.draft_logits + row * V, x0, x1, ld);
-  const int base = x0 + tid * EPT;
-  double r[EPT], mine = 0.0;
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    r[e] = 0.0;
-    if (base + e < x1) {
-      const double p = scaled_exp((double)lt[e] - Mt, a.inv_tau) / St;
-      const double q = C == 0.0 ? 0.0 : scaled_exp((double)ld[e] - Md, a.inv_tau) / Sd;
-      r[e] = fmax(p - C * q, 0.0);
-    }
-    mine += r[e];
-  }
-  double cum = before + block_exclusive_scan(mine, sh);
-  int pick = INT_MAX, last_pos = -1;
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    cum += r[e];
-    if (pick == INT_MAX && cum > thr) pick = base + e;
-    if (r[e] > 0.0) last_pos = base + e;
-  }
-  pick = block_int<false>(pick, sh);
-  last_pos = block_int<true>(last_pos, sh);
-  // (rounding between the piece masses and this prefix can leave the crossing just outside the piece: then
-  // the piece's last entry of positive mass)
-  if (pick == INT_MAX) pick = last_pos >= 0 ? last_pos : x0;
-
-  int32_t* path = a.accept_path + rb;
-  if (tid < T) path[tid] = tid <= depth ? sh.path[tid] : -1;
-  if (tid == 0) {
-    a.accept_len[b] = depth;
-    a.next_token[b] = pick;
-    reset_counter(a.seq_ctr + b);
-  }
-  if (tid < T) reset_counter(row_word(a, b, tid));
 }
 
 // Arrival of a finished row at its sequence; the sequence's last row runs the walk.
-template <bool VEC>
 __device__ __forceinline__ void row_done(const SampledArgs& a, int b, Shared& sh) {
-  if (threadIdx.x == 0) sh.flag = add_word(a.seq_ctr + b, 1u) == (uint32_t)(2 * a.T - 2);
+  __syncthreads();   // every thread has read the previous flag
+  if (threadIdx.x == 0)
+    sh.flag = __hip_atomic_fetch_add(a.seq_ctr + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              (uint32_t)(2 * a.T - 2);
   __syncthreads();
-  if (sh.flag) walk<VEC>(a, b, sh);
+  if (sh.flag) walk(a, b, sh);
 }
 
 // ------------------------------------------------------------------------------------------ stats pieces
-template <bool VEC>
+template <bool VEC, int SUB>
 __device__ void stats_piece(const SampledArgs& a, int b, int i, int j, Shared& sh) {
   const int tid = threadIdx.x;
   const size_t row = (size_t)b * a.T + i;
-  const int x0 = j * CHUNK, x1 = min(a.V, x0 + CHUNK);
-  float lt[EPT], ld[EPT];
-  load_piece<VEC>(a.target_logits + row * a.V, x0, x1, lt);
-  load_piece<VEC>(a.draft_logits + row * a.V, x0, x1, ld);
+  const float* trow = a.target_logits + row * a.V;
+  const float* drow = a.draft_logits + row * a.V;
+  // per thread: running maxima and sums relative to them (rescaled when a maximum grows)
   float mt = -INFINITY, md = -INFINITY;
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    mt = fmaxf(mt, lt[e]);
-    md = fmaxf(md, ld[e]);
-  }
-  mt = block_max(mt, sh);
-  md = block_max(md, sh);
   double st = 0.0, sd = 0.0;
-  const int base = x0 + tid * EPT;
-#pragma unroll
-  for (int e = 0; e < EPT; ++e)
-    if (base + e < x1) {
-      st += scaled_exp((double)lt[e] - (double)mt, a.inv_tau);
-      sd += scaled_exp((double)ld[e] - (double)md, a.inv_tau);
+  float lt[EPT], ld[EPT], nt[EPT], nd[EPT];
+  int x0 = j * SUB * SUBW;
+  load_sub<VEC>(trow, x0, min(a.V, x0 + SUBW), lt);
+  load_sub<VEC>(drow, x0, min(a.V, x0 + SUBW), ld);
+#pragma unroll 1
+  for (int sp = 0; sp < SUB; ++sp, x0 += SUBW) {
+    if (sp + 1 < SUB) {   // the next sub-piece's loads in flight during this one's arithmetic
+      const int y0 = x0 + SUBW;
+      load_sub<VEC>(trow, y0, min(a.V, y0 + SUBW), nt);
+      load_sub<VEC>(drow, y0, min(a.V, y0 + SUBW), nd);
     }
+    float ct = -INFINITY, cd = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      ct = fmaxf(ct, lt[e]);
+      cd = fmaxf(cd, ld[e]);
+    }
+    if (ct > mt) {
+      if (st != 0.0) st *= scaled_exp((double)mt - (double)ct, a.inv_tau, sh.tab);
+      mt = ct;
+    }
+    if (cd > md) {
+      if (sd != 0.0) sd *= scaled_exp((double)md - (double)cd, a.inv_tau, sh.tab);
+      md = cd;
+    }
+    const int base = x0 + tid * EPT, x1 = min(a.V, x0 + SUBW);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      if (base + e < x1) {
+        st += scaled_exp((double)lt[e] - (double)mt, a.inv_tau, sh.tab);
+        sd += scaled_exp((double)ld[e] - (double)md, a.inv_tau, sh.tab);
+      }
+    if (sp + 1 < SUB) {
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        lt[e] = nt[e];
+        ld[e] = nd[e];
+      }
+    }
+  }
+  const float bt = block_max(mt, sh), bd = block_max(md, sh);
+  if (st != 0.0) st *= scaled_exp((double)mt - (double)bt, a.inv_tau, sh.tab);
+  if (sd != 0.0) sd *= scaled_exp((double)md - (double)bd, a.inv_tau, sh.tab);
+  mt = bt;
+  md = bd;
   st = block_sum(st, sh);
   sd = block_sum(sd, sh);
-  uint32_t* w = row_word(a, b, i);
+  uint32_t* w = stats_word(a, b, i);
   if (tid == 0) {
     double* ps = a.piece_stat + (row * a.chunks + j) * 4;
     store_d(ps + 0, mt);
@@ -361,148 +419,233 @@ __device__ void stats_piece(const SampledArgs& a, int b, int i, int j, Shared& s
     store_d(ps + 2, md);
     store_d(ps + 3, sd);
     wait_vector_memory();
-    sh.flag = (add_word(w, kStatsOne) & 0xffffu) == (uint32_t)(a.chunks - 1);
+    sh.flag = arrive_last(w, (uint32_t)a.chunks);
   }
   __syncthreads();
   if (!sh.flag) return;
 
-  // the row's last piece: maxima, normalisers and the target mass of every piece
-  const double* ps = a.piece_stat + row * a.chunks * 4;
-  float Mt = -INFINITY, Md = -INFINITY;
-  for (int k = tid; k < a.chunks; k += NT) {
-    Mt = fmaxf(Mt, (float)load_d(ps + 4 * k + 0));
-    Md = fmaxf(Md, (float)load_d(ps + 4 * k + 2));
+  // the row's last piece: at a leaf, the token emitted if the walk ends here (the target's own distribution)
+  const int T = a.T;
+  const bool child = tid > i && tid < T && a.parent[(size_t)b * T + tid] == i;
+  if (!__syncthreads_or(child)) {
+    const RowStat rs = merge_stats(a, row, sh);
+    final_draw<VEC, SUB>(a, b, i, rs, 0.0, -1, sh);
   }
-  Mt = block_max(Mt, sh);
-  Md = block_max(Md, sh);
-  double St = 0.0, Sd = 0.0;
-  for (int k = tid; k < a.chunks; k += NT) {
-    St += load_d(ps + 4 * k + 1) * scaled_exp(load_d(ps + 4 * k + 0) - (double)Mt, a.inv_tau);
-    Sd += load_d(ps + 4 * k + 3) * scaled_exp(load_d(ps + 4 * k + 2) - (double)Md, a.inv_tau);
-  }
-  St = block_sum(St, sh);
-  Sd = block_sum(Sd, sh);
-  double* m = a.mass + ((size_t)b * 2 * a.T + i) * a.chunks;
-  for (int k = tid; k < a.chunks; k += NT)
-    store_d(m + k, load_d(ps + 4 * k + 1) * scaled_exp(load_d(ps + 4 * k + 0) - (double)Mt, a.inv_tau) / St);
-  if (tid == 0) {
-    double* rs = a.row_stat + row * 4;
-    store_d(rs + 0, Mt);
-    store_d(rs + 1, St);
-    store_d(rs + 2, Md);
-    store_d(rs + 3, Sd);
-  }
-  wait_vector_memory();
-  __syncthreads();
-  if (tid == 0) add_word(w, kStatsOne);   // the half now reads chunks + 1: published
-  row_done<VEC>(a, b, sh);
+  row_done(a, b, sh);
 }
 
 // ------------------------------------------------------------------------------------------- pass pieces
-template <bool VEC>
+template <bool VEC, int SUB>
 __device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = a.T;
   const size_t rb = (size_t)b * T;
-  if (tid < c) sh.par[tid] = a.parent[rb + tid];
-  const int n = a.parent[rb + c];
+  if (tid < T) sh.par[tid] = a.parent[rb + tid];
   __syncthreads();
+  const int n = sh.par[c];
   const bool valid = n >= 0 && n < c;
+  const int x = a.tokens[rb + c];
   double z = 0.0, C = 0.0, D = 1.0, CC = 1.0;
-  int slot = n;
+  int src = -1;
+  RowStat rs{};
   if (valid) {
-    int prev = -1;
-    for (int k = tid; k < c; k += NT)
-      if (k > n && sh.par[k] == n) prev = max(prev, k);
-    prev = block_int<true>(prev, sh);
     const size_t row = rb + n;
-    const int x0 = j * CHUNK, x1 = min(a.V, x0 + CHUNK);
+    const float* trow = a.target_logits + row * a.V;
+    const float* drow = a.draft_logits + row * a.V;
+    // one-sub-piece pieces: loaded now, p and q computed while the earlier siblings may still be running;
+    // larger pieces (where throughput matters more than the wait chain) are streamed after the waits
+    constexpr bool HOLD = SUB == 1;
+    const int x0 = j * SUB * SUBW, x1 = min(a.V, x0 + SUBW);
     float lt[EPT], ld[EPT];
-    load_piece<VEC>(a.target_logits + row * a.V, x0, x1, lt);
-    load_piece<VEC>(a.draft_logits + row * a.V, x0, x1, ld);
-    if (tid == 0) wait_half(row_word(a, b, n), 0, (uint32_t)a.chunks + 1);
+    if (HOLD) {
+      load_sub<VEC>(trow, x0, x1, lt);
+      load_sub<VEC>(drow, x0, x1, ld);
+    }
+    // c's earlier siblings (in index order) and whether c is n's last child
+    if (wave == 0) {
+      const int k0 = lane, k1 = lane + 64;
+      const bool s0 = k0 > n && k0 < c && sh.par[k0] == n;
+      const bool s1 = k1 > n && k1 < c && k1 < T && sh.par[k1] == n;
+      const bool l0 = k0 > c && k0 < T && sh.par[k0] == n;
+      const bool l1 = k1 > c && k1 < T && sh.par[k1] == n;
+      const uint64_t b0 = __ballot(s0), b1 = __ballot(s1);
+      const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+      if (s0) sh.sib[__builtin_popcountll(b0 & below)] = k0;
+      if (s1) sh.sib[__builtin_popcountll(b0) + __builtin_popcountll(b1 & below)] = k1;
+      const bool later = (__ballot(l0) | __ballot(l1)) != 0;
+      if (lane == 0) {
+        sh.nsib = __builtin_popcountll(b0) + __builtin_popcountll(b1);
+        sh.last_child = !later;
+      }
+      // every piece of n's statistics
+      if (lane == 0) {
+        const uint32_t* w = stats_word(a, b, n);
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)a.chunks) {
+          if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) break;
+          __builtin_amdgcn_s_sleep(2);
+        }
+      }
+    }
     __syncthreads();
-    const double* rs = a.row_stat + row * 4;
-    const double Mt = load_d(rs + 0), St = load_d(rs + 1), Md = load_d(rs + 2), Sd = load_d(rs + 3);
-    const int base = x0 + tid * EPT;
+    rs = merge_stats(a, row, sh);
     double p[EPT], q[EPT];
+    if (HOLD) {
+      const int base = x0 + tid * EPT;
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      const bool in = base + e < x1;
-      p[e] = in ? scaled_exp((double)lt[e] - Mt, a.inv_tau) / St : 0.0;
-      q[e] = in ? scaled_exp((double)ld[e] - Md, a.inv_tau) / Sd : 0.0;
+      for (int e = 0; e < EPT; ++e) {
+        const bool in = base + e < x1;
+        p[e] = in ? scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st : 0.0;
+        q[e] = in ? scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd : 0.0;
+      }
     }
-    if (prev >= 0) {
-      if (tid == 0) wait_half(row_word(a, b, prev), 16, (uint32_t)a.chunks + 1);
-      __syncthreads();
-      C = load_d(a.post + (rb + prev) * 4 + 0);
-      D = load_d(a.post + (rb + prev) * 4 + 1);
-      slot = (int)load_d(a.post + (rb + prev) * 4 + 2);
+    // the earlier siblings' residual masses: complete once their accumulators count every piece
+    const int nsib = sh.nsib;
+    if (wave == 0 && nsib > 0) {
+      const uint64_t* w0 = lane < nsib ? acc_word(a, b, sh.sib[lane]) : nullptr;
+      const uint64_t* w1 = lane + 64 < nsib ? acc_word(a, b, sh.sib[lane + 64]) : nullptr;
+      uint64_t v0 = 0, v1 = 0;
+      const uint64_t full = (uint64_t)a.chunks << kArrivalShift;
+      const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+      while (true) {
+        if (w0) v0 = load_u64(w0);
+        if (w1) v1 = load_u64(w1);
+        const bool done = (!w0 || (v0 & ~kMassMask) == full) && (!w1 || (v1 & ~kMassMask) == full);
+        if (__ballot(!done) == 0) break;
+        if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+      if (w0) sh.zs[lane] = (double)(v0 & kMassMask) * kFixUnit;
+      if (w1) sh.zs[lane + 64] = (double)(v1 & kMassMask) * kFixUnit;
     }
+    __syncthreads();
+    if (tid == 0) {
+      double c_run = 0.0, d_run = 1.0;
+      int s_run = -1;
+      for (int k = 0; k < nsib; ++k) {
+        const double zk = sh.zs[k];
+        if (zk > 0.0) {
+          c_run += d_run;
+          d_run = zk;
+          s_run = sh.sib[k];
+        }
+      }
+      sh.st_c = c_run;
+      sh.st_d = d_run;
+      sh.st_slot = s_run;
+    }
+    __syncthreads();
+    C = sh.st_c;
+    D = sh.st_d;
+    src = sh.st_slot;
     CC = C + D;
+    double px = 0.0, qx = 0.0;
+    bool mine = false;
+    if (HOLD) {
+      const int base = x0 + tid * EPT;
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) z += fmax(p[e] - CC * q[e], 0.0);
+      for (int e = 0; e < EPT; ++e) {
+        z += fmax(p[e] - CC * q[e], 0.0);
+        if (base + e == x && base + e < x1) {
+          px = p[e];
+          qx = q[e];
+          mine = true;
+        }
+      }
+    } else {
+      float nt[EPT], nd[EPT];
+      int y0 = x0;
+      load_sub<VEC>(trow, y0, min(a.V, y0 + SUBW), lt);
+      load_sub<VEC>(drow, y0, min(a.V, y0 + SUBW), ld);
+#pragma unroll 1
+      for (int sp = 0; sp < SUB; ++sp, y0 += SUBW) {
+        if (sp + 1 < SUB) {   // the next sub-piece's loads in flight during this one's arithmetic
+          load_sub<VEC>(trow, y0 + SUBW, min(a.V, y0 + 2 * SUBW), nt);
+          load_sub<VEC>(drow, y0 + SUBW, min(a.V, y0 + 2 * SUBW), nd);
+        }
+        const int base = y0 + tid * EPT, y1 = min(a.V, y0 + SUBW);
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+          if (base + e < y1) {
+            const double pe = scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+            const double qe = scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd;
+            z += fmax(pe - CC * qe, 0.0);
+            if (base + e == x) {
+              px = pe;
+              qx = qe;
+              mine = true;
+            }
+          }
+        }
+        if (sp + 1 < SUB) {
+#pragma unroll
+          for (int e = 0; e < EPT; ++e) {
+            lt[e] = nt[e];
+            ld[e] = nd[e];
+          }
+        }
+      }
+    }
+    // c's decision, by the thread holding its token
+    if (mine) store_coherent(a.kept + rb + c, (int32_t)(((double)a.uniforms[rb + c] * qx) * D < fmax(px - C * qx, 0.0)));
   }
+  if ((!valid || x < 0 || x >= a.V) && j == 0 && tid == 0) store_coherent(a.kept + rb + c, 0);
   z = block_sum(z, sh);
-  uint32_t* w = row_word(a, b, c);
-  double* m = a.mass + ((size_t)b * 2 * T + T + c) * a.chunks;
+  if (tid == 0) store_d(a.mass + (rb + c) * a.chunks + j, z);
+  wait_vector_memory();
+  __syncthreads();
   if (tid == 0) {
-    store_d(m + j, z);
-    wait_vector_memory();
-    sh.flag = ((add_word(w, kPassOne) >> 16) & 0xffffu) == (uint32_t)(a.chunks - 1);
+    const uint64_t mine = (uint64_t)rint(z * kFixScale);
+    const uint64_t old = __hip_atomic_fetch_add(acc_word(a, b, c), (1ull << kArrivalShift) + mine, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    sh.flag = (int)(old >> kArrivalShift) == a.chunks - 1;
+    sh.zs[0] = (double)((old & kMassMask) + mine) * kFixUnit;   // the row's whole residual mass
   }
   __syncthreads();
   if (!sh.flag) return;
-
-  // the row's last piece: the state after rejecting c
-  double Z = 0.0;
-  for (int k = tid; k < a.chunks; k += NT) Z += load_d(m + k);
-  Z = block_sum(Z, sh);
-  if (tid == 0) {
-    double* ps = a.post + (rb + c) * 4;
-    const bool moved = valid && Z > 0.0;
-    store_d(ps + 0, moved ? CC : C);
-    store_d(ps + 1, moved ? Z : D);
-    store_d(ps + 2, (double)(moved ? T + c : slot));
-    wait_vector_memory();
-    add_word(w, kPassOne);   // the half now reads chunks + 1: published
+  // c's last piece: if c is n's last child, the token emitted if the walk ends at n (every child rejected)
+  if (valid && sh.last_child) {
+    const bool moved = sh.zs[0] > 0.0;
+    final_draw<VEC, SUB>(a, b, n, rs, moved ? CC : C, moved ? c : src, sh);
+    __syncthreads();
   }
-  row_done<VEC>(a, b, sh);
+  row_done(a, b, sh);
 }
 
-template <bool VEC>
+template <bool VEC, int SUB>
 __global__ __launch_bounds__(NT) void tree_accept_sampled_kernel(SampledArgs a) {
   __shared__ Shared sh;
-  __shared__ uint32_t ticket_s;
-  if (threadIdx.x == 0) {
-    const uint32_t t = add_word(a.ticket, 1u);
-    if (t == gridDim.x - 1) reset_counter(a.ticket);   // every workgroup has drawn: clear for the next call
-    ticket_s = t;
-  }
+  sh.tab[threadIdx.x] = exp2((double)threadIdx.x * (1.0 / 256.0));
   __syncthreads();
-  const long long t = ticket_s;
+  const long long t = blockIdx.x;
   const long long stats = (long long)a.B * a.T * a.chunks;
   if (t < stats) {
     const int j = (int)(t % a.chunks);
     const long long r = t / a.chunks;
-    stats_piece<VEC>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
+    stats_piece<VEC, SUB>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
   } else {
     const long long u = t - stats;
     const long long per_child = (long long)a.B * a.chunks;
     const int c = 1 + (int)(u / per_child);
     const long long v = u % per_child;
-    pass_piece<VEC>(a, (int)(v / a.chunks), c, (int)(v % a.chunks), sh);
+    pass_piece<VEC, SUB>(a, (int)(v / a.chunks), c, (int)(v % a.chunks), sh);
   }
 }
 
 }  // namespace
 
 hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream) {
+  static_assert(NT == 256, "the exp table is filled one entry per thread");
   const long long grid = (long long)a.B * (2 * a.T - 1) * a.chunks;
-  if (a.vec4)
-    hipLaunchKernelGGL(tree_accept_sampled_kernel<true>, dim3((unsigned)grid), dim3(NT), 0, stream, a);
-  else
-    hipLaunchKernelGGL(tree_accept_sampled_kernel<false>, dim3((unsigned)grid), dim3(NT), 0, stream, a);
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(NT), 0, stream, a); };
+  const bool large = a.sub_pieces == kSampledSubLarge;
+  if (a.vec4) {
+    if (large) go(tree_accept_sampled_kernel<true, kSampledSubLarge>);
+    else go(tree_accept_sampled_kernel<true, 1>);
+  } else {
+    if (large) go(tree_accept_sampled_kernel<false, kSampledSubLarge>);
+    else go(tree_accept_sampled_kernel<false, 1>);
+  }
   return hipGetLastError();
 }
 

@@ -200,13 +200,17 @@ def test_sampled_accept_rejections_and_sizes(D):
     for B, T, V in [(1, 60, 32000), (16, 128, 152064), (3, 1, 1), (2, 7, 2049)]:
         assert lib.dreams_tree_accept_sampled_workspace_size(B, T, V, ctypes.byref(n)) == 0
         rows, chunks = B * T, (V + 2047) // 2048
-        assert n.value == 65536 + 2 * r256(rows * 32) + r256(rows * chunks * 32) + r256(rows * 2 * chunks * 8)
+        if rows * chunks > 4096:           # large pieces
+            chunks = (V + 8191) // 8192
+        assert n.value == 65536 + r256(rows * chunks * 32) + r256(rows * chunks * 8) + r256(rows * 8)
     assert lib.dreams_tree_accept_sampled_workspace_size(0, 60, 32000, ctypes.byref(n)) == 0 and n.value == 0
     assert lib.dreams_tree_accept_sampled_workspace_size(1, 0, 32000, ctypes.byref(n)) == -1
     assert lib.dreams_tree_accept_sampled_workspace_size(1, 129, 32000, ctypes.byref(n)) == -1
     assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, 0, ctypes.byref(n)) == -1
-    assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, (1 << 21) + 1, ctypes.byref(n)) == -2
-    assert lib.dreams_tree_accept_sampled_workspace_size(200, 128, 100, ctypes.byref(n)) == -2   # counters
+    assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, (1 << 21) + 1, ctypes.byref(n)) == 0   # large
+    assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, (1 << 23) + 1, ctypes.byref(n)) == -2
+    assert lib.dreams_tree_accept_sampled_workspace_size(31, 128, 100, ctypes.byref(n)) == 0
+    assert lib.dreams_tree_accept_sampled_workspace_size(32, 128, 100, ctypes.byref(n)) == -2    # counters
     assert lib.dreams_tree_accept_sampled_workspace_size(1, 60, 10, None) == -1
     fake = ctypes.c_void_p(0x100000)
     f = lib.dreams_tree_accept_sampled

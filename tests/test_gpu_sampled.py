@@ -173,3 +173,15 @@ def test_rejected_arguments(dev):
     for tau in (0.0, -1.0, float("inf"), float("nan")):
         with pytest.raises(dreams.DreamsError):
             dreams.tree_accept_sampled(z, z, i2, i2, u2, tau)
+
+
+@pytest.mark.parametrize("V", [20000, 20001])
+def test_large_pieces(dev, V):
+    """Enough rows that the vocabulary is cut into 8192-entry pieces (streamed in 2048-entry sub-pieces), with a
+    ragged last piece whose trailing sub-pieces lie wholly past the vocabulary; V = 20001 takes the scalar
+    loads."""
+    B, T = 30, 128
+    assert B * T * ((V + 2047) // 2048) > 4096
+    rng = np.random.default_rng(V)
+    tl, dl, tok, par, uni = random_case(rng, B, T, V, 8, 6, noise=0.7)
+    run_and_compare(dev, tl, dl, tok, par, uni, 1.0, "large pieces V=%d" % V)
