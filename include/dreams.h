@@ -2,10 +2,11 @@
  * dreams.h -- C ABI of libdreams.so, the MI355X (gfx950) tree-verification step of DREAM-S speculative
  * decoding for vision-language models.
  *
- * The step has three verbs (acceptance in two forms), run back to back on one HIP stream:
+ * The step has three verbs (acceptance in three forms), run back to back on one HIP stream:
  *   dreams_tree_verify_attn  tree-masked attention of the draft-token tree against the KV cache
  *   dreams_tree_accept       greedy acceptance of the longest target-consistent root-to-node path
  *   dreams_tree_accept_sampled  acceptance at temperature tau > 0 (accept-or-resample down the tree)
+ *   dreams_tree_accept_lm_head  greedy acceptance from final hidden states (LM head fused with the argmax)
  *   dreams_kv_commit         compaction of the accepted path's K/V into the cache
  *
  * Conventions shared by every entry point
@@ -280,6 +281,36 @@ dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int
                                            const int32_t* draft_tokens, const int32_t* parent,
                                            const float* uniforms, int32_t* accept_len, int32_t* accept_path,
                                            int32_t* next_token, void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream);
+
+/* Bytes of workspace dreams_tree_accept_lm_head needs (0 only when batch is 0): the 64 KiB counter region
+ * (unused by this verb, kept so that one workspace serves every verb) and 8 bytes per row per 64-entry tile
+ * of the vocabulary.  DREAMS_ERR_UNSUPPORTED if hidden is not a multiple of 256. */
+dreams_status_t dreams_tree_accept_lm_head_workspace_size(int32_t batch, int32_t num_nodes, int32_t hidden,
+                                                          int32_t vocab, size_t* bytes);
+
+/*
+ * dreams_tree_accept_lm_head -- dreams_tree_accept with the LM head fused in: the target logits of every tree
+ * node are formed from its final hidden state and the LM head's weight (the paper, Section 2, "Speculative
+ * decoding": the target's token at each position is the argmax of its logits),
+ *
+ *   logit[b,i,v] = sum_k hidden_states[b,i,k] * lm_weight[v,k]      (bf16 operands, fp32 accumulation)
+ *
+ * and the greedy rule of dreams_tree_accept is applied to them, without the logits ever being written to
+ * memory.  tgt[i] is the smallest index attaining the row maximum of the logits as computed here (fp32, a
+ * fixed order of accumulation); results are otherwise exactly those of dreams_tree_accept on these logits.
+ *
+ *   hidden         H, a multiple of 256
+ *   hidden_states  device [B, T, H] bfloat16, 16-byte aligned
+ *   lm_weight      device [V, H] bfloat16 (one row per vocabulary entry), 16-byte aligned
+ *   draft_tokens, parent, accept_len, accept_path, next_token, target_argmax: as for dreams_tree_accept
+ *   workspace      device, >= dreams_tree_accept_lm_head_workspace_size bytes (see "Workspaces" above).
+ */
+dreams_status_t dreams_tree_accept_lm_head(int32_t batch, int32_t num_nodes, int32_t hidden, int32_t vocab,
+                                           const void* hidden_states, const void* lm_weight,
+                                           const int32_t* draft_tokens, const int32_t* parent,
+                                           int32_t* accept_len, int32_t* accept_path, int32_t* next_token,
+                                           int32_t* target_argmax, void* workspace, size_t workspace_bytes,
                                            hipStream_t stream);
 
 /*

@@ -291,3 +291,28 @@ def attn_entropy_select(ae) -> int:
         if best_score is None or score < best_score:
             best, best_score = l, score
     return best
+
+
+def lm_head_logits(hidden_bits, weight_bits) -> np.ndarray:
+    """The target's logits from its final hidden states and its LM head (Section 2, "Speculative decoding":
+    the target's token at a position is the argmax of these): logit[..., v] = sum_k hidden[..., k] *
+    weight[v, k].  Inputs are bfloat16 bit patterns (uint16), decoded exactly; products and sums in fp64, the
+    one library step being numpy's matrix product.  hidden_bits [..., H], weight_bits [V, H] -> fp64 [..., V]."""
+    def decode(bits):
+        b = np.ascontiguousarray(bits, dtype=np.uint16)
+        return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    h = decode(hidden_bits)
+    w = decode(weight_bits)
+    return h @ w.T
+
+
+def tree_accept_from_argmax(target_argmax, tokens, parent):
+    """The greedy rule (oracle_tree_accept) on given per-node target tokens: one-hot logits at those tokens.
+    target_argmax, tokens, parent [B, T] int -> (accept_len, accept_path, next_token)."""
+    am = np.asarray(target_argmax, dtype=np.int64)
+    B, T = am.shape
+    V = int(max(am.max(initial=0), np.asarray(tokens).max(initial=0))) + 1
+    onehot = np.zeros((B, T, V), dtype=np.float32)
+    np.put_along_axis(onehot, am[:, :, None], 1.0, axis=2)
+    alen, path, nxt, _ = default().tree_accept(onehot, tokens, parent)
+    return alen, path, nxt

@@ -521,6 +521,93 @@ dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int
   return ok();
 }
 
+// ----------------------------------------------------------------------------------- LM head + argmax
+struct LmPlan {
+  int ntiles;
+  size_t val_off, idx_off, bytes;
+};
+
+dreams_status_t plan_lm_head(int32_t B, int32_t T, int32_t H, int32_t V, LmPlan* p) {
+  if (B < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", B);
+  if (T < 1 || T > kMaxNodes) return fail(DREAMS_ERR_INVALID_ARG, "num_nodes = %d outside [1, %d]", T, kMaxNodes);
+  if (V < 1) return fail(DREAMS_ERR_INVALID_ARG, "vocab = %d < 1", V);
+  if (H < 1) return fail(DREAMS_ERR_INVALID_ARG, "hidden = %d < 1", H);
+  if (H % kLmHiddenMultiple)
+    return fail(DREAMS_ERR_UNSUPPORTED, "hidden = %d is not a multiple of %d", H, kLmHiddenMultiple);
+  *p = LmPlan{};
+  if (B == 0) return DREAMS_OK;
+  const long long M = (long long)B * T, ntiles = ((long long)V + kLmTile - 1) / kLmTile;
+  if ((M + kLmTile - 1) / kLmTile > 65535) return fail(DREAMS_ERR_UNSUPPORTED, "batch * num_nodes too large");
+  p->ntiles = (int)ntiles;
+  size_t off = kCounterBytes;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  p->val_off = take((size_t)M * ntiles * sizeof(float));
+  p->idx_off = take((size_t)M * ntiles * sizeof(int32_t));
+  p->bytes = off;
+  return DREAMS_OK;
+}
+
+dreams_status_t dreams_tree_accept_lm_head_workspace_size(int32_t batch, int32_t num_nodes, int32_t hidden,
+                                                          int32_t vocab, size_t* bytes) {
+  if (!bytes) return fail(DREAMS_ERR_INVALID_ARG, "bytes is NULL");
+  LmPlan p;
+  dreams_status_t st = plan_lm_head(batch, num_nodes, hidden, vocab, &p);
+  if (st != DREAMS_OK) return st;
+  *bytes = p.bytes;
+  return ok();
+}
+
+dreams_status_t dreams_tree_accept_lm_head(int32_t batch, int32_t num_nodes, int32_t hidden, int32_t vocab,
+                                           const void* hidden_states, const void* lm_weight,
+                                           const int32_t* draft_tokens, const int32_t* parent,
+                                           int32_t* accept_len, int32_t* accept_path, int32_t* next_token,
+                                           int32_t* target_argmax, void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream) {
+  LmPlan p;
+  dreams_status_t st = plan_lm_head(batch, num_nodes, hidden, vocab, &p);
+  if (st != DREAMS_OK) return st;
+  if (batch == 0) return ok();
+  if (!hidden_states || !lm_weight || !draft_tokens || !parent || !accept_len || !accept_path || !next_token)
+    return fail(DREAMS_ERR_INVALID_ARG,
+                "hidden_states, lm_weight, draft_tokens, parent, accept_len, accept_path and next_token must not be "
+                "NULL");
+  if (!aligned(hidden_states, 16) || !aligned(lm_weight, 16))
+    return fail(DREAMS_ERR_INVALID_ARG, "hidden_states and lm_weight must be 16-byte aligned");
+  if (!aligned(draft_tokens, 4) || !aligned(parent, 4) || !aligned(accept_len, 4) || !aligned(accept_path, 4) ||
+      !aligned(next_token, 4) || (target_argmax && !aligned(target_argmax, 4)))
+    return fail(DREAMS_ERR_INVALID_ARG, "an int32 argument is not 4-byte aligned");
+  if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", p.bytes);
+  if (workspace_bytes < p.bytes)
+    return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, p.bytes);
+  if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  LmHeadArgs a{};
+  a.hidden = (const __bf16*)hidden_states;
+  a.weight = (const __bf16*)lm_weight;
+  a.tokens = draft_tokens;
+  a.parent = parent;
+  a.accept_len = accept_len;
+  a.accept_path = accept_path;
+  a.next_token = next_token;
+  a.target_argmax = target_argmax;
+  char* ws = (char*)workspace;
+  a.part_val = (float*)(ws + p.val_off);
+  a.part_idx = (int32_t*)(ws + p.idx_off);
+  a.B = batch;
+  a.T = num_nodes;
+  a.H = hidden;
+  a.V = vocab;
+  a.M = batch * num_nodes;
+  a.ntiles = p.ntiles;
+  hipError_t e = launch_lm_head_accept(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "LM head accept launch");
+  return ok();
+}
+
 dreams_status_t dreams_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream) {
   if (!src || !sink) return fail(DREAMS_ERR_INVALID_ARG, "src and sink must not be NULL");
   if (!aligned(src, 16) || bytes % 16 != 0)

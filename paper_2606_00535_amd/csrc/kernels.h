@@ -170,6 +170,30 @@ struct SampledArgs {
 
 hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream);
 
+// ------------------------------------------------------------------------------ LM head + argmax
+// A workgroup per (kLmTile vocabulary entries, kLmTile rows) of the logits hidden * weight^T, four waves
+// splitting the hidden axis; each row's best (value, index) per tile goes to part_val / part_idx, and a second
+// kernel (a workgroup per sequence) merges them and runs the greedy path scan.
+constexpr int kLmThreads = 256;
+constexpr int kLmTile = 64;
+constexpr int kLmHiddenMultiple = 256;   // the hidden size must be a multiple (four quarters of 64-deep steps)
+
+struct LmHeadArgs {
+  const __bf16* hidden;    // [M, H], M = B * T
+  const __bf16* weight;    // [V, H]
+  const int32_t* tokens;   // [B, T]
+  const int32_t* parent;   // [B, T]
+  int32_t* accept_len;     // [B]
+  int32_t* accept_path;    // [B, T]
+  int32_t* next_token;     // [B]
+  int32_t* target_argmax;  // [B, T] or nullptr
+  float* part_val;         // [M, ntiles]
+  int32_t* part_idx;       // [M, ntiles]
+  int B, T, H, V, M, ntiles;
+};
+
+hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream);
+
 // ------------------------------------------------------------------------------------------ commit
 constexpr int kCommitThreads = 256;
 constexpr int kCommitRowsPerPass = 32;

@@ -18,6 +18,7 @@
 //     smallest new member is the deepest consistent node (smallest index among equals).
 // The pieces travel through device-scope stores and loads (see kernels.h); the tree (tokens, parents) is
 // fetched by every workgroup at entry, ahead of its logits, for whichever one ends up finishing the sequence.
+#include "accept_scan.h"
 #include "kernels.h"
 
 #include <limits.h>
@@ -157,55 +158,7 @@ __global__ __launch_bounds__(kAcceptThreads) void tree_accept_kernel(AcceptArgs 
   if (a.target_argmax && tid < T) a.target_argmax[(size_t)b * T + tid] = am_s[tid];
   if (wave != 0) return;
 
-  // Path scan, by wave 0 alone (lane l holds nodes l and l + 64): a sweep from the root, one depth per round.
-  // A node joins the consistent set when its draft equals the target's token at its parent and the parent
-  // joined the round before; the set lives in two 64-bit wave-uniform masks grown by ballots.  The last
-  // non-empty round holds the deepest consistent nodes: the smallest index among them is `last`, the number
-  // of rounds its depth.
-  int par_h[2];
-  bool ok_h[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int i = lane + 64 * h;
-    const int p = i < T ? par_s[i] : -1;
-    par_h[h] = p;
-    ok_h[h] = i > 0 && i < T && p >= 0 && p < i && tok_s[i] == am_s[p];
-  }
-  auto in_set = [](uint64_t s0, uint64_t s1, int x) {
-    return (((x < 64 ? s0 : s1) >> (x & 63)) & 1ull) != 0;
-  };
-  uint64_t c0 = 1, c1 = 0;      // the root is always consistent
-  uint64_t l0 = 1, l1 = 0;      // the last round's new members
-  int depth = 0;
-  while (true) {
-    const bool j0 = ok_h[0] && !in_set(c0, c1, lane) && in_set(c0, c1, par_h[0]);
-    const bool j1 = ok_h[1] && !in_set(c0, c1, lane + 64) && in_set(c0, c1, par_h[1]);
-    const uint64_t n0 = __ballot(j0), n1 = __ballot(j1);
-    if ((n0 | n1) == 0) break;
-    c0 |= n0;
-    c1 |= n1;
-    l0 = n0;
-    l1 = n1;
-    ++depth;
-  }
-  const int last = l0 ? __builtin_ctzll(l0) : 64 + __builtin_ctzll(l1);
-  const int alen = depth;
-  int32_t* path = a.accept_path + (size_t)b * T;
-  if (lane == 0) {
-    a.accept_len[b] = alen;
-    a.next_token[b] = am_s[last];
-  }
-  // the path from the root to `last`, read off the parents held in the lanes (uniform steps, no LDS)
-  int j = last;
-  for (int k = alen; k >= 0; --k) {
-    if (lane == 0) path[k] = j;
-    j = j < 64 ? __builtin_amdgcn_readlane(par_h[0], j) : __builtin_amdgcn_readlane(par_h[1], j - 64);
-  }
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int i = lane + 64 * h;
-    if (i > alen && i < T) path[i] = -1;
-  }
+  path_scan_wave(am_s, tok_s, par_s, T, a.accept_len + b, a.accept_path + (size_t)b * T, a.next_token + b);
 }
 
 }  // namespace

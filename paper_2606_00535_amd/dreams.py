@@ -26,7 +26,7 @@ EXPORTS = (
     "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy", "dreams_attn_entropy_mean",
     "dreams_attn_entropy_select", "dreams_visual_importance_workspace_size", "dreams_visual_importance",
     "dreams_visual_topk", "dreams_visual_gather", "dreams_tree_accept_sampled_workspace_size",
-    "dreams_tree_accept_sampled",
+    "dreams_tree_accept_sampled", "dreams_tree_accept_lm_head_workspace_size", "dreams_tree_accept_lm_head",
 )
 
 
@@ -83,6 +83,8 @@ def lib():
                 L.dreams_tree_accept_sampled_workspace_size.argtypes = [I32, I32, I32, ctypes.POINTER(SZ)]
                 L.dreams_tree_accept_sampled.argtypes = [I32, I32, I32, ctypes.c_double, P, P, P, P, P, P, P, P, P,
                                                          SZ, P]
+                L.dreams_tree_accept_lm_head_workspace_size.argtypes = [I32, I32, I32, I32, ctypes.POINTER(SZ)]
+                L.dreams_tree_accept_lm_head.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P]
                 L.dreams_visual_gather.argtypes = [I32, I32, I32, I32, ctypes.c_int, P, P, I32, P, I32, P, P, P]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
@@ -415,6 +417,52 @@ def tree_accept_sampled(target_logits: torch.Tensor, draft_logits: torch.Tensor,
                                             _ptr(path), _ptr(nxt), _ptr(workspace),
                                             0 if workspace is None else workspace.numel(), st))
     return alen, path, nxt
+
+
+def tree_accept_lm_head_workspace_size(batch: int, num_nodes: int, hidden: int, vocab: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dreams_tree_accept_lm_head_workspace_size(batch, num_nodes, hidden, vocab, ctypes.byref(n)))
+    return n.value
+
+
+def tree_accept_lm_head(hidden_states: torch.Tensor, lm_weight: torch.Tensor, draft_tokens: torch.Tensor,
+                        parent: torch.Tensor, want_target_argmax: bool = False, outputs=None,
+                        workspace: Optional[torch.Tensor] = None, stream=None):
+    """dreams_tree_accept_lm_head.  hidden_states [B,T,H] bfloat16, lm_weight [V,H] bfloat16, draft_tokens /
+    parent [B,T] int32.  Returns (accept_len [B], accept_path [B,T], next_token [B], target_argmax [B,T] or
+    None), all int32.  `outputs` may pass preallocated (accept_len, accept_path, next_token, target_argmax)."""
+    dev = hidden_states.device
+    _need(hidden_states, "hidden_states", torch.bfloat16, dev, 3)
+    B, T, H = hidden_states.shape
+    _need(lm_weight, "lm_weight", torch.bfloat16, dev, 2)
+    V = lm_weight.shape[0]
+    if lm_weight.shape[1] != H:
+        raise ValueError("lm_weight must be [V, H] with the hidden size of hidden_states")
+    _need(draft_tokens, "draft_tokens", torch.int32, dev, 2)
+    _need(parent, "parent", torch.int32, dev, 2)
+    if tuple(draft_tokens.shape) != (B, T) or tuple(parent.shape) != (B, T):
+        raise ValueError("draft_tokens and parent must be [B, T]")
+    if outputs is None:
+        alen = torch.empty(B, dtype=torch.int32, device=dev)
+        path = torch.empty((B, T), dtype=torch.int32, device=dev)
+        nxt = torch.empty(B, dtype=torch.int32, device=dev)
+        am = torch.empty((B, T), dtype=torch.int32, device=dev) if want_target_argmax else None
+    else:
+        alen, path, nxt, am = outputs
+        for t, nm, shp in ((alen, "accept_len", (B,)), (path, "accept_path", (B, T)), (nxt, "next_token", (B,))):
+            _need(t, nm, torch.int32, dev)
+            if tuple(t.shape) != shp:
+                raise ValueError("%s has the wrong shape" % nm)
+        if am is not None:
+            _need(am, "target_argmax", torch.int32, dev)
+    st = _stream(stream)
+    nbytes = tree_accept_lm_head_workspace_size(B, T, H, V)
+    if workspace is None:
+        workspace = _workspace("accept_lm_head", nbytes, dev, st)
+    _check(lib().dreams_tree_accept_lm_head(B, T, H, V, _ptr(hidden_states), _ptr(lm_weight), _ptr(draft_tokens),
+                                            _ptr(parent), _ptr(alen), _ptr(path), _ptr(nxt), _ptr(am),
+                                            _ptr(workspace), 0 if workspace is None else workspace.numel(), st))
+    return alen, path, nxt, am
 
 
 def kv_commit(k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len_in: torch.Tensor, accept_path: torch.Tensor,

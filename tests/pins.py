@@ -903,7 +903,64 @@ def pin_sampled_output_distribution(orc):
         assert abs(first_acc.mean() - rate) <= 5 * se, (tau, first_acc.mean(), rate)
 
 
+# --------------------------------------------------------------------------------------- LM head + argmax
+def _bf16_bits(x):
+    b = np.asarray(x, dtype=np.float32).view(np.uint32)
+    assert np.all((b & 0xFFFF) == 0), "test values must be exactly representable in bf16"
+    return (b >> 16).astype(np.uint16)
+
+
+def pin_lm_head_one_hot_weights(orc):
+    """Weight rows that are scaled unit vectors pick single hidden entries: logit[m, v] = c_v * h[m, k_v]
+    exactly (V != H, so a transposed operand fails by shape or by value)."""
+    import oracle as O
+    rng = np.random.default_rng(51)
+    M, H, V = 7, 24, 40
+    h = rng.choice(np.array([-2.0, -0.5, 0.25, 1.0, 3.0], np.float32), size=(M, H))
+    k = rng.integers(0, H, size=V)
+    c = rng.choice(np.array([-1.0, 0.5, 2.0], np.float32), size=V)
+    w = np.zeros((V, H), np.float32)
+    w[np.arange(V), k] = c
+    got = O.lm_head_logits(_bf16_bits(h), _bf16_bits(w))
+    assert got.shape == (M, V)
+    np.testing.assert_array_equal(got, h[:, k].astype(np.float64) * c.astype(np.float64))
+
+
+def pin_lm_head_constant_closed_form(orc):
+    """Constant operands: every logit is H * a * b exactly; and bf16 bit patterns decode exactly (1.0 is
+    0x3F80, -2.5 is 0xC020)."""
+    import oracle as O
+    M, H, V = 3, 256, 5
+    h = np.full((M, H), 0x3F80, np.uint16)          # 1.0
+    w = np.full((V, H), 0xC020, np.uint16)          # -2.5
+    np.testing.assert_array_equal(O.lm_head_logits(h, w), np.full((M, V), -2.5 * H))
+
+
+def pin_lm_head_greedy_composition(orc):
+    """With an identity LM head (V = H) and one-hot hidden states at planted tokens, the logits' argmax is the
+    planted token of each node, and acceptance from the LM head equals the (separately pinned) greedy rule on
+    those logits, row order [B, T] included."""
+    import oracle as O
+    rng = np.random.default_rng(52)
+    B, T, H = 6, 12, 32
+    parent = np.stack([W.random_tree(rng, T, 4, 3) for _ in range(B)])
+    tgt = rng.integers(0, H, size=(B, T))
+    hid = np.zeros((B, T, H), np.float32)
+    np.put_along_axis(hid, tgt[:, :, None], 1.0, axis=2)
+    logits = O.lm_head_logits(_bf16_bits(hid), _bf16_bits(np.eye(H, dtype=np.float32)))
+    am = logits.argmax(axis=2)
+    np.testing.assert_array_equal(am, tgt)
+    tokens = np.where(rng.random((B, T)) < 0.7, tgt[np.arange(B)[:, None], np.maximum(parent, 0)],
+                      rng.integers(0, H, (B, T))).astype(np.int32)
+    got = O.tree_accept_from_argmax(am, tokens, parent)
+    want = orc.tree_accept(logits.astype(np.float32), tokens, parent)[:3]
+    for x, y in zip(got, want):
+        np.testing.assert_array_equal(x, y)
+
+
+LM_HEAD_PINS = [pin_lm_head_one_hot_weights, pin_lm_head_constant_closed_form, pin_lm_head_greedy_composition]
+
 SAMPLED_PINS = [pin_sampled_single_child_closed_form, pin_sampled_repeated_token_never_accepted_twice,
                 pin_sampled_low_temperature_is_greedy, pin_sampled_identical_models,
                 pin_sampled_output_distribution]
-ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS + VISUAL_PINS + SAMPLED_PINS
+ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS + VISUAL_PINS + SAMPLED_PINS + LM_HEAD_PINS

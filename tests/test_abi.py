@@ -221,3 +221,28 @@ def test_sampled_accept_rejections_and_sizes(D):
     assert f(1, 60, 10, 1.0, fake, None, fake, fake, fake, fake, fake, fake, fake, 1 << 20, None) == -1
     assert f(1, 60, 10, 1.0, fake, fake, fake, fake, fake, fake, fake, fake, None, 0, None) == -3
     assert f(1, 60, 10, 1.0, fake, fake, fake, fake, fake, fake, fake, fake, fake, 100, None) == -3
+
+
+def test_lm_head_accept_rejections_and_sizes(D):
+    lib = D.lib()
+    n = ctypes.c_size_t(0)
+
+    def r256(x):
+        return (x + 255) // 256 * 256
+
+    for B, T, H, V in [(1, 60, 4096, 32000), (16, 128, 3584, 152064), (2, 7, 256, 1)]:
+        assert lib.dreams_tree_accept_lm_head_workspace_size(B, T, H, V, ctypes.byref(n)) == 0
+        tiles = (V + 63) // 64
+        assert n.value == 65536 + 2 * r256(B * T * tiles * 4)
+    assert lib.dreams_tree_accept_lm_head_workspace_size(0, 60, 4096, 32000, ctypes.byref(n)) == 0 and n.value == 0
+    assert lib.dreams_tree_accept_lm_head_workspace_size(1, 60, 4000, 32000, ctypes.byref(n)) == -2   # H % 256
+    assert lib.dreams_tree_accept_lm_head_workspace_size(1, 60, 0, 32000, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_lm_head_workspace_size(1, 129, 4096, 32000, ctypes.byref(n)) == -1
+    assert lib.dreams_tree_accept_lm_head_workspace_size(1, 60, 4096, 0, ctypes.byref(n)) == -1
+    fake, odd = ctypes.c_void_p(0x100000), ctypes.c_void_p(0x100008)
+    f = lib.dreams_tree_accept_lm_head
+    assert f(0, 60, 4096, 100, None, None, None, None, None, None, None, None, None, 0, None) == 0
+    assert f(1, 60, 4096, 100, fake, None, fake, fake, fake, fake, fake, None, fake, 1 << 24, None) == -1
+    assert f(1, 60, 4096, 100, odd, fake, fake, fake, fake, fake, fake, None, fake, 1 << 24, None) == -1   # align
+    assert f(1, 60, 4096, 100, fake, fake, fake, fake, fake, fake, fake, None, None, 0, None) == -3
+    assert f(1, 60, 4096, 100, fake, fake, fake, fake, fake, fake, fake, None, fake, 100, None) == -3
