@@ -537,7 +537,7 @@ dreams_status_t plan_lm_head(int32_t B, int32_t T, int32_t H, int32_t V, LmPlan*
   *p = LmPlan{};
   if (B == 0) return DREAMS_OK;
   const long long M = (long long)B * T, ntiles = ((long long)V + kLmTile - 1) / kLmTile;
-  if ((M + kLmTile - 1) / kLmTile > 65535) return fail(DREAMS_ERR_UNSUPPORTED, "batch * num_nodes too large");
+  if ((M + kLmTile - 1) / kLmTile * ntiles > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
   p->ntiles = (int)ntiles;
   size_t off = kCounterBytes;
   auto take = [&](size_t bytes) {
@@ -603,6 +603,7 @@ dreams_status_t dreams_tree_accept_lm_head(int32_t batch, int32_t num_nodes, int
   a.V = vocab;
   a.M = batch * num_nodes;
   a.ntiles = p.ntiles;
+  a.mtiles = (a.M + kLmTile - 1) / kLmTile;
   hipError_t e = launch_lm_head_accept(a, stream);
   if (e != hipSuccess) return hip_fail(e, "LM head accept launch");
   return ok();

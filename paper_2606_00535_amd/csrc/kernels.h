@@ -189,7 +189,7 @@ struct LmHeadArgs {
   int32_t* target_argmax;  // [B, T] or nullptr
   float* part_val;         // [M, ntiles]
   int32_t* part_idx;       // [M, ntiles]
-  int B, T, H, V, M, ntiles;
+  int B, T, H, V, M, ntiles, mtiles;
 };
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream);

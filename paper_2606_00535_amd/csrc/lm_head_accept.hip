@@ -2,15 +2,16 @@
 // logits never reach HBM (the paper's Section 2, "Speculative decoding": the target's token at a position is
 // the argmax of its logits there; the logits are the final hidden state times the LM head's weight).
 //
-// lm_head_argmax_kernel: a workgroup per (64-entry vocabulary tile, 64-row tile) of the logits, four waves
-// splitting the hidden axis in quarters.  A wave streams its quarter of the tile's 64 weight rows and 64 hidden
-// rows with 16-byte loads straight into matrix-core operands (v_mfma_f32_16x16x32_bf16, weights as the A
-// operand, so that a lane's four outputs are four vocabulary entries of one row; the weights, read once, with
-// the non-temporal hint).  The four partial sums are added through LDS in wave order (each wave then owns 16
+// lm_head_argmax_kernel: a workgroup per (64-row tile, 64-entry vocabulary tile) of the logits, row tiles
+// fastest, four waves splitting the hidden axis in quarters.  A wave streams its quarter of the tile's 64
+// weight rows through a private two-stage LDS ring (LDS-DMA copies of whole 128-byte row pieces, non-temporal)
+// and reads the 64 hidden rows' operands straight from global memory (they stay in the caches); the products
+// run on v_mfma_f32_16x16x32_bf16 with the weights as the A operand, so that a lane's four outputs are four
+// vocabulary entries of one row.  The four partial sums are added through LDS in wave order (each wave then owns 16
 // vocabulary entries of the tile), and each row's best (value, index) over the tile's 64 entries is written:
 // ties go to the smallest index (fp32 comparison, -0.0 equal to +0.0), as for logits held in memory.
-// lm_head_finish_kernel: a workgroup per sequence; wave w merges rows w, w + 4, ... over every tile, then one
-// wave runs the greedy path scan.
+// lm_head_finish_kernel: a workgroup of 16 waves per sequence merges every row's candidates over the tiles
+// (the row's argmax) and one wave runs the greedy path scan on them.
 #include "accept_scan.h"
 #include "kernels.h"
 
@@ -24,52 +25,119 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int NT = kLmThreads, NW = NT / 64, TILE = kLmTile;
-constexpr int U = 2;   // 32-deep steps per batch of loads
 
 // true iff (v2, i2) beats (v1, i1): larger value, or equal value and smaller index
 __device__ __forceinline__ bool better(float v2, int i2, float v1, int i1) {
   return v2 > v1 || (v2 == v1 && i2 < i1);
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_void*)p; }
+// Wave-wide 16-byte copy from global memory into LDS: lane l's 16 bytes land at LDS byte address m0 + 16 l
+// (m0 wave-uniform); the weights are read once, so the copy carries the non-temporal hint.
+__device__ __forceinline__ void copy16_to_lds(uint32_t m0, const void* src) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(m0), "v"(src) : "memory");
+}
+// At most N of this wave's vector-memory operations still outstanding (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// A stage is 64 weight rows x 64 hidden entries (128 bytes per row, 8 KB), copied by 8 wave-wide copies of
+// 8 rows each; 16-byte chunk c of row r sits at position c ^ (r % 8) of the row, so that the 16 rows one
+// operand read touches fall on distinct banks (each copy lane fetches the chunk its position wants).
+constexpr int STAGE_K = 64, STAGE_BYTES = TILE * STAGE_K * 2, STAGES = 2;
+
 __global__ __launch_bounds__(NT) void lm_head_argmax_kernel(LmHeadArgs a) {
   static_assert(NW == 4 && TILE == 64, "four waves, each owning 16 of the tile's 64 vocabulary entries");
-  __shared__ f32x4 red[NW][16][64];   // [source wave][vocab sub-tile * 4 + row sub-tile][lane]
+  static_assert(NW * STAGES * STAGE_BYTES >= NW * 16 * 64 * 16, "the partial sums reuse the copy rings");
+  __shared__ __attribute__((aligned(16))) char ring[NW][STAGES][STAGE_BYTES];   // one ring per wave
   __shared__ float best_v[NW][TILE];
   __shared__ int best_i[NW][TILE];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, quad = lane >> 4;
-  const int n0 = blockIdx.x * TILE, m0 = blockIdx.y * TILE;
-  const int H = a.H, KQ = H / NW, k0 = wave * KQ;
+  // the row tiles of one vocabulary tile are consecutive workgroups, so its weights are fetched from HBM
+  // once and found in the caches by the others
+  const int mt = blockIdx.x % a.mtiles, nt = blockIdx.x / a.mtiles;
+  const int n0 = nt * TILE, m0 = mt * TILE;
+  const int H = a.H, KQ = H / NW, k0 = wave * KQ, nstages = KQ / STAGE_K;
 
-  // operand rows, clamped into the tensors (results of clamped rows are discarded below)
-  const __bf16* wrow[4];
+  // copy lanes: copy j moves rows 8 j + lane / 8, chunk position lane % 8 (logical chunk cpos ^ row % 8)
+  const int crow = lane >> 3, cchunk = (lane & 7) ^ (crow & 7);
+  const __bf16* csrc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    csrc[j] = a.weight + (size_t)min(n0 + 8 * j + crow, a.V - 1) * H + k0 + 8 * cchunk;
+  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(&ring[wave][0][0]));
+  auto issue = [&](int s) {   // the copies of stage s into ring slot s % STAGES
+    const uint32_t dst = ring_lds + (s % STAGES) * STAGE_BYTES;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * STAGE_K);
+  };
+  // hidden operand rows (clamped; their results are discarded below), read straight from global memory
   const __bf16* xrow[4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    wrow[t] = a.weight + (size_t)min(n0 + 16 * t + col, a.V - 1) * H + k0 + quad * 8;
-    xrow[t] = a.hidden + (size_t)min(m0 + 16 * t + col, a.M - 1) * H + k0 + quad * 8;
-  }
+  for (int r = 0; r < 4; ++r) xrow[r] = a.hidden + (size_t)min(m0 + 16 * r + col, a.M - 1) * H + k0 + quad * 8;
+
   f32x4 acc[4][4];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[t][r] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k < KQ; k += 32 * U) {
-    bf16x8 wa[U][4], xb[U][4];
+  // The hidden operands are loaded one stage ahead, before that stage's copies: the wait for stage s (at most
+  // 8 operations outstanding) then leaves exactly stage s + 1's copies in flight, which is also the wait the
+  // compiler derives for the hidden registers from the loads it can see.  The loop is unrolled by two so that
+  // the two register sets swap roles without copies (a copy would make the compiler wait for everything).
+  bf16x8 xa[2][4], xb[2][4];
+  auto load_hidden = [&](int s, bf16x8 (&dst)[2][4]) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dst[ks][r] = *(const bf16x8*)(xrow[r] + s * STAGE_K + 32 * ks);
+  };
+  auto compute = [&](int s, const bf16x8 (&x)[2][4]) {
+    const char* st = &ring[wave][s % STAGES][0];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 wa[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        wa[u][t] = __builtin_nontemporal_load((const bf16x8*)(wrow[t] + k + 32 * u));
-        xb[u][t] = *(const bf16x8*)(xrow[t] + k + 32 * u);
+        const int r = 16 * t + col, c = 4 * ks + quad;
+        wa[t] = *(const bf16x8*)(st + r * 128 + ((c ^ (r & 7)) << 4));
       }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[t][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[u][t], xb[u][r], acc[t][r], 0, 0, 0);
+        for (int r = 0; r < 4; ++r) acc[t][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], x[ks][r], acc[t][r], 0, 0, 0);
+    }
+  };
+  issue(0);
+  load_hidden(0, xa);
+  int s = 0;
+  for (; s + 2 < nstages; s += 2) {
+    load_hidden(s + 1, xb);
+    issue(s + 1);
+    wait_vm<8>();
+    compute(s, xa);
+    load_hidden(s + 2, xa);
+    issue(s + 2);
+    wait_vm<8>();
+    compute(s + 1, xb);
   }
+  if (s + 1 < nstages) {   // two stages left
+    load_hidden(s + 1, xb);
+    issue(s + 1);
+    wait_vm<8>();
+    compute(s, xa);
+    wait_vm<0>();
+    compute(s + 1, xb);
+  } else {                 // one stage left
+    wait_vm<0>();
+    compute(s, xa);
+  }
+  __syncthreads();   // every wave is done with its ring: the partial sums reuse it
+  f32x4 (*red)[16][64] = (f32x4(*)[16][64])&ring[0][0][0];
 
   // sum the four quarters: wave w owns vocabulary sub-tile w; the others' partials of it come through LDS
   f32x4 own[4];
@@ -123,54 +191,72 @@ __global__ __launch_bounds__(NT) void lm_head_argmax_kernel(LmHeadArgs a) {
         v = best_v[w][row];
         x = best_i[w][row];
       }
-    const size_t p = (size_t)(m0 + row) * a.ntiles + blockIdx.x;
+    const size_t p = (size_t)(m0 + row) * a.ntiles + nt;
     a.part_val[p] = v;
     a.part_idx[p] = x;
   }
 }
 
-__global__ __launch_bounds__(NT) void lm_head_finish_kernel(LmHeadArgs a) {
+// Each row's best over every tile, then the greedy path scan: a workgroup of 16 waves per sequence; wave w
+// merges rows w, w + 16, ..., two rows at a time with all of both rows' candidates in flight (up to 8 per lane
+// per row, then the next batch).
+constexpr int FIN_THREADS = 1024, FIN_WAVES = FIN_THREADS / 64, FIN_PER = 8;
+
+__device__ __forceinline__ void best_of_batch(const float* pv, const int* px, int p0, int n, int lane, float& v,
+                                              int& x) {
+  float cv[FIN_PER];
+  int cx[FIN_PER];
+#pragma unroll
+  for (int k = 0; k < FIN_PER; ++k) {
+    const int p = min(p0 + k * 64 + lane, n - 1);
+    cv[k] = pv[p];
+    cx[k] = px[p];
+  }
+#pragma unroll
+  for (int k = 0; k < FIN_PER; ++k)
+    if (p0 + k * 64 + lane < n && better(cv[k], cx[k], v, x)) {
+      v = cv[k];
+      x = cx[k];
+    }
+}
+__device__ __forceinline__ void wave_best(float& v, int& x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float v2 = __shfl_xor(v, off);
+    const int x2 = __shfl_xor(x, off);
+    if (better(v2, x2, v, x)) {
+      v = v2;
+      x = x2;
+    }
+  }
+}
+
+__global__ __launch_bounds__(FIN_THREADS) void lm_head_finish_kernel(LmHeadArgs a) {
   __shared__ int am_s[kMaxNodes], tok_s[kMaxNodes], par_s[kMaxNodes];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int b = blockIdx.x, T = a.T;
+  const int b = blockIdx.x, T = a.T, n = a.ntiles;
   if ((int)threadIdx.x < T) {
     tok_s[threadIdx.x] = a.tokens[(size_t)b * T + threadIdx.x];
     par_s[threadIdx.x] = a.parent[(size_t)b * T + threadIdx.x];
   }
-  for (int i = wave; i < T; i += NW) {
-    const size_t row = (size_t)b * T + i;
-    const float* pv = a.part_val + row * a.ntiles;
-    const int* px = a.part_idx + row * a.ntiles;
-    float v = -INFINITY;
-    int x = INT_MAX;
-    for (int p0 = 0; p0 < a.ntiles; p0 += 4 * 64) {   // four candidates per lane in flight
-      float cv[4];
-      int cx[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int p = min(p0 + k * 64 + lane, a.ntiles - 1);
-        cv[k] = pv[p];
-        cx[k] = px[p];
-      }
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        if (p0 + k * 64 + lane < a.ntiles && better(cv[k], cx[k], v, x)) {
-          v = cv[k];
-          x = cx[k];
-        }
+  for (int i = wave; i < T; i += 2 * FIN_WAVES) {
+    const int j = i + FIN_WAVES;   // the second row of the pair (may be past T)
+    const size_t ri = (size_t)b * T + i, rj = (size_t)b * T + min(j, T - 1);
+    float vi = -INFINITY, vj = -INFINITY;
+    int xi = INT_MAX, xj = INT_MAX;
+    for (int p0 = 0; p0 < n; p0 += FIN_PER * 64) {
+      best_of_batch(a.part_val + ri * n, a.part_idx + ri * n, p0, n, lane, vi, xi);
+      best_of_batch(a.part_val + rj * n, a.part_idx + rj * n, p0, n, lane, vj, xj);
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const float v2 = __shfl_xor(v, off);
-      const int x2 = __shfl_xor(x, off);
-      if (better(v2, x2, v, x)) {
-        v = v2;
-        x = x2;
-      }
-    }
+    wave_best(vi, xi);
+    wave_best(vj, xj);
     if (lane == 0) {
-      am_s[i] = x;
-      if (a.target_argmax) a.target_argmax[row] = x;
+      am_s[i] = xi;
+      if (a.target_argmax) a.target_argmax[ri] = xi;
+      if (j < T) {
+        am_s[j] = xj;
+        if (a.target_argmax) a.target_argmax[rj] = xj;
+      }
     }
   }
   __syncthreads();
@@ -181,11 +267,11 @@ __global__ __launch_bounds__(NT) void lm_head_finish_kernel(LmHeadArgs a) {
 }  // namespace
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream) {
-  const dim3 grid((unsigned)a.ntiles, (unsigned)((a.M + TILE - 1) / TILE));
+  const dim3 grid((unsigned)((long long)a.ntiles * a.mtiles));
   hipLaunchKernelGGL(lm_head_argmax_kernel, grid, dim3(NT), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(lm_head_finish_kernel, dim3((unsigned)a.B), dim3(NT), 0, stream, a);
+  hipLaunchKernelGGL(lm_head_finish_kernel, dim3((unsigned)a.B), dim3(FIN_THREADS), 0, stream, a);
   return hipGetLastError();
 }
 
