@@ -266,6 +266,53 @@ def main():
     smp_bytes = 2 * B * T * wl.vocab * 4 + B * T * 12
     smp_alen = sets[0]["salen"].cpu().numpy()
 
+    # greedy acceptance from the final hidden states (LM head fused with the argmax: the logits never reach
+    # memory): weight [V, Hq*D] ~ N(0, 0.02), bf16, rotated over enough copies to stream from HBM; the library
+    # GEMM into fp32 logits followed by dreams_tree_accept is timed the same way, as context
+    Hd = Hq * D
+    lm_gen = torch.Generator(device=dev)
+    lm_gen.manual_seed(wl.seed + 1)
+    R_lm = max(2, int(math.ceil(args.rotate_bytes / (wl.vocab * Hd * 2))))
+    lm_w = [(torch.randn((wl.vocab, Hd), generator=lm_gen, device=dev) * 0.02).to(torch.bfloat16)
+            for _ in range(R_lm)]
+    lm_h = torch.randn((B, T, Hd), generator=lm_gen, device=dev).to(torch.bfloat16)
+    lm_tok = torch.from_numpy(host.tokens).to(dev)
+    ws_lm = torch.zeros(max(1, dreams.tree_accept_lm_head_workspace_size(B, T, Hd, wl.vocab)), dtype=torch.uint8,
+                        device=dev)
+    lm_out = (sets[0]["alen"], sets[0]["path"], sets[0]["next"], None)
+    lm_logits = torch.empty((B * T, wl.vocab), dtype=torch.float32, device=dev)
+
+    def lm_fused():
+        for w in lm_w:
+            dreams.tree_accept_lm_head(lm_h, w, lm_tok, sets[0]["par"], outputs=lm_out, workspace=ws_lm)
+
+    def lm_unfused():
+        for w in lm_w:
+            lm_logits.copy_(torch.mm(lm_h.view(B * T, Hd), w.t()))
+            dreams.tree_accept(lm_logits.view(B, T, wl.vocab), lm_tok, sets[0]["par"], outputs=lm_out,
+                               workspace=ws_acc)
+
+    lm_us = {}
+    for name, fn in (("fused", lm_fused), ("unfused", lm_unfused)):
+        fn()
+        torch.cuda.synchronize()
+        g_lm = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_lm):
+            fn()
+        g_lm.replay()
+        torch.cuda.synchronize()
+        lm_reps = max(1, 60 // R_lm)
+        a0.record()
+        for _ in range(lm_reps):
+            g_lm.replay()
+        a1.record()
+        torch.cuda.synchronize()
+        lm_us[name] = a0.elapsed_time(a1) * 1e3 / (lm_reps * R_lm)
+        del g_lm
+    lm_bytes = wl.vocab * Hd * 2 + B * T * Hd * 2 + B * T * 12
+    lm_flops = 2.0 * B * T * wl.vocab * Hd
+    del lm_w, lm_logits
+
     # the attention call with every row's attention entropy as well (the layer-selection statistic), same method
     ents = [torch.empty((B, Hq, T), dtype=torch.float32, device=dev) for _ in range(NL)]
 
@@ -374,6 +421,11 @@ def main():
         "accept_sampled": {"us_per_launch": round(smp_us, 3), "bytes_per_launch": smp_bytes,
                            "GBps": round(smp_bytes / (smp_us * 1e-6) / 1e9, 1), "temperature": smp.temperature,
                            "mean_accept_len": round(float(smp_alen.mean()), 3)},
+        "accept_lm_head": {"us_per_launch": round(lm_us["fused"], 3), "hidden": Hd, "bytes_per_launch": lm_bytes,
+                           "GBps": round(lm_bytes / (lm_us["fused"] * 1e-6) / 1e9, 1),
+                           "frac_of_hbm_peak": round(lm_bytes / (lm_us["fused"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                           "TFLOPs": round(lm_flops / (lm_us["fused"] * 1e-6) / 1e12, 1),
+                           "library_gemm_then_accept_us": round(lm_us["unfused"], 3)},
         "visual_select": vis,
         "attention_entropy": {"us_per_launch": round(ent_us, 3), "bytes_per_launch": a_bytes + B * Hq * T * 4,
                               "GBps": round((a_bytes + B * Hq * T * 4) / (ent_us * 1e-6) / 1e9, 1)},
