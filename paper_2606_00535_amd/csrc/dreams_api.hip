@@ -523,7 +523,7 @@ dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int
 
 // ----------------------------------------------------------------------------------- LM head + argmax
 struct LmPlan {
-  int ntiles;
+  int tile, ntiles;
   size_t val_off, idx_off, bytes;
 };
 
@@ -536,8 +536,13 @@ dreams_status_t plan_lm_head(int32_t B, int32_t T, int32_t H, int32_t V, LmPlan*
     return fail(DREAMS_ERR_UNSUPPORTED, "hidden = %d is not a multiple of %d", H, kLmHiddenMultiple);
   *p = LmPlan{};
   if (B == 0) return DREAMS_OK;
-  const long long M = (long long)B * T, ntiles = ((long long)V + kLmTile - 1) / kLmTile;
-  if ((M + kLmTile - 1) / kLmTile * ntiles > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  // one 64-row tile while the rows fit it (the weights stream once); 128 x 128 tiles beyond, so that every
+  // operand tile is re-read half as often
+  const long long M = (long long)B * T;
+  const int tile = M <= kLmTile ? kLmTile : kLmTileBig;
+  const long long ntiles = ((long long)V + tile - 1) / tile;
+  if ((M + tile - 1) / tile * ntiles > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  p->tile = tile;
   p->ntiles = (int)ntiles;
   size_t off = kCounterBytes;
   auto take = [&](size_t bytes) {
@@ -603,7 +608,8 @@ dreams_status_t dreams_tree_accept_lm_head(int32_t batch, int32_t num_nodes, int
   a.V = vocab;
   a.M = batch * num_nodes;
   a.ntiles = p.ntiles;
-  a.mtiles = (a.M + kLmTile - 1) / kLmTile;
+  a.tile = p.tile;
+  a.mtiles = (a.M + p.tile - 1) / p.tile;
   hipError_t e = launch_lm_head_accept(a, stream);
   if (e != hipSuccess) return hip_fail(e, "LM head accept launch");
   return ok();

@@ -175,7 +175,8 @@ hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream);
 // splitting the hidden axis; each row's best (value, index) per tile goes to part_val / part_idx, and a second
 // kernel (a workgroup per sequence) merges them and runs the greedy path scan.
 constexpr int kLmThreads = 256;
-constexpr int kLmTile = 64;
+constexpr int kLmTile = 64;        // rows and vocabulary entries per workgroup while the rows fit one tile ...
+constexpr int kLmTileBig = 128;    // ... and beyond
 constexpr int kLmHiddenMultiple = 256;   // the hidden size must be a multiple (four quarters of 64-deep steps)
 
 struct LmHeadArgs {
@@ -190,6 +191,7 @@ struct LmHeadArgs {
   float* part_val;         // [M, ntiles]
   int32_t* part_idx;       // [M, ntiles]
   int B, T, H, V, M, ntiles, mtiles;
+  int tile;                // kLmTile or kLmTileBig
 };
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream);

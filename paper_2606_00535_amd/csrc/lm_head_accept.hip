@@ -197,6 +197,139 @@ __global__ __launch_bounds__(NT) void lm_head_argmax_kernel(LmHeadArgs a) {
   }
 }
 
+// wait_vm<PER * k> for a run-time k in [0, K]
+template <int PER, int K>
+__device__ __forceinline__ void wait_vm_steps(int k) {
+  if constexpr (K > 0) {
+    if (k >= K) {
+      wait_vm<PER * K>();
+      return;
+    }
+    wait_vm_steps<PER, K - 1>(k);
+  } else {
+    wait_vm<0>();
+  }
+}
+// Workgroup barrier after this wave's LDS reads have returned; outstanding copies stay in flight (a
+// __syncthreads() would also wait for them).  The wait is the compiler's own instruction (vmcnt and expcnt at
+// their maxima, lgkmcnt 0), so its bookkeeping knows every LDS read issued before the barrier has returned.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Large row counts: a workgroup per (128 rows, 128 vocabulary entries), four waves as 2 x 2 blocks of
+// 64 x 64 products, both operands staged in a shared four-stage LDS ring (a stage: 128 weight rows and 128
+// hidden rows x 64 hidden entries, 32 KB, copied by the four waves together, 8 wave-wide copies each), three
+// stages ahead; one barrier per stage hands a landed stage to every wave and frees the oldest.  Each operand
+// tile is read from the caches once per 128 rows or entries instead of once per 64.
+constexpr int BIG = 128, BIG_STAGES = 4, BIG_STAGE_BYTES = 2 * BIG * STAGE_K * 2;
+
+__global__ __launch_bounds__(NT) void lm_head_argmax_big_kernel(LmHeadArgs a) {
+  static_assert(NW == 4, "2 x 2 waves");
+  __shared__ __attribute__((aligned(16))) char ring[BIG_STAGES][BIG_STAGE_BYTES];   // [stage][W rows | X rows]
+  __shared__ float best_v[2][BIG];
+  __shared__ int best_i[2][BIG];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, quad = lane >> 4;
+  const int wr = wave >> 1, wn = wave & 1;   // this wave's 64 rows and 64 vocabulary entries of the tile
+  const int mt = blockIdx.x % a.mtiles, nt = blockIdx.x / a.mtiles;
+  const int n0 = nt * BIG, m0 = mt * BIG;
+  const int H = a.H, nstages = H / STAGE_K;
+
+  // copies: chunk q = 8 wave + j of a stage (q < 16: weight rows 8q.., else hidden rows 8(q - 16)..)
+  const int crow = lane >> 3, cchunk = (lane & 7) ^ (crow & 7);
+  const __bf16* csrc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int q = 8 * wave + j;
+    csrc[j] = q < 16 ? a.weight + (size_t)min(n0 + 8 * q + crow, a.V - 1) * H + 8 * cchunk
+                     : a.hidden + (size_t)min(m0 + 8 * (q - 16) + crow, a.M - 1) * H + 8 * cchunk;
+  }
+  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(&ring[0][0]));
+  auto issue = [&](int s) {
+    const uint32_t dst = ring_lds + (s % BIG_STAGES) * BIG_STAGE_BYTES + wave * 8 * 1024;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * STAGE_K);
+  };
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[t][r] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < BIG_STAGES - 1 && s < nstages; ++s) issue(s);
+  for (int s = 0; s < nstages; ++s) {
+    // this wave's copies of stage s have landed (later stages may stay in flight), then every wave's have
+    wait_vm_steps<8, BIG_STAGES - 2>(min(BIG_STAGES - 2, nstages - 1 - s));
+    barrier_lds();
+    // every wave is past stage s - 1: its slot takes stage s + 3
+    if (s + BIG_STAGES - 1 < nstages) issue(s + BIG_STAGES - 1);
+    const char* wst = &ring[s % BIG_STAGES][0];
+    const char* xst = wst + BIG * STAGE_K * 2;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 wa[4], xb[4];
+      const int c = 4 * ks + quad;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int rw = 64 * wn + 16 * t + col, rx = 64 * wr + 16 * t + col;
+        wa[t] = *(const bf16x8*)(wst + rw * 128 + ((c ^ (rw & 7)) << 4));
+        xb[t] = *(const bf16x8*)(xst + rx * 128 + ((c ^ (rx & 7)) << 4));
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[t][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], xb[r], acc[t][r], 0, 0, 0);
+    }
+  }
+
+  // each row's best over this wave's 64 entries (lane: rows 64 wr + 16 r + col, entries
+  // n0 + 64 wn + 16 t + 4 quad + e, visited in increasing order), then over the two vocabulary halves
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float v = -INFINITY;
+    int x = INT_MAX;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n = n0 + 64 * wn + 16 * t + 4 * quad + e;
+        if (n < a.V && (acc[t][r][e] > v || x == INT_MAX)) {
+          v = acc[t][r][e];
+          x = n;
+        }
+      }
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float v2 = __shfl_xor(v, off);
+      const int x2 = __shfl_xor(x, off);
+      if (better(v2, x2, v, x)) {
+        v = v2;
+        x = x2;
+      }
+    }
+    if (quad == 0) {
+      best_v[wn][64 * wr + 16 * r + col] = v;
+      best_i[wn][64 * wr + 16 * r + col] = x;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < BIG && m0 + (int)threadIdx.x < a.M) {
+    const int row = threadIdx.x;
+    float v = best_v[0][row];
+    int x = best_i[0][row];
+    if (better(best_v[1][row], best_i[1][row], v, x)) {
+      v = best_v[1][row];
+      x = best_i[1][row];
+    }
+    const size_t p = (size_t)(m0 + row) * a.ntiles + nt;
+    a.part_val[p] = v;
+    a.part_idx[p] = x;
+  }
+}
+
 // Each row's best over every tile, then the greedy path scan: a workgroup of 16 waves per sequence; wave w
 // merges rows w, w + 16, ..., two rows at a time with all of both rows' candidates in flight (up to 8 per lane
 // per row, then the next batch).
@@ -268,7 +401,10 @@ __global__ __launch_bounds__(FIN_THREADS) void lm_head_finish_kernel(LmHeadArgs 
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)((long long)a.ntiles * a.mtiles));
-  hipLaunchKernelGGL(lm_head_argmax_kernel, grid, dim3(NT), 0, stream, a);
+  if (a.tile == BIG)
+    hipLaunchKernelGGL(lm_head_argmax_big_kernel, grid, dim3(NT), 0, stream, a);
+  else
+    hipLaunchKernelGGL(lm_head_argmax_kernel, grid, dim3(NT), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(lm_head_finish_kernel, dim3((unsigned)a.B), dim3(FIN_THREADS), 0, stream, a);
