@@ -523,7 +523,7 @@ dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int
 
 // ----------------------------------------------------------------------------------- LM head + argmax
 struct LmPlan {
-  int tile, ntiles;
+  int tile, rows, ntiles;
   size_t val_off, idx_off, bytes;
 };
 
@@ -536,13 +536,15 @@ dreams_status_t plan_lm_head(int32_t B, int32_t T, int32_t H, int32_t V, LmPlan*
     return fail(DREAMS_ERR_UNSUPPORTED, "hidden = %d is not a multiple of %d", H, kLmHiddenMultiple);
   *p = LmPlan{};
   if (B == 0) return DREAMS_OK;
-  // one 64-row tile while the rows fit it (the weights stream once); 128 x 128 tiles beyond, so that every
-  // operand tile is re-read half as often
+  // one 64-row tile while the rows fit it (the weights stream once); beyond, 256 vocabulary entries by 128
+  // rows (up to 128 rows) or by 256 rows, so that every operand tile is re-read four to eight times less often
   const long long M = (long long)B * T;
   const int tile = M <= kLmTile ? kLmTile : kLmTileBig;
+  const int rows = M <= kLmTile ? kLmTile : M <= kLmMidRows ? kLmMidRows : kLmBigRows;
   const long long ntiles = ((long long)V + tile - 1) / tile;
-  if ((M + tile - 1) / tile * ntiles > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  if ((M + rows - 1) / rows * ntiles > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
   p->tile = tile;
+  p->rows = rows;
   p->ntiles = (int)ntiles;
   size_t off = kCounterBytes;
   auto take = [&](size_t bytes) {
@@ -609,7 +611,8 @@ dreams_status_t dreams_tree_accept_lm_head(int32_t batch, int32_t num_nodes, int
   a.M = batch * num_nodes;
   a.ntiles = p.ntiles;
   a.tile = p.tile;
-  a.mtiles = (a.M + p.tile - 1) / p.tile;
+  a.rows = p.rows;
+  a.mtiles = (a.M + p.rows - 1) / p.rows;
   hipError_t e = launch_lm_head_accept(a, stream);
   if (e != hipSuccess) return hip_fail(e, "LM head accept launch");
   return ok();

@@ -176,7 +176,9 @@ hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream);
 // kernel (a workgroup per sequence) merges them and runs the greedy path scan.
 constexpr int kLmThreads = 256;
 constexpr int kLmTile = 64;        // rows and vocabulary entries per workgroup while the rows fit one tile ...
-constexpr int kLmTileBig = 128;    // ... and beyond
+constexpr int kLmTileBig = 256;    // ... and beyond: vocabulary entries per workgroup, by 128 rows (at most
+constexpr int kLmMidRows = 128;    //     128 rows, three LDS ring stages) or by 256 rows (two stages)
+constexpr int kLmBigRows = 256;
 constexpr int kLmHiddenMultiple = 256;   // the hidden size must be a multiple (four quarters of 64-deep steps)
 
 struct LmHeadArgs {
@@ -192,6 +194,7 @@ struct LmHeadArgs {
   int32_t* part_idx;       // [M, ntiles]
   int B, T, H, V, M, ntiles, mtiles;
   int tile;                // kLmTile or kLmTileBig
+  int rows;                // rows per workgroup: kLmTile, kLmMidRows or kLmBigRows
 };
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream);

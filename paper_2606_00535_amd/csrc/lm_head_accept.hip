@@ -220,54 +220,56 @@ __device__ __forceinline__ void barrier_lds() {
   asm volatile("" ::: "memory");
 }
 
-// Large row counts: a workgroup per (128 rows, 128 vocabulary entries), four waves as 2 x 2 blocks of
-// 64 x 64 products, both operands staged in a shared four-stage LDS ring (a stage: 128 weight rows and 128
-// hidden rows x 64 hidden entries, 32 KB, copied by the four waves together, 8 wave-wide copies each), three
-// stages ahead; one barrier per stage hands a landed stage to every wave and frees the oldest.  Each operand
-// tile is read from the caches once per 128 rows or entries instead of once per 64.
-constexpr int BIG = 128, BIG_STAGES = 4, BIG_STAGE_BYTES = 2 * BIG * STAGE_K * 2;
+// Large row counts: a workgroup per (64 WR rows, 64 WN vocabulary entries), WR x WN waves as blocks of
+// 64 x 64 products, both operands staged in a shared LDS ring (a stage: 64 WN weight rows and 64 WR hidden
+// rows x 64 hidden entries, copied by all waves together), STAGES - 1 stages ahead; one barrier per stage
+// hands a landed stage to every wave and frees the oldest.  Each operand tile is read from the caches once
+// per 64 WR rows or 64 WN entries instead of once per 64.
 
-__global__ __launch_bounds__(NT) void lm_head_argmax_big_kernel(LmHeadArgs a) {
-  static_assert(NW == 4, "2 x 2 waves");
-  __shared__ __attribute__((aligned(16))) char ring[BIG_STAGES][BIG_STAGE_BYTES];   // [stage][W rows | X rows]
-  __shared__ float best_v[2][BIG];
-  __shared__ int best_i[2][BIG];
+template <int WR, int WN, int STAGES>
+__global__ __launch_bounds__(64 * WR * WN) void lm_head_argmax_big_kernel(LmHeadArgs a) {
+  constexpr int BIG_M = 64 * WR, BN = 64 * WN, WAVES = WR * WN, STAGE = (BN + BIG_M) * STAGE_K * 2;
+  constexpr int CPW = (BN + BIG_M) / 8 / WAVES;   // wave-wide copies (8 rows of 128 bytes) per wave per stage
+  static_assert(CPW * 8 * WAVES == BN + BIG_M, "the copies cover the stage");
+  __shared__ __attribute__((aligned(16))) char ring[STAGES][STAGE];   // [stage][W rows | X rows]
+  __shared__ float best_v[WN][BIG_M];
+  __shared__ int best_i[WN][BIG_M];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, quad = lane >> 4;
-  const int wr = wave >> 1, wn = wave & 1;   // this wave's 64 rows and 64 vocabulary entries of the tile
+  const int wr = wave / WN, wn = wave % WN;   // this wave's 64 rows and 64 vocabulary entries of the tile
   const int mt = blockIdx.x % a.mtiles, nt = blockIdx.x / a.mtiles;
-  const int n0 = nt * BIG, m0 = mt * BIG;
+  const int n0 = nt * BN, m0 = mt * BIG_M;
   const int H = a.H, nstages = H / STAGE_K;
 
-  // copies: chunk q = 8 wave + j of a stage (q < 16: weight rows 8q.., else hidden rows 8(q - 16)..)
+  // copies: chunk q = CPW wave + j of a stage (q < BN / 8: weight rows 8q.., else hidden rows 8(q - BN/8)..)
   const int crow = lane >> 3, cchunk = (lane & 7) ^ (crow & 7);
-  const __bf16* csrc[8];
+  const __bf16* csrc[CPW];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int q = 8 * wave + j;
-    csrc[j] = q < 16 ? a.weight + (size_t)min(n0 + 8 * q + crow, a.V - 1) * H + 8 * cchunk
-                     : a.hidden + (size_t)min(m0 + 8 * (q - 16) + crow, a.M - 1) * H + 8 * cchunk;
+  for (int j = 0; j < CPW; ++j) {
+    const int q = CPW * wave + j;
+    csrc[j] = q < BN / 8 ? a.weight + (size_t)min(n0 + 8 * q + crow, a.V - 1) * H + 8 * cchunk
+                         : a.hidden + (size_t)min(m0 + 8 * (q - BN / 8) + crow, a.M - 1) * H + 8 * cchunk;
   }
   const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(&ring[0][0]));
   auto issue = [&](int s) {
-    const uint32_t dst = ring_lds + (s % BIG_STAGES) * BIG_STAGE_BYTES + wave * 8 * 1024;
+    const uint32_t dst = ring_lds + (s % STAGES) * STAGE + wave * CPW * 1024;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * STAGE_K);
+    for (int j = 0; j < CPW; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * STAGE_K);
   };
   f32x4 acc[4][4];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[t][r] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < BIG_STAGES - 1 && s < nstages; ++s) issue(s);
+  for (int s = 0; s < STAGES - 1 && s < nstages; ++s) issue(s);
   for (int s = 0; s < nstages; ++s) {
     // this wave's copies of stage s have landed (later stages may stay in flight), then every wave's have
-    wait_vm_steps<8, BIG_STAGES - 2>(min(BIG_STAGES - 2, nstages - 1 - s));
+    wait_vm_steps<CPW, STAGES - 2>(min(STAGES - 2, nstages - 1 - s));
     barrier_lds();
-    // every wave is past stage s - 1: its slot takes stage s + 3
-    if (s + BIG_STAGES - 1 < nstages) issue(s + BIG_STAGES - 1);
-    const char* wst = &ring[s % BIG_STAGES][0];
-    const char* xst = wst + BIG * STAGE_K * 2;
+    // every wave is past stage s - 1: its slot takes stage s + STAGES - 1
+    if (s + STAGES - 1 < nstages) issue(s + STAGES - 1);
+    const char* wst = &ring[s % STAGES][0];
+    const char* xst = wst + BN * STAGE_K * 2;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 wa[4], xb[4];
@@ -286,7 +288,7 @@ __global__ __launch_bounds__(NT) void lm_head_argmax_big_kernel(LmHeadArgs a) {
   }
 
   // each row's best over this wave's 64 entries (lane: rows 64 wr + 16 r + col, entries
-  // n0 + 64 wn + 16 t + 4 quad + e, visited in increasing order), then over the two vocabulary halves
+  // n0 + 64 wn + 16 t + 4 quad + e, visited in increasing order), then over the WN vocabulary blocks
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     float v = -INFINITY;
@@ -316,14 +318,16 @@ __global__ __launch_bounds__(NT) void lm_head_argmax_big_kernel(LmHeadArgs a) {
     }
   }
   __syncthreads();
-  if (threadIdx.x < BIG && m0 + (int)threadIdx.x < a.M) {
+  if (threadIdx.x < BIG_M && m0 + (int)threadIdx.x < a.M) {
     const int row = threadIdx.x;
     float v = best_v[0][row];
     int x = best_i[0][row];
-    if (better(best_v[1][row], best_i[1][row], v, x)) {
-      v = best_v[1][row];
-      x = best_i[1][row];
-    }
+#pragma unroll
+    for (int w = 1; w < WN; ++w)
+      if (better(best_v[w][row], best_i[w][row], v, x)) {
+        v = best_v[w][row];
+        x = best_i[w][row];
+      }
     const size_t p = (size_t)(m0 + row) * a.ntiles + nt;
     a.part_val[p] = v;
     a.part_idx[p] = x;
@@ -401,8 +405,11 @@ __global__ __launch_bounds__(FIN_THREADS) void lm_head_finish_kernel(LmHeadArgs 
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)((long long)a.ntiles * a.mtiles));
-  if (a.tile == BIG)
-    hipLaunchKernelGGL(lm_head_argmax_big_kernel, grid, dim3(NT), 0, stream, a);
+  static_assert(kLmTileBig == 256, "four vocabulary waves");
+  if (a.rows == kLmBigRows)
+    hipLaunchKernelGGL((lm_head_argmax_big_kernel<4, 4, 2>), grid, dim3(1024), 0, stream, a);
+  else if (a.rows == kLmMidRows)
+    hipLaunchKernelGGL((lm_head_argmax_big_kernel<2, 4, 3>), grid, dim3(512), 0, stream, a);
   else
     hipLaunchKernelGGL(lm_head_argmax_kernel, grid, dim3(NT), 0, stream, a);
   hipError_t e = hipGetLastError();

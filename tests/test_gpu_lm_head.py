@@ -100,9 +100,11 @@ def test_llava7b_shape(dev):
 
 
 @pytest.mark.parametrize("B,T,H,V", [(1, 1, 256, 1), (1, 16, 256, 1000), (2, 60, 512, 4099), (3, 7, 768, 65),
-                                     (4, 128, 1024, 2048), (1, 64, 256, 64), (5, 13, 512, 12345)])
+                                     (4, 128, 1024, 2048), (1, 64, 256, 64), (5, 13, 512, 12345),
+                                     (3, 60, 768, 5000)])
 def test_ragged_shapes(dev, B, T, H, V):
-    """Rows and vocabularies that are not multiples of the 64 x 64 tile, a single node, a vocabulary of one."""
+    """Rows and vocabularies that are not multiples of the tiles (one 64-row tile up to 64 rows, 128 x 256 up to
+    128, 256 x 256 beyond), a single node, a vocabulary of one."""
     run_case(dev, np.random.default_rng(B * 1000 + T), B, T, H, V, "B=%d T=%d H=%d V=%d" % (B, T, H, V))
 
 
