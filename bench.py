@@ -268,7 +268,8 @@ def main():
 
     # greedy acceptance from the final hidden states (LM head fused with the argmax: the logits never reach
     # memory): weight [V, Hq*D] ~ N(0, 0.02), bf16, rotated over enough copies to stream from HBM; the library
-    # GEMM into fp32 logits followed by dreams_tree_accept is timed the same way, as context
+    # GEMM into fp32 logits (bf16 operands, fp32 output) followed by dreams_tree_accept is timed the same way,
+    # as context
     Hd = Hq * D
     lm_gen = torch.Generator(device=dev)
     lm_gen.manual_seed(wl.seed + 1)
@@ -280,17 +281,15 @@ def main():
     ws_lm = torch.zeros(max(1, dreams.tree_accept_lm_head_workspace_size(B, T, Hd, wl.vocab)), dtype=torch.uint8,
                         device=dev)
     lm_out = (sets[0]["alen"], sets[0]["path"], sets[0]["next"], None)
-    lm_logits = torch.empty((B * T, wl.vocab), dtype=torch.float32, device=dev)
 
     def lm_fused():
         for w in lm_w:
             dreams.tree_accept_lm_head(lm_h, w, lm_tok, sets[0]["par"], outputs=lm_out, workspace=ws_lm)
 
-    def lm_unfused():
+    def lm_unfused():   # fp32 logits straight from the bf16 operands, as the fused kernel accumulates them
         for w in lm_w:
-            lm_logits.copy_(torch.mm(lm_h.view(B * T, Hd), w.t()))
-            dreams.tree_accept(lm_logits.view(B, T, wl.vocab), lm_tok, sets[0]["par"], outputs=lm_out,
-                               workspace=ws_acc)
+            lg = torch.mm(lm_h.view(B * T, Hd), w.t(), out_dtype=torch.float32)
+            dreams.tree_accept(lg.view(B, T, wl.vocab), lm_tok, sets[0]["par"], outputs=lm_out, workspace=ws_acc)
 
     lm_us = {}
     for name, fn in (("fused", lm_fused), ("unfused", lm_unfused)):
@@ -311,7 +310,7 @@ def main():
         del g_lm
     lm_bytes = wl.vocab * Hd * 2 + B * T * Hd * 2 + B * T * 12
     lm_flops = 2.0 * B * T * wl.vocab * Hd
-    del lm_w, lm_logits
+    del lm_w
 
     # the attention call with every row's attention entropy as well (the layer-selection statistic), same method
     ents = [torch.empty((B, Hq, T), dtype=torch.float32, device=dev) for _ in range(NL)]
