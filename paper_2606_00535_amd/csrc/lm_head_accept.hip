@@ -226,39 +226,45 @@ __device__ __forceinline__ void barrier_lds() {
 // hands a landed stage to every wave and frees the oldest.  Each operand tile is read from the caches once
 // per 64 WR rows or 64 WN entries instead of once per 64.
 
-template <int WR, int WN, int STAGES>
+template <int WR, int WN, int TW, int SK, int STAGES>
 __global__ __launch_bounds__(64 * WR * WN) void lm_head_argmax_big_kernel(LmHeadArgs a) {
-  constexpr int BIG_M = 64 * WR, BN = 64 * WN, WAVES = WR * WN, STAGE = (BN + BIG_M) * STAGE_K * 2;
-  constexpr int CPW = (BN + BIG_M) / 8 / WAVES;   // wave-wide copies (8 rows of 128 bytes) per wave per stage
-  static_assert(CPW * 8 * WAVES == BN + BIG_M, "the copies cover the stage");
+  // a stage holds SK hidden entries of each of the tile's rows: RB bytes per row, CPR 16-byte chunks, chunk c
+  // of row r at position c ^ swz(r) (the 16 rows of one operand read on distinct banks)
+  constexpr int BIG_M = 64 * WR, WB = 16 * TW, BN = WB * WN, WAVES = WR * WN;
+  constexpr int RB = SK * 2, CPR = SK / 8, RPC = 1024 / RB, KS = SK / 32, STAGE = (BN + BIG_M) * RB;
+  constexpr int CPW = (BN + BIG_M) / RPC / WAVES;   // wave-wide copies (RPC rows each) per wave per stage
+  static_assert(CPW * RPC * WAVES == BN + BIG_M, "the copies cover the stage");
+  static_assert(SK == 64 || SK == 32, "64 or 32 hidden entries per stage");
+  auto swz = [](int r) { return SK == 64 ? (r & 7) : ((r >> 2) & 3); };
   __shared__ __attribute__((aligned(16))) char ring[STAGES][STAGE];   // [stage][W rows | X rows]
   __shared__ float best_v[WN][BIG_M];
   __shared__ int best_i[WN][BIG_M];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, quad = lane >> 4;
-  const int wr = wave / WN, wn = wave % WN;   // this wave's 64 rows and 64 vocabulary entries of the tile
+  const int wr = wave / WN, wn = wave % WN;   // this wave's 64 rows and WB vocabulary entries of the tile
   const int mt = blockIdx.x % a.mtiles, nt = blockIdx.x / a.mtiles;
   const int n0 = nt * BN, m0 = mt * BIG_M;
-  const int H = a.H, nstages = H / STAGE_K;
+  const int H = a.H, nstages = H / SK;
 
-  // copies: chunk q = CPW wave + j of a stage (q < BN / 8: weight rows 8q.., else hidden rows 8(q - BN/8)..)
-  const int crow = lane >> 3, cchunk = (lane & 7) ^ (crow & 7);
+  // copies: copy q = CPW wave + j of a stage moves rows RPC q .. (weight rows first, then hidden rows); lane
+  // l takes row RPC q + l / CPR, position l % CPR, i.e. the logical chunk that position holds
+  const int crow = lane / CPR, cchunk = (lane % CPR) ^ swz(crow);
   const __bf16* csrc[CPW];
 #pragma unroll
   for (int j = 0; j < CPW; ++j) {
     const int q = CPW * wave + j;
-    csrc[j] = q < BN / 8 ? a.weight + (size_t)min(n0 + 8 * q + crow, a.V - 1) * H + 8 * cchunk
-                         : a.hidden + (size_t)min(m0 + 8 * (q - BN / 8) + crow, a.M - 1) * H + 8 * cchunk;
+    csrc[j] = q < BN / RPC ? a.weight + (size_t)min(n0 + RPC * q + crow, a.V - 1) * H + 8 * cchunk
+                           : a.hidden + (size_t)min(m0 + RPC * (q - BN / RPC) + crow, a.M - 1) * H + 8 * cchunk;
   }
   const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(&ring[0][0]));
   auto issue = [&](int s) {
     const uint32_t dst = ring_lds + (s % STAGES) * STAGE + wave * CPW * 1024;
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * STAGE_K);
+    for (int j = 0; j < CPW; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * SK);
   };
-  f32x4 acc[4][4];
+  f32x4 acc[TW][4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int t = 0; t < TW; ++t)
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[t][r] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < STAGES - 1 && s < nstages; ++s) issue(s);
@@ -269,35 +275,39 @@ __global__ __launch_bounds__(64 * WR * WN) void lm_head_argmax_big_kernel(LmHead
     // every wave is past stage s - 1: its slot takes stage s + STAGES - 1
     if (s + STAGES - 1 < nstages) issue(s + STAGES - 1);
     const char* wst = &ring[s % STAGES][0];
-    const char* xst = wst + BN * STAGE_K * 2;
+    const char* xst = wst + BN * RB;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 wa[4], xb[4];
+    for (int ks = 0; ks < KS; ++ks) {
+      bf16x8 wa[TW], xb[4];
       const int c = 4 * ks + quad;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int rw = 64 * wn + 16 * t + col, rx = 64 * wr + 16 * t + col;
-        wa[t] = *(const bf16x8*)(wst + rw * 128 + ((c ^ (rw & 7)) << 4));
-        xb[t] = *(const bf16x8*)(xst + rx * 128 + ((c ^ (rx & 7)) << 4));
+      for (int t = 0; t < TW; ++t) {
+        const int rw = WB * wn + 16 * t + col;
+        wa[t] = *(const bf16x8*)(wst + rw * RB + ((c ^ swz(rw)) << 4));
       }
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < 4; ++t) {
+        const int rx = 64 * wr + 16 * t + col;
+        xb[t] = *(const bf16x8*)(xst + rx * RB + ((c ^ swz(rx)) << 4));
+      }
+#pragma unroll
+      for (int t = 0; t < TW; ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[t][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], xb[r], acc[t][r], 0, 0, 0);
     }
   }
 
-  // each row's best over this wave's 64 entries (lane: rows 64 wr + 16 r + col, entries
-  // n0 + 64 wn + 16 t + 4 quad + e, visited in increasing order), then over the WN vocabulary blocks
+  // each row's best over this wave's WB entries (lane: rows 64 wr + 16 r + col, entries
+  // n0 + WB wn + 16 t + 4 quad + e, visited in increasing order), then over the WN vocabulary blocks
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     float v = -INFINITY;
     int x = INT_MAX;
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int t = 0; t < TW; ++t)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int n = n0 + 64 * wn + 16 * t + 4 * quad + e;
+        const int n = n0 + WB * wn + 16 * t + 4 * quad + e;
         if (n < a.V && (acc[t][r][e] > v || x == INT_MAX)) {
           v = acc[t][r][e];
           x = n;
@@ -407,9 +417,9 @@ hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream) {
   const dim3 grid((unsigned)((long long)a.ntiles * a.mtiles));
   static_assert(kLmTileBig == 256, "four vocabulary waves");
   if (a.rows == kLmBigRows)
-    hipLaunchKernelGGL((lm_head_argmax_big_kernel<4, 4, 2>), grid, dim3(1024), 0, stream, a);
+    hipLaunchKernelGGL((lm_head_argmax_big_kernel<4, 4, 4, 64, 2>), grid, dim3(1024), 0, stream, a);
   else if (a.rows == kLmMidRows)
-    hipLaunchKernelGGL((lm_head_argmax_big_kernel<2, 4, 3>), grid, dim3(512), 0, stream, a);
+    hipLaunchKernelGGL((lm_head_argmax_big_kernel<2, 4, 4, 64, 3>), grid, dim3(512), 0, stream, a);
   else
     hipLaunchKernelGGL(lm_head_argmax_kernel, grid, dim3(NT), 0, stream, a);
   hipError_t e = hipGetLastError();
