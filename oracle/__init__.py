@@ -4,8 +4,10 @@ Only the test suite, the package smoke check and the benchmark's CPU-baseline le
 The product (the HIP library and its Python binding) never imports, links or calls it.
 
 Thin ctypes wrapper over ``oracle.c`` (plain C, fp64 accumulation; that file states what each function
-computes and which passage of the paper it follows).  The shared library is built with gcc by :func:`build`
--- no hipcc, no header shared with the HIP path.  :class:`Oracle` can also wrap a differently built copy of
+computes and which passage of the paper it follows), plus a few plain numpy definitions at the end of this
+file (the layer mean and choice of the attention entropy, the LM head's logits in fp64, the greedy rule on
+given per-node tokens).  The shared library is built with gcc by :func:`build` -- no hipcc, no header shared
+with the HIP path.  :class:`Oracle` can also wrap a differently built copy of
 the source (the mutation tests compile copies with planted mistakes to show that the pins catch them).
 """
 from __future__ import annotations
