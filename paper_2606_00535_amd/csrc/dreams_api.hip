@@ -610,7 +610,6 @@ dreams_status_t dreams_tree_accept_lm_head(int32_t batch, int32_t num_nodes, int
   a.V = vocab;
   a.M = batch * num_nodes;
   a.ntiles = p.ntiles;
-  a.tile = p.tile;
   a.rows = p.rows;
   a.mtiles = (a.M + p.rows - 1) / p.rows;
   hipError_t e = launch_lm_head_accept(a, stream);

@@ -193,8 +193,8 @@ struct LmHeadArgs {
   float* part_val;         // [M, ntiles]
   int32_t* part_idx;       // [M, ntiles]
   int B, T, H, V, M, ntiles, mtiles;
-  int tile;                // kLmTile or kLmTileBig
-  int rows;                // rows per workgroup: kLmTile, kLmMidRows or kLmBigRows
+  int rows;                // rows per workgroup: kLmTile (64 vocabulary entries each), else kLmMidRows or
+                           // kLmBigRows (kLmTileBig entries each)
 };
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream);
