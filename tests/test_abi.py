@@ -247,3 +247,20 @@ def test_lm_head_accept_rejections_and_sizes(D):
     assert f(1, 60, 4096, 100, odd, fake, fake, fake, fake, fake, fake, None, fake, 1 << 24, None) == -1   # align
     assert f(1, 60, 4096, 100, fake, fake, fake, fake, fake, fake, fake, None, None, 0, None) == -3
     assert f(1, 60, 4096, 100, fake, fake, fake, fake, fake, fake, fake, None, fake, 100, None) == -3
+
+
+def test_bindings_reject_bad_tensors_before_any_launch(D):
+    """The Python bindings of the newer verbs check dtypes, devices and shapes on the host (no GPU needed)."""
+    import torch
+    f32 = torch.zeros((1, 2, 8), dtype=torch.float32)
+    i32 = torch.zeros((1, 2), dtype=torch.int32)
+    u32 = torch.zeros((1, 2), dtype=torch.float32)
+    with pytest.raises(ValueError):        # host tensors
+        D.tree_accept_sampled(f32, f32, i32, i32, u32, 1.0)
+    with pytest.raises(TypeError):         # wrong dtype
+        D.tree_accept_sampled(f32.double(), f32, i32, i32, u32, 1.0)
+    bf = torch.zeros((1, 2, 256), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        D.tree_accept_lm_head(bf, torch.zeros((10, 256), dtype=torch.bfloat16), i32, i32)
+    with pytest.raises(TypeError):
+        D.tree_accept_lm_head(bf.float(), torch.zeros((10, 256), dtype=torch.bfloat16), i32, i32)
