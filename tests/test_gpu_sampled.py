@@ -185,3 +185,22 @@ def test_large_pieces(dev, V):
     rng = np.random.default_rng(V)
     tl, dl, tok, par, uni = random_case(rng, B, T, V, 8, 6, noise=0.7)
     run_and_compare(dev, tl, dl, tok, par, uni, 1.0, "large pieces V=%d" % V)
+
+
+def test_out_of_range_tokens_are_rejected(dev):
+    """A draft token outside [0, V) is rejected without a draw; since a rejection's residual update does not
+    depend on the rejected token, that equals a child whose token has exactly zero target mass (logit
+    -1e4 below the rest: exp underflows to 0 in fp64), which the oracle can evaluate."""
+    rng = np.random.default_rng(15)
+    B, T, V = 12, 30, 3001
+    tl, dl, tok, par, uni = random_case(rng, B, T, V, 5, 4)
+    bad = rng.random((B, T)) < 0.3
+    bad[:, 0] = False
+    tok_bad = np.where(bad, np.where(rng.random((B, T)) < 0.5, V, -1), tok).astype(np.int32)
+    tl_ref = tl.copy()
+    tl_ref[:, :, V - 1] = -1e4                     # token V - 1 now has exactly zero mass at every node
+    tok_ref = np.where(bad, V - 1, tok).astype(np.int32)
+    ga, gp, gn = gpu_sampled(dev, tl_ref, dl, tok_bad, par, uni, 1.0)
+    ra, rp, rn = oracle.tree_accept_sampled(tl_ref, dl, tok_ref, par, uni, 1.0)
+    assert np.array_equal(ga, ra) and np.array_equal(gp, rp) and np.array_equal(gn, rn)
+    assert np.all(gn != V - 1)
