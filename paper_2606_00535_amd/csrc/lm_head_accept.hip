@@ -10,6 +10,8 @@
 // vocabulary entries of one row.  The four partial sums are added through LDS in wave order (each wave then owns 16
 // vocabulary entries of the tile), and each row's best (value, index) over the tile's 64 entries is written:
 // ties go to the smallest index (fp32 comparison, -0.0 equal to +0.0), as for logits held in memory.
+// lm_head_argmax_big_kernel (more than 64 rows): 256 vocabulary entries by 128 or 256 rows per workgroup, both
+// operands through a shared LDS ring (see below).
 // lm_head_finish_kernel: a workgroup of 16 waves per sequence merges every row's candidates over the tiles
 // (the row's argmax) and one wave runs the greedy path scan on them.
 #include "accept_scan.h"
@@ -34,9 +36,15 @@ __device__ __forceinline__ bool better(float v2, int i2, float v1, int i1) {
 typedef __attribute__((address_space(3))) void lds_void;
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)(lds_void*)p; }
 // Wave-wide 16-byte copy from global memory into LDS: lane l's 16 bytes land at LDS byte address m0 + 16 l
-// (m0 wave-uniform); the weights are read once, so the copy carries the non-temporal hint.
+// (m0 wave-uniform).  STREAM adds the non-temporal hint, for data read once (the 64-row kernel's weights);
+// operands that other workgroups read again (the large tiles') are copied without it (gqa_long's shape:
+// 2.34 ms with the hint, 1.82 ms without).
+template <bool STREAM>
 __device__ __forceinline__ void copy16_to_lds(uint32_t m0, const void* src) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(m0), "v"(src) : "memory");
+  if (STREAM)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(m0), "v"(src) : "memory");
+  else
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0), "v"(src) : "memory");
 }
 // At most N of this wave's vector-memory operations still outstanding (they complete in issue order).
 template <int N>
@@ -73,7 +81,7 @@ __global__ __launch_bounds__(NT) void lm_head_argmax_kernel(LmHeadArgs a) {
   auto issue = [&](int s) {   // the copies of stage s into ring slot s % STAGES
     const uint32_t dst = ring_lds + (s % STAGES) * STAGE_BYTES;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * STAGE_K);
+    for (int j = 0; j < 8; ++j) copy16_to_lds<true>(dst + j * 1024, csrc[j] + s * STAGE_K);
   };
   // hidden operand rows (clamped; their results are discarded below), read straight from global memory
   const __bf16* xrow[4];
@@ -260,7 +268,7 @@ __global__ __launch_bounds__(64 * WR * WN) void lm_head_argmax_big_kernel(LmHead
   auto issue = [&](int s) {
     const uint32_t dst = ring_lds + (s % STAGES) * STAGE + wave * CPW * 1024;
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) copy16_to_lds(dst + j * 1024, csrc[j] + s * SK);
+    for (int j = 0; j < CPW; ++j) copy16_to_lds<false>(dst + j * 1024, csrc[j] + s * SK);
   };
   f32x4 acc[TW][4];
 #pragma unroll
