@@ -280,7 +280,8 @@ def main():
     lm_tok = torch.from_numpy(host.tokens).to(dev)
     ws_lm = torch.zeros(max(1, dreams.tree_accept_lm_head_workspace_size(B, T, Hd, wl.vocab)), dtype=torch.uint8,
                         device=dev)
-    lm_out = (sets[0]["alen"], sets[0]["path"], sets[0]["next"], None)
+    lm_out = (torch.empty(B, dtype=torch.int32, device=dev), torch.empty((B, T), dtype=torch.int32, device=dev),
+              torch.empty(B, dtype=torch.int32, device=dev), None)   # own outputs: set 0's are checked later
 
     def lm_fused():
         for w in lm_w:
