@@ -28,6 +28,9 @@
 // first exceeds u0 * total, and a block scan of that piece finds the token.  Probabilities are fp64, so that
 // the integer outcome is decided in the precision of the definition; exp is Tang's table-driven method.
 //
+// Pieces are 2048 entries (each thread holding 8, a pass piece computing p and q before its waits) while there
+// are at most 4096 statistics workgroups, else 8192 entries streamed in four 2048-entry parts after the waits.
+//
 // Forward progress.  A workgroup only waits for rows whose pieces all have smaller blockIdx (stats pieces come
 // first, pass pieces are ordered by child index), and workgroups are dispatched in blockIdx order, so every
 // wait ends; waits are nevertheless bounded (0.2 s), after which the results are unspecified.
