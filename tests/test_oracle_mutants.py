@@ -99,3 +99,44 @@ def test_pins_catch_planted_mistake(tmp_path, name, group, old, new):
         except (AssertionError, oracle.OracleError, ValueError, IndexError) as e:
             caught.append((pin.__name__, type(e).__name__))
     assert caught, "no pin caught mutant %s" % name
+
+
+# The LM head's oracle is plain numpy (oracle/__init__.py); its planted mistakes replace the function itself.
+def _decode(bits):
+    import numpy as np
+    return (np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _lm_swapped_operands(h, w):
+    hh, ww = _decode(h), _decode(w)
+    return ww @ hh.reshape(-1, hh.shape[-1]).T
+
+
+def _lm_low_half_decode(h, w):
+    import numpy as np
+    dec = lambda b: (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32)).view(np.float32).astype(np.float64)
+    return dec(h) @ dec(w).T
+
+
+def _lm_drops_last_k(h, w):
+    hh, ww = _decode(h), _decode(w)
+    return hh[..., :-1] @ ww[:, :-1].T
+
+
+def _lm_extra_term(h, w):
+    hh, ww = _decode(h), _decode(w)
+    return hh @ ww.T + hh[..., :1]
+
+
+@pytest.mark.parametrize("mutant", [_lm_swapped_operands, _lm_low_half_decode, _lm_drops_last_k, _lm_extra_term],
+                         ids=lambda f: f.__name__)
+def test_lm_head_pins_catch_planted_mistake(monkeypatch, mutant):
+    monkeypatch.setattr(oracle, "lm_head_logits", mutant)
+    orc = oracle.default()
+    caught = []
+    for pin in pins.LM_HEAD_PINS:
+        try:
+            pin(orc)
+        except (AssertionError, ValueError, IndexError) as e:
+            caught.append((pin.__name__, type(e).__name__))
+    assert caught, "no pin caught %s" % mutant.__name__
