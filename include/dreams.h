@@ -42,7 +42,8 @@ typedef enum {
   DREAMS_ERR_INVALID_ARG = -1,  /* a host-visible argument is out of range or a required pointer is NULL */
   DREAMS_ERR_UNSUPPORTED = -2,  /* valid in principle but not built (e.g. a head_dim other than 64/128)   */
   DREAMS_ERR_WORKSPACE = -3,    /* workspace NULL or smaller than the matching *_workspace_size           */
-  DREAMS_ERR_HIP = -4           /* the HIP runtime reported an error (device query or kernel launch)     */
+  DREAMS_ERR_HIP = -4,          /* the HIP runtime reported an error (device query or kernel launch)     */
+  DREAMS_ERR_DEVICE = -5        /* a kernel of an earlier call flagged a failure (dreams_workspace_status) */
 } dreams_status_t;
 
 typedef enum { DREAMS_F32 = 0, DREAMS_BF16 = 1 } dreams_dtype_t;
@@ -51,11 +52,26 @@ typedef enum { DREAMS_F32 = 0, DREAMS_BF16 = 1 } dreams_dtype_t;
  * Workspaces.  Every workspace (of either verb that takes one) begins with DREAMS_WORKSPACE_COUNTER_BYTES
  * bytes of arrival counters.  Zero-fill that region once, before the workspace is first used (zeroing the
  * whole buffer after allocating it does this).  Every call, of any shape, leaves the region zero again when it
- * completes, so one workspace of sufficient size can serve calls of different shapes and of both verbs one
- * after another.  Calls that overlap in time on one workspace (different streams without synchronisation)
- * race and give unspecified results.  Workspaces must be 256-byte aligned.
+ * completes, so one workspace of sufficient size can serve calls of different shapes and of every verb one
+ * after another.  The region's last 128 bytes hold failure flags instead of counters: a kernel that meets a
+ * condition it cannot complete under (listed at dreams_workspace_status) sets one and leaves it set until
+ * dreams_workspace_status reads and clears it.  Calls that overlap in time on one workspace (different
+ * streams without synchronisation) race and give unspecified results.  Workspaces must be 256-byte aligned.
  */
 #define DREAMS_WORKSPACE_COUNTER_BYTES 65536
+
+/*
+ * dreams_workspace_status -- the failures kernels flagged in `workspace` (device, 256-byte aligned, a workspace
+ * of any verb) since the last check.  Synchronises `stream`, reads the flags, clears them, and returns DREAMS_OK
+ * if none was set, else DREAMS_ERR_DEVICE with a message naming each flag.  The flags:
+ *   attention (more than one piece per row set): the pieces of one set did not all run on one XCD, so the
+ *       merge could not read their partial results from its XCD's L2 -- the rows of that set are NaN.  Not
+ *       expected on an MI355X (workgroup n runs on XCD n % 8).
+ *   sampled acceptance: a wait for another workgroup's result gave up (after 0.2 s); that call's integer
+ *       results are unspecified.
+ * Not for use under stream capture (it copies to the host and synchronises).
+ */
+dreams_status_t dreams_workspace_status(void* workspace, hipStream_t stream);
 
 /*
  * Shape of one tree-verification attention call.
@@ -91,6 +107,10 @@ typedef struct {
  * results live there, after the counter region every workspace starts with. */
 dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t* desc, size_t* bytes);
 
+/* Number of pieces dreams_tree_verify_attn cuts the key axis of every (sequence, KV head) into for `desc` on
+ * the current device (desc->num_splits, clamped, or the library's choice when it is 0). */
+dreams_status_t dreams_tree_verify_attn_splits(const dreams_attn_desc_t* desc, int32_t* splits);
+
 /*
  * dreams_tree_verify_attn -- the target model's parallel verification pass, attention part (the paper,
  * Section 2, "Speculative decoding": the target checks all draft tokens in one pass; Section 3.2 defines the
@@ -118,7 +138,9 @@ dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t*
  *   workspace  device, >= dreams_tree_verify_attn_workspace_size bytes (see "Workspaces" above), or NULL
  *              when that size is 0.
  * Arithmetic: bf16 products accumulated in fp32 on the matrix cores, softmax statistics in fp32, one
- * rounding of the probabilities to bf16 before the value product; output rounded to the nearest bf16.
+ * rounding of the probabilities to bf16 before the value product; output rounded to the nearest bf16.  With
+ * more than one piece of the key axis (dreams_tree_verify_attn_splits), each piece's output is rounded to
+ * bf16 once more before the pieces are merged in fp32.
  */
 dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
                                         const void* v_cache, const int32_t* kv_len, const int32_t* parent,
@@ -167,7 +189,7 @@ dreams_status_t dreams_attn_entropy_select(int32_t num_layers, const float* ae, 
  * kv_len; lse = that call's log-sum-exp output, [B, Hq, T]).  A visual slot at or past a sequence's prefix
  * length has importance 0; a row whose lse is -inf contributes nothing.  bf16 only (DREAMS_ERR_UNSUPPORTED
  * otherwise).  importance: device [B, vis_count] float (out).  Requires vis_begin >= 0, vis_count >= 1,
- * vis_begin + vis_count <= cache_capacity and B * ceil(vis_count / 256) <= DREAMS_WORKSPACE_COUNTER_BYTES / 4
+ * vis_begin + vis_count <= cache_capacity and B * ceil(vis_count / 256) <= (DREAMS_WORKSPACE_COUNTER_BYTES - 128) / 4
  * (DREAMS_ERR_UNSUPPORTED otherwise).  workspace: device, 256-byte aligned, >=
  * dreams_visual_importance_workspace_size bytes: the arrival-counter region every workspace starts with (see
  * "Workspaces" above), then B*Hkv*vis_count floats of per-KV-head partial sums.  Arithmetic: bf16 products, fp32
@@ -203,7 +225,7 @@ dreams_status_t dreams_visual_gather(int32_t batch, int32_t num_kv_heads, int32_
                                      void* v_out, hipStream_t stream);
 
 /* Bytes of workspace dreams_tree_accept needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if batch
- * exceeds DREAMS_WORKSPACE_COUNTER_BYTES / 4 (one arrival counter per sequence, plus up to 8 group counters
+ * exceeds (DREAMS_WORKSPACE_COUNTER_BYTES - 128) / 4 (one arrival counter per sequence, plus up to 8 group counters
  * per sequence while batch * 9 counters fit).  After the counters: one (value, index) pair per piece of each
  * row (rows of long vocabularies are cut into pieces). */
 dreams_status_t dreams_tree_accept_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
@@ -239,7 +261,7 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
 
 /* Bytes of workspace dreams_tree_accept_sampled needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if
  * vocab exceeds 2^23 or if the arrival counters (one word per sequence, then 16 bytes per row: batch *
- * num_nodes rows) do not fit in DREAMS_WORKSPACE_COUNTER_BYTES (about 4000 rows).  After the counters: per row
+ * num_nodes rows) do not fit in DREAMS_WORKSPACE_COUNTER_BYTES - 128 (about 4000 rows).  After the counters: per row
  * 8 bytes of flags plus 40 bytes per piece of the vocabulary (pieces of 2048 entries, or of 8192 once
  * batch * num_nodes * ceil(vocab / 2048) exceeds 4096). */
 dreams_status_t dreams_tree_accept_sampled_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,

@@ -64,14 +64,20 @@ dreams_status_t device_cus(int* cus) {
 // Every workspace starts with a fixed region of arrival counters, whatever the verb and shape, so a
 // workspace left zero by one call is valid for any other call.
 constexpr size_t kCounterBytes = DREAMS_WORKSPACE_COUNTER_BYTES;
-constexpr size_t kMaxCounters = kCounterBytes / sizeof(uint32_t);
+static_assert(kCounterBytes == 65536, "counter region layout (kernels.h)");
+// Counter words any verb may use; the region's last 128 bytes hold the device-side failure flags.
+constexpr size_t kMaxCounters = kCounterWords;
 
 struct AttnPlan {
   int G, rows_total, row_groups, units, splits;
   int rows_per_wg;   // query rows one workgroup owns
-  int merge_stride;  // words between the merge counters in the counter region; 0: separate merge kernel
-  size_t acc_off, ml_off, e_off, bytes;
+  int ctr_stride;    // 64-bit words between the sets' arrival counters in the counter region
+  int merge_parts;   // merging workgroups per set appended to the launch (0: the set's last piece merges it)
+  size_t o_off, ml_off, e_off, bytes;
 };
+
+// 64-bit set counters the counter region holds (at the closest spacing).
+constexpr long long kMaxSetCounters = (long long)kMaxCounters / 2;
 
 constexpr int kPieceMinKeys = 128;   // keys per piece of the key axis, at least
 
@@ -119,12 +125,14 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p, bool launchi
   const int max_len = d->max_kv_len > 0 ? d->max_kv_len : d->cache_capacity - d->num_nodes;
   const int n_keys = max_len + d->num_nodes;
   const int max_splits = (n_keys + kPieceMinKeys - 1) / kPieceMinKeys;
-  int cus = 0;
   int splits = d->num_splits;
-  if (splits == 0) {
-    // about one workgroup per compute unit (a workgroup holds most of a compute unit's LDS)
+  int cus = 0;
+  if (splits == 0 || launching) {
     st = device_cus(&cus);
     if (st != DREAMS_OK) return st;
+  }
+  if (splits == 0) {
+    // about one workgroup per compute unit (a workgroup holds most of a compute unit's LDS)
     const long long wgs = (long long)p->units * p->row_groups;
     splits = (int)((cus + wgs / 2) / wgs);
     // More workgroups than compute units: a last round of workgroups that fills less than half of the chip
@@ -136,30 +144,28 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p, bool launchi
   }
   if (splits > max_splits) splits = max_splits;
   if (splits > kAttnMaxSplits) splits = kAttnMaxSplits;
+  const long long sets = (long long)p->units * p->row_groups;
+  if (2 * sets > kMaxSetCounters) splits = 1;   // no room for the sets' arrival counters: one piece each
   if (splits < 1) splits = 1;
   p->splits = splits;
   const long long grid = 8LL * ((p->units + 7) / 8) * splits * p->row_groups;
   if (grid > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large: %lld workgroups", grid);
   if (splits > 1) {
-    // partial results of the pieces, after the counter region every workspace starts with
-    const size_t rows = (size_t)p->units * p->row_groups * splits * p->rows_per_wg;
-    // With more streaming workgroups than compute units, the pieces are merged in the same launch, where the
-    // merging overlaps the last round of streaming; with one round, a separate merge kernel is faster (its
-    // launch costs less than making every piece wait for its device-scope stores).  The merge in the launch
-    // takes two counters per (sequence, KV head, row group) in the counter region, each on a cache line of
-    // its own where there is room (atomics on one line serialise).
-    if (launching) {
-      if (cus == 0) {
-        st = device_cus(&cus);
-        if (st != DREAMS_OK) return st;
-      }
-      const long long sets = (long long)p->units * p->row_groups;
-      int stride = 32;
-      while (stride > 1 && 2 * sets * stride > (long long)kMaxCounters) stride >>= 1;
-      p->merge_stride = grid > cus && 2 * sets * stride <= (long long)kMaxCounters ? stride : 0;
-    }
-    p->acc_off = kCounterBytes;
-    p->ml_off = p->acc_off + align_up(rows * d->head_dim * sizeof(float), 256);
+    // two 64-bit counters per set (arrivals, finished merging workgroups), on a 128-byte line of their own
+    // where there is room (atomics on one line serialise), then the pieces' partial results after the counter
+    // region every workspace starts with
+    int stride = 16;
+    while (stride > 2 && sets * stride > kMaxSetCounters) stride >>= 1;
+    p->ctr_stride = stride;
+    // One round of streaming workgroups and at least 4 pieces per set: merging workgroups of 16 rows each,
+    // appended to the launch, spread each set's merge over several compute units as streaming ones finish
+    // (llava7b_layer, 8 pieces: 19.1 against 20.3 us).  Otherwise the set's last piece merges it: with 2 pieces
+    // that is one partial result to read (llava7b_full layer: 47.9 against 51.2 us), and with several rounds
+    // no workgroup holds a compute unit waiting while pieces of later rounds stream.
+    p->merge_parts = launching && grid <= cus && splits >= 4 ? p->rows_per_wg / 16 : 0;
+    const size_t rows = (size_t)sets * splits * p->rows_per_wg;
+    p->o_off = kCounterBytes;
+    p->ml_off = p->o_off + align_up(rows * d->head_dim * 2, 256);
     p->e_off = p->ml_off + align_up(rows * 2 * sizeof(float), 256);
     p->bytes = p->e_off + align_up(rows * sizeof(float), 256);
   }
@@ -289,11 +295,13 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
   a.lse = lse;
   a.entropy = entropy;
   char* ws = (char*)workspace;
-  a.part_acc = p.bytes ? (float*)(ws + p.acc_off) : nullptr;
+  a.part_o = p.bytes ? (__bf16*)(ws + p.o_off) : nullptr;
   a.part_ml = p.bytes ? (float*)(ws + p.ml_off) : nullptr;
   a.part_e = p.bytes ? (float*)(ws + p.e_off) : nullptr;
-  a.merge_ctr = p.bytes && p.merge_stride ? (uint32_t*)ws : nullptr;
-  a.merge_stride = p.merge_stride;
+  a.set_ctr = p.bytes ? (unsigned long long*)ws : nullptr;
+  a.ctr_stride = p.ctr_stride;
+  a.merge_parts = p.merge_parts;
+  a.err = p.bytes ? (uint32_t*)ws + kErrorWord : nullptr;
   a.B = desc->batch;
   a.Hq = desc->num_q_heads;
   a.Hkv = desc->num_kv_heads;
@@ -815,11 +823,40 @@ const char* dreams_status_string(dreams_status_t status) {
     case DREAMS_ERR_UNSUPPORTED: return "DREAMS_ERR_UNSUPPORTED: shape or type not supported by this build";
     case DREAMS_ERR_WORKSPACE: return "DREAMS_ERR_WORKSPACE: workspace missing or too small";
     case DREAMS_ERR_HIP: return "DREAMS_ERR_HIP: the HIP runtime reported an error";
+    case DREAMS_ERR_DEVICE: return "DREAMS_ERR_DEVICE: a kernel flagged a failure in the workspace";
   }
   return "unknown dreams status";
 }
 
 const char* dreams_last_error_message(void) { return g_error.c_str(); }
+
+dreams_status_t dreams_workspace_status(void* workspace, hipStream_t stream) {
+  if (!workspace) return fail(DREAMS_ERR_INVALID_ARG, "workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  uint32_t* word = (uint32_t*)workspace + kErrorWord;
+  uint32_t flags = 0;
+  hipError_t e = hipMemcpyAsync(&flags, word, sizeof(flags), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "reading the workspace's failure flags");
+  if (flags == 0) return ok();
+  e = hipMemsetAsync(word, 0, sizeof(flags), stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "clearing the workspace's failure flags");
+  std::string what;
+  if (flags & kErrXcdSplit) what += " [attention: pieces of one row set ran on different XCDs; outputs NaN]";
+  if (flags & kErrWaitTimeout) what += " [sampled acceptance: a bounded wait gave up; results unspecified]";
+  if (flags & ~(kErrXcdSplit | kErrWaitTimeout)) what += " [unknown flag]";
+  return fail(DREAMS_ERR_DEVICE, "failure flags 0x%x:%s", flags, what.c_str());
+}
+
+dreams_status_t dreams_tree_verify_attn_splits(const dreams_attn_desc_t* desc, int32_t* splits) {
+  if (!splits) return fail(DREAMS_ERR_INVALID_ARG, "splits is NULL");
+  AttnPlan p;
+  dreams_status_t st = plan_attn(desc, &p, false);
+  if (st != DREAMS_OK) return st;
+  *splits = p.splits;
+  return ok();
+}
 
 dreams_status_t dreams_check_tree_host(const int32_t* parent, int32_t num_nodes) {
   if (!parent) return fail(DREAMS_ERR_INVALID_ARG, "parent is NULL");

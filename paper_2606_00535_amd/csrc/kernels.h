@@ -10,7 +10,8 @@ namespace dreams {
 // Workgroups hand partial results to the last of them to finish through device-scope ("sc1") stores and
 // loads, which write through / read past the per-XCD L2 for exactly those words, plus a relaxed device-scope
 // atomic counter issued after an explicit wait for the stores.  Release/acquire fences would instead write
-// back and invalidate the whole L2 of the issuing XCD on every call.
+// back and invalidate the whole L2 of the issuing XCD on every call.  (On gfx950 an atomic is the same
+// instruction at every scope: it is always performed where every XCD sees it.)
 __device__ __forceinline__ void store_coherent(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -34,6 +35,27 @@ __device__ __forceinline__ void reset_counter(uint32_t* counter) {
   __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Index of the accelerator complex die (XCD) the calling wave runs on.  Workgroup n of a launch runs on XCD
+// n % 8 (the dispatcher deals workgroup ids round-robin over the dies); kernels that exchange data through a
+// die's own L2 check this at run time.
+__device__ __forceinline__ uint32_t xcd_id() {
+  uint32_t x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return x & 7u;
+}
+
+// ------------------------------------------------------------------------------ device-side failures
+// The last 128 bytes of every workspace's counter region hold sticky failure flags: a kernel that detects a
+// condition it cannot complete under sets a bit (device-scope atomic OR); dreams_workspace_status reports and
+// clears them.  The counters of every verb live below kCounterWords.
+constexpr int kCounterWords = (65536 - 128) / 4;    // words of the counter region that verbs may use
+constexpr int kErrorWord = (65536 - 128) / 4;       // word index of the failure flags
+constexpr uint32_t kErrXcdSplit = 1u;       // attention: pieces of one row set ran on different XCDs
+constexpr uint32_t kErrWaitTimeout = 2u;    // a bounded wait for other workgroups gave up
+__device__ __forceinline__ void raise_device_error(uint32_t* err, uint32_t bit) {
+  if (err) __hip_atomic_fetch_or(err, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ------------------------------------------------------------------------------------ tree attention
 // Matrix-core (bf16) path: one workgroup = 4 waves, each wave owning 16 (narrow) or 32 (wide) query rows of
 // one KV head for a whole piece of that head's key axis; the key axis of every (sequence, KV head, row
@@ -51,15 +73,21 @@ struct AttnArgs {
   void* out;              // [B, Hq, T, D]
   float* lse;             // [B, Hq, T] or nullptr
   float* entropy;         // [B, Hq, T] attention entropy of every row (nats), or nullptr
-  float* part_acc;        // [units * row_groups, splits, rows_per_wg, D]   (splits > 1 only)
-  float* part_ml;         // [units * row_groups, splits, rows_per_wg, 2]
-  float* part_e;          // [units * row_groups, splits, rows_per_wg]   (entropy terms; with entropy only)
-  // Merge in the same launch (splits > 1): the workgroups past the first `stream_wgs` merge the pieces of a
-  // (sequence, KV head, row group) once its pieces have arrived at merge_ctr[set * merge_stride]; their own
-  // arrivals are counted at merge_ctr[(sets + set) * merge_stride].  nullptr: a separate merge kernel.
-  uint32_t* merge_ctr;
-  int merge_stride;       // words between consecutive counters
+  // Several pieces per (sequence, KV head, row group) -- a "set": each piece stores its rows' normalised output
+  // (bf16) and softmax state, and the last piece of the set to arrive at the set's counter merges them.
+  __bf16* part_o;         // [sets, splits, rows_per_wg, D]   accumulator / sum, rounded to bf16
+  float* part_ml;         // [sets, splits, rows_per_wg, 2]   (max in log2 units, sum)
+  float* part_e;          // [sets, splits, rows_per_wg]      entropy terms (with entropy only)
+  // 64-bit arrival counter of set s at set_ctr[s * ctr_stride]: the arrivals in bits [0, 8), and per XCD x a
+  // 7-bit count of the set's pieces that ran there at bit 8 + 7x.  Zero between calls.
+  unsigned long long* set_ctr;
+  int ctr_stride;         // 64-bit words between consecutive set counters (>= 2 with merging workgroups: the
+                          // second word counts the set's finished merging workgroups)
+  // > 0: merge_parts merging workgroups per set (rows_per_wg / merge_parts rows each) follow the streaming ones
+  // in the same launch; 0: the last piece of each set merges it
+  int merge_parts;
   int stream_wgs;         // set by the launcher
+  uint32_t* err;          // the workspace's failure flags (splits > 1)
   int B, Hq, Hkv, G, T, D, S_cap;
   int units;              // B * Hkv
   int rows_per_wg;        // query rows of one workgroup (64 or 128)

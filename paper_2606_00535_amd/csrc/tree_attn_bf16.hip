@@ -25,13 +25,12 @@
 //   * Waves are arranged as KW key groups of 4/KW waves: the groups take alternate steps (group k the steps
 //     k, k+KW, ...) and each wave owns 16*RB rows, so a wave's operand reads serve as many rows as possible;
 //     the groups' (max, sum, accumulator) states are merged through LDS at the end.
-//   * With several pieces per (sequence, KV head, row group), each workgroup writes its rows' (max, sum,
-//     accumulator) to the workspace and the pieces are merged in piece order (so the result does not depend
-//     on scheduling), in one of two ways:
-//       - one round of workgroups: a second, small kernel; the kernel boundary makes the partial results
-//         visible across XCDs, with no device-scope stores, fences or counters on the streaming path;
-//       - several rounds: extra workgroups at the end of the same launch, which wait for their set's pieces
-//         (device-scope stores, then one arrival per piece) and merge them while the last round streams.
+//   * With several pieces per (sequence, KV head, row group) -- a set -- each workgroup stores its rows'
+//     output normalised by their softmax sum (bf16) and their (max, sum) to the workspace, then counts its
+//     arrival on the set's counter; the last piece of the set to arrive merges all of them, in piece order
+//     (so the result does not depend on which piece came last), in the same launch.  Nothing ever waits for
+//     another workgroup.  All pieces of a set run on one XCD (below), so their partial results stay in that
+//     XCD's L2: plain stores, non-temporal loads, no device-scope write-through and no second launch.
 //   * Workgroup ids are remapped so that all workgroups of one (sequence, KV head) run on the same XCD
 //     (consecutive ids are dealt round-robin over the 8 XCDs): row groups reading the same keys share them
 //     in that XCD's L2.
@@ -46,10 +45,14 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kStep = 32;          // keys per step
+// Bound on the merging workgroup's wait for its set's other pieces (100 MHz real-time ticks): 0.2 s, far
+// beyond any call.
+constexpr uint64_t kMergeWaitTicks = 20000000;
 constexpr float kLazyLog2 = 8.0f;  // slack of the running maximum, log2 units
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -111,20 +114,6 @@ __device__ __forceinline__ void barrier_lds() {
   asm volatile("" ::: "memory");
 }
 
-// Device-scope (sc1) accesses through a buffer resource over [base, base + bytes): coherent across the
-// XCDs' L2s, which the pieces' partial results need when the merge runs in the same launch.
-// (the buffer builtins take and return plain `vector_size` vectors: values cross to and from them by bit_cast
-// only, never by assignment)
-typedef uint32_t buf_b128 __attribute__((vector_size(16)));
-typedef uint32_t buf_b64 __attribute__((vector_size(8)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-constexpr int kDeviceScope = 16;   // sc1 bit of the buffer instructions' cache-policy operand
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-// Bound on a merging workgroup's wait for the pieces (100 MHz real-time ticks): 0.2 s, far beyond any call.
-constexpr uint64_t kMergeWaitTicks = 20000000;
-
 // Row layout in LDS: rows of D bf16, unpadded; the 16-byte chunk c of row r sits at position c ^ swz(r),
 // which spreads the 16 rows one operand read touches over distinct banks.  The swizzle repeats every 16
 // rows.  A step slot holds 32 K rows then 32 V rows; the query rows use the same layout.
@@ -140,103 +129,122 @@ struct Rows {
   __device__ static __forceinline__ int off(int r, int c) { return r * ROW + ((c ^ swz(r)) << 4); }
 };
 
-// Merge of a set's pieces by workgroups of the streaming launch (the ones past a.stream_wgs), laid out like
-// the merge kernel below: each wave covers 64 / (D/4) rows at 4 columns per lane; a set takes
-// ceil(R / (W * those rows)) workgroups.  They are dispatched after every streaming workgroup, so the pieces
-// they wait for are already running or done and never wait themselves: the wait ends.  The pieces' rows are
-// read with device-scope loads after their arrival count is complete; the last merging workgroup of the set
-// clears both counters for the next call.
+// Merge of a set's pieces for rows [r0, r0 + nrows) of the set, in piece order (so the result does not
+// depend on which piece finished last): out = sum_s w_s l_s o_s / sum_s w_s l_s, w_s = 2^(m_s - max_s m_s).
+// Piece `own` (if >= 0) is this workgroup's own, read from its LDS staging (row-major 16-byte pieces swizzled
+// by the row, with its (max, sum) and entropy terms); the others come from this XCD's L2 (not from this compute
+// unit's L1, which has never held them): non-temporal 16-byte loads, a row's pieces side by side, whole
+// 128-byte lines.  Rows at or past rows_valid are skipped.  good = false writes NaN rows (a failed wait).
 template <int D, int W, bool ENT>
-__device__ __forceinline__ void merge_in_launch(const AttnArgs& a, int m) {
-  constexpr int CPT = 4;                // columns per lane
-  constexpr int TPR = D / CPT;          // lanes per row
-  constexpr int MR = 64 / TPR;          // rows per wave
-  constexpr int CH = 8;                 // pieces per batch of loads
-  const int R = a.rows_per_wg, S = a.splits;
-  const int MB = (R + W * MR - 1) / (W * MR);
-  const int sets = a.units * a.row_groups;
-  const int pset = m / MB, mb = m - pset * MB;
-  const int wave = threadIdx.x >> 6, t = threadIdx.x & 63;
-  const int r = (mb * W + wave) * MR + t / TPR, c0 = (t % TPR) * CPT;
-  uint32_t* arrive = a.merge_ctr + (size_t)pset * a.merge_stride;
-  uint32_t* done = a.merge_ctr + (size_t)(sets + pset) * a.merge_stride;
+__device__ __forceinline__ void merge_pieces(const AttnArgs& a, size_t prow0, int R, __bf16* out_rows, float* lse_rows,
+                                             float* ent_rows, int rows_valid, int r0, int nrows, int own,
+                                             const unsigned char* own_rows, const float2* own_ml, const float* own_e,
+                                             bool good) {
+  constexpr int CPR = D / 8;
+  constexpr int TG = 2;     // items whose loads are in flight together
+  constexpr int PCH = 8;    // pieces per batch of loads
+  typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
+  const int S = a.splits;
+  const int items = nrows * CPR;
+  for (int base = 0; base < items; base += TG * 64 * W) {
+    int rl[TG], ch[TG];
+    bool live[TG];
+    float M[TG], lsum[TG], esum[TG];
+    float acc[TG][8];
+#pragma unroll
+    for (int t = 0; t < TG; ++t) {
+      const int item = base + t * 64 * W + (int)threadIdx.x;
+      rl[t] = r0 + item / CPR;
+      ch[t] = item % CPR;
+      live[t] = item < items && rl[t] < rows_valid;
+      M[t] = -INFINITY;
+      lsum[t] = esum[t] = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[t][e] = 0.f;
+    }
+    for (int s0 = 0; s0 < S; s0 += PCH) {
+      float2 ml[TG][PCH];
+      float ev[TG][PCH];
+      bf16x8m x[TG][PCH];
+#pragma unroll
+      for (int t = 0; t < TG; ++t)
+#pragma unroll
+        for (int k = 0; k < PCH; ++k) {
+          const int sp = min(s0 + k, S - 1);
+          const size_t pr = prow0 + (size_t)sp * R + rl[t];
+          if (!live[t]) {
+            ml[t][k] = make_float2(-INFINITY, 0.f);
+            ev[t][k] = 0.f;
+            x[t][k] = bf16x8m{};
+          } else if (sp == own) {
+            ml[t][k] = own_ml[rl[t]];
+            ev[t][k] = ENT ? own_e[rl[t]] : 0.f;
+            x[t][k] = *(const bf16x8m*)(own_rows + ((size_t)rl[t] * CPR + (ch[t] ^ (rl[t] & (CPR - 1)))) * 16);
+          } else {
+            const f32x2 mlv = __builtin_nontemporal_load((const f32x2*)(a.part_ml + 2 * pr));
+            ml[t][k] = make_float2(mlv.x, mlv.y);
+            ev[t][k] = ENT ? __builtin_nontemporal_load(a.part_e + pr) : 0.f;
+            x[t][k] = __builtin_nontemporal_load((const bf16x8m*)(a.part_o + pr * D + ch[t] * 8));
+          }
+        }
+#pragma unroll
+      for (int t = 0; t < TG; ++t) {
+        float Mn = M[t];
+#pragma unroll
+        for (int k = 0; k < PCH; ++k)
+          if (s0 + k < S) Mn = fmaxf(Mn, ml[t][k].x);
+        const float scale_old = M[t] == -INFINITY ? 0.f : fast_exp2(M[t] - Mn);
+        if (ENT) esum[t] = ent_term(scale_old, esum[t], M[t], Mn, lsum[t]);
+        lsum[t] *= scale_old;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[t][e] *= scale_old;
+#pragma unroll
+        for (int k = 0; k < PCH; ++k) {
+          const float w = (s0 + k >= S || ml[t][k].x == -INFINITY) ? 0.f : fast_exp2(ml[t][k].x - Mn);
+          if (ENT) esum[t] += ent_term(w, ev[t][k], ml[t][k].x, Mn, ml[t][k].y);
+          const float wl = w * ml[t][k].y;
+          lsum[t] += wl;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[t][e] = fmaf(wl, (float)x[t][k][e], acc[t][e]);
+        }
+        M[t] = Mn;
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TG; ++t) {
+      if (!live[t]) continue;
+      const float inv = !good ? NAN : lsum[t] > 0.f ? 1.0f / lsum[t] : 0.f;
+      bf16x8m res;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) res[e] = (__bf16)(acc[t][e] * inv);
+      *(bf16x8m*)(out_rows + (size_t)rl[t] * D + ch[t] * 8) = res;
+      if (ch[t] == 0) {
+        if (lse_rows) lse_rows[rl[t]] = !good ? NAN : lsum[t] > 0.f ? (M[t] + __log2f(lsum[t])) * kLn2 : -INFINITY;
+        if (ENT) ent_rows[rl[t]] = !good ? NAN : row_entropy(lsum[t], esum[t]);
+      }
+    }
+  }
+}
 
-  // wave 0 waits for the set's pieces; the others wait for wave 0
-  __shared__ int in_time_lds;
-  if (wave == 0) {
-    bool in_time = true;
-    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-    while (__hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)S) {
-      if (__builtin_amdgcn_s_memrealtime() - t0 > kMergeWaitTicks) {
-        in_time = false;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-    if (t == 0) in_time_lds = in_time;
+// Wait (one thread) until a set's arrival counter shows `expect` pieces, bounded by kMergeWaitTicks.  Returns 1
+// if they arrived and all ran on the caller's XCD, else 2 (and flags the workspace).
+__device__ __forceinline__ uint32_t wait_for_pieces(const AttnArgs& a, unsigned long long* ctr, int expect) {
+  const uint32_t x = xcd_id();
+  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  unsigned long long c;
+  while (((c = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffull) < (unsigned long long)expect) {
+    if (__builtin_amdgcn_s_memrealtime() - t0 > kMergeWaitTicks) break;
+    __builtin_amdgcn_s_sleep(1);
   }
-  __syncthreads();
-  const bool in_time = in_time_lds != 0;
-  // This workgroup is done with the arrival counter: count it as done now, so that the atomic's round trip
-  // overlaps the loads below; the last workgroup of the set clears both counters at its end.
-  uint32_t done_before = 0;
-  if (threadIdx.x == 0) done_before = __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-
-  if (r < R) {
-    const size_t row0 = (size_t)pset * S * R;   // the set's piece 0, row 0
-    const auto racc = buffer_rsrc(a.part_acc + row0 * D, (uint32_t)S * R * D * 4);
-    const auto rml = buffer_rsrc(a.part_ml + row0 * 2, (uint32_t)S * R * 8);
-    const auto re = buffer_rsrc(a.part_e + row0, (uint32_t)S * R * 4);
-    constexpr bool ent = ENT;
-    float M = -INFINITY, lsum = 0.f, esum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < S; s0 += CH) {
-      float2 ml[CH];
-      f32x4 x[CH];
-      float ev[CH];
-#pragma unroll
-      for (int k = 0; k < CH; ++k) {
-        const int pr = min(s0 + k, S - 1) * R + r;
-        const f32x2 mlv = __builtin_bit_cast(f32x2, __builtin_amdgcn_raw_buffer_load_b64(rml, pr * 8, 0, kDeviceScope));
-        ml[k] = make_float2(mlv.x, mlv.y);
-        x[k] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(racc, (pr * D + c0) * 4, 0, kDeviceScope));
-        ev[k] = ent ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(re, pr * 4, 0, kDeviceScope)) : 0.f;
-      }
-      float Mn = M;
-#pragma unroll
-      for (int k = 0; k < CH; ++k)
-        if (s0 + k < S) Mn = fmaxf(Mn, ml[k].x);
-      const float scale_old = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
-      esum = ent_term(scale_old, esum, M, Mn, lsum);
-      lsum *= scale_old;
-      acc *= scale_old;
-#pragma unroll
-      for (int k = 0; k < CH; ++k) {
-        const float w = (s0 + k >= S || ml[k].x == -INFINITY) ? 0.f : fast_exp2(ml[k].x - Mn);
-        esum += ent_term(w, ev[k], ml[k].x, Mn, ml[k].y);
-        lsum += w * ml[k].y;
-        acc += w * x[k];
-      }
-      M = Mn;
-    }
-    const int rg = pset % a.row_groups, u = pset / a.row_groups;
-    const int b = u / a.Hkv, g = u - b * a.Hkv;
-    const int row = rg * R + r;   // row within the KV head's G*T rows
-    if (row < a.G * a.T) {
-      const size_t orow = ((size_t)b * a.Hq + (size_t)g * a.G) * a.T + row;
-      const float inv = !in_time ? NAN : lsum > 0.f ? 1.0f / lsum : 0.f;
-      bf16x4 res;
-#pragma unroll
-      for (int e = 0; e < CPT; ++e) res[e] = (__bf16)(acc[e] * inv);
-      *(bf16x4*)((__bf16*)a.out + orow * D + c0) = res;
-      if (a.lse && c0 == 0) a.lse[orow] = !in_time ? NAN : lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
-      if (ent && c0 == 0) a.entropy[orow] = !in_time ? NAN : row_entropy(lsum, esum);
-    }
+  if ((c & 0xffull) != (unsigned long long)expect) {
+    raise_device_error(a.err, kErrWaitTimeout);
+    return 2;
   }
-  if (threadIdx.x == 0 && done_before == (uint32_t)MB - 1) {
-    reset_counter(done);
-    reset_counter(arrive);
+  if (((c >> (8 + 7 * x)) & 0x7full) != (unsigned long long)expect) {
+    raise_device_error(a.err, kErrXcdSplit);
+    return 2;
   }
+  return 1;
 }
 
 template <int D, int RB, int KW, int W, int NST, bool PIPE, bool ENT>
@@ -257,15 +265,40 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   static_assert(CPS * W == 4 * KW * C16 && CPS >= 1 && (C16 % CPS == 0 || CPS % C16 == 0), "copy split");
   static_assert(16 * L::ROW == C16 * 1024 && (16 / L::RPL) % L::CPR == 0, "swizzle repeats every 16 rows");
   static_assert(NSS * CPS + ((QB + W - 1) / W) * C16 + 8 <= 63, "outstanding copies fit the counter");
-  static_assert((size_t)(KW - 1) * R * (D + 3) * 4 <= (size_t)NST * L::SLOT, "group states fit the ring");
+  static_assert((size_t)(KW - 1) * R * D * 4 + (size_t)KW * R * 12 <= (size_t)NST * L::SLOT, "group states fit the ring");
 
   extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots
   __shared__ uint64_t anc_lds[2 * kMaxNodes];
-  __shared__ uint32_t meta_lds[4 * kMaxNodes];   // the sequence's parents or tree mask rows, as copied
-  __shared__ uint32_t stored_lds;                 // owner waves whose partial rows are stored (merge in launch)
+  __shared__ uint64_t meta_lds[2 * kMaxNodes];   // the sequence's parents or tree mask rows, as copied
+  __shared__ uint32_t merge_lds;                  // 1: merge the set's pieces; 2: merge, but write NaN rows
 
-  if (a.merge_ctr && (int)blockIdx.x >= a.stream_wgs) {
-    merge_in_launch<D, W, ENT>(a, (int)blockIdx.x - a.stream_wgs);
+  if (a.merge_parts > 0 && (int)blockIdx.x >= a.stream_wgs) {
+    // ---- a merging workgroup (after every streaming one, so the pieces it waits for are running or done):
+    // rows [part * R / merge_parts, ...) of one set, on the set's XCD
+    const int m = (int)blockIdx.x - a.stream_wgs;
+    const int mx = m & 7, ms = m >> 3;
+    const int per_unit = a.row_groups * a.merge_parts;
+    const int u = mx + 8 * (ms / per_unit);
+    if (u >= a.units) return;
+    const int within = ms - (ms / per_unit) * per_unit;
+    const int rg = within / a.merge_parts, part = within - rg * a.merge_parts;
+    constexpr int R = (W / KW) * 16 * RB;
+    const size_t pset = (size_t)u * a.row_groups + rg;
+    unsigned long long* ctr = a.set_ctr + pset * a.ctr_stride;
+    if (threadIdx.x == 0) merge_lds = wait_for_pieces(a, ctr, a.splits);
+    __syncthreads();
+    const int b = u / a.Hkv, g = u - b * a.Hkv;
+    const size_t orow0 = ((size_t)b * a.Hq + (size_t)g * a.G) * a.T + (size_t)rg * R;
+    const int nrows = R / a.merge_parts;
+    merge_pieces<D, W, ENT>(a, pset * a.splits * R, R, (__bf16*)a.out + orow0 * D, a.lse ? a.lse + orow0 : nullptr,
+                            ENT ? a.entropy + orow0 : nullptr, min(R, a.G * a.T - rg * R), part * nrows, nrows, -1,
+                            nullptr, nullptr, nullptr, merge_lds == 1);
+    // the set's last merging workgroup clears both counters for the next call
+    if (threadIdx.x == 0 &&
+        __hip_atomic_fetch_add(ctr + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned long long)a.merge_parts - 1) {
+      __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(ctr + 1, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     return;
   }
 
@@ -286,7 +319,6 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   const int rows_total = a.G * T;
   const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(ring));
   const int kv_len_b = a.kv_len[b];   // issued before the copies below, ahead of their traffic
-  if (tid == 0) stored_lds = 0;       // (published by the prologue's barriers)
 
   // ---- this workgroup's piece of the key axis, planned from the host's bound on the key count
   int piece = (a.max_keys + a.splits - 1) / a.splits;
@@ -384,7 +416,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   if (need_anc && tid < T) {
     uint64_t m0 = 0, m1 = 0;
     if (a.mask) {
-      const uint64_t* mr = (const uint64_t*)meta_lds + tid * Wm;
+      const uint64_t* mr = meta_lds + tid * Wm;
       m0 = mr[0];
       m1 = Wm > 1 ? mr[1] : 0;
     } else {
@@ -658,192 +690,173 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     }
   }
 
-  // ---- key groups 1.. hand their states to group 0 through LDS (merged in group order)
-  if constexpr (KW > 1) {
+  // ---- key groups: group k finalises output columns [16*DBK*k, 16*DBK*(k+1)) of its rows, from every group's
+  // state for those columns (exchanged through LDS, merged in group order)
+  constexpr int DBK = DB / KW;     // 16-column blocks of the output this wave finalises
+  static_assert(DB % KW == 0, "column share");
+  f32x4 fin[RB][DBK];
+  if constexpr (KW == 1) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int dd = 0; dd < DBK; ++dd) fin[rb][dd] = o[rb][dd];
+  } else {
     barrier_lds();   // every wave is done with the ring
-    // accumulators as [KW-1][D/4][R] 16-byte chunks: the 16 lanes of a quad touch 256 consecutive bytes,
-    // so neither the writes nor the reads below conflict on banks
+    // [owner group][source group, own one left out][DBK*4 16-byte chunks][R rows]: the 16 lanes of a quad touch
+    // 256 consecutive bytes, so neither the writes nor the reads conflict on banks
     f32x4* st_o = (f32x4*)ring;
-    float2* st_ml = (float2*)(st_o + (KW - 1) * R * (D / 4));  // [KW-1][R]
-    float* st_e = (float*)(st_ml + (KW - 1) * R);                // [KW-1][R]
-    if (kw > 0) {
+    float2* st_ml = (float2*)(st_o + (size_t)KW * (KW - 1) * DBK * 4 * R);   // [KW][R]
+    float* st_e = (float*)(st_ml + KW * R);                                   // [KW][R]
+    auto chunk = [&](int owner, int source, int dd, int row) {
+      return ((owner * (KW - 1) + (source < owner ? source : source - 1)) * DBK * 4 + dd * 4 + quad) * R + row;
+    };
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const int row = (kw - 1) * R + rh * RW + rb * 16 + col;
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = rh * RW + rb * 16 + col;
 #pragma unroll
-        for (int d = 0; d < DB; ++d) st_o[((kw - 1) * (D / 4) + d * 4 + quad) * R + rh * RW + rb * 16 + col] = o[rb][d];
-        if (quad == 0) {
-          st_ml[row] = make_float2(m_run[rb], l_run[rb]);
-          if (ENT) st_e[row] = e_run[rb];
-        }
+      for (int d = 0; d < DB; ++d)
+        if (d / DBK != kw) st_o[chunk(d / DBK, kw, d % DBK, row)] = o[rb][d];
+      if (quad == 0) {
+        st_ml[kw * R + row] = make_float2(m_run[rb], l_run[rb]);
+        if (ENT) st_e[kw * R + row] = e_run[rb];
       }
     }
     barrier_lds();
-    if (kw == 0) {
 #pragma unroll
-      for (int k = 1; k < KW; ++k) {
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = rh * RW + rb * 16 + col;
+      float mk[KW], lk[KW], ek[KW];
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const int row = (k - 1) * R + rh * RW + rb * 16 + col;
-          const float2 ml = st_ml[row];
-          const float M = fmaxf(m_run[rb], ml.x);
-          const float w0 = m_run[rb] == -INFINITY ? 0.f : fast_exp2(m_run[rb] - M);
-          const float w1 = ml.x == -INFINITY ? 0.f : fast_exp2(ml.x - M);
-          if (ENT) e_run[rb] = ent_term(w0, e_run[rb], m_run[rb], M, l_run[rb]) + ent_term(w1, st_e[row], ml.x, M, ml.y);
-          m_run[rb] = M;
-          l_run[rb] = l_run[rb] * w0 + ml.y * w1;
+      for (int k = 0; k < KW; ++k) {
+        const float2 ml = st_ml[k * R + row];
+        mk[k] = k == kw ? m_run[rb] : ml.x;
+        lk[k] = k == kw ? l_run[rb] : ml.y;
+        ek[k] = ENT ? (k == kw ? e_run[rb] : st_e[k * R + row]) : 0.f;
+      }
+      float M = mk[0];
 #pragma unroll
-          for (int d = 0; d < DB; ++d) o[rb][d] = o[rb][d] * w0 + st_o[((k - 1) * (D / 4) + d * 4 + quad) * R + rh * RW + rb * 16 + col] * w1;
+      for (int k = 1; k < KW; ++k) M = fmaxf(M, mk[k]);
+      float L = 0.f, E = 0.f;
+#pragma unroll
+      for (int dd = 0; dd < DBK; ++dd) fin[rb][dd] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < KW; ++k) {
+        const float w = mk[k] == -INFINITY ? 0.f : fast_exp2(mk[k] - M);
+        if (ENT) E += ent_term(w, ek[k], mk[k], M, lk[k]);
+        L += w * lk[k];
+#pragma unroll
+        for (int dd = 0; dd < DBK; ++dd) {
+          f32x4 x;
+          if (k == kw) {   // this wave's own state: block kw*DBK + dd of o (kw is wave-uniform)
+            x = o[rb][dd];
+#pragma unroll
+            for (int j = 1; j < KW; ++j)
+              if (j == kw) x = o[rb][j * DBK + dd];
+          } else {
+            x = st_o[chunk(kw, k, dd, row)];
+          }
+          fin[rb][dd] += w * x;
         }
       }
+      m_run[rb] = M;
+      l_run[rb] = L;
+      e_run[rb] = E;
     }
   }
-  const bool owner = kw == 0;   // the waves that now hold the workgroup's final states
+  const int c0 = kw * DBK * 16 + quad * 4;   // first output column of this lane's block dd = 0
 
-  // ---- a single piece: normalise and write.  Rows of one KV head are consecutive in memory.
-  if (a.splits == 1) {
-    if (!owner) return;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int row = rg * R + rh * RW + rb * 16 + col;
-      if (row >= rows_total) continue;
-      const size_t orow = qrow0 + row;
-      const float inv = l_run[rb] > 0.f ? 1.0f / l_run[rb] : 0.f;
-#pragma unroll
-      for (int d = 0; d < DB; ++d) {
-        bf16x4 res;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) res[e] = (__bf16)(o[rb][d][e] * inv);
-        *(bf16x4*)((__bf16*)a.out + orow * D + d * 16 + quad * 4) = res;
-      }
-      if (a.lse && quad == 0)
-        a.lse[orow] = l_run[rb] > 0.f ? (m_run[rb] + __log2f(l_run[rb])) * kLn2 : -INFINITY;
-      if (ENT && quad == 0) a.entropy[orow] = row_entropy(l_run[rb], e_run[rb]);
-    }
-    return;
-  }
-
-  // ---- several pieces: write this piece's unnormalised rows and (max, sum) for the merge
-  if (!owner) return;
-  const size_t pset = (size_t)u * a.row_groups + rg;
-  if (a.merge_ctr) {
-    // merged in this launch: device-scope stores, then one arrival per workgroup once every owner wave's
-    // stores have completed
-    const size_t row0 = pset * a.splits * R;
-    const auto racc = buffer_rsrc(a.part_acc + row0 * D, (uint32_t)a.splits * R * D * 4);
-    const auto rml = buffer_rsrc(a.part_ml + row0 * 2, (uint32_t)a.splits * R * 8);
-    const auto re = buffer_rsrc(a.part_e + row0, (uint32_t)a.splits * R * 4);
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int pr = split * R + rh * RW + rb * 16 + col;   // row within the set's pieces
-#pragma unroll
-      for (int d = 0; d < DB; ++d)
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(buf_b128, o[rb][d]), racc, (pr * D + d * 16 + quad * 4) * 4, 0,
-                                               kDeviceScope);
-      if (quad == 0) {
-        const f32x2 mlv = {m_run[rb], l_run[rb]};
-        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(buf_b64, mlv), rml, pr * 8, 0, kDeviceScope);
-        if (ENT) __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, e_run[rb]), re, pr * 4, 0, kDeviceScope);
-      }
-    }
-    wait_vector_memory();
-    if (lane == 0 &&
-        __hip_atomic_fetch_add(&stored_lds, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == (uint32_t)WR - 1)
-      __hip_atomic_fetch_add(a.merge_ctr + pset * a.merge_stride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return;
-  }
-  // separate merge kernel: plain stores, which the kernel boundary makes visible to it
+  // ---- the workgroup's rows, normalised and rounded to bf16, go row-major into LDS (after the key groups'
+  // exchange area; 16-byte pieces of a row XOR-swizzled by the row, so neither the matrix-core-layout writes
+  // nor the row reads conflict on banks), with each row's (max, sum) and entropy term; they are then written
+  // out as whole 16-byte pieces of rows.
+  constexpr int CPR = D / 8;                  // 16-byte pieces per row
+  constexpr size_t XBYTES = KW > 1 ? ((size_t)(KW - 1) * R * D * 4 + (size_t)KW * R * 12 + 1023) / 1024 * 1024 : 0;
+  static_assert(XBYTES + (size_t)R * D * 2 + (size_t)R * 12 <= (size_t)NST * L::SLOT, "row staging fits the ring");
+  unsigned char* row_lds = ring + XBYTES;                               // [R][CPR] 16-byte pieces
+  float2* ml_lds = (float2*)(row_lds + (size_t)R * D * 2);              // [R]
+  float* e_lds = (float*)(ml_lds + R);                                  // [R]
+  auto row_piece = [&](int r, int ch) { return row_lds + ((size_t)r * CPR + (ch ^ (r & (CPR - 1)))) * 16; };
+  if constexpr (KW == 1) barrier_lds();   // every wave's last operand reads of the ring have returned
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const size_t pr = (pset * a.splits + split) * R + rh * RW + rb * 16 + col;
+    const int rl = rh * RW + rb * 16 + col;
+    const float inv = l_run[rb] > 0.f ? 1.0f / l_run[rb] : 0.f;
 #pragma unroll
-    for (int d = 0; d < DB; ++d) *(f32x4*)(a.part_acc + pr * D + d * 16 + quad * 4) = o[rb][d];
-    if (quad == 0) {
-      *(float2*)(a.part_ml + 2 * pr) = make_float2(m_run[rb], l_run[rb]);
-      if (ENT) a.part_e[pr] = e_run[rb];
+    for (int dd = 0; dd < DBK; ++dd) {
+      bf16x4 res;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) res[e] = (__bf16)(fin[rb][dd][e] * inv);
+      const int c = c0 + dd * 16;
+      *(bf16x4*)(row_piece(rl, c / 8) + (c % 8) * 2) = res;
+    }
+    if (kw == 0 && quad == 0) {
+      ml_lds[rl] = make_float2(m_run[rb], l_run[rb]);
+      if (ENT) e_lds[rl] = e_run[rb];
     }
   }
-}
+  barrier_lds();
 
-// Merge of the key-axis pieces: out = sum_s w_s acc_s / sum_s w_s l_s with w_s = 2^(m_s - max_s m_s), in
-// piece order.  A one-wave workgroup merges the 64 / (D/4) rows (2 for D = 128, 4 for D = 64) of one
-// (sequence, KV head, row group) that its lanes cover at 4 columns (one 16-byte load per piece) each, so the
-// merge spreads over many compute units with many requests in flight.  All loads of a chunk of 8 pieces are
-// issued before any is used.
-template <int D>
-constexpr int merge_rows() { return 64 / (D / 4); }
-template <int D, bool ENT>
-__global__ __launch_bounds__(64) void tree_attn_merge_kernel(AttnArgs a) {
-  constexpr int CPT = 4;                // columns per thread
-  constexpr int TPR = D / CPT;          // threads per row
-  constexpr int MR = merge_rows<D>();   // rows per workgroup
-  static_assert(TPR * MR == 64, "one wave per workgroup");
-  constexpr int CH = 8;                 // pieces per batch of loads
-  typedef float fv __attribute__((ext_vector_type(CPT)));
-  const int R = a.rows_per_wg;
-  const int blocks = R / MR;
-  // same XCD as the streaming kernel's workgroups of this (sequence, KV head): ids dealt round-robin over
-  // the 8 XCDs, unit u on XCD u % 8
-  const int n = blockIdx.x;
-  const int xcd = n & 7, slot = n >> 3;
-  const int per_unit = a.row_groups * blocks;
-  const int u = xcd + 8 * (slot / per_unit);
-  if (u >= a.units) return;
-  const int within = slot - (slot / per_unit) * per_unit;
-  const int rg = within / blocks, rblk = within - rg * blocks;
-  const int pset = u * a.row_groups + rg;
-  const int b = u / a.Hkv, g = u - b * a.Hkv;
-  const int t = threadIdx.x, r = rblk * MR + t / TPR, c0 = (t % TPR) * CPT;
-  const int row = rg * R + r;                     // row within the KV head's G*T rows
+  // (row, 16-byte piece) items of the workgroup's rows, dealt to the threads
+  constexpr int ITEMS = (R * CPR + 64 * W - 1) / (64 * W);   // items per thread
   const int S = a.splits;
-  const size_t prow0 = (size_t)pset * S * R + r;  // this row in piece 0; piece s adds s * R
-
-  constexpr bool ent = ENT;
-  float M = -INFINITY, lsum = 0.f, esum = 0.f;
-  fv acc = {};
-  for (int s0 = 0; s0 < S; s0 += CH) {
-    float2 ml[CH];
-    fv x[CH];
-    float ev[CH];
+  const size_t pset = (size_t)u * a.row_groups + rg;
+  const size_t prow0 = pset * S * R;   // the set's piece 0, row 0
+  const int rows_valid = min(R, rows_total - rg * R);
+  // With several pieces, either merging workgroups appended to the launch merge the set (every piece stores
+  // its rows), or the set's last piece does (it is the last of the set to be dispatched, so every piece it
+  // waits for is already running or done; its own rows stay in LDS).  A single piece writes the output.  Rows
+  // of one KV head are consecutive in memory.
+  const bool merger = S > 1 && a.merge_parts == 0 && split == S - 1;
+  if (!merger) {
+    __bf16* dst = S == 1 ? (__bf16*)a.out + (qrow0 + (size_t)rg * R) * D : a.part_o + (prow0 + (size_t)split * R) * D;
 #pragma unroll
-    for (int k = 0; k < CH; ++k) {
-      const size_t pr = prow0 + (size_t)min(s0 + k, S - 1) * R;
-      ml[k] = *(const float2*)(a.part_ml + 2 * pr);
-      x[k] = *(const fv*)(a.part_acc + pr * D + c0);
-      ev[k] = ent ? a.part_e[pr] : 0.f;
+    for (int t = 0; t < ITEMS; ++t) {
+      const int item = t * 64 * W + tid;
+      const int r = item / CPR, ch = item % CPR;
+      if (item < R * CPR && r < rows_valid) *(u32x4*)(dst + (size_t)r * D + ch * 8) = *(const u32x4*)row_piece(r, ch);
     }
-    float Mn = M;
-#pragma unroll
-    for (int k = 0; k < CH; ++k)
-      if (s0 + k < S) Mn = fmaxf(Mn, ml[k].x);
-    const float scale_old = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - Mn);
-    esum = ent_term(scale_old, esum, M, Mn, lsum);
-    lsum *= scale_old;
-    acc *= scale_old;
-#pragma unroll
-    for (int k = 0; k < CH; ++k) {
-      const float w = (s0 + k >= S || ml[k].x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ml[k].x - Mn);
-      esum += ent_term(w, ev[k], ml[k].x, Mn, ml[k].y);
-      lsum += w * ml[k].y;
-      acc += w * x[k];
+    if (tid < rows_valid) {
+      const float2 ml = ml_lds[tid];
+      if (S == 1) {
+        const size_t orow = qrow0 + rg * R + tid;
+        if (a.lse) a.lse[orow] = ml.y > 0.f ? (ml.x + __log2f(ml.y)) * kLn2 : -INFINITY;
+        if (ENT) a.entropy[orow] = row_entropy(ml.y, e_lds[tid]);
+      } else {
+        const size_t pr = prow0 + (size_t)split * R + tid;
+        *(float2*)(a.part_ml + 2 * pr) = ml;
+        if (ENT) a.part_e[pr] = e_lds[tid];
+      }
     }
-    M = Mn;
+    if (S == 1) return;
+    // Count this piece's arrival once its stores have reached the L2.  The counter's low byte counts the
+    // arrivals and a 7-bit field per XCD counts where they ran: the merge reads the pieces' rows from its own
+    // XCD's L2, which is right only if they all ran there (workgroup n runs on XCD n % 8, and the pieces of a
+    // set and its merging workgroups share n % 8).
+    wait_vector_memory();
+    __syncthreads();
+    if (tid == 0)
+      __hip_atomic_fetch_add(a.set_ctr + pset * a.ctr_stride, 1ull + (1ull << (8 + 7 * xcd_id())), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    return;
   }
-  if (row >= a.G * a.T) return;
-  const size_t orow = ((size_t)b * a.Hq + (size_t)g * a.G) * a.T + row;
-  const float inv = lsum > 0.f ? 1.0f / lsum : 0.f;
-  __bf16 res[CPT];
-#pragma unroll
-  for (int e = 0; e < CPT; ++e) res[e] = (__bf16)(acc[e] * inv);
-  __builtin_memcpy((__bf16*)a.out + orow * D + c0, res, sizeof(res));
-  if (a.lse && c0 == 0) a.lse[orow] = lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
-  if (ent && c0 == 0) a.entropy[orow] = row_entropy(lsum, esum);
+
+  // ---- the set's last piece merges it: wait for the other S - 1 pieces, clear the counter for the next call
+  unsigned long long* ctr = a.set_ctr + pset * a.ctr_stride;
+  if (tid == 0) {
+    merge_lds = wait_for_pieces(a, ctr, S - 1);
+    __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  const size_t orow0 = qrow0 + (size_t)rg * R;
+  merge_pieces<D, W, ENT>(a, prow0, R, (__bf16*)a.out + orow0 * D, a.lse ? a.lse + orow0 : nullptr,
+                          ENT ? a.entropy + orow0 : nullptr, rows_valid, 0, R, split, row_lds, ml_lds, e_lds,
+                          merge_lds == 1);
 }
 
 template <int D, int RB, int KW, int W, int NST, bool ENT>
 hipError_t launch_streaming(const AttnArgs& a, hipStream_t stream) {
   constexpr size_t lds = (size_t)NST * Rows<D>::SLOT;
-  static_assert(lds + 2 * kMaxNodes * 8 + 4 * kMaxNodes * 4 + 64 <= 160 * 1024, "LDS budget");
+  static_assert(lds + 2 * kMaxNodes * 8 + 2 * kMaxNodes * 8 + 64 <= 160 * 1024, "LDS budget");
   // two sets of operand registers fit beside one 16-row block's state, not beside two
   auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST, RB == 1, ENT>;
   static bool configured = false;
@@ -853,23 +866,14 @@ hipError_t launch_streaming(const AttnArgs& a, hipStream_t stream) {
     configured = true;
   }
   if (a.rows_per_wg != 16 * RB * (W / KW)) return hipErrorInvalidValue;
+  if (a.splits > 1 && (!a.part_o || !a.part_ml || !a.set_ctr || (ENT && !a.part_e))) return hipErrorInvalidValue;
   const unsigned units_rounded = (a.units + 7) / 8 * 8;
   const unsigned grid = units_rounded * (unsigned)(a.splits * a.row_groups);
-  if (a.splits > 1 && a.merge_ctr) {
-    // the merging workgroups follow the streaming ones in the same launch
-    constexpr int MRW = W * merge_rows<D>();
-    const unsigned merge_wgs = (unsigned)(a.units * a.row_groups) * ((a.rows_per_wg + MRW - 1) / MRW);
-    AttnArgs b = a;
-    b.stream_wgs = (int)grid;
-    hipLaunchKernelGGL(kern, dim3(grid + merge_wgs), dim3(64 * W), lds, stream, b);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * W), lds, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.splits == 1) return e;
-  const unsigned mgrid = units_rounded * a.row_groups * (a.rows_per_wg / merge_rows<D>());
-  auto merge = tree_attn_merge_kernel<D, ENT>;
-  hipLaunchKernelGGL(merge, dim3(mgrid), dim3(64), 0, stream, a);
+  AttnArgs b = a;
+  b.stream_wgs = (int)grid;
+  const unsigned merge_wgs = a.splits > 1 && a.merge_parts > 0 ? units_rounded * a.row_groups * a.merge_parts : 0;
+  if (merge_wgs && (a.rows_per_wg % a.merge_parts != 0 || a.ctr_stride < 2)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(kern, dim3(grid + merge_wgs), dim3(64 * W), lds, stream, b);
   return hipGetLastError();
 }
 

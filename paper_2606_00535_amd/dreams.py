@@ -17,6 +17,7 @@ import torch
 LIBRARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdreams.so")
 
 DREAMS_OK, DREAMS_ERR_INVALID_ARG, DREAMS_ERR_UNSUPPORTED, DREAMS_ERR_WORKSPACE, DREAMS_ERR_HIP = 0, -1, -2, -3, -4
+DREAMS_ERR_DEVICE = -5
 DREAMS_F32, DREAMS_BF16 = 0, 1
 
 # every symbol include/dreams.h declares
@@ -27,6 +28,7 @@ EXPORTS = (
     "dreams_attn_entropy_select", "dreams_visual_importance_workspace_size", "dreams_visual_importance",
     "dreams_visual_topk", "dreams_visual_gather", "dreams_tree_accept_sampled_workspace_size",
     "dreams_tree_accept_sampled", "dreams_tree_accept_lm_head_workspace_size", "dreams_tree_accept_lm_head",
+    "dreams_workspace_status", "dreams_tree_verify_attn_splits",
 )
 
 
@@ -86,12 +88,14 @@ def lib():
                 L.dreams_tree_accept_lm_head_workspace_size.argtypes = [I32, I32, I32, I32, ctypes.POINTER(SZ)]
                 L.dreams_tree_accept_lm_head.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P]
                 L.dreams_visual_gather.argtypes = [I32, I32, I32, I32, ctypes.c_int, P, P, I32, P, I32, P, P, P]
+                L.dreams_workspace_status.argtypes = [P, P]
+                L.dreams_tree_verify_attn_splits.argtypes = [ctypes.POINTER(AttnDesc), ctypes.POINTER(I32)]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
                           "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy",
                           "dreams_attn_entropy_mean", "dreams_attn_entropy_select",
                           "dreams_visual_importance_workspace_size", "dreams_visual_importance", "dreams_visual_topk",
-                          "dreams_visual_gather"):
+                          "dreams_visual_gather", "dreams_workspace_status", "dreams_tree_verify_attn_splits"):
                     getattr(L, f).restype = ctypes.c_int
                 _lib = L
     return _lib
@@ -158,6 +162,26 @@ def tree_verify_attn_workspace_size(desc: AttnDesc) -> int:
     n = ctypes.c_size_t(0)
     _check(lib().dreams_tree_verify_attn_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
     return n.value
+
+
+def tree_verify_attn_splits(desc: AttnDesc) -> int:
+    """dreams_tree_verify_attn_splits: pieces of the key axis the library uses for `desc`."""
+    n = ctypes.c_int32(0)
+    _check(lib().dreams_tree_verify_attn_splits(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def workspace_status(workspace: torch.Tensor, stream=None) -> None:
+    """dreams_workspace_status: raises DreamsError (DREAMS_ERR_DEVICE) if a kernel flagged a failure in
+    `workspace` since the last check; clears the flags."""
+    _need(workspace, "workspace", torch.uint8, workspace.device)
+    _check(lib().dreams_workspace_status(_ptr(workspace), _stream(stream)))
+
+
+def cached_workspaces():
+    """The workspaces the binding created (one per device, stream and verb)."""
+    with _ws_lock:
+        return list(_ws.values())
 
 
 def tree_verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor,

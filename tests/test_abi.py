@@ -81,8 +81,15 @@ def test_attn_workspace_size_formula(D):
     assert st == 0
     rows = 32 * 1 * 8 * 64
     up = lambda x: (x + 255) // 256 * 256
-    assert n == 65536 + up(rows * 128 * 4) + up(rows * 2 * 4) + up(rows * 4)
+    # bf16 partial outputs, fp32 (max, sum) and entropy terms
+    assert n == 65536 + up(rows * 128 * 2) + up(rows * 2 * 4) + up(rows * 4)
     assert D.lib().dreams_last_error_message().decode() == ""
+    s = ctypes.c_int32(0)
+    assert D.lib().dreams_tree_verify_attn_splits(ctypes.byref(desc), ctypes.byref(s)) == 0 and s.value == 8
+    assert D.lib().dreams_tree_verify_attn_splits(ctypes.byref(_desc(D, num_splits=4000)), ctypes.byref(s)) == 0
+    assert s.value == 25
+    assert D.lib().dreams_tree_verify_attn_splits(ctypes.byref(_desc(D, num_splits=3, dtype=D.DREAMS_F32)),
+                                                  ctypes.byref(s)) == 0 and s.value == 1
     assert _ws(D, _desc(D, num_splits=1))[1] == 0
     assert _ws(D, _desc(D, dtype=D.DREAMS_F32, num_splits=4))[1] == 0
     # a request above one piece per 128 keys (3200 slots -> 25) or above 32 pieces is reduced
@@ -160,9 +167,16 @@ def test_check_tree_host(D):
 
 def test_status_strings(D):
     lib = D.lib()
-    for s in (0, -1, -2, -3, -4):
+    for s in (0, -1, -2, -3, -4, -5):
         assert lib.dreams_status_string(s).decode().startswith("DREAMS_")
     assert b"unknown" in lib.dreams_status_string(42)
+
+
+def test_workspace_status_rejects_bad_arguments(D):
+    lib = D.lib()
+    assert lib.dreams_workspace_status(None, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_workspace_status(ctypes.c_void_p(4096 + 16), None) == D.DREAMS_ERR_WORKSPACE
+    assert lib.dreams_last_error_message().decode() != ""
 
 
 def test_stream_read_rejects_bad_arguments(D):

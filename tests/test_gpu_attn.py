@@ -5,7 +5,11 @@ bound derived from the bf16 path's arithmetic.  The probabilities are rounded to
 product and the output is rounded to bf16 once (unit roundoff u = 2^-8: bf16 keeps 8 significant bits),
 everything else is fp32, so per element
     |out - ref| <= u * (sum_j p_j |v_j| / sum_j p_j + |ref|)     (+ fp32 noise),
-and the first term is exactly the oracle's output on |V|.  The tests allow 1.02x that plus 1e-6.
+and the first term is exactly the oracle's output on |V|.  With the key axis in several pieces, each piece's
+output (a weighted mean of its V rows, so at most its share of sum p|v| / sum p) is rounded to bf16 once more
+before the fp32 merge, which adds the first term once more:
+    |out - ref| <= u * (2 sum_j p_j |v_j| / sum_j p_j + |ref|).
+The tests allow 1.02x the bound that applies to the call plus 1e-6.
 """
 import numpy as np
 import pytest
@@ -19,8 +23,12 @@ from paper_2606_00535_amd import workload as W
 pytestmark = pytest.mark.gpu
 
 
-def bf16_bound(absref, ref):
-    return 1.02 * 2.0 ** -8 * (absref + np.abs(ref)) + 1e-6
+def bf16_bound(absref, ref, splits=1):
+    return 1.02 * 2.0 ** -8 * ((2 if splits > 1 else 1) * absref + np.abs(ref)) + 1e-6
+
+
+def splits_of(q, k, num_splits=0, max_kv_len=0):
+    return dreams.tree_verify_attn_splits(dreams.attn_desc(q, k, num_splits=num_splits, max_kv_len=max_kv_len))
 
 
 def oracle_layer(batch, li, abs_v=False, parent=None, mask=None):
@@ -30,17 +38,18 @@ def oracle_layer(batch, li, abs_v=False, parent=None, mask=None):
                             batch.wl.num_kv_heads, tree_mask=mask)
 
 
-def check_bf16(out, lse, batch, li, label, ref=None, absref=None, mask=None):
+def check_bf16(out, lse, batch, li, label, ref=None, absref=None, mask=None, splits=1):
     if ref is None:
         ref = oracle_layer(batch, li, mask=mask)
     if absref is None:
         absref = oracle_layer(batch, li, abs_v=True, mask=mask)[0]
     o_ref, l_ref = ref
     mx, _, o = attn_errors(out, o_ref)
-    bound = bf16_bound(absref, o_ref)
+    bound = bf16_bound(absref, o_ref, splits)
     worst = float(np.max(np.abs(o - o_ref) / bound))
     lerr = float(np.nanmax(np.abs(lse.cpu().numpy() - l_ref))) if lse is not None else 0.0
-    note("%s: max_abs=%.3e (contract %.0e) worst/bound=%.3f lse_err=%.2e" % (label, mx, ATTN_TOL_BF16, worst, lerr))
+    note("%s: splits=%d max_abs=%.3e (contract %.0e) worst/bound=%.3f lse_err=%.2e"
+         % (label, splits, mx, ATTN_TOL_BF16, worst, lerr))
     assert mx <= ATTN_TOL_BF16, label
     assert worst <= 1.0, label
     assert lerr <= LSE_TOL, label
@@ -125,11 +134,11 @@ def test_bf16_parity(dev, case, variant):
     note("bf16 %s %s" % (variant, case))
     out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=splits)
     torch.cuda.synchronize()
-    check_bf16(out, lse, batch, 0, "bf16 %s %s" % (variant, case))
+    check_bf16(out, lse, batch, 0, "bf16 %s %s" % (variant, case), splits=splits_of(q, k, splits))
 
 
-# More streaming workgroups than the 256 compute units with several pieces each: the pieces are merged by
-# workgroups of the same launch (every row configuration that reaches that path at these sizes).
+# More workgroups than the 256 compute units, several pieces per row set: the last piece of each set to arrive
+# merges it while other sets still stream (every row configuration, D = 64 and 128).
 FUSED_CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits): grid = 8*ceil(2*Hkv/8) * splits * row_groups
     (128, 64, 64, 16, 4, 3, 400, 4),   # 16-row workgroups (4 waves): 512 workgroups
     (64, 48, 48, 60, 6, 4, 700, 3),    # 64 rows, head_dim 64: 288
@@ -139,14 +148,14 @@ FUSED_CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits): grid = 8*ceil(2*Hk
 
 
 @pytest.mark.parametrize("case", FUSED_CASES, ids=lambda c: "D%d_Hq%d_Hkv%d_T%d_L%d_S%d" % (c[0], c[1], c[2], c[3], c[6], c[7]))
-def test_merge_in_launch(dev, case):
+def test_many_workgroups(dev, case):
     D, Hq, Hkv, T, depth, br, L, splits = case
     wl = small_wl(head_dim=D, num_q_heads=Hq, num_kv_heads=Hkv, num_nodes=T, depth=depth, max_branch=br, kv_len=L)
     batch = W.make_batch(wl, with_logits=False, kv_lens=[L, max(0, L - 37)])
     q, k, v, kv, par = layer_tensors(batch, 0, dev)
     desc = dreams.attn_desc(q, k, num_splits=splits)
     ws = torch.zeros(dreams.tree_verify_attn_workspace_size(desc), dtype=torch.uint8, device=dev)
-    note("merge in launch %s" % (case,))
+    note("many workgroups %s" % (case,))
     ref = oracle_layer(batch, 0)
     absref = oracle_layer(batch, 0, abs_v=True)[0]
     first = None
@@ -155,11 +164,12 @@ def test_merge_in_launch(dev, case):
         torch.cuda.synchronize()
         cur = out.view(torch.int16).cpu().numpy()
         if first is None:
-            check_bf16(out, lse, batch, 0, "merge in launch %s" % (case,), ref, absref)
+            check_bf16(out, lse, batch, 0, "many workgroups %s" % (case,), ref, absref, splits=splits)
             first = cur
         else:
             assert np.array_equal(cur, first), rep   # same result on every call
     assert not ws[:65536].cpu().numpy().any()       # counters left zero
+    dreams.workspace_status(ws)                      # no failure flagged
 
 
 @pytest.mark.parametrize("scale", [-0.07, 0.0, 0.31])
@@ -170,12 +180,13 @@ def test_scale_sign_and_zero(dev, scale):
     q, k, v, kv, par = layer_tensors(batch, 0, dev)
     note("scale %g" % scale)
     out, lse = dreams.tree_verify_attn(q, k, v, kv, par, scale=scale, num_splits=2)
+    splits = splits_of(q, k, 2)
     torch.cuda.synchronize()
     v32 = f32(batch.v_cache[0])
     args = (f32(batch.q[0]), f32(batch.k_cache[0]))
     ref = oracle.tree_attn(*args, v32, batch.kv_len, batch.parent, scale, wl.num_kv_heads)
     absref = oracle.tree_attn(*args, np.abs(v32), batch.kv_len, batch.parent, scale, wl.num_kv_heads)[0]
-    check_bf16(out, lse, batch, 0, "scale %g" % scale, ref, absref)
+    check_bf16(out, lse, batch, 0, "scale %g" % scale, ref, absref, splits=splits)
 
 
 def test_split_sweep_agrees(dev):
@@ -189,9 +200,9 @@ def test_split_sweep_agrees(dev):
         note("split sweep S=%d" % s)
         out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=s)
         torch.cuda.synchronize()
-        outs.append(check_bf16(out, lse, batch, 0, "split %d" % s, ref, absref))
+        outs.append(check_bf16(out, lse, batch, 0, "split %d" % s, ref, absref, splits=splits_of(q, k, s)))
     for o in outs[1:]:
-        assert np.max(np.abs(o - outs[0])) <= 2 * 2.0 ** -8 * (np.abs(outs[0]).max() + 1)
+        assert np.max(np.abs(o - outs[0])) <= 3 * 2.0 ** -8 * (np.abs(outs[0]).max() + 1)
 
 
 def test_repeat_is_bitwise_identical(dev):
@@ -221,6 +232,7 @@ def test_workspace_left_zero(dev):
     torch.cuda.synchronize()
     cnt = ws[:65536].cpu().numpy()          # the arrival counters open every workspace
     assert not cnt.any()
+    dreams.workspace_status(ws)
 
 
 def test_nonancestor_perturbation_bitwise(dev):
@@ -326,12 +338,13 @@ def test_llava7b_layer_full_parity(dev):
     note("llava7b_layer: B=1 Hq=32 D=128 L=3136 T=60 (auto splits)")
     out, lse = dreams.tree_verify_attn(q, k, v, kv, par)
     torch.cuda.synchronize()
-    check_bf16(out, lse, batch, 0, "llava7b_layer")
+    splits = splits_of(q, k)
+    check_bf16(out, lse, batch, 0, "llava7b_layer", splits=splits)
     bdom = W.make_tree_dominant(batch)
     q, k, v, kv, par = layer_tensors(bdom, 0, dev)
     out, lse = dreams.tree_verify_attn(q, k, v, kv, par)
     torch.cuda.synchronize()
-    check_bf16(out, lse, bdom, 0, "llava7b_layer tree_dominant")
+    check_bf16(out, lse, bdom, 0, "llava7b_layer tree_dominant", splits=splits)
 
 
 def sampled_rows(rng, B, Hq, T, n):
@@ -359,7 +372,7 @@ def test_full_size_sampled_rows(dev, name, layers):
         o = out.float().cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]].astype(np.float64)
         l = lse.cpu().numpy()[rows[:, 0], rows[:, 1], rows[:, 2]]
         mx = float(np.abs(o - ref).max())
-        worst = float(np.max(np.abs(o - ref) / bf16_bound(absref, ref)))
+        worst = float(np.max(np.abs(o - ref) / bf16_bound(absref, ref, splits_of(q, k, 0, wl.max_kv_len))))
         note("  max_abs=%.3e worst/bound=%.3f lse=%.2e" % (mx, worst, float(np.abs(l - lref).max())))
         assert mx <= ATTN_TOL_BF16 and worst <= 1.0 and float(np.abs(l - lref).max()) <= LSE_TOL
         # property at any size: every output row is a convex combination of V rows -> bounded by max |V|
