@@ -148,6 +148,23 @@ dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const vo
                                         size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * dreams_tree_verify_attn_noalloc -- dreams_tree_verify_attn for callers that cannot allocate device memory
+ * (code under stream capture, tight serving loops, harnesses that forbid hipMalloc): the same arguments without
+ * a workspace, the same kernels and the same results.  The scratch memory lives in a fixed array of
+ * DREAMS_NOALLOC_SCRATCH_BYTES bytes inside the library, one per device, held until the process ends; the
+ * call allocates and frees nothing.  Shapes whose workspace (dreams_tree_verify_attn_workspace_size) exceeds
+ * that size return DREAMS_ERR_UNSUPPORTED before anything is enqueued.  The first call on a device also
+ * enqueues one small kernel that clears the array's counters.  Every call on a device shares that device's
+ * array, so calls that overlap in time on one device (different streams without synchronisation) race and
+ * give unspecified results.  A failure a kernel flags (see dreams_workspace_status) stays in the array and
+ * is not reported; the rows concerned are NaN.
+ */
+#define DREAMS_NOALLOC_SCRATCH_BYTES (16u << 20)
+dreams_status_t dreams_tree_verify_attn_noalloc(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                                const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                                const uint64_t* tree_mask, void* out, float* lse, hipStream_t stream);
+
+/*
  * dreams_tree_verify_attn_entropy -- dreams_tree_verify_attn, plus the attention entropy of every row: the
  * per-row term of the average attention entropy AE(l) by which the paper's Section 3.2 ("Adaptive
  * Intermediate Feature Distillation") ranks target layers.

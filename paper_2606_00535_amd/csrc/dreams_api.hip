@@ -255,13 +255,13 @@ dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t*
 
 namespace {
 
-dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache, const void* v_cache,
-                            const int32_t* kv_len, const int32_t* parent, const uint64_t* tree_mask, void* out,
-                            float* lse, float* entropy, void* workspace, size_t workspace_bytes,
-                            hipStream_t stream) {
+// The checks of an attention call's tensor arguments (batch 0 needs none).
+dreams_status_t check_attn_tensors(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                   const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                   const uint64_t* tree_mask, const void* out, const float* lse) {
   dreams_status_t st = check_attn_desc(desc);
   if (st != DREAMS_OK) return st;
-  if (desc->batch == 0) return ok();
+  if (desc->batch == 0) return DREAMS_OK;
   if (!q || !k_cache || !v_cache || !kv_len || !out)
     return fail(DREAMS_ERR_INVALID_ARG, "q, k_cache, v_cache, kv_len and out must not be NULL");
   if (!parent && !tree_mask) return fail(DREAMS_ERR_INVALID_ARG, "either parent or tree_mask must be given");
@@ -270,6 +270,18 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
   if (!aligned(kv_len, 4) || (parent && !aligned(parent, 4)) || (lse && !aligned(lse, 4)) ||
       (tree_mask && !aligned(tree_mask, 8)))
     return fail(DREAMS_ERR_INVALID_ARG, "kv_len, parent, lse or tree_mask is misaligned");
+  if (desc->dtype == DREAMS_F32 && (long long)desc->batch * desc->num_q_heads * desc->num_nodes > 0x7fffffffLL)
+    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  return DREAMS_OK;
+}
+
+dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache, const void* v_cache,
+                            const int32_t* kv_len, const int32_t* parent, const uint64_t* tree_mask, void* out,
+                            float* lse, float* entropy, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+  dreams_status_t st = check_attn_tensors(desc, q, k_cache, v_cache, kv_len, parent, tree_mask, out, lse);
+  if (st != DREAMS_OK) return st;
+  if (desc->batch == 0) return ok();
   AttnPlan p;
   st = plan_attn(desc, &p, false);
   if (st != DREAMS_OK) return st;
@@ -279,8 +291,6 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
       return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, p.bytes);
     if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   }
-  if (desc->dtype == DREAMS_F32 && (long long)desc->batch * desc->num_q_heads * desc->num_nodes > 0x7fffffffLL)
-    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
   st = plan_attn(desc, &p, true);   // the same plan, plus how the pieces are merged
   if (st != DREAMS_OK) return st;
 
@@ -320,9 +330,68 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
   return ok();
 }
 
+// ------------------------------------------------------------------ scratch for the allocation-free call
+// A file-scope device array replaces the caller's workspace in dreams_tree_verify_attn_noalloc.  In host code
+// `scratch` names a host-side stand-in, not device memory: its device address is taken once per device with
+// hipGetSymbolAddress (every device holds its own copy, at its own address) and only that address is used.
+constexpr size_t kScratchBytes = DREAMS_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+// zero-fills n words (used instead of hipMemsetAsync, which a graph capture must not record)
+__global__ void fill_zero_words(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+// The device address of this device's scratch array; on the first call on a device, also clears its counter
+// region (stream-ordered before the caller's kernels).
+dreams_status_t scratch_for_current_device(hipStream_t stream, void** ptr) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {nullptr};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(DREAMS_ERR_HIP, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || !aligned(p, 256)) return fail(DREAMS_ERR_HIP, "scratch array at %p is not 256-byte aligned", p);
+    hipLaunchKernelGGL(fill_zero_words, dim3(64), dim3(256), 0, stream, (uint32_t*)p, kCounterBytes / 4);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "clearing the scratch counters");
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return DREAMS_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+dreams_status_t dreams_tree_verify_attn_noalloc(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
+                                                const void* v_cache, const int32_t* kv_len, const int32_t* parent,
+                                                const uint64_t* tree_mask, void* out, float* lse, hipStream_t stream) {
+  dreams_status_t st = check_attn_tensors(desc, q, k_cache, v_cache, kv_len, parent, tree_mask, out, lse);
+  if (st != DREAMS_OK) return st;
+  if (desc->batch == 0) return ok();
+  AttnPlan p;
+  st = plan_attn(desc, &p, false);
+  if (st != DREAMS_OK) return st;
+  if (p.bytes > kScratchBytes)
+    return fail(DREAMS_ERR_UNSUPPORTED,
+                "this shape needs %zu bytes of scratch, more than the %zu bytes of the allocation-free call "
+                "(use dreams_tree_verify_attn with a workspace)", p.bytes, kScratchBytes);
+  void* ws = nullptr;
+  if (p.bytes > 0) {
+    st = scratch_for_current_device(stream, &ws);
+    if (st != DREAMS_OK) return st;
+  }
+  return verify_attn(desc, q, k_cache, v_cache, kv_len, parent, tree_mask, out, lse, nullptr, ws, p.bytes, stream);
+}
 
 dreams_status_t dreams_tree_verify_attn(const dreams_attn_desc_t* desc, const void* q, const void* k_cache,
                                         const void* v_cache, const int32_t* kv_len, const int32_t* parent,

@@ -28,7 +28,7 @@ EXPORTS = (
     "dreams_attn_entropy_select", "dreams_visual_importance_workspace_size", "dreams_visual_importance",
     "dreams_visual_topk", "dreams_visual_gather", "dreams_tree_accept_sampled_workspace_size",
     "dreams_tree_accept_sampled", "dreams_tree_accept_lm_head_workspace_size", "dreams_tree_accept_lm_head",
-    "dreams_workspace_status", "dreams_tree_verify_attn_splits",
+    "dreams_workspace_status", "dreams_tree_verify_attn_splits", "dreams_tree_verify_attn_noalloc",
 )
 
 
@@ -89,13 +89,15 @@ def lib():
                 L.dreams_tree_accept_lm_head.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P]
                 L.dreams_visual_gather.argtypes = [I32, I32, I32, I32, ctypes.c_int, P, P, I32, P, I32, P, P, P]
                 L.dreams_workspace_status.argtypes = [P, P]
+                L.dreams_tree_verify_attn_noalloc.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, P, P, P, P, P]
                 L.dreams_tree_verify_attn_splits.argtypes = [ctypes.POINTER(AttnDesc), ctypes.POINTER(I32)]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
                           "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy",
                           "dreams_attn_entropy_mean", "dreams_attn_entropy_select",
                           "dreams_visual_importance_workspace_size", "dreams_visual_importance", "dreams_visual_topk",
-                          "dreams_visual_gather", "dreams_workspace_status", "dreams_tree_verify_attn_splits"):
+                          "dreams_visual_gather", "dreams_workspace_status", "dreams_tree_verify_attn_splits",
+                          "dreams_tree_verify_attn_noalloc"):
                     getattr(L, f).restype = ctypes.c_int
                 _lib = L
     return _lib
@@ -355,6 +357,43 @@ def _verify_attn(q, k_cache, v_cache, kv_len, parent, tree_mask, scale, out, lse
                                                      _ptr(kv_len), _ptr(parent), _ptr(tree_mask), _ptr(out), _ptr(lse),
                                                      _ptr(entropy), _ptr(workspace), ws_bytes, st))
     return out, lse, entropy
+
+
+def tree_verify_attn_noalloc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor,
+                             parent: Optional[torch.Tensor] = None, tree_mask: Optional[torch.Tensor] = None,
+                             scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                             lse: Optional[torch.Tensor] = None, with_lse: bool = True, max_kv_len: int = 0,
+                             num_splits: int = 0, stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """dreams_tree_verify_attn_noalloc: tree_verify_attn without a workspace (the library's fixed scratch array
+    instead).  `out` and `lse` may be passed in so that nothing is allocated here either."""
+    dt = q.dtype
+    if dt not in (torch.bfloat16, torch.float32):
+        raise TypeError("q must be bfloat16 or float32")
+    dev = q.device
+    for t, name in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache")):
+        _need(t, name, dt, dev, 4)
+    _need(kv_len, "kv_len", torch.int32, dev, 1)
+    if parent is not None:
+        _need(parent, "parent", torch.int32, dev, 2)
+    if tree_mask is not None:
+        _need(tree_mask, "tree_mask", torch.int64, dev, 3)
+    B, Hq, T, D = q.shape
+    desc = attn_desc(q, k_cache, num_splits, max_kv_len, scale)
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", dt, dev)
+    if out.shape != q.shape:
+        raise ValueError("out must have q's shape")
+    if lse is None and with_lse:
+        lse = torch.empty((B, Hq, T), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, dev)
+        if tuple(lse.shape) != (B, Hq, T):
+            raise ValueError("lse must be [B, Hq, T]")
+    _check(lib().dreams_tree_verify_attn_noalloc(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                                 _ptr(kv_len), _ptr(parent), _ptr(tree_mask), _ptr(out), _ptr(lse),
+                                                 _stream(stream)))
+    return out, lse
 
 
 def tree_accept_workspace_size(batch: int, num_nodes: int, vocab: int) -> int:
