@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "tree-verify steps/sec + achieved HBM GB/s (% peak), LLaVA-1.6-7B shape, 1 GPU"
 HBM_PEAK_GBPS = 8000.0
+BF16_DENSE_PEAK_TFLOPS = 2500.0
 
 
 def parse():
@@ -44,6 +45,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true", help="skip the CPU baseline and the parity spot check")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the other workloads' sub-objects (full_pass, llava13b_layer, gqa_long, tiny)")
+    ap.add_argument("--repeats", type=int, default=30, help="event-timed repeats behind each p10/p50/p90")
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="for rocprofv3 --pmc runs: a plain device copy of known size, then attention launches; "
                          "prints what each launch should move and exits")
@@ -92,6 +96,181 @@ def measured_traffic(workload: str):
     if not rec or rec.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
     return rec.get("bytes_per_launch")
+
+
+def attn_flops_per_layer(wl, kv_len, parent) -> float:
+    """Algorithmic flops of one tree-attention launch: q.k and p.v over the visible keys of every row,
+    4 * D * Hq * sum_b sum_i (L_b + depth_i + 1)."""
+    total = 0
+    for b in range(wl.batch):
+        par = parent[b]
+        depth = np.zeros(len(par), dtype=np.int64)
+        for i in range(1, len(par)):
+            depth[i] = depth[par[i]] + 1
+        total += int((int(kv_len[b]) + depth + 1).sum())
+    return 4.0 * wl.head_dim * wl.num_q_heads * total
+
+
+def dist(xs):
+    """p10 / p50 / p90 / mean of a list of per-call times (us)."""
+    a = np.sort(np.asarray(xs, dtype=np.float64))
+    return {"p10": round(float(np.percentile(a, 10)), 3), "p50": round(float(np.percentile(a, 50)), 3),
+            "p90": round(float(np.percentile(a, 90)), 3), "mean": round(float(a.mean()), 3), "repeats": int(a.size)}
+
+
+def replay_times_us(torch, graph, calls_per_replay, repeats):
+    """Each of `repeats` replays of `graph` timed alone with HIP events on the capturing (current) stream; the
+    time per call in us, one value per replay."""
+    graph.replay()
+    torch.cuda.synchronize()
+    out = []
+    for _ in range(repeats):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1) * 1e3 / calls_per_replay)
+    return out
+
+
+def capture(torch, fn):
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    return g
+
+
+def gpu_clocks():
+    """The GPU's current clocks as rocm-smi reports them (read only; nothing is set), or None."""
+    import shutil
+    import subprocess
+    exe = shutil.which("rocm-smi") or ("/opt/rocm/bin/rocm-smi" if os.path.exists("/opt/rocm/bin/rocm-smi") else None)
+    if exe is None:
+        return None
+    try:
+        r = subprocess.run([exe, "--showclocks"], capture_output=True, text=True, timeout=30)
+    except (OSError, subprocess.SubprocessError):
+        return None
+    clocks = {}
+    for line in r.stdout.splitlines():
+        low = line.lower()
+        for key in ("sclk", "mclk", "fclk", "socclk"):
+            if key + " clock level" in low and "(" in line and ")" in line:
+                clocks.setdefault(key, line[line.rindex("(") + 1:line.rindex(")")].strip())
+    return clocks or None
+
+
+def make_sets(torch, dev, wl, rotate_bytes, with_logits=True, min_sets=2):
+    """Input sets of workload `wl` resident on the device: topology, lengths, logits and draft tokens from the
+    seeded generator; q/k/v drawn on the device with a seeded generator (same N(0,1) distributions).  Enough
+    distinct sets (at least min_sets) that `rotate_bytes` are touched before a set comes round again."""
+    from paper_2606_00535_amd import workload as W
+    NL, B, Hq, Hkv, T, D = wl.num_layers, wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.num_nodes, wl.head_dim
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    host = W.make_batch(wl, layers=[], with_logits=with_logits)
+    S = host.k_cache.shape[3]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.seed)
+
+    def draw(shape, std=1.0):
+        x = torch.randn(shape, generator=gen, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        return x.to(tdt)
+
+    per_set = NL * 2 * B * Hkv * S * D * (2 if tdt == torch.bfloat16 else 4) + (host.logits.nbytes if with_logits else 0)
+    R = max(min_sets, int(math.ceil(rotate_bytes / per_set)))
+    base = dict(q=draw((NL, B, Hq, T, D), wl.q_std), k=draw((NL, B, Hkv, S, D)), v=draw((NL, B, Hkv, S, D)),
+                kv=torch.from_numpy(host.kv_len).to(dev), par=torch.from_numpy(host.parent).to(dev))
+    if with_logits:
+        base["logits"] = torch.from_numpy(host.logits).to(dev)
+        base["tok"] = torch.from_numpy(host.tokens).to(dev)
+    sets = []
+    for r in range(R):
+        st = {key: (val if r == 0 else val.clone()) for key, val in base.items()}
+        st["out"] = torch.empty((NL, B, Hq, T, D), dtype=tdt, device=dev)
+        st["alen"] = torch.empty(B, dtype=torch.int32, device=dev)
+        st["path"] = torch.empty((B, T), dtype=torch.int32, device=dev)
+        st["next"] = torch.empty(B, dtype=torch.int32, device=dev)
+        st["kv_out"] = torch.empty(B, dtype=torch.int32, device=dev)
+        sets.append(st)
+    return host, sets, R, tdt
+
+
+def measure_workload(torch, dev, name, args):
+    """One other workload's verify step, graph-replayed over rotated input sets: the whole step (every layer's
+    attention, acceptance, commit where the workload has it), the attention call alone and acceptance alone,
+    each as p10/p50/p90 over `args.repeats` event-timed replays."""
+    from paper_2606_00535_amd import dreams
+    from paper_2606_00535_amd import workload as W
+    wl = W.WORKLOADS[name]
+    NL, B, Hq, T = wl.num_layers, wl.batch, wl.num_q_heads, wl.num_nodes
+    # (the fp32 case is latency-bound and a few MB: two sets, no cache rotation)
+    host, sets, R, tdt = make_sets(torch, dev, wl, args.rotate_bytes if wl.dtype == "bf16" else 0)
+    desc = dreams.attn_desc(sets[0]["q"][0], sets[0]["k"][0], 0, wl.max_kv_len)
+    ws_attn = torch.zeros(max(1, dreams.tree_verify_attn_workspace_size(desc)), dtype=torch.uint8, device=dev)
+    ws_acc = torch.zeros(max(1, dreams.tree_accept_workspace_size(B, T, wl.vocab)), dtype=torch.uint8, device=dev)
+
+    def attention(st):
+        for l in range(NL):
+            dreams.tree_verify_attn(st["q"][l], st["k"][l], st["v"][l], st["kv"], st["par"], out=st["out"][l],
+                                    with_lse=False, max_kv_len=wl.max_kv_len, workspace=ws_attn)
+
+    def accept(st):
+        dreams.tree_accept(st["logits"], st["tok"], st["par"], outputs=(st["alen"], st["path"], st["next"], None),
+                           workspace=ws_acc)
+
+    def commit(st):
+        dreams.kv_commit(st["k"], st["v"], st["kv"], st["path"], st["alen"], kv_len_out=st["kv_out"])
+
+    def step(st):
+        attention(st)
+        accept(st)
+        if wl.commit:
+            commit(st)
+
+    for r in range(R):
+        step(sets[r])
+    torch.cuda.synchronize()
+    reps = max(1, args.repeats)
+    step_us = replay_times_us(torch, capture(torch, lambda: [step(st) for st in sets]), R, reps)
+    attn_us = replay_times_us(torch, capture(torch, lambda: [attention(st) for st in sets]), R * NL, reps)
+    acc_us = replay_times_us(torch, capture(torch, lambda: [accept(st) for st in sets]), R, reps)
+    a_bytes = attn_bytes_per_layer(wl, host.kv_len)
+    a_flops = attn_flops_per_layer(wl, host.kv_len, host.parent)
+    acc_b = accept_bytes(wl)
+    ok = True
+    if ws_attn.numel() >= 65536:
+        try:
+            dreams.workspace_status(ws_attn)
+        except dreams.DreamsError:
+            ok = False
+    res = {"workload": name, "layers": NL, "batch": B, "q_heads": Hq, "kv_heads": wl.num_kv_heads,
+           "head_dim": wl.head_dim, "dtype": wl.dtype, "kv_len": [int(x) for x in host.kv_len],
+           "tree_nodes": T, "vocab": wl.vocab, "rotated_input_sets": R,
+           "splits": dreams.tree_verify_attn_splits(desc),
+           "step_us": dist(step_us), "steps_per_s": round(1e6 / np.median(step_us), 2),
+           "attention": {"us_per_launch": dist(attn_us), "bytes_per_launch": a_bytes, "flops_per_launch": a_flops}}
+    a50 = np.median(attn_us)
+    res["attention"]["GBps"] = round(a_bytes / (a50 * 1e-6) / 1e9, 1)
+    res["attention"]["frac_of_hbm_peak"] = round(a_bytes / (a50 * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    res["attention"]["TFLOPs"] = round(a_flops / (a50 * 1e-6) / 1e12, 1)
+    res["attention"]["frac_of_bf16_dense_peak"] = round(a_flops / (a50 * 1e-6) / 1e12 / BF16_DENSE_PEAK_TFLOPS, 4)
+    res["accept"] = {"us_per_launch": dist(acc_us), "bytes_per_launch": acc_b,
+                     "GBps": round(acc_b / (np.median(acc_us) * 1e-6) / 1e9, 1)}
+    step_bytes = NL * a_bytes + acc_b
+    if wl.commit:
+        com_b = commit_bytes(wl, sets[0]["path"].cpu().numpy(), sets[0]["alen"].cpu().numpy())
+        res["commit_bytes"] = com_b
+        step_bytes += com_b
+    res["step_algorithmic_bytes"] = step_bytes
+    res["step_GBps"] = round(step_bytes / (np.median(step_us) * 1e-6) / 1e9, 1)
+    res["step_frac_of_hbm_peak"] = round(step_bytes / (np.median(step_us) * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    res["workspace_flags_clear"] = ok
+    del sets, ws_attn, ws_acc
+    torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -198,6 +377,8 @@ def main():
     ms = e0.elapsed_time(e1)
     ms_per_step = ms / K
     steps_per_s = 1e3 / ms_per_step
+    # the same step, as a distribution: each of args.repeats replays of the R-step graph timed alone
+    step_dist = dist(replay_times_us(torch, g_full, R, max(1, args.repeats)))
 
     # ---- attention kernel alone: a graph of attention launches over the rotated sets, HIP events around it
     n_att = max(R, args.attn_launches // (R * NL) * R)
@@ -215,6 +396,7 @@ def main():
     a1.record()
     torch.cuda.synchronize()
     attn_us = a0.elapsed_time(a1) * 1e3 / (reps * R * NL)
+    attn_dist = dist(replay_times_us(torch, g_att, R * NL, max(1, args.repeats)))
 
     # accept alone, same method
     g_acc = torch.cuda.CUDAGraph()
@@ -381,6 +563,20 @@ def main():
         vis["gather_GBps"] = round(gat_bytes / (vis["gather_us"] * 1e-6) / 1e9, 1)
 
     stream = stream_peak(torch, dev)
+    try:
+        dreams.workspace_status(ws_attn) if ws_attn.numel() >= 65536 else None
+        flags_clear = True
+    except dreams.DreamsError:
+        flags_clear = False
+
+    # the other workloads, each its own sub-object (the 32-layer step with commit, the 13B layer, the
+    # matrix-core-bound GQA shape, the tiny fp32 case); the main workload's sets stay resident meanwhile
+    extras = {}
+    if not (args.no_extras or args.profile_only):
+        for key, name in (("full_pass", "llava7b_full"), ("llava13b_layer", "llava13b_layer"),
+                          ("gqa_long", "gqa_long"), ("tiny", "tiny")):
+            if name != args.workload:
+                extras[key] = measure_workload(torch, dev, name, args)
 
     kv_len = host.kv_len
     a_bytes = attn_bytes_per_layer(wl, kv_len)
@@ -414,8 +610,10 @@ def main():
         "step_algorithmic_bytes": step_bytes,
         "step_GBps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "wall_ms_timed_region": round(wall_ms, 3),
-        "attention": {"us_per_launch": round(attn_us, 3), "bytes_per_launch": a_bytes,
-                      "GBps": round(attn_gbps, 1), "splits": "auto" if splits_used == 0 else splits_used},
+        "step_us": step_dist,
+        "attention": {"us_per_launch": round(attn_us, 3), "us_dist": attn_dist, "bytes_per_launch": a_bytes,
+                      "GBps": round(attn_gbps, 1), "splits": dreams.tree_verify_attn_splits(desc),
+                      "workspace_flags_clear": flags_clear},
         "accept": {"us_per_launch": round(acc_us, 3), "bytes_per_launch": acc_b,
                    "GBps": round(acc_b / (acc_us * 1e-6) / 1e9, 1)},
         "accept_sampled": {"us_per_launch": round(smp_us, 3), "bytes_per_launch": smp_bytes,
@@ -433,7 +631,9 @@ def main():
                      "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic)},
         "stream_peak": dict(stream, attention_frac_of_read=round(attn_gbps / stream["read_GBps"], 4)),
+        "gpu_clocks": gpu_clocks(),
     }
+    result.update(extras)
 
     if not (args.no_cpu_baseline or args.profile_only):
         result["cpu_baseline"], result["parity_spot_check"] = cpu_baseline(wl, sets[0], host, args.cpu_seconds)
@@ -527,6 +727,26 @@ def cpu_baseline(wl, st, host, seconds):
     base = {"value": round(1.0 / step_s, 4), "unit": "verify-steps/s", "cores": oracle.num_threads(),
             "kind": "oracle", "sample": sample, "seconds": round(time.perf_counter() - t0, 2),
             "affinity_cores": len(os.sched_getaffinity(0))}
+    # the same oracle on one thread: a shorter sample of the same step (a quarter of the time budget)
+    threads = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        reps1, t1, a1 = 0, time.perf_counter(), 0.0
+        while True:
+            a = time.perf_counter()
+            for i in range(len(layers)):
+                oracle.tree_attn(q[i], k[i], v[i], host.kv_len, host.parent, scale, wl.num_kv_heads, with_lse=False)
+            b = time.perf_counter()
+            oracle.tree_accept(host.logits, host.tokens, host.parent)
+            c = time.perf_counter()
+            a1 += (b - a) / len(layers) * NL + (c - b)
+            reps1 += 1
+            if time.perf_counter() - t1 >= seconds / 4:
+                break
+    finally:
+        oracle.set_num_threads(threads)
+    base["one_thread"] = {"value": round(reps1 / a1, 4), "unit": "verify-steps/s", "cores": 1,
+                          "sample": "%d repetitions of the same step" % reps1}
     path_ok = bool(np.array_equal(st["path"].cpu().numpy(), acc[1]) and
                    np.array_equal(st["alen"].cpu().numpy(), acc[0]) and np.array_equal(st["next"].cpu().numpy(), acc[2]))
     check = {"accept_bit_exact": path_ok, "attention_tol": 2e-2}

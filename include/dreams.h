@@ -62,16 +62,30 @@ typedef enum { DREAMS_F32 = 0, DREAMS_BF16 = 1 } dreams_dtype_t;
 
 /*
  * dreams_workspace_status -- the failures kernels flagged in `workspace` (device, 256-byte aligned, a workspace
- * of any verb) since the last check.  Synchronises `stream`, reads the flags, clears them, and returns DREAMS_OK
- * if none was set, else DREAMS_ERR_DEVICE with a message naming each flag.  The flags:
+ * of any verb, workspace_bytes >= DREAMS_WORKSPACE_COUNTER_BYTES, else DREAMS_ERR_WORKSPACE) since the last
+ * check.  Synchronises `stream`, reads the flags, clears them, and returns DREAMS_OK if none was set, else
+ * DREAMS_ERR_DEVICE with a message naming each flag.  The flags:
  *   attention (more than one piece per row set): the pieces of one set did not all run on one XCD, so the
  *       merge could not read their partial results from its XCD's L2 -- the rows of that set are NaN.  Not
  *       expected on an MI355X (workgroup n runs on XCD n % 8).
- *   sampled acceptance: a wait for another workgroup's result gave up (after 0.2 s); that call's integer
- *       results are unspecified.
- * Not for use under stream capture (it copies to the host and synchronises).
+ *   a wait for another workgroup's results gave up (dreams_set_wait_limit; attention merges, sampled
+ *       acceptance): that call's results are unspecified (attention rows NaN).
+ * After a flagged failure, zero the workspace's counter region before it serves another call: arrivals that
+ * came after a wait gave up can remain there.  Not for use under stream capture (it copies to the host and
+ * synchronises).
  */
-dreams_status_t dreams_workspace_status(void* workspace, hipStream_t stream);
+dreams_status_t dreams_workspace_status(void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * dreams_set_wait_limit -- the bound, in seconds (0 .. 60, default 0.2), on every wait of one workgroup for
+ * another's results inside the library's kernels: the merging workgroups of dreams_tree_verify_attn (several
+ * pieces per row set) and the pieces of dreams_tree_accept_sampled.  Those waits always end in normal operation
+ * (a workgroup only waits for ones dispatched before it); a wait that reaches the bound gives up, its call's
+ * results are unspecified, and the workspace's failure flag is set (dreams_workspace_status).  A limit of 0
+ * makes every such wait give up at once, which exercises that path.  Applies to calls enqueued after it;
+ * process-wide.
+ */
+dreams_status_t dreams_set_wait_limit(double seconds);
 
 /*
  * Shape of one tree-verification attention call.

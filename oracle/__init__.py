@@ -79,11 +79,16 @@ class Oracle:
             f.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
+        lib.oracle_set_num_threads.argtypes = [I]
+        lib.oracle_set_num_threads.restype = None
         self.lib = lib
         self.path = lib_path
 
     def num_threads(self) -> int:
         return int(self.lib.oracle_num_threads())
+
+    def set_num_threads(self, n: int) -> None:
+        self.lib.oracle_set_num_threads(int(n))
 
     def tree_attn(self, q, k_cache, v_cache, kv_len, parent, scale: float, num_kv_heads: int,
                   tree_mask=None, with_lse: bool = True):
@@ -233,6 +238,10 @@ def default() -> Oracle:
 
 def num_threads() -> int:
     return default().num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    default().set_num_threads(n)
 
 
 def tree_attn(*a, **kw):

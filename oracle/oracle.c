@@ -526,3 +526,6 @@ int oracle_kv_commit(int NL, int64_t layer_stride_elems, int B, int Hkv, int D, 
 
 /* Number of threads the parallel loops above use (reported beside CPU timings). */
 int oracle_num_threads(void) { return omp_get_max_threads(); }
+
+/* Threads of the parallel loops above (n >= 1); used to time the oracle on one core beside all of them. */
+void oracle_set_num_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }

@@ -6,6 +6,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <atomic>
 #include <mutex>
 #include <string>
 
@@ -17,6 +18,9 @@ using namespace dreams;
 namespace {
 
 thread_local std::string g_error;
+
+// Bound on every in-kernel wait for another workgroup (100 MHz real-time ticks); see dreams_set_wait_limit.
+std::atomic<uint64_t> g_wait_ticks{kDefaultWaitTicks};
 
 dreams_status_t fail(dreams_status_t st, const char* fmt, ...) {
   char buf[512];
@@ -311,6 +315,7 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
   a.set_ctr = p.bytes ? (unsigned long long*)ws : nullptr;
   a.ctr_stride = p.ctr_stride;
   a.merge_parts = p.merge_parts;
+  a.wait_ticks = g_wait_ticks.load(std::memory_order_relaxed);
   a.err = p.bytes ? (uint32_t*)ws + kErrorWord : nullptr;
   a.B = desc->batch;
   a.Hq = desc->num_q_heads;
@@ -593,6 +598,8 @@ dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int
   a.chunks = p.chunks;
   a.sub_pieces = p.sub_pieces;
   a.vec4 = (vocab % 4 == 0) && aligned(target_logits, 16) && aligned(draft_logits, 16);
+  a.err = ctr + kErrorWord;
+  a.wait_ticks = g_wait_ticks.load(std::memory_order_relaxed);
   hipError_t e = launch_tree_accept_sampled(a, stream);
   if (e != hipSuccess) return hip_fail(e, "sampled tree accept launch");
   return ok();
@@ -899,9 +906,12 @@ const char* dreams_status_string(dreams_status_t status) {
 
 const char* dreams_last_error_message(void) { return g_error.c_str(); }
 
-dreams_status_t dreams_workspace_status(void* workspace, hipStream_t stream) {
+dreams_status_t dreams_workspace_status(void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!workspace) return fail(DREAMS_ERR_INVALID_ARG, "workspace is NULL");
   if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < kCounterBytes)
+    return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, less than its %zu-byte counter region", workspace_bytes,
+                kCounterBytes);
   uint32_t* word = (uint32_t*)workspace + kErrorWord;
   uint32_t flags = 0;
   hipError_t e = hipMemcpyAsync(&flags, word, sizeof(flags), hipMemcpyDeviceToHost, stream);
@@ -913,9 +923,18 @@ dreams_status_t dreams_workspace_status(void* workspace, hipStream_t stream) {
   if (e != hipSuccess) return hip_fail(e, "clearing the workspace's failure flags");
   std::string what;
   if (flags & kErrXcdSplit) what += " [attention: pieces of one row set ran on different XCDs; outputs NaN]";
-  if (flags & kErrWaitTimeout) what += " [sampled acceptance: a bounded wait gave up; results unspecified]";
+  if (flags & kErrWaitTimeout)
+    what += " [a bounded wait for another workgroup gave up (attention merge or sampled acceptance); results "
+            "unspecified]";
   if (flags & ~(kErrXcdSplit | kErrWaitTimeout)) what += " [unknown flag]";
   return fail(DREAMS_ERR_DEVICE, "failure flags 0x%x:%s", flags, what.c_str());
+}
+
+dreams_status_t dreams_set_wait_limit(double seconds) {
+  if (!(seconds >= 0.0) || seconds > 60.0)
+    return fail(DREAMS_ERR_INVALID_ARG, "wait limit %g s is outside [0, 60]", seconds);
+  g_wait_ticks.store((uint64_t)(seconds * 1e8), std::memory_order_relaxed);
+  return ok();
 }
 
 dreams_status_t dreams_tree_verify_attn_splits(const dreams_attn_desc_t* desc, int32_t* splits) {

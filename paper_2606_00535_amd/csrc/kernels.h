@@ -52,6 +52,9 @@ constexpr int kCounterWords = (65536 - 128) / 4;    // words of the counter regi
 constexpr int kErrorWord = (65536 - 128) / 4;       // word index of the failure flags
 constexpr uint32_t kErrXcdSplit = 1u;       // attention: pieces of one row set ran on different XCDs
 constexpr uint32_t kErrWaitTimeout = 2u;    // a bounded wait for other workgroups gave up
+// Default bound on every wait of one workgroup for another's results: 0.2 s of the 100 MHz real-time clock,
+// far beyond any call (dreams_set_wait_limit changes it).
+constexpr uint64_t kDefaultWaitTicks = 20000000;
 __device__ __forceinline__ void raise_device_error(uint32_t* err, uint32_t bit) {
   if (err) __hip_atomic_fetch_or(err, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -88,6 +91,7 @@ struct AttnArgs {
   int merge_parts;
   int stream_wgs;         // set by the launcher
   uint32_t* err;          // the workspace's failure flags (splits > 1)
+  uint64_t wait_ticks;    // bound on a merging workgroup's wait (100 MHz real-time ticks)
   int B, Hq, Hkv, G, T, D, S_cap;
   int units;              // B * Hkv
   int rows_per_wg;        // query rows of one workgroup (64 or 128)
@@ -194,6 +198,8 @@ struct SampledArgs {
   int B, T, V, chunks;
   int sub_pieces;              // 1 or kSampledSubLarge
   int vec4;                    // both logits tensors 16-byte aligned and V % 4 == 0
+  uint32_t* err;               // the workspace's failure flags
+  uint64_t wait_ticks;         // bound on every wait for another workgroup (100 MHz real-time ticks)
 };
 
 hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream);

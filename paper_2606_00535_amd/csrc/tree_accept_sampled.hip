@@ -33,7 +33,9 @@
 //
 // Forward progress.  A workgroup only waits for rows whose pieces all have smaller blockIdx (stats pieces come
 // first, pass pieces are ordered by child index), and workgroups are dispatched in blockIdx order, so every
-// wait ends; waits are nevertheless bounded (0.2 s), after which the results are unspecified.
+// wait ends; waits are nevertheless bounded (0.2 s by default), after which the results are unspecified and the
+// workspace's failure flag is set.  Nothing a wait that gave up leaves behind is used as a memory index (piece and
+// token positions are clamped, node indices come from the tree), and every arrival word still returns to zero.
 //
 // Results cross workgroups through device-scope stores and loads, published before a relaxed device-scope
 // atomic on an arrival word (see kernels.h).  The walker of each sequence clears that sequence's arrival words,
@@ -47,7 +49,6 @@ namespace dreams {
 namespace {
 
 constexpr int NT = kSampledThreads, NW = NT / 64;
-constexpr uint64_t kWaitTicks = 20000000;          // 100 MHz real-time ticks: 0.2 s
 constexpr uint64_t kMassMask = (1ull << 53) - 1;   // accumulator: fixed-point mass in the low 53 bits,
 constexpr int kArrivalShift = 53;                  // arrivals above
 constexpr double kFixScale = 2251799813685248.0;   // 2^51 units per unit of mass
@@ -101,6 +102,7 @@ struct Shared {
   int st_slot;
   int fin_piece;
   double fin_before, fin_thr;
+  int gave_up;                     // a wait of this workgroup reached its bound
 };
 
 // Block reductions: every lane reduces its wave by a butterfly, lane 0's value is kept, waves are combined in
@@ -444,6 +446,7 @@ __device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh
   const int T = a.T;
   const size_t rb = (size_t)b * T;
   if (tid < T) sh.par[tid] = a.parent[rb + tid];
+  if (tid == 0) sh.gave_up = 0;
   __syncthreads();
   const int n = sh.par[c];
   const bool valid = n >= 0 && n < c;
@@ -485,7 +488,11 @@ __device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh
         const uint32_t* w = stats_word(a, b, n);
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
         while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)a.chunks) {
-          if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) break;
+          if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
+            raise_device_error(a.err, kErrWaitTimeout);
+            sh.gave_up = 1;
+            break;
+          }
           __builtin_amdgcn_s_sleep(2);
         }
       }
@@ -515,7 +522,13 @@ __device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh
         if (w1) v1 = load_u64(w1);
         const bool done = (!w0 || (v0 & ~kMassMask) == full) && (!w1 || (v1 & ~kMassMask) == full);
         if (__ballot(!done) == 0) break;
-        if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) break;
+        if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
+          if (lane == 0) {
+            raise_device_error(a.err, kErrWaitTimeout);
+            sh.gave_up = 1;
+          }
+          break;
+        }
         __builtin_amdgcn_s_sleep(2);
       }
       if (w0) sh.zs[lane] = (double)(v0 & kMassMask) * kFixUnit;
@@ -598,7 +611,10 @@ __device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh
   wait_vector_memory();
   __syncthreads();
   if (tid == 0) {
-    const uint64_t mine = (uint64_t)rint(z * kFixScale);
+    // A piece's mass is at most 1 (up to rounding); after a wait gave up it is meaningless and counts as 0, so
+    // that it can never carry into the arrival bits: the count, and with it the walk, still completes.
+    const double zc = sh.gave_up ? 0.0 : fmin(fmax(z, 0.0), 2.0);
+    const uint64_t mine = (uint64_t)rint(zc * kFixScale);
     const uint64_t old = __hip_atomic_fetch_add(acc_word(a, b, c), (1ull << kArrivalShift) + mine, __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
     sh.flag = (int)(old >> kArrivalShift) == a.chunks - 1;

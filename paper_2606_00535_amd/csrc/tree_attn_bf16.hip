@@ -50,9 +50,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kStep = 32;          // keys per step
-// Bound on the merging workgroup's wait for its set's other pieces (100 MHz real-time ticks): 0.2 s, far
-// beyond any call.
-constexpr uint64_t kMergeWaitTicks = 20000000;
 constexpr float kLazyLog2 = 8.0f;  // slack of the running maximum, log2 units
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -226,14 +223,14 @@ __device__ __forceinline__ void merge_pieces(const AttnArgs& a, size_t prow0, in
   }
 }
 
-// Wait (one thread) until a set's arrival counter shows `expect` pieces, bounded by kMergeWaitTicks.  Returns 1
+// Wait (one thread) until a set's arrival counter shows `expect` pieces, bounded by a.wait_ticks.  Returns 1
 // if they arrived and all ran on the caller's XCD, else 2 (and flags the workspace).
 __device__ __forceinline__ uint32_t wait_for_pieces(const AttnArgs& a, unsigned long long* ctr, int expect) {
   const uint32_t x = xcd_id();
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
   unsigned long long c;
   while (((c = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffull) < (unsigned long long)expect) {
-    if (__builtin_amdgcn_s_memrealtime() - t0 > kMergeWaitTicks) break;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) break;
     __builtin_amdgcn_s_sleep(1);
   }
   if ((c & 0xffull) != (unsigned long long)expect) {

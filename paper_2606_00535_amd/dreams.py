@@ -29,6 +29,7 @@ EXPORTS = (
     "dreams_visual_topk", "dreams_visual_gather", "dreams_tree_accept_sampled_workspace_size",
     "dreams_tree_accept_sampled", "dreams_tree_accept_lm_head_workspace_size", "dreams_tree_accept_lm_head",
     "dreams_workspace_status", "dreams_tree_verify_attn_splits", "dreams_tree_verify_attn_noalloc",
+    "dreams_set_wait_limit",
 )
 
 
@@ -88,7 +89,8 @@ def lib():
                 L.dreams_tree_accept_lm_head_workspace_size.argtypes = [I32, I32, I32, I32, ctypes.POINTER(SZ)]
                 L.dreams_tree_accept_lm_head.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P]
                 L.dreams_visual_gather.argtypes = [I32, I32, I32, I32, ctypes.c_int, P, P, I32, P, I32, P, P, P]
-                L.dreams_workspace_status.argtypes = [P, P]
+                L.dreams_workspace_status.argtypes = [P, SZ, P]
+                L.dreams_set_wait_limit.argtypes = [ctypes.c_double]
                 L.dreams_tree_verify_attn_noalloc.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, P, P, P, P, P]
                 L.dreams_tree_verify_attn_splits.argtypes = [ctypes.POINTER(AttnDesc), ctypes.POINTER(I32)]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
@@ -97,7 +99,7 @@ def lib():
                           "dreams_attn_entropy_mean", "dreams_attn_entropy_select",
                           "dreams_visual_importance_workspace_size", "dreams_visual_importance", "dreams_visual_topk",
                           "dreams_visual_gather", "dreams_workspace_status", "dreams_tree_verify_attn_splits",
-                          "dreams_tree_verify_attn_noalloc"):
+                          "dreams_tree_verify_attn_noalloc", "dreams_set_wait_limit"):
                     getattr(L, f).restype = ctypes.c_int
                 _lib = L
     return _lib
@@ -177,7 +179,12 @@ def workspace_status(workspace: torch.Tensor, stream=None) -> None:
     """dreams_workspace_status: raises DreamsError (DREAMS_ERR_DEVICE) if a kernel flagged a failure in
     `workspace` since the last check; clears the flags."""
     _need(workspace, "workspace", torch.uint8, workspace.device)
-    _check(lib().dreams_workspace_status(_ptr(workspace), _stream(stream)))
+    _check(lib().dreams_workspace_status(_ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def set_wait_limit(seconds: float) -> None:
+    """dreams_set_wait_limit: bound on every in-kernel wait for another workgroup (default 0.2 s)."""
+    _check(lib().dreams_set_wait_limit(float(seconds)))
 
 
 def cached_workspaces():

@@ -172,10 +172,18 @@ def test_status_strings(D):
     assert b"unknown" in lib.dreams_status_string(42)
 
 
+def test_wait_limit_range(D):
+    lib = D.lib()
+    for bad in (-1.0, 61.0, float("nan")):
+        assert lib.dreams_set_wait_limit(bad) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_set_wait_limit(0.2) == 0
+
+
 def test_workspace_status_rejects_bad_arguments(D):
     lib = D.lib()
-    assert lib.dreams_workspace_status(None, None) == D.DREAMS_ERR_INVALID_ARG
-    assert lib.dreams_workspace_status(ctypes.c_void_p(4096 + 16), None) == D.DREAMS_ERR_WORKSPACE
+    assert lib.dreams_workspace_status(None, 65536, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_workspace_status(ctypes.c_void_p(4096 + 16), 65536, None) == D.DREAMS_ERR_WORKSPACE
+    assert lib.dreams_workspace_status(ctypes.c_void_p(4096), 65535, None) == D.DREAMS_ERR_WORKSPACE
     assert lib.dreams_last_error_message().decode() != ""
 
 
