@@ -58,7 +58,7 @@ def _check(rc: int, what: str):
 
 
 class Oracle:
-    """The oracle's four entry points over one built library."""
+    """The oracle's entry points over one built library."""
 
     def __init__(self, lib_path: str):
         lib = ctypes.CDLL(lib_path)
@@ -73,9 +73,11 @@ class Oracle:
         lib.oracle_visual_importance.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P, I, I, P]
         lib.oracle_visual_topk.argtypes = [I, I, I, P, P]
         lib.oracle_visual_gather.argtypes = [I, I, I, I, I, P, P, I, P, I, P, P]
+        lib.oracle_prefill_attn_stats.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, P, P]
+        lib.oracle_prefill_visual_importance.argtypes = [I, I, I, I, I, I, ctypes.c_double, P, P, P, I, I, P]
         for f in (lib.oracle_tree_attn, lib.oracle_tree_attn_rows, lib.oracle_tree_accept, lib.oracle_kv_commit,
                   lib.oracle_tree_attn_entropy, lib.oracle_visual_importance, lib.oracle_visual_topk,
-                  lib.oracle_visual_gather):
+                  lib.oracle_visual_gather, lib.oracle_prefill_attn_stats, lib.oracle_prefill_visual_importance):
             f.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
@@ -158,6 +160,36 @@ class Oracle:
                                                _p(_c(kv_len, np.int32)), _p(_c(parent, np.int32)),
                                                _p(_c(tree_mask, np.uint64)), int(vis_begin), int(vis_count), _p(imp))
         _check(rc, "oracle_visual_importance")
+        return imp
+
+    def prefill_attn_stats(self, q, k_cache, prompt_len, scale: float, num_kv_heads: int):
+        """Causal attention of a prompt's own rows (row i sees slots 0..i): (lse, entropy), each [B, Hq, N]
+        float64; rows at or past prompt_len[b] get -inf and 0."""
+        q = _c(q, np.float32)
+        k_cache = _c(k_cache, np.float32)
+        B, Hq, N, D = q.shape
+        S_cap = k_cache.shape[2]
+        assert k_cache.shape == (B, num_kv_heads, S_cap, D)
+        lse = np.empty((B, Hq, N), dtype=np.float64)
+        ent = np.empty((B, Hq, N), dtype=np.float64)
+        rc = self.lib.oracle_prefill_attn_stats(B, Hq, num_kv_heads, N, D, S_cap, float(scale), _p(q), _p(k_cache),
+                                                _p(_c(prompt_len, np.int32)), _p(lse), _p(ent))
+        _check(rc, "oracle_prefill_attn_stats")
+        return lse, ent
+
+    def prefill_visual_importance(self, q, k_cache, prompt_len, scale: float, num_kv_heads: int, vis_begin: int,
+                                  vis_count: int):
+        """Eq. 2 over a prompt's causal attention: [B, vis_count] float64."""
+        q = _c(q, np.float32)
+        k_cache = _c(k_cache, np.float32)
+        B, Hq, N, D = q.shape
+        S_cap = k_cache.shape[2]
+        assert k_cache.shape == (B, num_kv_heads, S_cap, D)
+        imp = np.empty((B, vis_count), dtype=np.float64)
+        rc = self.lib.oracle_prefill_visual_importance(B, Hq, num_kv_heads, N, D, S_cap, float(scale), _p(q),
+                                                       _p(k_cache), _p(_c(prompt_len, np.int32)), int(vis_begin),
+                                                       int(vis_count), _p(imp))
+        _check(rc, "oracle_prefill_visual_importance")
         return imp
 
     def visual_topk(self, importance, r: int):
@@ -278,6 +310,28 @@ def visual_topk(*a, **kw):
 
 def visual_gather(*a, **kw):
     return default().visual_gather(*a, **kw)
+
+
+def prefill_attn_stats(*a, **kw):
+    return default().prefill_attn_stats(*a, **kw)
+
+
+def prefill_visual_importance(*a, **kw):
+    return default().prefill_visual_importance(*a, **kw)
+
+
+def prefill_attn_entropy_mean(entropy, prompt_len) -> float:
+    """AE of one layer over prompts (Section 3.2): the mean of the entropies of the prompt rows i < n_b of every
+    head and sequence (entropy [B, Hq, N]), summed in fp64."""
+    e = np.asarray(entropy, dtype=np.float64)
+    n = np.asarray(prompt_len, dtype=np.int64)
+    total, count = 0.0, 0
+    for b in range(e.shape[0]):
+        total += float(e[b, :, :n[b]].sum())
+        count += e.shape[1] * int(n[b])
+    if count == 0:
+        raise OracleError("prefill_attn_entropy_mean of no rows")
+    return total / count
 
 
 def attn_entropy_mean(entropy) -> float:

@@ -46,6 +46,11 @@
  *      I_j = (1/(H*Q)) sum_h sum_i A[h,i,j]; the r most important tokens are kept (ties to the smaller
  *      index), listed in increasing token order, and their K/V rows gathered into a compact cache.
  *
+ *  oracle_prefill_attn_stats / oracle_prefill_visual_importance
+ *      The same two statistics over a prompt's own causal attention (row i sees slots 0..i), which is where the
+ *      paper reads them: Eq. 2 with the final layer's weights of the prefilling pass, AE(l) over the layer's
+ *      n x n attention of the prompt (Sections 3.1 and 3.2).
+ *
  *  oracle_tree_attn_entropy
  *      Attention entropy of every verification row: -sum_j A_ij log A_ij over the row's attention
  *      probabilities, the per-row quantity whose mean over rows and heads is the average attention entropy
@@ -521,6 +526,108 @@ int oracle_kv_commit(int NL, int64_t layer_stride_elems, int B, int Hkv, int D, 
         }
       }
   for (int b = 0; b < B; ++b) kv_len_out[b] = kv_len_in[b] + accept_len[b] + 1;
+  return 0;
+}
+
+/*
+ * Prefill attention statistics.  Eq. 2 (Section 3.1) scores the visual tokens with the final layer's attention
+ * weights of the prefilling pass, and AE(l) (Section 3.2) averages the entropy of a layer's attention rows over
+ * the n prompt tokens: both are read off the attention of the prompt's own positions among themselves.  Prompt
+ * b holds n_b = prompt_len[b] tokens: keys at cache slots 0..n_b-1, queries at rows 0..n_b-1 of q.  Row i of
+ * query head h attends slots 0..i (the decoder's causal mask):
+ *     A[h,i,j] = exp(scale * q_i.k_j) / sum_{j' <= i} exp(scale * q_i.k_j'),   j <= i.
+ * Rows i >= n_b are not queries of the prompt.  Layouts: q [B,Hq,N,D]; k [B,Hkv,S_cap,D]; query head h reads
+ * KV head h / (Hq/Hkv).
+ */
+static int prefill_args_ok(int B, int Hq, int Hkv, int N, int D, int S_cap, const int32_t* prompt_len) {
+  if (B < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || N < 1 || D < 1 || S_cap < N) return ORACLE_BAD_ARG;
+  for (int b = 0; b < B; ++b)
+    if (prompt_len[b] < 0 || prompt_len[b] > N) return ORACLE_BAD_ARG;
+  return 0;
+}
+
+/* Scores of row (b, h, i) over slots 0..i into score[]; returns their maximum. */
+static double prefill_scores(int Hq, int Hkv, int N, int D, int S_cap, double scale, const float* q, const float* k,
+                             int b, int h, int i, double* score) {
+  const int g = h / (Hq / Hkv);
+  const float* qi = q + (((size_t)b * Hq + h) * N + i) * D;
+  const float* kb = k + ((size_t)b * Hkv + g) * (size_t)S_cap * D;
+  double m = -INFINITY;
+  for (int s = 0; s <= i; ++s) {
+    double dot = 0.0;
+    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];
+    score[s] = scale * dot;
+    if (score[s] > m) m = score[s];
+  }
+  return m;
+}
+
+/* lse [B,Hq,N] = log sum_{j<=i} exp(scale q_i.k_j) (natural log) and entropy [B,Hq,N] = -sum_j A_ij log A_ij
+ * of every prompt row; rows i >= n_b get lse = -inf and entropy 0.  Either output may be NULL. */
+int oracle_prefill_attn_stats(int B, int Hq, int Hkv, int N, int D, int S_cap, double scale, const float* q,
+                              const float* k, const int32_t* prompt_len, double* lse, double* entropy) {
+  int rc = prefill_args_ok(B, Hq, Hkv, N, D, S_cap, prompt_len);
+  if (rc) return rc;
+#pragma omp parallel
+  {
+    double* score = (double*)malloc(sizeof(double) * (size_t)N);
+#pragma omp for collapse(2) schedule(dynamic)
+    for (int b = 0; b < B; ++b)
+      for (int h = 0; h < Hq; ++h)
+        for (int i = 0; i < N; ++i) {
+          const size_t row = ((size_t)b * Hq + h) * N + i;
+          if (i >= prompt_len[b]) {
+            if (lse) lse[row] = -INFINITY;
+            if (entropy) entropy[row] = 0.0;
+            continue;
+          }
+          const double m = prefill_scores(Hq, Hkv, N, D, S_cap, scale, q, k, b, h, i, score);
+          double l = 0.0;
+          for (int s = 0; s <= i; ++s) l += exp(score[s] - m);
+          if (lse) lse[row] = m + log(l);
+          if (entropy) {
+            double H = 0.0;
+            for (int s = 0; s <= i; ++s) {
+              const double p = exp(score[s] - m) / l;   /* A[h,i,s] */
+              if (p > 0.0) H -= p * log(p);
+            }
+            entropy[row] = H;
+          }
+        }
+    free(score);
+  }
+  return 0;
+}
+
+/* Eq. 2 over the prompt: importance [B, vis_count], importance[b][j] = (1/(Hq*n_b)) sum_h sum_{i<n_b}
+ * A[h,i,vis_begin+j] (a slot past row i gets nothing from it, so a slot at or past n_b has importance 0); a
+ * sequence with n_b = 0 has all zeros. */
+int oracle_prefill_visual_importance(int B, int Hq, int Hkv, int N, int D, int S_cap, double scale, const float* q,
+                                     const float* k, const int32_t* prompt_len, int vis_begin, int vis_count,
+                                     double* importance) {
+  int rc = prefill_args_ok(B, Hq, Hkv, N, D, S_cap, prompt_len);
+  if (rc) return rc;
+  if (vis_begin < 0 || vis_count < 1 || vis_begin + vis_count > S_cap) return ORACLE_BAD_ARG;
+#pragma omp parallel for schedule(dynamic)
+  for (int b = 0; b < B; ++b) {
+    double* score = (double*)malloc(sizeof(double) * (size_t)N);
+    double* imp = importance + (size_t)b * vis_count;
+    for (int j = 0; j < vis_count; ++j) imp[j] = 0.0;
+    const int n = prompt_len[b];
+    for (int h = 0; h < Hq; ++h)
+      for (int i = 0; i < n; ++i) {
+        const double m = prefill_scores(Hq, Hkv, N, D, S_cap, scale, q, k, b, h, i, score);
+        double l = 0.0;
+        for (int s = 0; s <= i; ++s) l += exp(score[s] - m);
+        for (int j = 0; j < vis_count; ++j) {
+          const int slot = vis_begin + j;
+          if (slot <= i) imp[j] += exp(score[slot] - m) / l;   /* A[h,i,slot]; later slots are masked */
+        }
+      }
+    if (n > 0)
+      for (int j = 0; j < vis_count; ++j) imp[j] /= (double)Hq * n;
+    free(score);
+  }
   return 0;
 }
 

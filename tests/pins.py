@@ -703,6 +703,127 @@ VISUAL_PINS = [pin_visual_bruteforce, pin_visual_uniform_closed_form, pin_visual
                pin_visual_topk_and_gather]
 
 
+# ----------------------------------------------------------------------------- prefill statistics (causal)
+def _prefill_inputs(rng, B, Hq, Hkv, N, D, S_cap):
+    q = rng.standard_normal((B, Hq, N, D)).astype(np.float32)
+    k = rng.standard_normal((B, Hkv, S_cap, D)).astype(np.float32)
+    return q, k
+
+
+def pin_prefill_uniform_closed_form(orc):
+    """Equal keys: prompt row i spreads 1/(i+1) over slots 0..i, so lse_i = s_i + ln(i+1) (s_i = scale q_i.k),
+    its entropy is ln(i+1), and slot j's importance is (1/n) sum_{i=j}^{n-1} 1/(i+1) = (H_n - H_j)/n with
+    harmonic numbers H (0 at or past n); rows at or past n are not queries.  Ragged prompts, an offset window
+    and grouped heads."""
+    rng = np.random.default_rng(61)
+    B, Hq, Hkv, N, D, S = 3, 4, 2, 23, 8, 29
+    q, k = _prefill_inputs(rng, B, Hq, Hkv, N, D, S)
+    kc = np.broadcast_to(k[:, :, :1], k.shape).copy()
+    lens = np.array([23, 9, 1], np.int32)
+    scale = 0.4
+    lse, ent = orc.prefill_attn_stats(q, kc, lens, scale, Hkv)
+    for b in range(B):
+        n = int(lens[b])
+        for h in range(Hq):
+            s = scale * (q[b, h, :n].astype(np.float64) @ kc[b, h // 2, 0].astype(np.float64))
+            i = np.arange(n)
+            assert np.max(np.abs(lse[b, h, :n] - (s + np.log(i + 1.0)))) <= 1e-12, (b, h)
+            assert np.max(np.abs(ent[b, h, :n] - np.log(i + 1.0))) <= 1e-12, (b, h)
+            assert np.all(lse[b, h, n:] == -np.inf) and np.all(ent[b, h, n:] == 0.0)
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, S + 1))])   # H[m] = 1 + 1/2 + ... + 1/m
+    for v0, nv in ((0, S), (5, 11)):
+        imp = orc.prefill_visual_importance(q, kc, lens, scale, Hkv, v0, nv)
+        for b in range(B):
+            n = int(lens[b])
+            j = v0 + np.arange(nv)
+            ref = np.where(j < n, (H[n] - H[np.minimum(j, n)]) / n, 0.0)
+            assert np.max(np.abs(imp[b] - ref)) <= 1e-14, (b, v0)
+
+
+def pin_prefill_mass_balance(orc):
+    """Every prompt row's attention sums to one, so over a window covering the whole prompt the importances of a
+    sequence sum to one (the mean over its Hq*n rows), whatever the scores; an empty prompt has none."""
+    rng = np.random.default_rng(62)
+    B, Hq, Hkv, N, D, S = 4, 6, 3, 31, 8, 32
+    q, k = _prefill_inputs(rng, B, Hq, Hkv, N, D, S)
+    q *= 3.0
+    lens = np.array([31, 17, 0, 2], np.int32)
+    imp = orc.prefill_visual_importance(q, k, lens, 0.5, Hkv, 0, S)
+    for b in range(B):
+        expect = 1.0 if lens[b] > 0 else 0.0
+        assert abs(imp[b].sum() - expect) <= 1e-13, b
+        assert np.all(imp[b, lens[b]:] == 0.0) and np.all(imp[b] >= 0.0)
+
+
+def pin_prefill_chain_tree_agrees(orc):
+    """A prompt's rows L0..n-1 are the rows of a chain-shaped tree of n - L0 nodes over a committed prefix of L0
+    slots (node t at slot L0 + t sees the prefix and nodes 0..t): their lse and entropy equal the tree oracle's
+    (itself pinned to brute force and to library causal attention).  Telescoping the importance over prompt
+    lengths L0 and n leaves exactly the tree rows, so for a prefix slot j < L0,
+    n I_j(n) - L0 I_j(L0) = T I_j(tree)."""
+    rng = np.random.default_rng(63)
+    for B, Hq, Hkv, N, D, L0 in ((2, 4, 2, 40, 16, 25), (1, 3, 1, 12, 8, 0), (1, 2, 2, 70, 8, 5)):
+        S = N + 3
+        q, k = _prefill_inputs(rng, B, Hq, Hkv, N, D, S)
+        T = N - L0
+        lens = np.full(B, N, np.int32)
+        lse, ent = orc.prefill_attn_stats(q, k, lens, 0.35, Hkv)
+        chain = np.tile(W.chain_tree(T)[None], (B, 1))
+        kv = np.full(B, L0, np.int32)
+        qt = np.ascontiguousarray(q[:, :, L0:N])
+        vv = np.zeros_like(k)
+        _, lse_t = orc.tree_attn(qt, k, vv, kv, chain, 0.35, Hkv)
+        ent_t = orc.tree_attn_entropy(qt, k, kv, chain, 0.35, Hkv)
+        assert np.max(np.abs(lse[:, :, L0:N] - lse_t)) <= 1e-12
+        assert np.max(np.abs(ent[:, :, L0:N] - ent_t)) <= 1e-12
+        if L0 > 0:
+            imp_n = orc.prefill_visual_importance(q, k, lens, 0.35, Hkv, 0, L0)
+            imp_0 = orc.prefill_visual_importance(q, k, np.full(B, L0, np.int32), 0.35, Hkv, 0, L0)
+            imp_t = orc.visual_importance(qt, k, kv, chain, 0.35, Hkv, 0, L0)
+            assert np.max(np.abs(N * imp_n - L0 * imp_0 - T * imp_t)) <= 1e-12
+
+
+def pin_prefill_single_and_two_slots(orc):
+    """Row 0 sees only slot 0: lse = s_00, entropy 0; with a one-token prompt slot 0 has importance 1.  Row 1
+    sees two slots with score gap d: the binary entropy ln(1 + e^-d) + d e^-d / (1 + e^-d), d >= 0."""
+    rng = np.random.default_rng(64)
+    B, Hq, Hkv, N, D, S = 2, 2, 1, 6, 8, 6
+    for trial in range(10):
+        q, k = _prefill_inputs(rng, B, Hq, Hkv, N, D, S)
+        q *= rng.uniform(0.2, 3.0)
+        lse, ent = orc.prefill_attn_stats(q, k, np.array([6, 2], np.int32), 0.5, Hkv)
+        for b in range(B):
+            for h in range(Hq):
+                qd, kd = q[b, h].astype(np.float64), k[b, 0].astype(np.float64)
+                assert abs(lse[b, h, 0] - 0.5 * (qd[0] @ kd[0])) <= 1e-13
+                assert ent[b, h, 0] == 0.0
+                d = abs(0.5 * (qd[1] @ kd[1] - qd[1] @ kd[0]))
+                Hb = np.log1p(np.exp(-d)) + d * np.exp(-d) / (1.0 + np.exp(-d))
+                assert abs(ent[b, h, 1] - Hb) <= 1e-12, (trial, b, h)
+        imp = orc.prefill_visual_importance(q, k, np.array([1, 1], np.int32), 0.5, Hkv, 0, 3)
+        assert np.array_equal(imp, np.array([[1.0, 0.0, 0.0]] * B))
+
+
+def pin_prefill_layer_entropy_mean(orc):
+    """AE over prompts with equal keys: row i has entropy ln(i+1), so the mean over the sum(n_b) rows of every
+    head is sum_b ln(n_b!) / sum_b n_b (log-gamma); each row counts once whatever the padding N."""
+    from math import lgamma
+    import oracle as oracle_mod
+    rng = np.random.default_rng(65)
+    B, Hq, Hkv, N, D, S = 3, 4, 4, 40, 8, 40
+    q, k = _prefill_inputs(rng, B, Hq, Hkv, N, D, S)
+    kc = np.broadcast_to(k[:, :, :1], k.shape).copy()
+    lens = np.array([40, 7, 19], np.int32)
+    _, ent = orc.prefill_attn_stats(q, kc, lens, 0.3, Hkv)
+    ae = oracle_mod.prefill_attn_entropy_mean(ent, lens)
+    ref = sum(lgamma(int(n) + 1) for n in lens) / float(lens.sum())
+    assert abs(ae - ref) <= 1e-12
+
+
+PREFILL_PINS = [pin_prefill_uniform_closed_form, pin_prefill_mass_balance, pin_prefill_chain_tree_agrees,
+                pin_prefill_single_and_two_slots, pin_prefill_layer_entropy_mean]
+
+
 # ------------------------------------------------------------------------------------ sampled acceptance
 def _softmax(logits, tau):
     z = np.asarray(logits, dtype=np.float64) / tau
@@ -963,4 +1084,5 @@ LM_HEAD_PINS = [pin_lm_head_one_hot_weights, pin_lm_head_constant_closed_form, p
 SAMPLED_PINS = [pin_sampled_single_child_closed_form, pin_sampled_repeated_token_never_accepted_twice,
                 pin_sampled_low_temperature_is_greedy, pin_sampled_identical_models,
                 pin_sampled_output_distribution]
-ALL_PINS = ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS + VISUAL_PINS + SAMPLED_PINS + LM_HEAD_PINS
+ALL_PINS = (ATTN_PINS + ACCEPT_PINS + COMMIT_PINS + ENTROPY_PINS + VISUAL_PINS + PREFILL_PINS + SAMPLED_PINS
+            + LM_HEAD_PINS)

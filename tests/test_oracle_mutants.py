@@ -8,7 +8,7 @@ import pytest
 import oracle
 import pins
 
-ATTN, ACC, COM, ENT, VIS, SMP = "attn", "accept", "commit", "entropy", "visual", "sampled"
+ATTN, ACC, COM, ENT, VIS, SMP, PRE = "attn", "accept", "commit", "entropy", "visual", "sampled", "prefill"
 MUTANTS = [
     ("drop_scale", ATTN, "score[s] = scale * dot;", "score[s] = dot;"),
     ("wrong_kv_head", ATTN, "const int g = h / G;", "const int g = h % Hkv;"),
@@ -59,6 +59,20 @@ MUTANTS = [
      "    score[s] = dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;"),
     ("entropy_self_hidden", ENT, "  visible_nodes(parent ? parent + (size_t)b * T : NULL,\n                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);\n  const int n = L + T;\n  double m = -INFINITY;\n  for (int s = 0; s < n; ++s) {\n    if (s >= L && !visible[s - L]) continue;\n    double dot = 0.0;\n    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];\n    score[s] = scale * dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;",
      "  visible_nodes(parent ? parent + (size_t)b * T : NULL,\n                tree_mask ? tree_mask + ((size_t)b * T + i) * W : NULL, T, i, visible);\n  visible[i] = 0;\n  const int n = L + T;\n  double m = -INFINITY;\n  for (int s = 0; s < n; ++s) {\n    if (s >= L && !visible[s - L]) continue;\n    double dot = 0.0;\n    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)kb[(size_t)s * D + d];\n    score[s] = scale * dot;\n    if (score[s] > m) m = score[s];\n  }\n  if (m == -INFINITY) return 0.0;"),
+    ("prefill_causal_strict", PRE, "  for (int s = 0; s <= i; ++s) {\n    double dot = 0.0;",
+     "  for (int s = 0; s < i; ++s) {\n    double dot = 0.0;"),
+    ("prefill_wrong_kv_head", PRE, "const int g = h / (Hq / Hkv);", "const int g = h % Hkv;"),
+    ("prefill_query_row_zero", PRE, "const float* qi = q + (((size_t)b * Hq + h) * N + i) * D;",
+     "const float* qi = q + (((size_t)b * Hq + h) * N) * D;"),
+    ("prefill_lse_without_max", PRE, "if (lse) lse[row] = m + log(l);", "if (lse) lse[row] = log(l);"),
+    ("prefill_entropy_unnormalised", PRE, "const double p = exp(score[s] - m) / l;   /* A[h,i,s] */",
+     "const double p = exp(score[s] - m);   /* A[h,i,s] */"),
+    ("prefill_norm_capacity", PRE, "imp[j] /= (double)Hq * n;", "imp[j] /= (double)Hq * N;"),
+    ("prefill_norm_rows_only", PRE, "imp[j] /= (double)Hq * n;", "imp[j] /= (double)n;"),
+    ("prefill_padding_rows_counted", PRE, "      for (int i = 0; i < n; ++i) {\n        const double m = prefill_scores",
+     "      for (int i = 0; i < N; ++i) {\n        const double m = prefill_scores"),
+    ("prefill_window_offset_ignored", PRE, "const int slot = vis_begin + j;", "const int slot = j;"),
+    ("prefill_diagonal_dropped", PRE, "if (slot <= i) imp[j]", "if (slot < i) imp[j]"),
     ("sampled_ratio_inverted", SMP, "if ((double)u[c] * q[x] < r[x]) {", "if ((double)u[c] * r[x] < q[x]) {"),
     ("sampled_residual_unclamped", SMP, "r[y] = (r[y] > q[y] ? r[y] - q[y] : 0.0) / z;", "r[y] = (r[y] - q[y]) / z;"),
     ("sampled_residual_not_updated", SMP, "r[y] = (r[y] > q[y] ? r[y] - q[y] : 0.0) / z;", "r[y] = r[y];"),
@@ -80,7 +94,7 @@ MUTANTS = [
      "    accept_len[b] = depth + 1;\n    next_token[b] = pick"),
 ]
 GROUPS = {ATTN: pins.ATTN_PINS, ACC: pins.ACCEPT_PINS, COM: pins.COMMIT_PINS, ENT: pins.ENTROPY_PINS,
-          VIS: pins.VISUAL_PINS, SMP: pins.SAMPLED_PINS}
+          VIS: pins.VISUAL_PINS, SMP: pins.SAMPLED_PINS, PRE: pins.PREFILL_PINS}
 
 
 @pytest.mark.parametrize("name,group,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
@@ -135,6 +149,31 @@ def test_lm_head_pins_catch_planted_mistake(monkeypatch, mutant):
     orc = oracle.default()
     caught = []
     for pin in pins.LM_HEAD_PINS:
+        try:
+            pin(orc)
+        except (AssertionError, ValueError, IndexError) as e:
+            caught.append((pin.__name__, type(e).__name__))
+    assert caught, "no pin caught %s" % mutant.__name__
+
+
+# The layer mean of prompt-row entropies is plain numpy too.
+def _ae_all_rows(entropy, prompt_len):
+    import numpy as np
+    return float(np.asarray(entropy, np.float64).mean())
+
+
+def _ae_mean_of_sequence_means(entropy, prompt_len):
+    import numpy as np
+    e = np.asarray(entropy, np.float64)
+    return float(np.mean([e[b, :, :int(n)].mean() for b, n in enumerate(prompt_len)]))
+
+
+@pytest.mark.parametrize("mutant", [_ae_all_rows, _ae_mean_of_sequence_means], ids=lambda f: f.__name__)
+def test_prefill_entropy_mean_pins_catch_planted_mistake(monkeypatch, mutant):
+    monkeypatch.setattr(oracle, "prefill_attn_entropy_mean", mutant)
+    orc = oracle.default()
+    caught = []
+    for pin in pins.PREFILL_PINS:
         try:
             pin(orc)
         except (AssertionError, ValueError, IndexError) as e:
