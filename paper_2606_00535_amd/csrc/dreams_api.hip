@@ -75,8 +75,7 @@ constexpr size_t kMaxCounters = kCounterWords;
 struct AttnPlan {
   int G, rows_total, row_groups, units, splits;
   int rows_per_wg;   // query rows one workgroup owns
-  int ctr_stride;    // 64-bit words between the sets' arrival counters in the counter region
-  int merge_parts;   // merging workgroups per set appended to the launch (0: the set's last piece merges it)
+  int ctr_stride;    // 64-bit words between the sets' counters in the counter region
   size_t o_off, ml_off, e_off, bytes;
 };
 
@@ -113,8 +112,7 @@ dreams_status_t check_attn_desc(const dreams_attn_desc_t* d) {
   return DREAMS_OK;
 }
 
-// `launching`: also decide how the pieces are merged (which needs the device; the workspace size does not)
-dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p, bool launching) {
+dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   dreams_status_t st = check_attn_desc(d);
   if (st != DREAMS_OK) return st;
   *p = AttnPlan{};
@@ -130,12 +128,10 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p, bool launchi
   const int n_keys = max_len + d->num_nodes;
   const int max_splits = (n_keys + kPieceMinKeys - 1) / kPieceMinKeys;
   int splits = d->num_splits;
-  int cus = 0;
-  if (splits == 0 || launching) {
+  if (splits == 0) {
+    int cus = 0;
     st = device_cus(&cus);
     if (st != DREAMS_OK) return st;
-  }
-  if (splits == 0) {
     // about one workgroup per compute unit (a workgroup holds most of a compute unit's LDS)
     const long long wgs = (long long)p->units * p->row_groups;
     splits = (int)((cus + wgs / 2) / wgs);
@@ -155,18 +151,12 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p, bool launchi
   const long long grid = 8LL * ((p->units + 7) / 8) * splits * p->row_groups;
   if (grid > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large: %lld workgroups", grid);
   if (splits > 1) {
-    // two 64-bit counters per set (arrivals, finished merging workgroups), on a 128-byte line of their own
+    // two 64-bit counter words per set (arrivals and leavers; started and done), on a 128-byte line of their own
     // where there is room (atomics on one line serialise), then the pieces' partial results after the counter
     // region every workspace starts with
     int stride = 16;
     while (stride > 2 && sets * stride > kMaxSetCounters) stride >>= 1;
     p->ctr_stride = stride;
-    // One round of streaming workgroups and at least 4 pieces per set: merging workgroups of 16 rows each,
-    // appended to the launch, spread each set's merge over several compute units as streaming ones finish
-    // (llava7b_layer, 8 pieces: 19.1 against 20.3 us).  Otherwise the set's last piece merges it: with 2 pieces
-    // that is one partial result to read (llava7b_full layer: 47.9 against 51.2 us), and with several rounds
-    // no workgroup holds a compute unit waiting while pieces of later rounds stream.
-    p->merge_parts = launching && grid <= cus && splits >= 4 ? p->rows_per_wg / 16 : 0;
     const size_t rows = (size_t)sets * splits * p->rows_per_wg;
     p->o_off = kCounterBytes;
     p->ml_off = p->o_off + align_up(rows * d->head_dim * 2, 256);
@@ -249,7 +239,7 @@ extern "C" {
 dreams_status_t dreams_tree_verify_attn_workspace_size(const dreams_attn_desc_t* desc, size_t* bytes) {
   if (!bytes) return fail(DREAMS_ERR_INVALID_ARG, "bytes is NULL");
   AttnPlan p;
-  dreams_status_t st = plan_attn(desc, &p, false);
+  dreams_status_t st = plan_attn(desc, &p);
   if (st != DREAMS_OK) return st;
   *bytes = p.bytes;
   return ok();
@@ -287,7 +277,7 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
   if (st != DREAMS_OK) return st;
   if (desc->batch == 0) return ok();
   AttnPlan p;
-  st = plan_attn(desc, &p, false);
+  st = plan_attn(desc, &p);
   if (st != DREAMS_OK) return st;
   if (p.bytes > 0) {
     if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", p.bytes);
@@ -295,8 +285,6 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
       return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, p.bytes);
     if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   }
-  st = plan_attn(desc, &p, true);   // the same plan, plus how the pieces are merged
-  if (st != DREAMS_OK) return st;
 
   AttnArgs a{};
   a.q = q;
@@ -314,7 +302,6 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
   a.part_e = p.bytes ? (float*)(ws + p.e_off) : nullptr;
   a.set_ctr = p.bytes ? (unsigned long long*)ws : nullptr;
   a.ctr_stride = p.ctr_stride;
-  a.merge_parts = p.merge_parts;
   a.wait_ticks = g_wait_ticks.load(std::memory_order_relaxed);
   a.err = p.bytes ? (uint32_t*)ws + kErrorWord : nullptr;
   a.B = desc->batch;
@@ -384,7 +371,7 @@ dreams_status_t dreams_tree_verify_attn_noalloc(const dreams_attn_desc_t* desc, 
   if (st != DREAMS_OK) return st;
   if (desc->batch == 0) return ok();
   AttnPlan p;
-  st = plan_attn(desc, &p, false);
+  st = plan_attn(desc, &p);
   if (st != DREAMS_OK) return st;
   if (p.bytes > kScratchBytes)
     return fail(DREAMS_ERR_UNSUPPORTED,
@@ -940,7 +927,7 @@ dreams_status_t dreams_set_wait_limit(double seconds) {
 dreams_status_t dreams_tree_verify_attn_splits(const dreams_attn_desc_t* desc, int32_t* splits) {
   if (!splits) return fail(DREAMS_ERR_INVALID_ARG, "splits is NULL");
   AttnPlan p;
-  dreams_status_t st = plan_attn(desc, &p, false);
+  dreams_status_t st = plan_attn(desc, &p);
   if (st != DREAMS_OK) return st;
   *splits = p.splits;
   return ok();

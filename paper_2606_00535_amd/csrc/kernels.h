@@ -77,21 +77,16 @@ struct AttnArgs {
   float* lse;             // [B, Hq, T] or nullptr
   float* entropy;         // [B, Hq, T] attention entropy of every row (nats), or nullptr
   // Several pieces per (sequence, KV head, row group) -- a "set": each piece stores its rows' normalised output
-  // (bf16) and softmax state, and the last piece of the set to arrive at the set's counter merges them.
+  // (bf16) and softmax state, and the set's pieces merge them, each a slice of the rows.
   __bf16* part_o;         // [sets, splits, rows_per_wg, D]   accumulator / sum, rounded to bf16
   float* part_ml;         // [sets, splits, rows_per_wg, 2]   (max in log2 units, sum)
   float* part_e;          // [sets, splits, rows_per_wg]      entropy terms (with entropy only)
-  // 64-bit arrival counter of set s at set_ctr[s * ctr_stride]: the arrivals in bits [0, 8), and per XCD x a
-  // 7-bit count of the set's pieces that ran there at bit 8 + 7x.  Zero between calls.
+  // Two 64-bit counter words of set s at set_ctr[s * ctr_stride]: arrivals, pieces that left their rows to the
+  // last arrival and an off-XCD mark; pieces started and pieces done with the counters.  Zero between calls.
   unsigned long long* set_ctr;
-  int ctr_stride;         // 64-bit words between consecutive set counters (>= 2 with merging workgroups: the
-                          // second word counts the set's finished merging workgroups)
-  // > 0: merge_parts merging workgroups per set (rows_per_wg / merge_parts rows each) follow the streaming ones
-  // in the same launch; 0: the last piece of each set merges it
-  int merge_parts;
-  int stream_wgs;         // set by the launcher
+  int ctr_stride;         // 64-bit words between consecutive sets' counters (>= 2)
   uint32_t* err;          // the workspace's failure flags (splits > 1)
-  uint64_t wait_ticks;    // bound on a merging workgroup's wait (100 MHz real-time ticks)
+  uint64_t wait_ticks;    // bound on a piece's wait for the rest of its set (100 MHz real-time ticks)
   int B, Hq, Hkv, G, T, D, S_cap;
   int units;              // B * Hkv
   int rows_per_wg;        // query rows of one workgroup (64 or 128)

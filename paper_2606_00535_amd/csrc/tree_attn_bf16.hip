@@ -122,7 +122,15 @@ struct Rows {
   static constexpr int HALF = kStep * ROW;    // bytes of the K (or V) part of a step
   static constexpr int SLOT = 2 * HALF;       // bytes of a step
   static constexpr int C16 = 16 * ROW / 1024; // wave-wide 1 KB copies per 16 rows
-  __device__ static __forceinline__ int swz(int r) { return (r / RPL) % CPR; }
+  // D = 128 (one row per 256-byte bank line): gfx950 serves a 16-byte read (ds_read_b128) in groups of lanes
+  // and a transposing 8-byte read (ds_read_b64_tr_b16) in two halves of 32 lanes over 64 banks.  The key
+  // reads touch rows (m%4)*4 + m/4 at one chunk, the value reads rows 4j+q, q in {0,1} (or {2,3}), at an
+  // aligned pair of chunks; swz(r) = 4*((r/4)%4) + 2*(r%2) + 1 puts both on distinct banks (measured: 213 and
+  // 165 B/clk per compute unit, against 126 and 122 with r % 16).  D = 64: two rows per bank line.
+  __device__ static __forceinline__ int swz(int r) {
+    if constexpr (D == 128) return ((r >> 2) & 3) * 4 + (r & 1) * 2 + 1;
+    return (r / RPL) % CPR;
+  }
   __device__ static __forceinline__ int off(int r, int c) { return r * ROW + ((c ^ swz(r)) << 4); }
 };
 
@@ -223,27 +231,6 @@ __device__ __forceinline__ void merge_pieces(const AttnArgs& a, size_t prow0, in
   }
 }
 
-// Wait (one thread) until a set's arrival counter shows `expect` pieces, bounded by a.wait_ticks.  Returns 1
-// if they arrived and all ran on the caller's XCD, else 2 (and flags the workspace).
-__device__ __forceinline__ uint32_t wait_for_pieces(const AttnArgs& a, unsigned long long* ctr, int expect) {
-  const uint32_t x = xcd_id();
-  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-  unsigned long long c;
-  while (((c = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffull) < (unsigned long long)expect) {
-    if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) break;
-    __builtin_amdgcn_s_sleep(1);
-  }
-  if ((c & 0xffull) != (unsigned long long)expect) {
-    raise_device_error(a.err, kErrWaitTimeout);
-    return 2;
-  }
-  if (((c >> (8 + 7 * x)) & 0x7full) != (unsigned long long)expect) {
-    raise_device_error(a.err, kErrXcdSplit);
-    return 2;
-  }
-  return 1;
-}
-
 template <int D, int RB, int KW, int W, int NST, bool PIPE, bool ENT>
 __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   constexpr int WR = W / KW;          // waves per key group; each owns a different slice of the rows
@@ -267,37 +254,8 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots
   __shared__ uint64_t anc_lds[2 * kMaxNodes];
   __shared__ uint64_t meta_lds[2 * kMaxNodes];   // the sequence's parents or tree mask rows, as copied
-  __shared__ uint32_t merge_lds;                  // 1: merge the set's pieces; 2: merge, but write NaN rows
-
-  if (a.merge_parts > 0 && (int)blockIdx.x >= a.stream_wgs) {
-    // ---- a merging workgroup (after every streaming one, so the pieces it waits for are running or done):
-    // rows [part * R / merge_parts, ...) of one set, on the set's XCD
-    const int m = (int)blockIdx.x - a.stream_wgs;
-    const int mx = m & 7, ms = m >> 3;
-    const int per_unit = a.row_groups * a.merge_parts;
-    const int u = mx + 8 * (ms / per_unit);
-    if (u >= a.units) return;
-    const int within = ms - (ms / per_unit) * per_unit;
-    const int rg = within / a.merge_parts, part = within - rg * a.merge_parts;
-    constexpr int R = (W / KW) * 16 * RB;
-    const size_t pset = (size_t)u * a.row_groups + rg;
-    unsigned long long* ctr = a.set_ctr + pset * a.ctr_stride;
-    if (threadIdx.x == 0) merge_lds = wait_for_pieces(a, ctr, a.splits);
-    __syncthreads();
-    const int b = u / a.Hkv, g = u - b * a.Hkv;
-    const size_t orow0 = ((size_t)b * a.Hq + (size_t)g * a.G) * a.T + (size_t)rg * R;
-    const int nrows = R / a.merge_parts;
-    merge_pieces<D, W, ENT>(a, pset * a.splits * R, R, (__bf16*)a.out + orow0 * D, a.lse ? a.lse + orow0 : nullptr,
-                            ENT ? a.entropy + orow0 : nullptr, min(R, a.G * a.T - rg * R), part * nrows, nrows, -1,
-                            nullptr, nullptr, nullptr, merge_lds == 1);
-    // the set's last merging workgroup clears both counters for the next call
-    if (threadIdx.x == 0 &&
-        __hip_atomic_fetch_add(ctr + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned long long)a.merge_parts - 1) {
-      __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(ctr + 1, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    return;
-  }
+  __shared__ uint32_t merge_lds;                  // slices of the set's rows this workgroup merges
+  __shared__ uint32_t good_lds;                   // 0: a wait gave up (the merged rows are written as NaN)
 
   // ---- work item
   const int n = blockIdx.x;
@@ -395,6 +353,10 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   }
   const int fa = min(NSS - QSS, nsp);
   for (int j = 0; j < fa; ++j) issue_super(j);
+  // this piece has started (the merge at the end relies on knowing that every piece of the set runs)
+  if (a.splits > 1 && tid == 0)
+    __hip_atomic_fetch_add(a.set_ctr + ((size_t)u * a.row_groups + rg) * a.ctr_stride + 1, 1ull, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 
   // ---- prologue: prefix length, ancestor sets, queries (all overlapping the copies above)
   int Lp = kv_len_b;
@@ -799,12 +761,9 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   const size_t pset = (size_t)u * a.row_groups + rg;
   const size_t prow0 = pset * S * R;   // the set's piece 0, row 0
   const int rows_valid = min(R, rows_total - rg * R);
-  // With several pieces, either merging workgroups appended to the launch merge the set (every piece stores
-  // its rows), or the set's last piece does (it is the last of the set to be dispatched, so every piece it
-  // waits for is already running or done; its own rows stay in LDS).  A single piece writes the output.  Rows
-  // of one KV head are consecutive in memory.
-  const bool merger = S > 1 && a.merge_parts == 0 && split == S - 1;
-  if (!merger) {
+  // One piece writes the output; with several, every piece stores its rows (normalised, bf16), their (max,
+  // sum) and entropy terms as piece `split` of its set.  Rows of one KV head are consecutive in memory.
+  {
     __bf16* dst = S == 1 ? (__bf16*)a.out + (qrow0 + (size_t)rg * R) * D : a.part_o + (prow0 + (size_t)split * R) * D;
 #pragma unroll
     for (int t = 0; t < ITEMS; ++t) {
@@ -824,30 +783,70 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
         if (ENT) a.part_e[pr] = e_lds[tid];
       }
     }
-    if (S == 1) return;
-    // Count this piece's arrival once its stores have reached the L2.  The counter's low byte counts the
-    // arrivals and a 7-bit field per XCD counts where they ran: the merge reads the pieces' rows from its own
-    // XCD's L2, which is right only if they all ran there (workgroup n runs on XCD n % 8, and the pieces of a
-    // set and its merging workgroups share n % 8).
-    wait_vector_memory();
-    __syncthreads();
-    if (tid == 0)
-      __hip_atomic_fetch_add(a.set_ctr + pset * a.ctr_stride, 1ull + (1ull << (8 + 7 * xcd_id())), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-    return;
   }
+  if (S == 1) return;
 
-  // ---- the set's last piece merges it: wait for the other S - 1 pieces, clear the counter for the next call
+  // ---- the set's merge, spread over its pieces.  Word 0 of the set's counters takes one arrival per piece
+  // (low byte), a bit per piece that leaves its rows to others (bits 8..39) and a bit for a piece that ran off
+  // the set's XCD (bit 63); word 1 counts the pieces that started (low byte) and that are done with the
+  // counters (second byte).  A piece whose set has started completely waits for every arrival and merges its
+  // own slice of the rows: every piece it waits for is running and arrives without waiting for anything.  A
+  // piece that finds a piece of its set not yet started leaves, and the last piece to arrive merges the slices
+  // of every piece that left (it waits for nothing).  So every wait ends, and each slice is merged once.  The
+  // pieces' rows are read from this XCD's L2 (all pieces of a set share blockIdx % 8, hence the XCD).  The last
+  // piece done with the counters clears both words for the next call.
   unsigned long long* ctr = a.set_ctr + pset * a.ctr_stride;
+  wait_vector_memory();   // this piece's rows have reached the L2
+  __syncthreads();
   if (tid == 0) {
-    merge_lds = wait_for_pieces(a, ctr, S - 1);
-    __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool coop = (__hip_atomic_load(ctr + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 0xffull) ==
+                      (unsigned long long)S;
+    const bool off_xcd = xcd_id() != (uint32_t)xcd;
+    const unsigned long long old = __hip_atomic_fetch_add(
+        ctr, 1ull | (coop ? 0ull : 1ull << (8 + split)) | (off_xcd ? 1ull << 63 : 0ull), __ATOMIC_RELAXED,
+        __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = (old & 0xffull) == (unsigned long long)(S - 1);
+    unsigned long long now = old + 1ull;
+    bool good = true;
+    if (coop && !last) {
+      const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+      while (((now = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffull) <
+             (unsigned long long)S) {
+        if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
+          raise_device_error(a.err, kErrWaitTimeout);
+          good = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    if (now >> 63) {
+      raise_device_error(a.err, kErrXcdSplit);
+      good = false;
+    }
+    // slices this workgroup merges: its own (cooperative), and the leavers' (last arrival)
+    uint32_t slices = coop ? 1u << split : 0u;
+    if (last) slices |= (uint32_t)((old >> 8) & 0xffffffffull) | (coop ? 0u : 1u << split);
+    merge_lds = slices;
+    good_lds = good ? 1u : 0u;
   }
   __syncthreads();
+  const uint32_t slices = merge_lds;
   const size_t orow0 = qrow0 + (size_t)rg * R;
-  merge_pieces<D, W, ENT>(a, prow0, R, (__bf16*)a.out + orow0 * D, a.lse ? a.lse + orow0 : nullptr,
-                          ENT ? a.entropy + orow0 : nullptr, rows_valid, 0, R, split, row_lds, ml_lds, e_lds,
-                          merge_lds == 1);
+  for (int k = 0; k < S; ++k) {
+    if (!((slices >> k) & 1u)) continue;
+    const int r0 = k * R / S, r1 = (k + 1) * R / S;
+    merge_pieces<D, W, ENT>(a, prow0, R, (__bf16*)a.out + orow0 * D, a.lse ? a.lse + orow0 : nullptr,
+                            ENT ? a.entropy + orow0 : nullptr, rows_valid, r0, r1 - r0, split, row_lds, ml_lds,
+                            e_lds, good_lds == 1u);
+  }
+  if (tid == 0) {
+    const unsigned long long d = __hip_atomic_fetch_add(ctr + 1, 1ull << 8, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (((d >> 8) & 0xffull) == (unsigned long long)(S - 1)) {
+      __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(ctr + 1, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
 }
 
 template <int D, int RB, int KW, int W, int NST, bool ENT>
@@ -864,13 +863,10 @@ hipError_t launch_streaming(const AttnArgs& a, hipStream_t stream) {
   }
   if (a.rows_per_wg != 16 * RB * (W / KW)) return hipErrorInvalidValue;
   if (a.splits > 1 && (!a.part_o || !a.part_ml || !a.set_ctr || (ENT && !a.part_e))) return hipErrorInvalidValue;
+  if (a.splits > 1 && a.ctr_stride < 2) return hipErrorInvalidValue;
   const unsigned units_rounded = (a.units + 7) / 8 * 8;
   const unsigned grid = units_rounded * (unsigned)(a.splits * a.row_groups);
-  AttnArgs b = a;
-  b.stream_wgs = (int)grid;
-  const unsigned merge_wgs = a.splits > 1 && a.merge_parts > 0 ? units_rounded * a.row_groups * a.merge_parts : 0;
-  if (merge_wgs && (a.rows_per_wg % a.merge_parts != 0 || a.ctr_stride < 2)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(kern, dim3(grid + merge_wgs), dim3(64 * W), lds, stream, b);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * W), lds, stream, a);
   return hipGetLastError();
 }
 
