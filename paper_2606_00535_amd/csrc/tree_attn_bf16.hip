@@ -136,99 +136,83 @@ struct Rows {
 
 // Merge of a set's pieces for rows [r0, r0 + nrows) of the set, in piece order (so the result does not
 // depend on which piece finished last): out = sum_s w_s l_s o_s / sum_s w_s l_s, w_s = 2^(m_s - max_s m_s).
-// Piece `own` (if >= 0) is this workgroup's own, read from its LDS staging (row-major 16-byte pieces swizzled
-// by the row, with its (max, sum) and entropy terms); the others come from this XCD's L2 (not from this compute
-// unit's L1, which has never held them): non-temporal 16-byte loads, a row's pieces side by side, whole
-// 128-byte lines.  Rows at or past rows_valid are skipped.  good = false writes NaN rows (a failed wait).
+// Every piece's rows come from this XCD's L2 (not from this compute unit's L1, which has never held them):
+// non-temporal 16-byte loads, a row's pieces side by side, whole 128-byte lines.  The loads are issued
+// unconditionally (addresses clamped into the set), so that all of them are in flight together (loads under a
+// branch are each waited for before the branch joins); waves with no row of the slice skip it.  Rows at or
+// past rows_valid are not written.  good = false writes NaN rows (a failed wait).
 template <int D, int W, bool ENT>
 __device__ __forceinline__ void merge_pieces(const AttnArgs& a, size_t prow0, int R, __bf16* out_rows, float* lse_rows,
-                                             float* ent_rows, int rows_valid, int r0, int nrows, int own,
-                                             const unsigned char* own_rows, const float2* own_ml, const float* own_e,
-                                             bool good) {
+                                             float* ent_rows, int rows_valid, int r0, int nrows, bool good) {
   constexpr int CPR = D / 8;
-  constexpr int TG = 2;     // items whose loads are in flight together
   constexpr int PCH = 8;    // pieces per batch of loads
   typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
   const int S = a.splits;
   const int items = nrows * CPR;
-  for (int base = 0; base < items; base += TG * 64 * W) {
-    int rl[TG], ch[TG];
-    bool live[TG];
-    float M[TG], lsum[TG], esum[TG];
-    float acc[TG][8];
+  const int wave = (int)threadIdx.x >> 6;
+  for (int base = 0; base < items; base += 64 * W) {
+    if (base + 64 * wave >= items) break;   // (wave-uniform) nothing left for this wave
+    const int item = base + (int)threadIdx.x;
+    const int ch = item % CPR;
+    const bool live = item < items && r0 + item / CPR < rows_valid;
+    const int rl = min(r0 + item / CPR, R - 1);   // (a dead item's loads stay inside the set)
+    float M = -INFINITY, lsum = 0.f, esum = 0.f;
+    float acc[8];
 #pragma unroll
-    for (int t = 0; t < TG; ++t) {
-      const int item = base + t * 64 * W + (int)threadIdx.x;
-      rl[t] = r0 + item / CPR;
-      ch[t] = item % CPR;
-      live[t] = item < items && rl[t] < rows_valid;
-      M[t] = -INFINITY;
-      lsum[t] = esum[t] = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[t][e] = 0.f;
-    }
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
     for (int s0 = 0; s0 < S; s0 += PCH) {
-      float2 ml[TG][PCH];
-      float ev[TG][PCH];
-      bf16x8m x[TG][PCH];
+      f32x2 ml[PCH];
+      float ev[PCH];
+      bf16x8m x[PCH];
 #pragma unroll
-      for (int t = 0; t < TG; ++t)
-#pragma unroll
-        for (int k = 0; k < PCH; ++k) {
-          const int sp = min(s0 + k, S - 1);
-          const size_t pr = prow0 + (size_t)sp * R + rl[t];
-          if (!live[t]) {
-            ml[t][k] = make_float2(-INFINITY, 0.f);
-            ev[t][k] = 0.f;
-            x[t][k] = bf16x8m{};
-          } else if (sp == own) {
-            ml[t][k] = own_ml[rl[t]];
-            ev[t][k] = ENT ? own_e[rl[t]] : 0.f;
-            x[t][k] = *(const bf16x8m*)(own_rows + ((size_t)rl[t] * CPR + (ch[t] ^ (rl[t] & (CPR - 1)))) * 16);
-          } else {
-            const f32x2 mlv = __builtin_nontemporal_load((const f32x2*)(a.part_ml + 2 * pr));
-            ml[t][k] = make_float2(mlv.x, mlv.y);
-            ev[t][k] = ENT ? __builtin_nontemporal_load(a.part_e + pr) : 0.f;
-            x[t][k] = __builtin_nontemporal_load((const bf16x8m*)(a.part_o + pr * D + ch[t] * 8));
-          }
-        }
-#pragma unroll
-      for (int t = 0; t < TG; ++t) {
-        float Mn = M[t];
-#pragma unroll
-        for (int k = 0; k < PCH; ++k)
-          if (s0 + k < S) Mn = fmaxf(Mn, ml[t][k].x);
-        const float scale_old = M[t] == -INFINITY ? 0.f : fast_exp2(M[t] - Mn);
-        if (ENT) esum[t] = ent_term(scale_old, esum[t], M[t], Mn, lsum[t]);
-        lsum[t] *= scale_old;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[t][e] *= scale_old;
-#pragma unroll
-        for (int k = 0; k < PCH; ++k) {
-          const float w = (s0 + k >= S || ml[t][k].x == -INFINITY) ? 0.f : fast_exp2(ml[t][k].x - Mn);
-          if (ENT) esum[t] += ent_term(w, ev[t][k], ml[t][k].x, Mn, ml[t][k].y);
-          const float wl = w * ml[t][k].y;
-          lsum[t] += wl;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[t][e] = fmaf(wl, (float)x[t][k][e], acc[t][e]);
-        }
-        M[t] = Mn;
+      for (int k = 0; k < PCH; ++k) {
+        const size_t pr = prow0 + (size_t)min(s0 + k, S - 1) * R + rl;
+        ml[k] = __builtin_nontemporal_load((const f32x2*)(a.part_ml + 2 * pr));
+        ev[k] = ENT ? __builtin_nontemporal_load(a.part_e + pr) : 0.f;
+        x[k] = __builtin_nontemporal_load((const bf16x8m*)(a.part_o + pr * D + ch * 8));
       }
+      float Mn = M;
+#pragma unroll
+      for (int k = 0; k < PCH; ++k)
+        if (s0 + k < S) Mn = fmaxf(Mn, ml[k].x);
+      const float scale_old = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
+      if (ENT) esum = ent_term(scale_old, esum, M, Mn, lsum);
+      lsum *= scale_old;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] *= scale_old;
+#pragma unroll
+      for (int k = 0; k < PCH; ++k) {
+        const float w = (s0 + k >= S || ml[k].x == -INFINITY) ? 0.f : fast_exp2(ml[k].x - Mn);
+        if (ENT) esum += ent_term(w, ev[k], ml[k].x, Mn, ml[k].y);
+        const float wl = w * ml[k].y;
+        lsum += wl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(wl, (float)x[k][e], acc[e]);
+      }
+      M = Mn;
     }
+    if (!live) continue;
+    const float inv = !good ? NAN : lsum > 0.f ? 1.0f / lsum : 0.f;
+    bf16x8m res;
 #pragma unroll
-    for (int t = 0; t < TG; ++t) {
-      if (!live[t]) continue;
-      const float inv = !good ? NAN : lsum[t] > 0.f ? 1.0f / lsum[t] : 0.f;
-      bf16x8m res;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) res[e] = (__bf16)(acc[t][e] * inv);
-      *(bf16x8m*)(out_rows + (size_t)rl[t] * D + ch[t] * 8) = res;
-      if (ch[t] == 0) {
-        if (lse_rows) lse_rows[rl[t]] = !good ? NAN : lsum[t] > 0.f ? (M[t] + __log2f(lsum[t])) * kLn2 : -INFINITY;
-        if (ENT) ent_rows[rl[t]] = !good ? NAN : row_entropy(lsum[t], esum[t]);
-      }
+    for (int e = 0; e < 8; ++e) res[e] = (__bf16)(acc[e] * inv);
+    *(bf16x8m*)(out_rows + (size_t)rl * D + ch * 8) = res;
+    if (ch == 0) {
+      if (lse_rows) lse_rows[rl] = !good ? NAN : lsum > 0.f ? (M + __log2f(lsum)) * kLn2 : -INFINITY;
+      if (ENT) ent_rows[rl] = !good ? NAN : row_entropy(lsum, esum);
     }
   }
+}
+
+// LDS of a workgroup: the ring, the query rows when they sit beside it, the ancestor sets and the tree as
+// copied (static), and a few words.
+template <int D, int NST>
+constexpr bool q_beside_ring(int R) {
+  return (size_t)NST * Rows<D>::SLOT + (size_t)R * D * 2 + 4 * kMaxNodes * 8 + 64 <= 160 * 1024;
+}
+template <int D, int NST>
+constexpr size_t dynamic_lds(int R) {
+  return (size_t)NST * Rows<D>::SLOT + (q_beside_ring<D, NST>(R) ? (size_t)R * D * 2 : 0);
 }
 
 template <int D, int RB, int KW, int W, int NST, bool PIPE, bool ENT>
@@ -241,8 +225,11 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   using L = Rows<D>;
   constexpr int C16 = L::C16;         // wave-wide copies per 16 rows
   constexpr int NSS = NST / KW;       // ring slots in super-steps (KW consecutive steps, one per key group)
-  constexpr int QSLOTS = (R * L::ROW + L::SLOT - 1) / L::SLOT;   // step slots the query rows occupy
-  constexpr int QSS = (QSLOTS + KW - 1) / KW;                      // ... in super-steps
+  // The query rows get an LDS region of their own beside the ring where it fits (so the first copies fill the
+  // whole ring); otherwise they occupy the ring's last step slots until the prologue has read them.
+  constexpr bool QSEP = q_beside_ring<D, NST>(R);
+  constexpr int QSLOTS = QSEP ? 0 : (R * L::ROW + L::SLOT - 1) / L::SLOT;   // step slots the query rows occupy
+  constexpr int QSS = (QSLOTS + KW - 1) / KW;                                // ... in super-steps
   constexpr int CPS = 4 * KW * C16 / W;   // copies per wave per super-step (4*KW blocks of 16 rows)
   constexpr int QB = R / 16;          // 16-row blocks of query rows, dealt to the waves round-robin
   static_assert(W % KW == 0 && (NST & (NST - 1)) == 0 && NSS > QSS && NSS >= 2, "ring layout");
@@ -251,7 +238,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   static_assert(NSS * CPS + ((QB + W - 1) / W) * C16 + 8 <= 63, "outstanding copies fit the counter");
   static_assert((size_t)(KW - 1) * R * D * 4 + (size_t)KW * R * 12 <= (size_t)NST * L::SLOT, "group states fit the ring");
 
-  extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots
+  extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // NST step slots (+ the query rows)
   __shared__ uint64_t anc_lds[2 * kMaxNodes];
   __shared__ uint64_t meta_lds[2 * kMaxNodes];   // the sequence's parents or tree mask rows, as copied
   __shared__ uint32_t merge_lds;                  // slices of the set's rows this workgroup merges
@@ -328,7 +315,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 
   // ---- first copies: the query rows (into the last step slots), the tree (wave 0), then the ring
   const size_t qrow0 = ((size_t)b * a.Hq + (size_t)g * a.G) * T;   // row 0 of this KV head's query rows
-  const unsigned char* qslab = ring + (NST - QSLOTS) * L::SLOT;
+  const unsigned char* qslab = QSEP ? ring + NST * L::SLOT : ring + (NST - QSLOTS) * L::SLOT;
 #pragma unroll
   for (int qb = wave; qb < QB; qb += W) {
 #pragma unroll
@@ -604,18 +591,19 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     }
     auto half_step = [&](int js, const Ops& cur, Ops& nxt) {
       const bool more = js + 1 < nsa;
+      // Every wave has computed super-step js-1, and its reads of super-step js (issued before that) have
+      // returned: the slots of super-step js take the copies of super-step js+NSS at once, without waiting for
+      // super-step js+1 to land.
+      barrier_lds();
+      if (js + NSS < nsa) issue_super(js + NSS);
       if (more) {
-        wait_vm_steps<CPS, NSS - 2>(issued_by(js) - 2 - js);   // ... and of super-step js+1
+        wait_vm_steps<CPS, NSS - 1>(issued_by(js + 1) - 2 - js);   // this wave's copies of super-step js+1
         zero_tail(js + 1);
       }
-      // super-step js+1 complete in LDS for every wave; every wave's reads of super-step js have returned,
-      // so its slots take the copies of super-step js+NSS.  (Also taken after the last super-step, so that
-      // on every path the operands of super-step js are known to have landed in registers.)
+      // super-step js+1 complete in LDS for every wave.  (Also taken after the last super-step, so that on
+      // every path the operands of super-step js are known to have landed in registers.)
       barrier_lds();
-      if (more) {
-        if (js + NSS < nsa) issue_super(js + NSS);
-        if ((js + 1) * KW + kw < nact) read_ops(nxt, js + 1);
-      }
+      if (more && (js + 1) * KW + kw < nact) read_ops(nxt, js + 1);
       __builtin_amdgcn_sched_barrier(0);
       if (js * KW + kw < nact) compute(cur, js * KW + kw);
     };
@@ -837,8 +825,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     if (!((slices >> k) & 1u)) continue;
     const int r0 = k * R / S, r1 = (k + 1) * R / S;
     merge_pieces<D, W, ENT>(a, prow0, R, (__bf16*)a.out + orow0 * D, a.lse ? a.lse + orow0 : nullptr,
-                            ENT ? a.entropy + orow0 : nullptr, rows_valid, r0, r1 - r0, split, row_lds, ml_lds,
-                            e_lds, good_lds == 1u);
+                            ENT ? a.entropy + orow0 : nullptr, rows_valid, r0, r1 - r0, good_lds == 1u);
   }
   if (tid == 0) {
     const unsigned long long d = __hip_atomic_fetch_add(ctr + 1, 1ull << 8, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -851,7 +838,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
 
 template <int D, int RB, int KW, int W, int NST, bool ENT>
 hipError_t launch_streaming(const AttnArgs& a, hipStream_t stream) {
-  constexpr size_t lds = (size_t)NST * Rows<D>::SLOT;
+  constexpr size_t lds = dynamic_lds<D, NST>(16 * RB * (W / KW));
   static_assert(lds + 2 * kMaxNodes * 8 + 2 * kMaxNodes * 8 + 64 <= 160 * 1024, "LDS budget");
   // two sets of operand registers fit beside one 16-row block's state, not beside two
   auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST, RB == 1, ENT>;
