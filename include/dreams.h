@@ -255,6 +255,58 @@ dreams_status_t dreams_visual_gather(int32_t batch, int32_t num_kv_heads, int32_
                                      int32_t vis_begin, const int32_t* keep, int32_t keep_count, void* k_out,
                                      void* v_out, hipStream_t stream);
 
+/*
+ * Prefill statistics: the same quantities over a prompt's own causal attention, which is where the paper reads
+ * them -- Eq. 2 (Section 3.1, "Visual Token Compression") scores visual tokens with the final layer's attention
+ * weights of the prefilling pass, and AE(l) (Section 3.2) averages the attention entropy of a layer's rows over
+ * the n prompt tokens.  Prompt b holds n_b = prompt_len[b] tokens (clamped to [0, num_rows]): queries in rows
+ * 0..n_b-1 of q [B, Hq, num_rows, D], keys in slots 0..n_b-1 of k_cache [B, Hkv, cache_capacity, D], both bf16,
+ * caller-owned device buffers; query head h reads KV head h / (Hq/Hkv).  Row i attends slots 0..i:
+ *   A[b,h,i,j] = exp(scale * q_i . k_j - lse[b,h,i]),  lse[b,h,i] = log sum_{j <= i} exp(scale * q_i . k_j).
+ * Arithmetic: bf16 products, fp32 sums.  head_dim 64 or 128 (DREAMS_ERR_UNSUPPORTED otherwise).
+ */
+typedef struct {
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t num_rows;        /* N: rows per head of q, the longest prompt */
+  int32_t cache_capacity;  /* slots per (sequence, KV head) of k_cache, >= num_rows */
+  float scale;
+} dreams_prefill_desc_t;
+
+/*
+ * dreams_prefill_attn_stats -- lse[b,h,i] (natural log) and entropy[b,h,i] = -sum_{j<=i} A log A (nats) of every
+ * prompt row; rows i >= n_b get lse = -inf and entropy 0.  lse and entropy: device [B, Hq, num_rows] float,
+ * either may be NULL.  Nothing is allocated; no workspace.
+ */
+dreams_status_t dreams_prefill_attn_stats(const dreams_prefill_desc_t* desc, const void* q, const void* k_cache,
+                                          const int32_t* prompt_len, float* lse, float* entropy,
+                                          hipStream_t stream);
+
+/*
+ * dreams_prefill_attn_entropy_mean -- AE of one layer over prompts (Section 3.2): the sum of entropy
+ * [B, Hq, num_rows] (as dreams_prefill_attn_stats wrote it: 0 past each prompt) over Hq * sum_b n_b rows, summed
+ * in fp64 in a fixed order; 0 when no prompt has a row.  ae: device, one float (out).
+ */
+dreams_status_t dreams_prefill_attn_entropy_mean(int32_t batch, int32_t num_q_heads, int32_t num_rows,
+                                                 const float* entropy, const int32_t* prompt_len, float* ae,
+                                                 hipStream_t stream);
+
+/*
+ * dreams_prefill_visual_importance -- Eq. 2 over the prompt: for visual token j (slot vis_begin + j),
+ *   importance[b,j] = (1 / (Hq * n_b)) * sum_h sum_{i < n_b} A[b,h,i,vis_begin+j]
+ * (a slot past row i gets nothing from it; a slot at or past n_b has importance 0; n_b = 0 gives 0).  lse: the
+ * [B, Hq, num_rows] output of dreams_prefill_attn_stats on the same inputs.  Requires vis_begin >= 0,
+ * vis_count >= 1, vis_begin + vis_count <= num_rows.  workspace: as for dreams_visual_importance (size from
+ * dreams_visual_importance_workspace_size(batch, num_kv_heads, vis_count); its counter region zero, and left
+ * zero).  importance: device [B, vis_count] float (out).  The heads are summed in head order (reproducible).
+ */
+dreams_status_t dreams_prefill_visual_importance(const dreams_prefill_desc_t* desc, const void* q, const void* k_cache,
+                                                 const int32_t* prompt_len, const float* lse, int32_t vis_begin,
+                                                 int32_t vis_count, float* importance, void* workspace,
+                                                 size_t workspace_bytes, hipStream_t stream);
+
 /* Bytes of workspace dreams_tree_accept needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if batch
  * exceeds (DREAMS_WORKSPACE_COUNTER_BYTES - 128) / 4 (one arrival counter per sequence, plus up to 8 group counters
  * per sequence while batch * 9 counters fit).  After the counters: one (value, index) pair per piece of each

@@ -774,6 +774,117 @@ dreams_status_t dreams_visual_importance(const dreams_attn_desc_t* desc, const v
   return ok();
 }
 
+// ------------------------------------------------------------------------------ prefill attention statistics
+namespace {
+dreams_status_t check_prefill_desc(const dreams_prefill_desc_t* d) {
+  if (!d) return fail(DREAMS_ERR_INVALID_ARG, "desc is NULL");
+  if (d->batch < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", d->batch);
+  if (d->num_q_heads < 1 || d->num_kv_heads < 1 || d->num_q_heads % d->num_kv_heads != 0)
+    return fail(DREAMS_ERR_INVALID_ARG, "num_q_heads = %d must be a positive multiple of num_kv_heads = %d",
+                d->num_q_heads, d->num_kv_heads);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(DREAMS_ERR_UNSUPPORTED, "head_dim = %d (supported: 64, 128)", d->head_dim);
+  if (d->num_rows < 1 || d->cache_capacity < d->num_rows)
+    return fail(DREAMS_ERR_INVALID_ARG, "num_rows = %d must be in [1, cache_capacity = %d]", d->num_rows,
+                d->cache_capacity);
+  if (!isfinite(d->scale)) return fail(DREAMS_ERR_INVALID_ARG, "scale is not finite");
+  if ((long long)d->batch * d->num_q_heads * ((d->num_rows + 255) / 256) > 0x7fffffffLL)
+    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  return DREAMS_OK;
+}
+}  // namespace
+
+dreams_status_t dreams_prefill_attn_stats(const dreams_prefill_desc_t* desc, const void* q, const void* k_cache,
+                                          const int32_t* prompt_len, float* lse, float* entropy, hipStream_t stream) {
+  dreams_status_t st = check_prefill_desc(desc);
+  if (st != DREAMS_OK) return st;
+  if (desc->batch == 0 || (!lse && !entropy)) return ok();
+  if (!q || !k_cache || !prompt_len) return fail(DREAMS_ERR_INVALID_ARG, "q, k_cache and prompt_len must not be NULL");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(prompt_len, 4) || !aligned(lse, 4) || !aligned(entropy, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "q and k_cache must be 16-byte aligned, prompt_len, lse and entropy 4-byte");
+  PrefillArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.prompt_len = prompt_len;
+  a.lse = lse;
+  a.entropy = entropy;
+  a.B = desc->batch;
+  a.Hq = desc->num_q_heads;
+  a.Hkv = desc->num_kv_heads;
+  a.G = desc->num_q_heads / desc->num_kv_heads;
+  a.N = desc->num_rows;
+  a.D = desc->head_dim;
+  a.S_cap = desc->cache_capacity;
+  a.scale_log2 = desc->scale * 1.4426950408889634f;
+  hipError_t e = launch_prefill_stats(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "prefill statistics launch");
+  return ok();
+}
+
+dreams_status_t dreams_prefill_attn_entropy_mean(int32_t batch, int32_t num_q_heads, int32_t num_rows,
+                                                 const float* entropy, const int32_t* prompt_len, float* ae,
+                                                 hipStream_t stream) {
+  if (batch < 1 || num_q_heads < 1 || num_rows < 1)
+    return fail(DREAMS_ERR_INVALID_ARG, "batch = %d, num_q_heads = %d and num_rows = %d must be >= 1", batch,
+                num_q_heads, num_rows);
+  if (!entropy || !prompt_len || !ae) return fail(DREAMS_ERR_INVALID_ARG, "entropy, prompt_len and ae must not be NULL");
+  if (!aligned(entropy, 4) || !aligned(prompt_len, 4) || !aligned(ae, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "entropy, prompt_len or ae is misaligned");
+  hipError_t e = launch_prefill_entropy_mean(batch, num_q_heads, num_rows, entropy, prompt_len, ae, stream);
+  if (e != hipSuccess) return hip_fail(e, "prefill entropy mean launch");
+  return ok();
+}
+
+dreams_status_t dreams_prefill_visual_importance(const dreams_prefill_desc_t* desc, const void* q, const void* k_cache,
+                                                 const int32_t* prompt_len, const float* lse, int32_t vis_begin,
+                                                 int32_t vis_count, float* importance, void* workspace,
+                                                 size_t workspace_bytes, hipStream_t stream) {
+  dreams_status_t st = check_prefill_desc(desc);
+  if (st != DREAMS_OK) return st;
+  if (vis_begin < 0 || vis_count < 1 || (long long)vis_begin + vis_count > desc->num_rows)
+    return fail(DREAMS_ERR_INVALID_ARG, "visual tokens [%d, %d + %d) are not inside the prompt (%d rows)", vis_begin,
+                vis_begin, vis_count, desc->num_rows);
+  const size_t need = visual_workspace_bytes(desc->batch, desc->num_kv_heads, vis_count);
+  if (desc->batch == 0) return ok();
+  if (!q || !k_cache || !prompt_len || !lse || !importance)
+    return fail(DREAMS_ERR_INVALID_ARG, "q, k_cache, prompt_len, lse and importance must not be NULL");
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(prompt_len, 4) || !aligned(lse, 4) || !aligned(importance, 4))
+    return fail(DREAMS_ERR_INVALID_ARG, "q and k_cache must be 16-byte aligned, prompt_len, lse and importance 4-byte");
+  if (!workspace) return fail(DREAMS_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+  if (workspace_bytes < need)
+    return fail(DREAMS_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed", workspace_bytes, need);
+  if (!aligned(workspace, 256)) return fail(DREAMS_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if ((long long)desc->batch * desc->num_kv_heads * ((vis_count + 63) / 64) > 0x7fffffffLL)
+    return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  const int stride = visual_counter_stride(desc->batch, vis_count);
+  if (stride == 0)
+    return fail(DREAMS_ERR_UNSUPPORTED, "batch * ceil(vis_count / 256) = %lld exceeds %zu arrival counters",
+                (long long)desc->batch * ((vis_count + 255) / 256), kMaxCounters);
+  VisualArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.kv_len = prompt_len;
+  a.lse = lse;
+  a.prefill = 1;
+  a.counters = (uint32_t*)workspace;
+  a.counter_stride = stride;
+  a.partial = (float*)((char*)workspace + kCounterBytes);
+  a.importance = importance;
+  a.B = desc->batch;
+  a.Hq = desc->num_q_heads;
+  a.Hkv = desc->num_kv_heads;
+  a.G = desc->num_q_heads / desc->num_kv_heads;
+  a.T = desc->num_rows;
+  a.D = desc->head_dim;
+  a.S_cap = desc->cache_capacity;
+  a.vis_begin = vis_begin;
+  a.vis_count = vis_count;
+  a.scale_log2 = desc->scale * 1.4426950408889634f;
+  hipError_t e = launch_visual_importance(a, stream);
+  if (e != hipSuccess) return hip_fail(e, "prefill visual importance launch");
+  return ok();
+}
+
 dreams_status_t dreams_visual_topk(int32_t batch, int32_t vis_count, int32_t keep_count, const float* importance,
                                    int32_t* keep, hipStream_t stream) {
   if (batch < 0) return fail(DREAMS_ERR_INVALID_ARG, "batch = %d < 0", batch);

@@ -108,8 +108,11 @@ constexpr int kVisualMaxTokens = 8192;   // visual tokens per sequence the top-r
 struct VisualArgs {
   const void* q;          // [B, Hq, T, D] bf16
   const void* k;          // [B, Hkv, S_cap, D] bf16
-  const int32_t* kv_len;  // [B]
+  const int32_t* kv_len;  // [B] (verification rows: the prefix; prefill rows: the prompt length)
   const float* lse;       // [B, Hq, T] natural log-sum-exp of every row (from the attention call)
+  // 0: the rows are a verification call's tree rows (every row sees the whole prefix); 1: the rows are a
+  // prompt's own positions (T = the rows per head, row i sees slots 0..i, rows i >= kv_len[b] do not count)
+  int prefill;
   float* partial;         // [B, Hkv, vis_count] workspace
   uint32_t* counters;     // [B, ceil(vis_count / 256)] arrival counters, counter_stride words apart (zero)
   int counter_stride;
@@ -128,6 +131,20 @@ struct VisualGatherArgs {
   int row_bytes;          // D * element size, a multiple of 16
 };
 hipError_t launch_visual_importance(const VisualArgs& a, hipStream_t stream);
+
+// ---------------------------------------------------------------------------- prefill attention statistics
+struct PrefillArgs {
+  const void* q;               // [B, Hq, N, D] bf16: the prompt's queries
+  const void* k;               // [B, Hkv, S_cap, D] bf16: the prompt's keys in slots 0..N-1
+  const int32_t* prompt_len;   // [B] n_b (clamped to [0, N])
+  float* lse;                  // [B, Hq, N] or nullptr
+  float* entropy;              // [B, Hq, N] or nullptr
+  int B, Hq, Hkv, G, N, D, S_cap;
+  float scale_log2;            // scale * log2(e)
+};
+hipError_t launch_prefill_stats(const PrefillArgs& a, hipStream_t stream);
+hipError_t launch_prefill_entropy_mean(int B, int Hq, int N, const float* entropy, const int32_t* prompt_len, float* ae,
+                                       hipStream_t stream);
 hipError_t launch_visual_topk(int B, int n, int r, const float* importance, int32_t* keep, hipStream_t stream);
 hipError_t launch_visual_gather(const VisualGatherArgs& a, hipStream_t stream);
 

@@ -11,6 +11,8 @@
 //     are read once and each workgroup reads one head's queries.
 //     The last KV head to finish a block of tokens (an arrival counter per (sequence, block)) forms
 //     I_j = (sum over KV heads, in order) / (Hq*T).
+//     With a prompt's own rows (the prefilling pass, which is where Eq. 2 reads the target's attention), row i of
+//     every query head sees slots 0..i, only rows i < n_b count, and I_j is the same sum over (Hq*n_b).
 //   * visual_topk_kernel: one workgroup per sequence: radix selection of the r-th largest importance over
 //     order-preserving integer keys in LDS, then the kept tokens in token order by prefix sums (ties between
 //     equal importances go to the smaller token).
@@ -43,7 +45,8 @@ __global__ __launch_bounds__(256) void visual_importance_kernel(VisualArgs a) {
   const int col = lane & 15, quad = lane >> 4;
   const int T = a.T, rows = a.G * T;
   int L = a.kv_len[b];
-  L = L < 0 ? 0 : (L > a.S_cap - T ? a.S_cap - T : L);
+  if (a.prefill) L = L < 0 ? 0 : (L > T ? T : L);   // the prompt's length
+  else L = L < 0 ? 0 : (L > a.S_cap - T ? a.S_cap - T : L);
 
   // the wave's tokens j0 .. j0 + 16*KB - 1: key rows as A operands (row col of each 16-token block); the
   // outputs of block kb are tokens j0 + 16*kb + 4*quad + e
@@ -70,7 +73,38 @@ __global__ __launch_bounds__(256) void visual_importance_kernel(VisualArgs a) {
   for (int kb = 0; kb < KB; ++kb) acc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
   // 64 query rows at a time: all of their loads are issued together (one memory round trip per 64 rows)
   constexpr int QC = 4;
-  for (int r0 = 0; r0 < rows; r0 += 16 * QC) {
+  if (a.prefill) {
+    // A prompt's own rows: row i of each of the G heads sees slots 0..i, and only rows i < L count.  Rows below
+    // the wave's first token see none of its tokens, so each head's walk starts there.
+    const int istart = max(0, a.vis_begin + j0) & ~15;
+    for (int hh = 0; hh < a.G; ++hh)
+      for (int i0 = istart; i0 < L; i0 += 16 * QC) {
+        bf16x8 qf[QC][DS];
+        float lse[QC];
+#pragma unroll
+        for (int c = 0; c < QC; ++c) load_q(qf[c], lse[c], hh * T + i0 + 16 * c);   // (a lane past its head's rows is dead: i >= L)
+#pragma unroll
+        for (int c = 0; c < QC; ++c) {
+          const int i = i0 + 16 * c + col;
+          const bool live = i < L && lse[c] != -INFINITY;
+          const float lse2 = live ? lse[c] * 1.4426950408889634f : 0.f;
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) {
+            f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ds = 0; ds < DS; ++ds) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][ds], qf[c][ds], s, 0, 0, 0);
+            if (live) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int slot = a.vis_begin + j0 + kb * 16 + quad * 4 + e;
+                if (slot <= i) acc[kb][e] += __builtin_amdgcn_exp2f(fmaf(s[e], a.scale_log2, -lse2));
+              }
+            }
+          }
+        }
+      }
+  }
+  for (int r0 = 0; r0 < (a.prefill ? 0 : rows); r0 += 16 * QC) {
     bf16x8 qf[QC][DS];
     float lse[QC];
 #pragma unroll
@@ -133,7 +167,8 @@ __global__ __launch_bounds__(256) void visual_importance_kernel(VisualArgs a) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) sum += x[k];
   }
-  a.importance[(size_t)b * a.vis_count + j] = sum / ((float)a.Hq * (float)T);
+  const float rows_counted = a.prefill ? (float)L : (float)T;   // rows per head that count
+  a.importance[(size_t)b * a.vis_count + j] = rows_counted > 0.f ? sum / ((float)a.Hq * rows_counted) : 0.f;
 }
 
 // Order-preserving key of an fp32 value: larger value <=> larger key; -0.0 is taken as +0.0 (they compare

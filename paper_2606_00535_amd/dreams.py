@@ -29,7 +29,8 @@ EXPORTS = (
     "dreams_visual_topk", "dreams_visual_gather", "dreams_tree_accept_sampled_workspace_size",
     "dreams_tree_accept_sampled", "dreams_tree_accept_lm_head_workspace_size", "dreams_tree_accept_lm_head",
     "dreams_workspace_status", "dreams_tree_verify_attn_splits", "dreams_tree_verify_attn_noalloc",
-    "dreams_set_wait_limit",
+    "dreams_set_wait_limit", "dreams_prefill_attn_stats", "dreams_prefill_attn_entropy_mean",
+    "dreams_prefill_visual_importance",
 )
 
 
@@ -43,6 +44,12 @@ class AttnDesc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("num_nodes", ctypes.c_int32), ("cache_capacity", ctypes.c_int32),
                 ("max_kv_len", ctypes.c_int32), ("num_splits", ctypes.c_int32), ("dtype", ctypes.c_int),
+                ("scale", ctypes.c_float)]
+
+
+class PrefillDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("num_rows", ctypes.c_int32), ("cache_capacity", ctypes.c_int32),
                 ("scale", ctypes.c_float)]
 
 
@@ -93,13 +100,18 @@ def lib():
                 L.dreams_set_wait_limit.argtypes = [ctypes.c_double]
                 L.dreams_tree_verify_attn_noalloc.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, P, P, P, P, P]
                 L.dreams_tree_verify_attn_splits.argtypes = [ctypes.POINTER(AttnDesc), ctypes.POINTER(I32)]
+                L.dreams_prefill_attn_stats.argtypes = [ctypes.POINTER(PrefillDesc), P, P, P, P, P, P]
+                L.dreams_prefill_attn_entropy_mean.argtypes = [I32, I32, I32, P, P, P, P]
+                L.dreams_prefill_visual_importance.argtypes = [ctypes.POINTER(PrefillDesc), P, P, P, P, I32, I32, P, P,
+                                                               SZ, P]
                 for f in ("dreams_tree_verify_attn_workspace_size", "dreams_tree_verify_attn",
                           "dreams_tree_accept_workspace_size", "dreams_tree_accept", "dreams_kv_commit",
                           "dreams_check_tree_host", "dreams_stream_read", "dreams_tree_verify_attn_entropy",
                           "dreams_attn_entropy_mean", "dreams_attn_entropy_select",
                           "dreams_visual_importance_workspace_size", "dreams_visual_importance", "dreams_visual_topk",
                           "dreams_visual_gather", "dreams_workspace_status", "dreams_tree_verify_attn_splits",
-                          "dreams_tree_verify_attn_noalloc", "dreams_set_wait_limit"):
+                          "dreams_tree_verify_attn_noalloc", "dreams_set_wait_limit", "dreams_prefill_attn_stats",
+                          "dreams_prefill_attn_entropy_mean", "dreams_prefill_visual_importance"):
                     getattr(L, f).restype = ctypes.c_int
                 _lib = L
     return _lib
@@ -278,6 +290,77 @@ def visual_importance(q: torch.Tensor, k_cache: torch.Tensor, kv_len: torch.Tens
                                           vis_begin, vis_count, _ptr(importance), _ptr(workspace),
                                           0 if workspace is None else workspace.numel() * workspace.element_size(),
                                           st))
+    return importance
+
+
+def prefill_desc(q: torch.Tensor, k_cache: torch.Tensor, scale: Optional[float] = None) -> PrefillDesc:
+    B, Hq, N, D = q.shape
+    return PrefillDesc(B, Hq, k_cache.shape[1], D, N, k_cache.shape[2],
+                       float(1.0 / math.sqrt(D) if scale is None else scale))
+
+
+def prefill_attn_stats(q: torch.Tensor, k_cache: torch.Tensor, prompt_len: torch.Tensor, scale: Optional[float] = None,
+                       lse: Optional[torch.Tensor] = None, entropy: Optional[torch.Tensor] = None,
+                       with_lse: bool = True, with_entropy: bool = True, stream=None):
+    """dreams_prefill_attn_stats: the causal attention of a prompt's own rows (row i sees slots 0..i).  q
+    [B,Hq,N,D] and k_cache [B,Hkv,S_cap,D] bf16, prompt_len [B] int32.  Returns (lse, entropy), each [B,Hq,N]
+    float32 or None."""
+    dev = q.device
+    _need(q, "q", torch.bfloat16, dev, 4)
+    _need(k_cache, "k_cache", torch.bfloat16, dev, 4)
+    _need(prompt_len, "prompt_len", torch.int32, dev, 1)
+    B, Hq, N, D = q.shape
+    if with_lse and lse is None:
+        lse = torch.empty((B, Hq, N), dtype=torch.float32, device=dev)
+    if with_entropy and entropy is None:
+        entropy = torch.empty((B, Hq, N), dtype=torch.float32, device=dev)
+    for t, nm in ((lse, "lse"), (entropy, "entropy")):
+        if t is not None:
+            _need(t, nm, torch.float32, dev, 3)
+    desc = prefill_desc(q, k_cache, scale)
+    _check(lib().dreams_prefill_attn_stats(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(prompt_len), _ptr(lse),
+                                           _ptr(entropy), _stream(stream)))
+    return lse, entropy
+
+
+def prefill_attn_entropy_mean(entropy: torch.Tensor, prompt_len: torch.Tensor, ae: Optional[torch.Tensor] = None,
+                              stream=None) -> torch.Tensor:
+    """dreams_prefill_attn_entropy_mean: AE of one layer over prompts from entropy [B,Hq,N].  Returns [1] float32."""
+    _need(entropy, "entropy", torch.float32, entropy.device, 3)
+    _need(prompt_len, "prompt_len", torch.int32, entropy.device, 1)
+    if ae is None:
+        ae = torch.empty(1, dtype=torch.float32, device=entropy.device)
+    B, Hq, N = entropy.shape
+    _check(lib().dreams_prefill_attn_entropy_mean(B, Hq, N, _ptr(entropy), _ptr(prompt_len), _ptr(ae),
+                                                  _stream(stream)))
+    return ae
+
+
+def prefill_visual_importance(q: torch.Tensor, k_cache: torch.Tensor, prompt_len: torch.Tensor, lse: torch.Tensor,
+                              vis_begin: int, vis_count: int, scale: Optional[float] = None,
+                              importance: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                              stream=None) -> torch.Tensor:
+    """dreams_prefill_visual_importance (Eq. 2 over the prompt's causal attention): lse [B,Hq,N] from
+    prefill_attn_stats.  Returns importance [B, vis_count] float32."""
+    dev = q.device
+    _need(q, "q", torch.bfloat16, dev, 4)
+    _need(k_cache, "k_cache", torch.bfloat16, dev, 4)
+    _need(prompt_len, "prompt_len", torch.int32, dev, 1)
+    _need(lse, "lse", torch.float32, dev, 3)
+    B = q.shape[0]
+    if importance is None:
+        importance = torch.empty((B, vis_count), dtype=torch.float32, device=dev)
+    else:
+        _need(importance, "importance", torch.float32, dev)
+    nbytes = visual_importance_workspace_size(B, k_cache.shape[1], vis_count)
+    st = _stream(stream)
+    if workspace is None:
+        workspace = _workspace("visual", nbytes, dev, st)
+    desc = prefill_desc(q, k_cache, scale)
+    _check(lib().dreams_prefill_visual_importance(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(prompt_len),
+                                                  _ptr(lse), vis_begin, vis_count, _ptr(importance), _ptr(workspace),
+                                                  0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                                  st))
     return importance
 
 

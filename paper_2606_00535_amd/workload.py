@@ -31,6 +31,7 @@ _T_TOPOLOGY, _T_AGREE, _T_LEN, _T_LOGITS, _T_TOKENS = 0, 1, 2, 3, 4
 _T_Q, _T_KPRE, _T_VPRE, _T_KTREE, _T_VTREE = 10, 11, 12, 13, 14
 _T_VARIANT = 20
 _T_DRAFT, _T_DRAFT_TOKENS, _T_UNIFORMS = 30, 31, 32
+_T_PROMPT_Q, _T_PROMPT_K = 40, 41
 
 
 @dataclass(frozen=True)
@@ -347,3 +348,38 @@ def make_sampled(wl: Workload, *, temperature: float = 1.0, draft_noise: float =
             tokens[b, i] = int(np.argmax(dl[b, parent[b, i]] / np.float32(temperature) + g))
         uniforms[b] = rng_for(wl.seed, 0, b, _T_UNIFORMS).random(T, dtype=np.float32)
     return SampledInputs(tl, dl, tokens, parent, uniforms, float(temperature))
+
+
+# ------------------------------------------------------------------------------------------- prompt (prefill)
+@dataclasses.dataclass
+class Prompt:
+    """A prefilling pass's query and key rows: q [B, Hq, N, D] and k_cache [B, Hkv, S_cap, D] (bf16 bits), the
+    prompt of sequence b in rows / slots 0..prompt_len[b]-1 (the rest of q is drawn too, the rest of the cache
+    is zero), and the visual-token window [vis_begin, vis_begin + vis_count) inside it."""
+    q: np.ndarray
+    k_cache: np.ndarray
+    prompt_len: np.ndarray
+    vis_begin: int
+    vis_count: int
+    num_kv_heads: int
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / float(np.sqrt(self.q.shape[3]))
+
+
+def make_prompt(batch: int, num_q_heads: int, num_kv_heads: int, head_dim: int, prompt_lens: Sequence[int],
+                vis_begin: int, vis_count: int, *, num_rows: Optional[int] = None, cache_capacity: Optional[int] = None,
+                q_std: float = 1.0, seed: int = 0) -> Prompt:
+    """Seeded N(0, q_std^2) queries and N(0, 1) keys of every prompt position, rounded to bf16, one stream per
+    (sequence, tensor).  num_rows defaults to the longest prompt, cache_capacity to num_rows rounded up to 64."""
+    lens = np.asarray(prompt_lens, dtype=np.int32)
+    N = int(num_rows if num_rows is not None else max(1, int(lens.max(initial=1))))
+    S = int(cache_capacity if cache_capacity is not None else (N + 63) // 64 * 64)
+    q = np.empty((batch, num_q_heads, N, head_dim), dtype=np.uint16)
+    k = np.zeros((batch, num_kv_heads, S, head_dim), dtype=np.uint16)
+    for b in range(batch):
+        q[b] = _draw(rng_for(seed, 0, b, _T_PROMPT_Q), (num_q_heads, N, head_dim), q_std, "bf16")
+        n = int(min(max(lens[b], 0), N))
+        k[b, :, :n] = _draw(rng_for(seed, 0, b, _T_PROMPT_K), (num_kv_heads, n, head_dim), 1.0, "bf16")
+    return Prompt(q, k, lens, int(vis_begin), int(vis_count), int(num_kv_heads))

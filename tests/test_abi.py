@@ -212,6 +212,45 @@ def test_entropy_entry_points_reject_bad_arguments(D):
     assert lib.dreams_attn_entropy_select(4, ctypes.c_void_p(0x100001), fake, None) == D.DREAMS_ERR_INVALID_ARG
 
 
+def test_prefill_entry_points_reject_bad_arguments(D):
+    lib = D.lib()
+    fake = ctypes.c_void_p(0x100000)
+    ok = dict(batch=2, num_q_heads=8, num_kv_heads=2, head_dim=128, num_rows=300, cache_capacity=320, scale=0.088)
+
+    def pdesc(**kw):
+        d = dict(ok)
+        d.update(kw)
+        return D.PrefillDesc(**d)
+
+    def stats(desc, q=fake, k=fake, pl=fake, lse=fake, ent=fake):
+        return lib.dreams_prefill_attn_stats(ctypes.byref(desc), q, k, pl, lse, ent, None)
+
+    assert lib.dreams_prefill_attn_stats(None, fake, fake, fake, fake, fake, None) == D.DREAMS_ERR_INVALID_ARG
+    assert stats(pdesc(num_q_heads=6, num_kv_heads=4)) == D.DREAMS_ERR_INVALID_ARG
+    assert stats(pdesc(head_dim=96)) == D.DREAMS_ERR_UNSUPPORTED
+    assert stats(pdesc(num_rows=0)) == D.DREAMS_ERR_INVALID_ARG
+    assert stats(pdesc(cache_capacity=299)) == D.DREAMS_ERR_INVALID_ARG
+    assert stats(pdesc(scale=float("inf"))) == D.DREAMS_ERR_INVALID_ARG
+    assert stats(pdesc(), q=None) == D.DREAMS_ERR_INVALID_ARG
+    assert stats(pdesc(), pl=ctypes.c_void_p(0x100002)) == D.DREAMS_ERR_INVALID_ARG
+    assert stats(pdesc(batch=0)) == D.DREAMS_OK                    # nothing to do, nothing launched
+    assert stats(pdesc(), lse=None, ent=None) == D.DREAMS_OK       # no output asked for
+    assert lib.dreams_prefill_attn_entropy_mean(0, 8, 300, fake, fake, fake, None) == D.DREAMS_ERR_INVALID_ARG
+    assert lib.dreams_prefill_attn_entropy_mean(2, 8, 300, fake, None, fake, None) == D.DREAMS_ERR_INVALID_ARG
+
+    def imp(desc, vb, vc, ws=fake, nbytes=1 << 24, lse=fake):
+        return lib.dreams_prefill_visual_importance(ctypes.byref(desc), fake, fake, fake, lse, vb, vc, fake, ws,
+                                                    nbytes, None)
+
+    assert imp(pdesc(), 0, 301) == D.DREAMS_ERR_INVALID_ARG      # past the prompt rows
+    assert imp(pdesc(), -1, 10) == D.DREAMS_ERR_INVALID_ARG
+    assert imp(pdesc(), 0, 0) == D.DREAMS_ERR_INVALID_ARG
+    assert imp(pdesc(), 0, 300, lse=None) == D.DREAMS_ERR_INVALID_ARG
+    assert imp(pdesc(), 0, 300, ws=None) == D.DREAMS_ERR_WORKSPACE
+    assert imp(pdesc(), 0, 300, nbytes=65536) == D.DREAMS_ERR_WORKSPACE
+    assert imp(pdesc(), 0, 300, ws=ctypes.c_void_p(0x100040)) == D.DREAMS_ERR_WORKSPACE
+
+
 def test_sampled_accept_rejections_and_sizes(D):
     lib = D.lib()
     n = ctypes.c_size_t(0)
