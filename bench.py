@@ -273,6 +273,57 @@ def measure_workload(torch, dev, name, args):
     return res
 
 
+def measure_prefill(torch, dev, args, N=3136, n_img=2880, H=32, D=128):
+    """The prefill statistics at the LLaVA-1.6-7B prompt shape (3136 tokens, the first 2880 visual, 32 heads of
+    128): causal lse and entropy of every row, the layer's AE over the prompt, Eq. 2 importance of the visual
+    tokens, and the top-r choice (one in five), each verb graph-replayed alone; TFLOP/s of the two matrix-core
+    passes against the dense bf16 peak.  Inputs: seeded N(0,1) bf16 q and k drawn on the device."""
+    from paper_2606_00535_amd import dreams
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    S = (N + 63) // 64 * 64
+    sets = []
+    for _ in range(2):
+        st = {"q": torch.randn((1, H, N, D), generator=gen, device=dev).to(torch.bfloat16),
+              "k": torch.randn((1, H, S, D), generator=gen, device=dev).to(torch.bfloat16),
+              "pl": torch.full((1,), N, dtype=torch.int32, device=dev)}
+        st["lse"] = torch.empty((1, H, N), dtype=torch.float32, device=dev)
+        st["ent"] = torch.empty((1, H, N), dtype=torch.float32, device=dev)
+        st["ae"] = torch.empty(1, dtype=torch.float32, device=dev)
+        st["imp"] = torch.empty((1, n_img), dtype=torch.float32, device=dev)
+        st["keep"] = torch.empty((1, n_img // 5), dtype=torch.int32, device=dev)
+        sets.append(st)
+    ws = torch.zeros(dreams.visual_importance_workspace_size(1, H, n_img), dtype=torch.uint8, device=dev)
+    verbs = {
+        "stats": lambda st: dreams.prefill_attn_stats(st["q"], st["k"], st["pl"], lse=st["lse"], entropy=st["ent"]),
+        "entropy_mean": lambda st: dreams.prefill_attn_entropy_mean(st["ent"], st["pl"], ae=st["ae"]),
+        "importance": lambda st: dreams.prefill_visual_importance(st["q"], st["k"], st["pl"], st["lse"], 0, n_img,
+                                                                  importance=st["imp"], workspace=ws),
+        "topk": lambda st: dreams.visual_topk(st["imp"], n_img // 5, keep=st["keep"]),
+    }
+    res = {"workload": "llava7b_prompt", "prompt_tokens": N, "image_tokens": n_img, "keep": n_img // 5,
+           "q_heads": H, "kv_heads": H, "head_dim": D, "dtype": "bf16"}
+    for name in ("stats", "entropy_mean", "importance", "topk"):
+        for st in sets:
+            verbs[name](st)
+        torch.cuda.synchronize()
+        g = capture(torch, lambda: [verbs[name](st) for st in sets])
+        us = replay_times_us(torch, g, len(sets), max(1, args.repeats))
+        res[name + "_us"] = dist(us)
+    # algorithmic flops: q.k over the visible keys of every row (stats), over every (row, visual key) pair with
+    # key <= row (importance)
+    stats_flops = 2.0 * D * H * (N * (N + 1) / 2)
+    imp_flops = 2.0 * D * H * sum(N - j for j in range(n_img))
+    for name, fl in (("stats", stats_flops), ("importance", imp_flops)):
+        t = res[name + "_us"]["p50"] * 1e-6
+        res[name + "_flops"] = fl
+        res[name + "_TFLOPs"] = round(fl / t / 1e12, 1)
+        res[name + "_frac_of_bf16_dense_peak"] = round(fl / t / 1e12 / BF16_DENSE_PEAK_TFLOPS, 4)
+    del sets, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -577,6 +628,7 @@ def main():
                           ("gqa_long", "gqa_long"), ("tiny", "tiny")):
             if name != args.workload:
                 extras[key] = measure_workload(torch, dev, name, args)
+        extras["prefill_select"] = measure_prefill(torch, dev, args)
 
     kv_len = host.kv_len
     a_bytes = attn_bytes_per_layer(wl, kv_len)
