@@ -77,9 +77,16 @@ def commit_bytes(wl, path, alen) -> int:
 
 
 def kernel_source_hash() -> str:
+    """sha256/16 of the attention kernel's source with comments and blank space removed (so that the hash
+    changes with the code, not with its comments)."""
+    import re
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(ROOT, "paper_2606_00535_amd", "csrc", "tree_attn_bf16.hip"))):
-        h.update(open(f, "rb").read())
+        src = open(f).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", "", src)
+        src = "\n".join(line.strip() for line in src.splitlines() if line.strip())
+        h.update(src.encode())
     return h.hexdigest()[:16]
 
 

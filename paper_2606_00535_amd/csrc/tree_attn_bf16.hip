@@ -5,32 +5,33 @@
 // prefix slots and the slots of node i's ancestors-or-self.
 //
 // Work decomposition
-//   * A workgroup of 4 waves owns R = 64*RB query rows of one KV head (the rows of the G query heads sharing
-//     it are packed: row r -> head r / T, node r % T, which is also their order in memory) and one piece of
-//     that head's key axis.  Wave w owns rows [16*RB*w, 16*RB*(w+1)) for every key of the piece, so there
-//     is no merge between waves, and every K/V byte the workgroup reads serves all of its rows.
+//   * A workgroup of W waves (4 or 8) owns R query rows of one KV head (the rows of the G query heads sharing it
+//     are packed: row r -> head r / T, node r % T, which is also their order in memory) and one piece of that
+//     head's key axis.  Each wave owns 16*RB rows of its key group (below) for every key the group takes, and
+//     every K/V byte the workgroup reads serves all of its rows.
 //   * K/V stream through a ring of NST step slots in LDS (a step = 32 keys: 32 K rows then 32 V rows).  The
-//     four waves each copy a quarter of every step straight from global memory into LDS
-//     (global_load_lds_dwordx4: no registers in between), NST-1 steps ahead, so up to NST-1 steps per
-//     compute unit are in flight.  One barrier per step hands a landed step to all waves and frees the slot
-//     of the previous step for the next copy.  The copies are issued with inline assembly and waited for by
-//     exact count; nothing else in the kernel loads through the vector memory path before the epilogue, so
-//     the compiler never inserts a wait that would drain the ring.
+//     waves copy their share of every step straight from global memory into LDS (global_load_lds_dwordx4: no
+//     registers in between), a whole ring ahead.  One barrier per super-step hands a landed step to all waves;
+//     in the pipelined loop a second one frees the slots every wave has read, which are refilled at once.  The
+//     copies are issued with inline assembly and waited for by exact count; nothing else in the kernel loads
+//     through the vector memory path before the epilogue, so the compiler never inserts a wait that would
+//     drain the ring.
 //   * Each lane fetches the source chunk that lands where an XOR-swizzled row layout wants it, which makes
 //     both operand reads below bank-conflict free:
 //       S^T = K Q^T        v_mfma_f32_16x16x32_bf16, K rows as the A operand (16-byte LDS reads)
 //       online softmax     per query row; each lane holds one row's scores, 4-way cross-lane reductions
 //       O^T += V^T P^T     A operand read with ds_read_b64_tr_b16 (a 4 x 16 transposing LDS read); the
 //                          probabilities are already in B-operand layout, so they never leave registers.
-//   * Waves are arranged as KW key groups of 4/KW waves: the groups take alternate steps (group k the steps
-//     k, k+KW, ...) and each wave owns 16*RB rows, so a wave's operand reads serve as many rows as possible;
-//     the groups' (max, sum, accumulator) states are merged through LDS at the end.
-//   * With several pieces per (sequence, KV head, row group) -- a set -- each workgroup stores its rows'
-//     output normalised by their softmax sum (bf16) and their (max, sum) to the workspace, then counts its
-//     arrival on the set's counter; the last piece of the set to arrive merges all of them, in piece order
-//     (so the result does not depend on which piece came last), in the same launch.  Nothing ever waits for
-//     another workgroup.  All pieces of a set run on one XCD (below), so their partial results stay in that
-//     XCD's L2: plain stores, non-temporal loads, no device-scope write-through and no second launch.
+//   * Waves are arranged as KW key groups of W/KW waves: the groups take alternate steps (group k the steps
+//     k, k+KW, ...), so a wave's operand reads serve as many rows as possible; the groups' (max, sum,
+//     accumulator) states are merged through LDS at the end.
+//   * With several pieces per (sequence, KV head, row group) -- a set -- each piece stores its rows' output
+//     normalised by their softmax sum (bf16) and their (max, sum) to the workspace and arrives on the set's
+//     counter.  A piece whose set has fully started waits for every arrival and merges its own slice of the
+//     rows; a piece that finds its set not yet fully started leaves its slice to the last arrival.  So a wait
+//     is only ever for a running piece.  The merge goes in piece order, so the result does not depend on which
+//     piece came last.  All pieces of a set run on one XCD (below), so their rows are exchanged through that
+//     XCD's L2: plain stores, no device-scope write-through, no second launch.
 //   * Workgroup ids are remapped so that all workgroups of one (sequence, KV head) run on the same XCD
 //     (consecutive ids are dealt round-robin over the 8 XCDs): row groups reading the same keys share them
 //     in that XCD's L2.
