@@ -151,7 +151,7 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
   const long long grid = 8LL * ((p->units + 7) / 8) * splits * p->row_groups;
   if (grid > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large: %lld workgroups", grid);
   if (splits > 1) {
-    // two 64-bit counter words per set (arrivals and leavers; started and done), on a 128-byte line of their own
+    // a 64-bit counter word per set (started, arrived, which arrived) and a free one, on a 128-byte line of their own
     // where there is room (atomics on one line serialise), then the pieces' partial results after the counter
     // region every workspace starts with
     int stride = 16;

@@ -81,8 +81,8 @@ struct AttnArgs {
   __bf16* part_o;         // [sets, splits, rows_per_wg, D]   accumulator / sum, rounded to bf16
   float* part_ml;         // [sets, splits, rows_per_wg, 2]   (max in log2 units, sum)
   float* part_e;          // [sets, splits, rows_per_wg]      entropy terms (with entropy only)
-  // Two 64-bit counter words of set s at set_ctr[s * ctr_stride]: arrivals, pieces that left their rows to the
-  // last arrival and an off-XCD mark; pieces started and pieces done with the counters.  Zero between calls.
+  // The 64-bit counter word of set s at set_ctr[s * ctr_stride]: pieces started, pieces arrived, a bit per
+  // arrived piece and an off-XCD mark (the next word is kept free).  Zero between calls.
   unsigned long long* set_ctr;
   int ctr_stride;         // 64-bit words between consecutive sets' counters (>= 2)
   uint32_t* err;          // the workspace's failure flags (splits > 1)

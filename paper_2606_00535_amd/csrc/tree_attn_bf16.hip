@@ -28,9 +28,9 @@
 //   * With several pieces per (sequence, KV head, row group) -- a set -- each piece stores its rows' output
 //     normalised by their softmax sum (bf16) and their (max, sum) to the workspace and arrives on the set's
 //     counter.  A piece whose set has fully started waits for every arrival and merges its own slice of the
-//     rows; a piece that finds its set not yet fully started leaves its slice to the last arrival.  So a wait
-//     is only ever for a running piece.  The merge goes in piece order, so the result does not depend on which
-//     piece came last.  All pieces of a set run on one XCD (below), so their rows are exchanged through that
+//     rows; a piece that finds its set not yet fully started leaves its slice to the piece that started last,
+//     which learnt at its start which pieces had already arrived.  So a wait is only ever for a running piece.
+//     The merge goes in piece order, so the result does not depend on which piece came last.  All pieces of a set run on one XCD (below), so their rows are exchanged through that
 //     XCD's L2: plain stores, no device-scope write-through, no second launch.
 //   * Workgroup ids are remapped so that all workgroups of one (sequence, KV head) run on the same XCD
 //     (consecutive ids are dealt round-robin over the 8 XCDs): row groups reading the same keys share them
@@ -341,10 +341,13 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   }
   const int fa = min(NSS - QSS, nsp);
   for (int j = 0; j < fa; ++j) issue_super(j);
-  // this piece has started (the merge at the end relies on knowing that every piece of the set runs)
+  // This piece has started (the merge at the end relies on knowing that every piece of the set runs).  The
+  // counter's value before this start is kept (thread 0) until the epilogue: the piece that starts last finds
+  // there the pieces that arrived before the whole set was running, whose rows it then merges.
+  unsigned long long start_old = 0;
   if (a.splits > 1 && tid == 0)
-    __hip_atomic_fetch_add(a.set_ctr + ((size_t)u * a.row_groups + rg) * a.ctr_stride + 1, 1ull, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+    start_old = __hip_atomic_fetch_add(a.set_ctr + ((size_t)u * a.row_groups + rg) * a.ctr_stride, 1ull,
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
   // ---- prologue: prefix length, ancestor sets, queries (all overlapping the copies above)
   int Lp = kv_len_b;
@@ -775,32 +778,35 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   }
   if (S == 1) return;
 
-  // ---- the set's merge, spread over its pieces.  Word 0 of the set's counters takes one arrival per piece
-  // (low byte), a bit per piece that leaves its rows to others (bits 8..39) and a bit for a piece that ran off
-  // the set's XCD (bit 63); word 1 counts the pieces that started (low byte) and that are done with the
-  // counters (second byte).  A piece whose set has started completely waits for every arrival and merges its
+  // ---- the set's merge, spread over its pieces.  One 64-bit counter word per set: pieces started (bits
+  // 0..7), pieces arrived (bits 8..15), a bit per arrived piece (16..47) and a bit for a piece that ran off the
+  // set's XCD (63).  A piece that arrives when its whole set has started waits for every arrival and merges its
   // own slice of the rows: every piece it waits for is running and arrives without waiting for anything.  A
-  // piece that finds a piece of its set not yet started leaves, and the last piece to arrive merges the slices
-  // of every piece that left (it waits for nothing).  So every wait ends, and each slice is merged once.  The
-  // pieces' rows are read from this XCD's L2 (all pieces of a set share blockIdx % 8, hence the XCD).  The last
-  // piece done with the counters clears both words for the next call.
+  // piece that arrives earlier leaves; the piece whose start completed the set saw it among the arrived bits
+  // then, and merges its slice too (that piece arrives after the set is complete, so it never leaves).  So
+  // every wait ends, and each slice is merged once.  The last arrival puts the word back to zero for the next
+  // call; a waiting piece takes either the full count or that zero as the end of its wait.  The pieces' rows
+  // are read from this XCD's L2 (all pieces of a set share blockIdx % 8, hence the XCD).
   unsigned long long* ctr = a.set_ctr + pset * a.ctr_stride;
   wait_vector_memory();   // this piece's rows have reached the L2
   __syncthreads();
   if (tid == 0) {
-    const bool coop = (__hip_atomic_load(ctr + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 0xffull) ==
-                      (unsigned long long)S;
     const bool off_xcd = xcd_id() != (uint32_t)xcd;
-    const unsigned long long old = __hip_atomic_fetch_add(
-        ctr, 1ull | (coop ? 0ull : 1ull << (8 + split)) | (off_xcd ? 1ull << 63 : 0ull), __ATOMIC_RELAXED,
-        __HIP_MEMORY_SCOPE_AGENT);
-    const bool last = (old & 0xffull) == (unsigned long long)(S - 1);
-    unsigned long long now = old + 1ull;
+    const unsigned long long old =
+        __hip_atomic_fetch_add(ctr, (1ull << 8) | (1ull << (16 + split)) | (off_xcd ? 1ull << 63 : 0ull),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool coop = (old & 0xffull) == (unsigned long long)S;
+    const bool last = ((old >> 8) & 0xffull) == (unsigned long long)(S - 1);
     bool good = true;
-    if (coop && !last) {
+    bool split_xcd = off_xcd || (old >> 63) != 0;
+    if (last) {
+      __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else if (coop) {
       const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-      while (((now = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffull) <
-             (unsigned long long)S) {
+      for (;;) {
+        const unsigned long long now = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (now >> 63) split_xcd = true;
+        if (((now >> 8) & 0xffull) == (unsigned long long)S || (now & 0xffffull) == 0ull) break;
         if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
           raise_device_error(a.err, kErrWaitTimeout);
           good = false;
@@ -809,13 +815,14 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
         __builtin_amdgcn_s_sleep(1);
       }
     }
-    if (now >> 63) {
+    if (split_xcd) {
       raise_device_error(a.err, kErrXcdSplit);
       good = false;
     }
-    // slices this workgroup merges: its own (cooperative), and the leavers' (last arrival)
+    // slices this workgroup merges: its own (when it waited), and those of the pieces that left before this
+    // piece's start completed the set
     uint32_t slices = coop ? 1u << split : 0u;
-    if (last) slices |= (uint32_t)((old >> 8) & 0xffffffffull) | (coop ? 0u : 1u << split);
+    if ((start_old & 0xffull) == (unsigned long long)(S - 1)) slices |= (uint32_t)((start_old >> 16) & 0xffffffffull);
     merge_lds = slices;
     good_lds = good ? 1u : 0u;
   }
@@ -827,13 +834,6 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     const int r0 = k * R / S, r1 = (k + 1) * R / S;
     merge_pieces<D, W, ENT>(a, prow0, R, (__bf16*)a.out + orow0 * D, a.lse ? a.lse + orow0 : nullptr,
                             ENT ? a.entropy + orow0 : nullptr, rows_valid, r0, r1 - r0, good_lds == 1u);
-  }
-  if (tid == 0) {
-    const unsigned long long d = __hip_atomic_fetch_add(ctr + 1, 1ull << 8, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (((d >> 8) & 0xffull) == (unsigned long long)(S - 1)) {
-      __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(ctr + 1, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
   }
 }
 
