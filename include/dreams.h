@@ -390,7 +390,7 @@ dreams_status_t dreams_tree_accept_sampled(int32_t batch, int32_t num_nodes, int
 
 /* Bytes of workspace dreams_tree_accept_lm_head needs (0 only when batch is 0): the 64 KiB counter region
  * (unused by this verb, kept so that one workspace serves every verb) and 8 bytes per row per tile of the
- * vocabulary (tiles of 64 entries while batch * num_nodes <= 64, else of 256).  DREAMS_ERR_UNSUPPORTED if
+ * vocabulary (tiles of 128 entries while batch * num_nodes <= 64, else of 256).  DREAMS_ERR_UNSUPPORTED if
  * hidden is not a multiple of 256. */
 dreams_status_t dreams_tree_accept_lm_head_workspace_size(int32_t batch, int32_t num_nodes, int32_t hidden,
                                                           int32_t vocab, size_t* bytes);

@@ -607,10 +607,11 @@ dreams_status_t plan_lm_head(int32_t B, int32_t T, int32_t H, int32_t V, LmPlan*
     return fail(DREAMS_ERR_UNSUPPORTED, "hidden = %d is not a multiple of %d", H, kLmHiddenMultiple);
   *p = LmPlan{};
   if (B == 0) return DREAMS_OK;
-  // one 64-row tile while the rows fit it (the weights stream once); beyond, 256 vocabulary entries by 128
+  // one 64-row tile while the rows fit it (the weights stream once, 128 vocabulary entries per workgroup); beyond,
+  // 256 vocabulary entries by 128
   // rows (up to 128 rows) or by 256 rows, so that every operand tile is re-read four to eight times less often
   const long long M = (long long)B * T;
-  const int tile = M <= kLmTile ? kLmTile : kLmTileBig;
+  const int tile = M <= kLmTile ? kLmTileSmall : kLmTileBig;
   const int rows = M <= kLmTile ? kLmTile : M <= kLmMidRows ? kLmMidRows : kLmBigRows;
   const long long ntiles = ((long long)V + tile - 1) / tile;
   if ((M + rows - 1) / rows * ntiles > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");

@@ -217,11 +217,12 @@ struct SampledArgs {
 hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream);
 
 // ------------------------------------------------------------------------------ LM head + argmax
-// A workgroup per (kLmTile vocabulary entries, kLmTile rows) of the logits hidden * weight^T, four waves
-// splitting the hidden axis; each row's best (value, index) per tile goes to part_val / part_idx, and a second
-// kernel (a workgroup per sequence) merges them and runs the greedy path scan.
+// A workgroup per (vocabulary tile, row tile) of the logits hidden * weight^T; each row's best (value, index)
+// per vocabulary tile goes to part_val / part_idx, and a second kernel (a workgroup per sequence) merges them
+// and runs the greedy path scan.
 constexpr int kLmThreads = 256;
-constexpr int kLmTile = 64;        // rows and vocabulary entries per workgroup while the rows fit one tile ...
+constexpr int kLmTile = 64;        // rows per workgroup while the rows fit one tile (by kLmTileSmall entries) ...
+constexpr int kLmTileSmall = 128;  //     (vocabulary entries: 8 waves of 16)
 constexpr int kLmTileBig = 256;    // ... and beyond: vocabulary entries per workgroup, by 128 rows (at most
 constexpr int kLmMidRows = 128;    //     128 rows, three LDS ring stages) or by 256 rows (two stages)
 constexpr int kLmBigRows = 256;
@@ -239,7 +240,7 @@ struct LmHeadArgs {
   float* part_val;         // [M, ntiles]
   int32_t* part_idx;       // [M, ntiles]
   int B, T, H, V, M, ntiles, mtiles;
-  int rows;                // rows per workgroup: kLmTile (64 vocabulary entries each), else kLmMidRows or
+  int rows;                // rows per workgroup: kLmTile (kLmTileSmall vocabulary entries each), else kLmMidRows or
                            // kLmBigRows (kLmTileBig entries each)
 };
 

@@ -2,13 +2,12 @@
 // logits never reach HBM (the paper's Section 2, "Speculative decoding": the target's token at a position is
 // the argmax of its logits there; the logits are the final hidden state times the LM head's weight).
 //
-// lm_head_argmax_kernel: a workgroup per (64-row tile, 64-entry vocabulary tile) of the logits, row tiles
-// fastest, four waves splitting the hidden axis in quarters.  A wave streams its quarter of the tile's 64
-// weight rows through a private two-stage LDS ring (LDS-DMA copies of whole 128-byte row pieces, non-temporal)
-// and reads the 64 hidden rows' operands straight from global memory (they stay in the caches); the products
-// run on v_mfma_f32_16x16x32_bf16 with the weights as the A operand, so that a lane's four outputs are four
-// vocabulary entries of one row.  The four partial sums are added through LDS in wave order (each wave then owns 16
-// vocabulary entries of the tile), and each row's best (value, index) over the tile's 64 entries is written:
+// lm_head_argmax_kernel: a workgroup of 8 waves per (64-row tile, 128-entry vocabulary tile) of the logits,
+// row tiles fastest; wave w owns the tile's vocabulary entries 16 w .. 16 w + 15 over the whole hidden axis.
+// Each wave streams its 16 weight rows through a private LDS ring (LDS-DMA copies of whole 128-byte row pieces,
+// several 64-deep stages ahead), and the tile's 64 hidden rows go through LDS once for all eight waves.  The
+// products run on v_mfma_f32_16x16x32_bf16 with the weights as the A operand, so that a lane's four outputs are
+// four vocabulary entries of one row.  Each row's best (value, index) over the tile's entries is written:
 // ties go to the smallest index (fp32 comparison, -0.0 equal to +0.0), as for logits held in memory.
 // lm_head_argmax_big_kernel (more than 64 rows): 256 vocabulary entries by 128 or 256 rows per workgroup, both
 // operands through a shared LDS ring (see below).
@@ -26,7 +25,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int NT = kLmThreads, NW = NT / 64, TILE = kLmTile;
+constexpr int NT = kLmThreads, NW = NT / 64;
 
 // true iff (v2, i2) beats (v1, i1): larger value, or equal value and smaller index
 __device__ __forceinline__ bool better(float v2, int i2, float v1, int i1) {
@@ -52,160 +51,6 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// A stage is 64 weight rows x 64 hidden entries (128 bytes per row, 8 KB), copied by 8 wave-wide copies of
-// 8 rows each; 16-byte chunk c of row r sits at position c ^ (r % 8) of the row, so that the 16 rows one
-// operand read touches fall on distinct banks (each copy lane fetches the chunk its position wants).
-constexpr int STAGE_K = 64, STAGE_BYTES = TILE * STAGE_K * 2, STAGES = 2;
-
-__global__ __launch_bounds__(NT) void lm_head_argmax_kernel(LmHeadArgs a) {
-  static_assert(NW == 4 && TILE == 64, "four waves, each owning 16 of the tile's 64 vocabulary entries");
-  static_assert(NW * STAGES * STAGE_BYTES >= NW * 16 * 64 * 16, "the partial sums reuse the copy rings");
-  __shared__ __attribute__((aligned(16))) char ring[NW][STAGES][STAGE_BYTES];   // one ring per wave
-  __shared__ float best_v[NW][TILE];
-  __shared__ int best_i[NW][TILE];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int col = lane & 15, quad = lane >> 4;
-  // the row tiles of one vocabulary tile are consecutive workgroups, so its weights are fetched from HBM
-  // once and found in the caches by the others
-  const int mt = blockIdx.x % a.mtiles, nt = blockIdx.x / a.mtiles;
-  const int n0 = nt * TILE, m0 = mt * TILE;
-  const int H = a.H, KQ = H / NW, k0 = wave * KQ, nstages = KQ / STAGE_K;
-
-  // copy lanes: copy j moves rows 8 j + lane / 8, chunk position lane % 8 (logical chunk cpos ^ row % 8)
-  const int crow = lane >> 3, cchunk = (lane & 7) ^ (crow & 7);
-  const __bf16* csrc[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j)
-    csrc[j] = a.weight + (size_t)min(n0 + 8 * j + crow, a.V - 1) * H + k0 + 8 * cchunk;
-  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(&ring[wave][0][0]));
-  auto issue = [&](int s) {   // the copies of stage s into ring slot s % STAGES
-    const uint32_t dst = ring_lds + (s % STAGES) * STAGE_BYTES;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) copy16_to_lds<true>(dst + j * 1024, csrc[j] + s * STAGE_K);
-  };
-  // hidden operand rows (clamped; their results are discarded below), read straight from global memory
-  const __bf16* xrow[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) xrow[r] = a.hidden + (size_t)min(m0 + 16 * r + col, a.M - 1) * H + k0 + quad * 8;
-
-  f32x4 acc[4][4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[t][r] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // The hidden operands are loaded one stage ahead, before that stage's copies: the wait for stage s (at most
-  // 8 operations outstanding) then leaves exactly stage s + 1's copies in flight, which is also the wait the
-  // compiler derives for the hidden registers from the loads it can see.  The loop is unrolled by two so that
-  // the two register sets swap roles without copies (a copy would make the compiler wait for everything).
-  bf16x8 xa[2][4], xb[2][4];
-  auto load_hidden = [&](int s, bf16x8 (&dst)[2][4]) {
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) dst[ks][r] = *(const bf16x8*)(xrow[r] + s * STAGE_K + 32 * ks);
-  };
-  auto compute = [&](int s, const bf16x8 (&x)[2][4]) {
-    const char* st = &ring[wave][s % STAGES][0];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 wa[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int r = 16 * t + col, c = 4 * ks + quad;
-        wa[t] = *(const bf16x8*)(st + r * 128 + ((c ^ (r & 7)) << 4));
-      }
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[t][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], x[ks][r], acc[t][r], 0, 0, 0);
-    }
-  };
-  issue(0);
-  load_hidden(0, xa);
-  int s = 0;
-  for (; s + 2 < nstages; s += 2) {
-    load_hidden(s + 1, xb);
-    issue(s + 1);
-    wait_vm<8>();
-    compute(s, xa);
-    load_hidden(s + 2, xa);
-    issue(s + 2);
-    wait_vm<8>();
-    compute(s + 1, xb);
-  }
-  if (s + 1 < nstages) {   // two stages left
-    load_hidden(s + 1, xb);
-    issue(s + 1);
-    wait_vm<8>();
-    compute(s, xa);
-    wait_vm<0>();
-    compute(s + 1, xb);
-  } else {                 // one stage left
-    wait_vm<0>();
-    compute(s, xa);
-  }
-  __syncthreads();   // every wave is done with its ring: the partial sums reuse it
-  f32x4 (*red)[16][64] = (f32x4(*)[16][64])&ring[0][0][0];
-
-  // sum the four quarters: wave w owns vocabulary sub-tile w; the others' partials of it come through LDS
-  f32x4 own[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      if (t == wave) own[r] = acc[t][r];
-      else red[wave][t * 4 + r][lane] = acc[t][r];
-    }
-  __syncthreads();
-  // lane (col, quad) of wave w: rows 16 r + col, vocabulary entries n0 + 16 w + 4 quad + e
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int src = 0; src < NW; ++src) s += src == wave ? own[r] : red[src][wave * 4 + r][lane];
-    float v = -INFINITY;
-    int x = INT_MAX;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int n = n0 + 16 * wave + 4 * quad + e;
-      if (n < a.V && (s[e] > v || x == INT_MAX)) {
-        v = s[e];
-        x = n;
-      }
-    }
-#pragma unroll
-    for (int off = 16; off <= 32; off <<= 1) {
-      const float v2 = __shfl_xor(v, off);
-      const int x2 = __shfl_xor(x, off);
-      if (better(v2, x2, v, x)) {
-        v = v2;
-        x = x2;
-      }
-    }
-    if (quad == 0) {
-      best_v[wave][16 * r + col] = v;
-      best_i[wave][16 * r + col] = x;
-    }
-  }
-  __syncthreads();
-  // each row's best over the tile's four sub-tiles, in vocabulary order
-  if (threadIdx.x < TILE && m0 + (int)threadIdx.x < a.M) {
-    const int row = threadIdx.x;
-    float v = best_v[0][row];
-    int x = best_i[0][row];
-#pragma unroll
-    for (int w = 1; w < NW; ++w)
-      if (better(best_v[w][row], best_i[w][row], v, x)) {
-        v = best_v[w][row];
-        x = best_i[w][row];
-      }
-    const size_t p = (size_t)(m0 + row) * a.ntiles + nt;
-    a.part_val[p] = v;
-    a.part_idx[p] = x;
-  }
-}
-
-// wait_vm<PER * k> for a run-time k in [0, K]
 template <int PER, int K>
 __device__ __forceinline__ void wait_vm_steps(int k) {
   if constexpr (K > 0) {
@@ -233,6 +78,210 @@ __device__ __forceinline__ void barrier_lds() {
 // rows x 64 hidden entries, copied by all waves together), STAGES - 1 stages ahead; one barrier per stage
 // hands a landed stage to every wave and frees the oldest.  Each operand tile is read from the caches once
 // per 64 WR rows or 64 WN entries instead of once per 64.
+
+constexpr int FIN_THREADS = 1024, FIN_WAVES = FIN_THREADS / 64, FIN_PER = 8;
+
+__device__ __forceinline__ void best_of_batch(const float* pv, const int* px, int p0, int n, int lane, float& v,
+                                              int& x) {
+  float cv[FIN_PER];
+  int cx[FIN_PER];
+#pragma unroll
+  for (int k = 0; k < FIN_PER; ++k) {
+    const int p = min(p0 + k * 64 + lane, n - 1);
+    cv[k] = pv[p];
+    cx[k] = px[p];
+  }
+#pragma unroll
+  for (int k = 0; k < FIN_PER; ++k)
+    if (p0 + k * 64 + lane < n && better(cv[k], cx[k], v, x)) {
+      v = cv[k];
+      x = cx[k];
+    }
+}
+__device__ __forceinline__ void wave_best(float& v, int& x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float v2 = __shfl_xor(v, off);
+    const int x2 = __shfl_xor(x, off);
+    if (better(v2, x2, v, x)) {
+      v = v2;
+      x = x2;
+    }
+  }
+}
+
+__global__ __launch_bounds__(FIN_THREADS) void lm_head_finish_kernel(LmHeadArgs a) {
+  __shared__ int am_s[kMaxNodes], tok_s[kMaxNodes], par_s[kMaxNodes];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int b = blockIdx.x, T = a.T, n = a.ntiles;
+  if ((int)threadIdx.x < T) {
+    tok_s[threadIdx.x] = a.tokens[(size_t)b * T + threadIdx.x];
+    par_s[threadIdx.x] = a.parent[(size_t)b * T + threadIdx.x];
+  }
+  for (int i = wave; i < T; i += 2 * FIN_WAVES) {
+    const int j = i + FIN_WAVES;   // the second row of the pair (may be past T)
+    const size_t ri = (size_t)b * T + i, rj = (size_t)b * T + min(j, T - 1);
+    float vi = -INFINITY, vj = -INFINITY;
+    int xi = INT_MAX, xj = INT_MAX;
+    for (int p0 = 0; p0 < n; p0 += FIN_PER * 64) {
+      best_of_batch(a.part_val + ri * n, a.part_idx + ri * n, p0, n, lane, vi, xi);
+      best_of_batch(a.part_val + rj * n, a.part_idx + rj * n, p0, n, lane, vj, xj);
+    }
+    wave_best(vi, xi);
+    wave_best(vj, xj);
+    if (lane == 0) {
+      am_s[i] = xi;
+      if (a.target_argmax) a.target_argmax[ri] = xi;
+      if (j < T) {
+        am_s[j] = xj;
+        if (a.target_argmax) a.target_argmax[rj] = xj;
+      }
+    }
+  }
+  __syncthreads();
+  if (wave == 0)
+    path_scan_wave(am_s, tok_s, par_s, T, a.accept_len + b, a.accept_path + (size_t)b * T, a.next_token + b);
+}
+
+// The 64-row kernel.  A stage is 64 hidden entries (128 bytes of a row).  Per stage, each wave copies its 16
+// weight rows into its ring slot (two wave-wide LDS-DMA copies of 8 rows x 128 bytes) and loads 16 bytes of the
+// tile's hidden rows per thread into registers (thread t: row t / 8, chunk t % 8); a stage's hidden rows are
+// written to one of three shared LDS buffers one stage before they are used, and a barrier publishes them.
+// Every vector-memory operation of the loop is issued by inline assembly and waited for by exact count: a
+// stage is issued DW - 1 stages ahead, and at stage s the wave waits for stage s + 1, leaving DW - 2 stages of
+// copies in flight.  The 16-byte chunk c of a row r sits at position c ^ (r % 8) of its 128-byte LDS row, so
+// that the 16 rows one operand read touches fall on distinct banks.
+constexpr int LM_WAVES = kLmTileSmall / 16, LM_SK = 64, LM_DW = 8, LM_XBUF = 3;
+constexpr int LM_WSLOT = 16 * LM_SK * 2, LM_XSTAGE = kLmTile * LM_SK * 2;
+constexpr size_t LM_LDS = (size_t)LM_WAVES * LM_DW * LM_WSLOT + (size_t)LM_XBUF * LM_XSTAGE;
+
+__device__ __forceinline__ void load16_async(bf16x8& dst, const void* src) {
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(dst) : "v"(src) : "memory");
+}
+// wait until at most N of this wave's vector-memory operations are outstanding; x (the data of a load issued
+// before them) is tied to the wait, so that no use of it is scheduled ahead of it
+template <int N>
+__device__ __forceinline__ void wait_vm_tied(bf16x8& x) {
+  asm volatile("s_waitcnt vmcnt(%1)" : "+v"(x) : "n"(N) : "memory");
+}
+
+__global__ __launch_bounds__(64 * LM_WAVES) void lm_head_argmax_kernel(LmHeadArgs a) {
+  static_assert(kLmTile == 64 && LM_WAVES == 8, "64 rows; eight waves, each owning 16 vocabulary entries");
+  static_assert(LM_LDS + 2 * LM_WAVES * kLmTile * 4 <= 160 * 1024, "LDS budget");
+  extern __shared__ __attribute__((aligned(1024))) char lm_lds[];
+  char* wring = lm_lds;                                         // [wave][DW][16 rows x 128 B]
+  char* xs = lm_lds + (size_t)LM_WAVES * LM_DW * LM_WSLOT;      // [3][64 rows x 128 B]
+  __shared__ float best_v[LM_WAVES][kLmTile];
+  __shared__ int best_i[LM_WAVES][kLmTile];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, quad = lane >> 4;
+  // the row tiles of one vocabulary tile are consecutive workgroups, so its weights are fetched from HBM once
+  // and found in the caches by the others
+  const int mt = blockIdx.x % a.mtiles, nt = blockIdx.x / a.mtiles;
+  const int n0 = nt * kLmTileSmall + 16 * wave, m0 = mt * kLmTile;
+  const int H = a.H, nstages = H / LM_SK;
+  // weight copies: copy j brings rows 8 j + lane / 8 of the wave's 16 (clamped past the vocabulary: their
+  // results are discarded), chunk position lane % 8, i.e. the row's chunk (lane % 8) ^ (row % 8)
+  const int crow = lane >> 3, cchunk = (lane & 7) ^ (crow & 7);
+  const __bf16* wsrc0 = a.weight + (size_t)min(n0 + crow, a.V - 1) * H + 8 * cchunk;
+  const __bf16* wsrc1 = a.weight + (size_t)min(n0 + 8 + crow, a.V - 1) * H + 8 * cchunk;
+  const uint32_t wring_lds = __builtin_amdgcn_readfirstlane(lds_addr(wring + (size_t)wave * LM_DW * LM_WSLOT));
+  // hidden piece of this thread: row t / 8 (clamped past the rows), chunk t % 8, written at c ^ (r % 8)
+  const int xr = threadIdx.x >> 3, xc = threadIdx.x & 7;
+  const __bf16* xsrc = a.hidden + (size_t)min(m0 + xr, a.M - 1) * H + 8 * xc;
+  const int xw = xr * 128 + ((xc ^ (xr & 7)) << 4);
+
+  bf16x8 hv[LM_DW];
+  auto issue = [&](int slot, int s) {
+    const int k = min(s, nstages - 1) * LM_SK;   // (stages past the end repeat the last one, unused)
+    const uint32_t dst = wring_lds + slot * LM_WSLOT;
+    copy16_to_lds<true>(dst, wsrc0 + k);
+    copy16_to_lds<true>(dst + 1024, wsrc1 + k);
+    load16_async(hv[slot], xsrc + k);
+  };
+  f32x4 acc[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int slot, int s) {
+    const char* wst = wring + ((size_t)wave * LM_DW + slot) * LM_WSLOT;
+    const char* xst = xs + (size_t)(s % LM_XBUF) * LM_XSTAGE;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int c = 4 * ks + quad;
+      const bf16x8 wa = *(const bf16x8*)(wst + col * 128 + ((c ^ (col & 7)) << 4));
+      bf16x8 xb[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) xb[r] = *(const bf16x8*)(xst + (16 * r + col) * 128 + ((c ^ (col & 7)) << 4));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xb[r], acc[r], 0, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int j = 0; j < LM_DW - 1; ++j) issue(j, j);
+  wait_vm_tied<3 * (LM_DW - 2)>(hv[0]);   // stage 0 has landed
+  *(bf16x8*)(xs + xw) = hv[0];
+  // Stage s: its slot's registers and ring slot take stage s + DW - 1 (the slot held stage s - 1, whose
+  // weights were read by this wave's products and whose hidden rows went to LDS before); stage s + 1 lands and
+  // its hidden rows go to their LDS buffer; the barrier publishes them and retires every wave's reads of the
+  // buffer stage s + 2 will take; then stage s is computed.
+  for (int s0 = 0; s0 < nstages; s0 += LM_DW) {
+#pragma unroll
+    for (int j = 0; j < LM_DW; ++j) {
+      const int s = s0 + j;
+      if (s >= nstages) break;
+      issue((j + LM_DW - 1) % LM_DW, s + LM_DW - 1);
+      wait_vm_tied<3 * (LM_DW - 2)>(hv[(j + 1) % LM_DW]);
+      *(bf16x8*)(xs + (size_t)((s + 1) % LM_XBUF) * LM_XSTAGE + xw) = hv[(j + 1) % LM_DW];
+      barrier_lds();
+      compute(j, s);
+    }
+  }
+  wait_vm<0>();   // copies issued past the last stage land before the workgroup's LDS is released
+
+  // lane (col, quad) of wave w: rows 16 r + col, vocabulary entries n0 + 4 quad + e
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float v = -INFINITY;
+    int x = INT_MAX;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int n = n0 + 4 * quad + e;
+      if (n < a.V && (acc[r][e] > v || x == INT_MAX)) {
+        v = acc[r][e];
+        x = n;
+      }
+    }
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float v2 = __shfl_xor(v, off);
+      const int x2 = __shfl_xor(x, off);
+      if (better(v2, x2, v, x)) {
+        v = v2;
+        x = x2;
+      }
+    }
+    if (quad == 0) {
+      best_v[wave][16 * r + col] = v;
+      best_i[wave][16 * r + col] = x;
+    }
+  }
+  __syncthreads();
+  // each row's best over the tile's sub-tiles, in vocabulary order
+  if (threadIdx.x < kLmTile && m0 + (int)threadIdx.x < a.M) {
+    const int row = threadIdx.x;
+    float v = best_v[0][row];
+    int x = best_i[0][row];
+#pragma unroll
+    for (int w = 1; w < LM_WAVES; ++w)
+      if (better(best_v[w][row], best_i[w][row], v, x)) {
+        v = best_v[w][row];
+        x = best_i[w][row];
+      }
+    const size_t p = (size_t)(m0 + row) * a.ntiles + nt;
+    a.part_val[p] = v;
+    a.part_idx[p] = x;
+  }
+}
 
 template <int WR, int WN, int TW, int SK, int STAGES>
 __global__ __launch_bounds__(64 * WR * WN) void lm_head_argmax_big_kernel(LmHeadArgs a) {
@@ -355,70 +404,6 @@ __global__ __launch_bounds__(64 * WR * WN) void lm_head_argmax_big_kernel(LmHead
 // Each row's best over every tile, then the greedy path scan: a workgroup of 16 waves per sequence; wave w
 // merges rows w, w + 16, ..., two rows at a time with all of both rows' candidates in flight (up to 8 per lane
 // per row, then the next batch).
-constexpr int FIN_THREADS = 1024, FIN_WAVES = FIN_THREADS / 64, FIN_PER = 8;
-
-__device__ __forceinline__ void best_of_batch(const float* pv, const int* px, int p0, int n, int lane, float& v,
-                                              int& x) {
-  float cv[FIN_PER];
-  int cx[FIN_PER];
-#pragma unroll
-  for (int k = 0; k < FIN_PER; ++k) {
-    const int p = min(p0 + k * 64 + lane, n - 1);
-    cv[k] = pv[p];
-    cx[k] = px[p];
-  }
-#pragma unroll
-  for (int k = 0; k < FIN_PER; ++k)
-    if (p0 + k * 64 + lane < n && better(cv[k], cx[k], v, x)) {
-      v = cv[k];
-      x = cx[k];
-    }
-}
-__device__ __forceinline__ void wave_best(float& v, int& x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float v2 = __shfl_xor(v, off);
-    const int x2 = __shfl_xor(x, off);
-    if (better(v2, x2, v, x)) {
-      v = v2;
-      x = x2;
-    }
-  }
-}
-
-__global__ __launch_bounds__(FIN_THREADS) void lm_head_finish_kernel(LmHeadArgs a) {
-  __shared__ int am_s[kMaxNodes], tok_s[kMaxNodes], par_s[kMaxNodes];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int b = blockIdx.x, T = a.T, n = a.ntiles;
-  if ((int)threadIdx.x < T) {
-    tok_s[threadIdx.x] = a.tokens[(size_t)b * T + threadIdx.x];
-    par_s[threadIdx.x] = a.parent[(size_t)b * T + threadIdx.x];
-  }
-  for (int i = wave; i < T; i += 2 * FIN_WAVES) {
-    const int j = i + FIN_WAVES;   // the second row of the pair (may be past T)
-    const size_t ri = (size_t)b * T + i, rj = (size_t)b * T + min(j, T - 1);
-    float vi = -INFINITY, vj = -INFINITY;
-    int xi = INT_MAX, xj = INT_MAX;
-    for (int p0 = 0; p0 < n; p0 += FIN_PER * 64) {
-      best_of_batch(a.part_val + ri * n, a.part_idx + ri * n, p0, n, lane, vi, xi);
-      best_of_batch(a.part_val + rj * n, a.part_idx + rj * n, p0, n, lane, vj, xj);
-    }
-    wave_best(vi, xi);
-    wave_best(vj, xj);
-    if (lane == 0) {
-      am_s[i] = xi;
-      if (a.target_argmax) a.target_argmax[ri] = xi;
-      if (j < T) {
-        am_s[j] = xj;
-        if (a.target_argmax) a.target_argmax[rj] = xj;
-      }
-    }
-  }
-  __syncthreads();
-  if (wave == 0)
-    path_scan_wave(am_s, tok_s, par_s, T, a.accept_len + b, a.accept_path + (size_t)b * T, a.next_token + b);
-}
-
 }  // namespace
 
 hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream) {
@@ -428,8 +413,16 @@ hipError_t launch_lm_head_accept(const LmHeadArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL((lm_head_argmax_big_kernel<4, 4, 4, 64, 2>), grid, dim3(1024), 0, stream, a);
   else if (a.rows == kLmMidRows)
     hipLaunchKernelGGL((lm_head_argmax_big_kernel<2, 4, 4, 64, 3>), grid, dim3(512), 0, stream, a);
-  else
-    hipLaunchKernelGGL(lm_head_argmax_kernel, grid, dim3(NT), 0, stream, a);
+  else {
+    static bool configured = false;
+    if (!configured) {
+      hipError_t e = hipFuncSetAttribute((const void*)lm_head_argmax_kernel,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)LM_LDS);
+      if (e != hipSuccess) return e;
+      configured = true;
+    }
+    hipLaunchKernelGGL(lm_head_argmax_kernel, grid, dim3(64 * LM_WAVES), LM_LDS, stream, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(lm_head_finish_kernel, dim3((unsigned)a.B), dim3(FIN_THREADS), 0, stream, a);

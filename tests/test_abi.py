@@ -293,7 +293,7 @@ def test_lm_head_accept_rejections_and_sizes(D):
 
     for B, T, H, V in [(1, 60, 4096, 32000), (16, 128, 3584, 152064), (2, 7, 256, 1)]:
         assert lib.dreams_tree_accept_lm_head_workspace_size(B, T, H, V, ctypes.byref(n)) == 0
-        tile = 64 if B * T <= 64 else 256          # one 64-row tile, else 128 x 256 tiles
+        tile = 128 if B * T <= 64 else 256         # one 64-row tile by 128 entries, else 128 x 256 tiles
         tiles = (V + tile - 1) // tile
         assert n.value == 65536 + 2 * r256(B * T * tiles * 4)
     assert lib.dreams_tree_accept_lm_head_workspace_size(0, 60, 4096, 32000, ctypes.byref(n)) == 0 and n.value == 0
