@@ -817,6 +817,8 @@ dreams_status_t dreams_prefill_attn_stats(const dreams_prefill_desc_t* desc, con
   a.D = desc->head_dim;
   a.S_cap = desc->cache_capacity;
   a.scale_log2 = desc->scale * 1.4426950408889634f;
+  st = device_cus(&a.cus);
+  if (st != DREAMS_OK) return st;
   hipError_t e = launch_prefill_stats(a, stream);
   if (e != hipSuccess) return hip_fail(e, "prefill statistics launch");
   return ok();

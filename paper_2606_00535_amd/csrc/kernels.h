@@ -141,6 +141,7 @@ struct PrefillArgs {
   float* entropy;              // [B, Hq, N] or nullptr
   int B, Hq, Hkv, G, N, D, S_cap;
   float scale_log2;            // scale * log2(e)
+  int cus;                     // compute units of the device (the workgroup order pairs long and short rows)
 };
 hipError_t launch_prefill_stats(const PrefillArgs& a, hipStream_t stream);
 hipError_t launch_prefill_entropy_mean(int B, int Hq, int N, const float* entropy, const int32_t* prompt_len, float* ae,

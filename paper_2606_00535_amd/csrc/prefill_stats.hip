@@ -13,8 +13,8 @@
 //     Each lane keeps, for each of its 2 rows, an online (reference, sum, entropy term) over the keys its
 //     quad sees, in log2 units; the reference only moves when a score passes it by more than 2^8 (the sums
 //     stay finite and the statistics do not depend on it), and the four quads are merged at the end.  Only
-//     16-key blocks that cross the diagonal or the prompt's end are masked.  Workgroups are ordered from the
-//     last rows (the most keys) to the first.
+//     16-key blocks that cross the diagonal or the prompt's end are masked.  Workgroups are ordered so that
+//     the row blocks with the most keys start first and share a compute unit with those with the fewest.
 //   * prefill_entropy_mean_kernel: one workgroup, the fp64 mean of the prompt rows' entropies over every head
 //     and sequence (rows i >= n_b hold 0 and do not count).
 #include "kernels.h"
@@ -119,10 +119,14 @@ __global__ __launch_bounds__(64 * kWaves, 2) void prefill_stats_kernel(PrefillAr
   constexpr int CPW = STAGE / 1024 / kWaves;     // wave-wide 1 KB copies per wave per stage
   static_assert(CPW >= 1 && CPW * 1024 * kWaves == STAGE, "copy split");
   extern __shared__ __attribute__((aligned(1024))) unsigned char ring[];   // kStages x STAGE
-  const int nblk = (a.N + kRowsPerWg - 1) / kRowsPerWg;
-  const int n = blockIdx.x;
-  const int blk = nblk - 1 - n % nblk;   // the row blocks with the most keys first
-  const int bh = n / nblk;
+  // Workgroup order: row blocks with the most keys first, one per compute unit; the workgroups beyond the
+  // first round (which share a compute unit with one of the first) take the blocks in the opposite order, so
+  // that the longest block is paired with the shortest.
+  const int nblk = (a.N + kRowsPerWg - 1) / kRowsPerWg, BH = a.B * a.Hq;
+  const int n = blockIdx.x, W = gridDim.x;
+  const int rank = (n >= a.cus && W <= 2 * a.cus) ? W - 1 - (n - a.cus) : n;
+  const int blk = nblk - 1 - rank / BH;
+  const int bh = rank - (rank / BH) * BH;
   const int h = bh % a.Hq, b = bh / a.Hq;
   const int g = h / a.G;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -196,33 +200,52 @@ __global__ __launch_bounds__(64 * kWaves, 2) void prefill_stats_kernel(PrefillAr
 #pragma unroll
       for (int rb = 0; rb < kRB; ++rb) s[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ds], qf[rb][ds], s[rb], 0, 0, 0);
     const bool edge = kk0 + 15 > rw0 || kk0 + 16 > nb;   // (wave-uniform) a key past some row or the prompt
+    if (!edge) {
+      // every key visible: the reference moves (rarely) when a score passes it by more than 2^8, then each
+      // score costs one fma, one exp2, one add and one fma
+      float zmax[kRB];
+      bool grow = false;
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) {
+        zmax[rb] = c * fmaxf(fmaxf(s[rb][0], s[rb][1]), fmaxf(s[rb][2], s[rb][3]));
+        grow |= zmax[rb] > m[rb] + kLazyLog2;
+      }
+      if (__any(grow)) {
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb)
+          if (zmax[rb] > m[rb] + kLazyLog2) rescale(m[rb], l[rb], e[rb], zmax[rb]);
+      }
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const float d = fmaf(s[rb][t], c, -m[rb]);
+          const float p = __builtin_amdgcn_exp2f(d);
+          l[rb] += p;
+          e[rb] = fmaf(p, d, e[rb]);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
       float z[4];
-      if (edge) {
-        const int row = rw0 + rb * 16 + col;
+      const int row = rw0 + rb * 16 + col;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int key = kk0 + 4 * t + quad;
-          z[t] = (key > row || key >= nb) ? -INFINITY : s[rb][t] * c;
-        }
-      } else {
-#pragma unroll
-        for (int t = 0; t < 4; ++t) z[t] = s[rb][t] * c;
+      for (int t = 0; t < 4; ++t) {
+        const int key = kk0 + 4 * t + quad;
+        z[t] = (key > row || key >= nb) ? -INFINITY : s[rb][t] * c;
       }
       const float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
       if (zmax > m[rb] + kLazyLog2) rescale(m[rb], l[rb], e[rb], zmax);
       if (m[rb] != -INFINITY) {
-        float ps = 0.f, es = 0.f;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const float d = fmaxf(z[t] - m[rb], -1.0e4f);   // (a masked key: p = 0 and a zero term)
           const float p = __builtin_amdgcn_exp2f(d);
-          ps += p;
-          es = fmaf(p, d, es);
+          l[rb] += p;
+          e[rb] = fmaf(p, d, e[rb]);
         }
-        l[rb] += ps;
-        e[rb] += es;
       }
     }
   };
