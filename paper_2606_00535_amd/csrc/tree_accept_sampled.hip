@@ -9,33 +9,33 @@
 //
 // The residual after k rejections at a node has the closed form r_k = max(p - C_k q, 0) / D_k, with C_0 = 0,
 // D_0 = 1, and after rejecting one more child C_{k+1} = C_k + D_k, D_{k+1} = sum_x max(p - C_{k+1} q, 0) (both
-// unchanged when that sum is zero).  It depends on how many siblings were rejected, not on their tokens, so
-// every child's test and every node's emitted token can be prepared before the walk:
-//   (1) "stats" pieces, one workgroup per piece of each row: maximum and sum of exp((l - max) / tau), target and
-//       draft.  Whoever needs a row's maxima and normalisers merges its pieces' statistics itself once all have
-//       arrived (the same order everywhere, so the same bits); at a leaf, the row's last piece draws the token
-//       emitted if the walk ends there.
-//   (2) "pass" pieces, one workgroup per piece of each child c of node n: the state before c follows from the
-//       residual masses of c's earlier siblings; the piece adds its part of c's residual mass
-//       sum max(p - (C + D) q, 0) and its arrival to c's 64-bit accumulator in one atomic (fixed point, units
-//       of 2^-51, so the sum does not depend on the order of arrival), and the piece holding c's token decides c
-//       (u q(x) D < max(p(x) - C q(x), 0)).  The last piece of n's last child draws the token emitted if the
-//       walk ends at n.  Pass pieces wait for n's statistics and for the accumulators of c's earlier siblings,
-//       a chain of waits as long as the widest sibling group.
-//   (3) the sequence's last row to finish walks the tree by ballots (the first kept child of each node) and
+// unchanged when that sum is zero).  So the children of a node need only the node's own p and q: one workgroup
+// per piece of each row (2048 entries, each thread holding 8, or 8192 in four parts for problems of many
+// pieces) keeps that piece's logits in registers for the whole call and
+//   (1) computes the piece's maxima and sums of exp((l - max) / tau), target and draft, and waits for the row's
+//       other pieces; every piece then merges the row's statistics itself, in piece order (the same bits
+//       everywhere), and forms p and q of its entries;
+//   (2) takes the node's children in index order: child c, token x, is decided by the piece holding x
+//       (u q(x) D < max(p(x) - C q(x), 0)) against the state its earlier siblings left; each piece adds its part
+//       of c's residual mass sum max(p - (C + D) q, 0) and its arrival to c's 64-bit accumulator in one atomic
+//       (fixed point, units of 2^-51, so the sum does not depend on the order of arrival) and waits for the
+//       whole sum before the next child -- a chain of waits as long as the node's sibling group, among the
+//       row's own pieces;
+//   (3) draws the token emitted if the walk ends at the node: the prefix of the piece masses (of the last
+//       child that moved the state, or of p) finds the piece where the cumulative mass first exceeds
+//       u0 * total, and that piece alone finds the token by a block scan; the row's last piece to finish
+//       counts the row as done;
+//   (4) the sequence's last row to finish walks the tree by ballots (the first kept child of each node) and
 //       emits the token prepared for the node it stops at.
-// Emitted tokens: the prefix of the piece masses in piece order finds the piece where the cumulative mass
-// first exceeds u0 * total, and a block scan of that piece finds the token.  Probabilities are fp64, so that
-// the integer outcome is decided in the precision of the definition; exp is Tang's table-driven method.
+// Probabilities are fp64, so that the integer outcome is decided in the precision of the definition; exp is
+// Tang's table-driven method.
 //
-// Pieces are 2048 entries (each thread holding 8, a pass piece computing p and q before its waits) while there
-// are at most 4096 statistics workgroups, else 8192 entries streamed in four 2048-entry parts after the waits.
-//
-// Forward progress.  A workgroup only waits for rows whose pieces all have smaller blockIdx (stats pieces come
-// first, pass pieces are ordered by child index), and workgroups are dispatched in blockIdx order, so every
-// wait ends; waits are nevertheless bounded (0.2 s by default), after which the results are unspecified and the
-// workspace's failure flag is set.  Nothing a wait that gave up leaves behind is used as a memory index (piece and
-// token positions are clamped, node indices come from the tree), and every arrival word still returns to zero.
+// Forward progress.  A workgroup only waits for the other pieces of its own row, which are consecutive
+// workgroups and wait for nothing outside the row; workgroups are dispatched in blockIdx order, so every wait
+// ends.  Waits are nevertheless bounded (0.2 s by default), after which the results are unspecified and the
+// workspace's failure flag is set.  Nothing a wait that gave up leaves behind is used as a memory index (piece
+// and token positions are clamped, node indices come from the tree), and every arrival word still returns to
+// zero.
 //
 // Results cross workgroups through device-scope stores and loads, published before a relaxed device-scope
 // atomic on an arrival word (see kernels.h).  The walker of each sequence clears that sequence's arrival words,
@@ -89,7 +89,7 @@ __device__ __forceinline__ double scaled_exp(double d, double inv_tau, const dou
 struct Shared {
   double tab[256];                 // 2^(j/256)
   double pm[kSampledMaxChunks];    // piece masses of the emitted token's distribution
-  double zs[kMaxNodes];            // residual masses of earlier siblings
+  double zs[kMaxNodes];            // this piece's part of each child's residual mass
   double red_d[NW];
   float red_f[NW];
   int red_i[NW];
@@ -103,6 +103,7 @@ struct Shared {
   int fin_piece;
   double fin_before, fin_thr;
   int gave_up;                     // a wait of this workgroup reached its bound
+  double rs_mt, rs_ist, rs_md, rs_isd;   // the row's merged statistics
 };
 
 // Block reductions: every lane reduces its wave by a butterfly, lane 0's value is kept, waves are combined in
@@ -203,6 +204,36 @@ struct RowStat {
 __device__ RowStat merge_stats(const SampledArgs& a, size_t row, Shared& sh) {
   const int tid = threadIdx.x;
   const double* ps = a.piece_stat + row * a.chunks * 4;
+  if (a.chunks <= 64) {
+    // one wave, lane k holding piece k: all loads in one round trip, butterfly reductions (the same order in
+    // every workgroup)
+    if (tid < 64) {
+      const bool in = tid < a.chunks;
+      const double v0 = in ? load_d(ps + 4 * tid + 0) : -INFINITY, v1 = in ? load_d(ps + 4 * tid + 1) : 0.0;
+      const double v2 = in ? load_d(ps + 4 * tid + 2) : -INFINITY, v3 = in ? load_d(ps + 4 * tid + 3) : 0.0;
+      float mt = (float)v0, md = (float)v2;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        mt = fmaxf(mt, __shfl_xor(mt, off));
+        md = fmaxf(md, __shfl_xor(md, off));
+      }
+      double st = in ? v1 * scaled_exp(v0 - (double)mt, a.inv_tau, sh.tab) : 0.0;
+      double sd = in ? v3 * scaled_exp(v2 - (double)md, a.inv_tau, sh.tab) : 0.0;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        st += __shfl_xor(st, off);
+        sd += __shfl_xor(sd, off);
+      }
+      if (tid == 0) {
+        sh.rs_mt = mt;
+        sh.rs_ist = 1.0 / st;
+        sh.rs_md = md;
+        sh.rs_isd = 1.0 / sd;
+      }
+    }
+    __syncthreads();
+    return RowStat{sh.rs_mt, sh.rs_ist, sh.rs_md, sh.rs_isd};
+  }
   float mt = -INFINITY, md = -INFINITY;
   for (int k = tid; k < a.chunks; k += NT) {
     mt = fmaxf(mt, (float)load_d(ps + 4 * k + 0));
@@ -218,95 +249,6 @@ __device__ RowStat merge_stats(const SampledArgs& a, size_t row, Shared& sh) {
   st = block_sum(st, sh);
   sd = block_sum(sd, sh);
   return RowStat{mt, 1.0 / st, md, 1.0 / sd};
-}
-
-// The token emitted if the walk ends at node n with residual max(p - C q, 0): its piece masses are those of
-// child `src`'s residual, or, for src < 0, the target's own (from n's piece statistics).  Stored to
-// final_token by thread 0 (every thread then waits for its stores).
-template <bool VEC, int SUB>
-__device__ void final_draw(const SampledArgs& a, int b, int n, const RowStat& rs, double C, int src, Shared& sh) {
-  const int tid = threadIdx.x, T = a.T, V = a.V;
-  const size_t row = (size_t)b * T + n;
-  if (src >= 0) {
-    const double* m = a.mass + ((size_t)b * T + src) * a.chunks;
-    for (int k = tid; k < a.chunks; k += NT) sh.pm[k] = load_d(m + k);
-  } else {
-    const double* ps = a.piece_stat + row * a.chunks * 4;
-    for (int k = tid; k < a.chunks; k += NT)
-      sh.pm[k] = load_d(ps + 4 * k + 1) * scaled_exp(load_d(ps + 4 * k + 0) - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    double total = 0.0;
-    for (int k = 0; k < a.chunks; ++k) total += sh.pm[k];
-    const double thr = (double)a.uniforms[(size_t)b * T] * total;
-    double cum = 0.0, before = 0.0, pos_before = 0.0;
-    int piece = -1, pos_piece = 0;
-    for (int k = 0; k < a.chunks; ++k) {
-      const double mk = sh.pm[k];
-      if (mk > 0.0) {
-        pos_piece = k;
-        pos_before = cum;
-      }
-      if (cum + mk > thr) {
-        piece = k;
-        before = cum;
-        break;
-      }
-      cum += mk;
-    }
-    if (piece < 0) {   // no crossing (an all-zero residual): the last piece of positive mass
-      piece = pos_piece;
-      before = pos_before;
-    }
-    sh.fin_piece = piece;
-    sh.fin_before = before;
-    sh.fin_thr = thr;
-  }
-  __syncthreads();
-  const int piece = sh.fin_piece;
-  const double thr = sh.fin_thr;
-  double before = sh.fin_before;
-  const float* trow = a.target_logits + row * V;
-  const float* drow = a.draft_logits + row * V;
-  int pick = INT_MAX, last_pos = -1;
-#pragma unroll 1
-  for (int sp = 0; sp < SUB && pick == INT_MAX; ++sp) {
-    const int x0 = (piece * SUB + sp) * SUBW, x1 = min(V, x0 + SUBW);
-    if (x0 >= V) break;
-    float lt[EPT], ld[EPT];
-    load_sub<VEC>(trow, x0, x1, lt);
-    load_sub<VEC>(drow, x0, x1, ld);
-    const int base = x0 + tid * EPT;
-    double r[EPT], mine = 0.0;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      r[e] = 0.0;
-      if (base + e < x1) {
-        const double p = scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
-        const double q = C == 0.0 ? 0.0 : scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd;
-        r[e] = fmax(p - C * q, 0.0);
-      }
-      mine += r[e];
-    }
-    double total;
-    double cum = before + block_exclusive_scan(mine, total, sh);
-    int pk = INT_MAX, lp = -1;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      cum += r[e];
-      if (pk == INT_MAX && cum > thr) pk = base + e;
-      if (r[e] > 0.0) lp = base + e;
-    }
-    pick = block_int<false>(pk, sh);
-    last_pos = max(last_pos, block_int<true>(lp, sh));
-    before += total;
-  }
-  // (rounding between the piece masses and this prefix can leave the crossing just outside the piece: then
-  // the piece's last entry of positive mass)
-  if (pick == INT_MAX) pick = last_pos >= 0 ? last_pos : min(V - 1, piece * SUB * SUBW);
-  if (tid == 0) store_coherent(a.final_token + row, pick);
-  wait_vector_memory();
 }
 
 // ---------------------------------------------------------------------------------------------------- walk
@@ -349,286 +291,321 @@ __device__ void walk(const SampledArgs& a, int b, Shared& sh) {
   }
 }
 
-// Arrival of a finished row at its sequence; the sequence's last row runs the walk.
-__device__ __forceinline__ void row_done(const SampledArgs& a, int b, Shared& sh) {
-  __syncthreads();   // every thread has read the previous flag
-  if (threadIdx.x == 0)
-    sh.flag = __hip_atomic_fetch_add(a.seq_ctr + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-              (uint32_t)(2 * a.T - 2);
-  __syncthreads();
-  if (sh.flag) walk(a, b, sh);
-}
-
-// ------------------------------------------------------------------------------------------ stats pieces
+// ------------------------------------------------------------------------------------------- row pieces
+// Workgroup (b, n, j): piece j of row n.  Its logits stay in registers for the whole call.
 template <bool VEC, int SUB>
-__device__ void stats_piece(const SampledArgs& a, int b, int i, int j, Shared& sh) {
-  const int tid = threadIdx.x;
-  const size_t row = (size_t)b * a.T + i;
-  const float* trow = a.target_logits + row * a.V;
-  const float* drow = a.draft_logits + row * a.V;
-  // per thread: running maxima and sums relative to them (rescaled when a maximum grows)
-  float mt = -INFINITY, md = -INFINITY;
-  double st = 0.0, sd = 0.0;
-  float lt[EPT], ld[EPT], nt[EPT], nd[EPT];
-  int x0 = j * SUB * SUBW;
-  load_sub<VEC>(trow, x0, min(a.V, x0 + SUBW), lt);
-  load_sub<VEC>(drow, x0, min(a.V, x0 + SUBW), ld);
+__device__ void row_piece(const SampledArgs& a, int b, int n, int j, Shared& sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int T = a.T, V = a.V;
+  const size_t rb = (size_t)b * T, row = rb + n;
+  const float* trow = a.target_logits + row * V;
+  const float* drow = a.draft_logits + row * V;
+  // One-part pieces keep their logits (and later p and q) in registers; four-part pieces stream their parts
+  // from memory in every pass (the registers would not hold them).
+  constexpr bool HOLD = SUB == 1;
+  float lt0[EPT], ld0[EPT];
+  if (HOLD) {
+    load_sub<VEC>(trow, j * SUBW, min(V, j * SUBW + SUBW), lt0);
+    load_sub<VEC>(drow, j * SUBW, min(V, j * SUBW + SUBW), ld0);
+  }
+  // f(sp, e, x, target logit, draft logit) for every entry x < V of the piece, in order
+  auto entries = [&](auto&& f) {
+    if (HOLD) {
+      const int base = j * SUBW + tid * EPT;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e)
+        if (base + e < V) f(0, e, base + e, lt0[e], ld0[e]);
+    } else {
 #pragma unroll 1
-  for (int sp = 0; sp < SUB; ++sp, x0 += SUBW) {
-    if (sp + 1 < SUB) {   // the next sub-piece's loads in flight during this one's arithmetic
-      const int y0 = x0 + SUBW;
-      load_sub<VEC>(trow, y0, min(a.V, y0 + SUBW), nt);
-      load_sub<VEC>(drow, y0, min(a.V, y0 + SUBW), nd);
-    }
-    float ct = -INFINITY, cd = -INFINITY;
+      for (int sp = 0; sp < SUB; ++sp) {
+        const int x0 = (j * SUB + sp) * SUBW;
+        if (x0 >= V) break;
+        float ta[EPT], da[EPT];
+        load_sub<VEC>(trow, x0, min(V, x0 + SUBW), ta);
+        load_sub<VEC>(drow, x0, min(V, x0 + SUBW), da);
+        const int base = x0 + tid * EPT;
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-      ct = fmaxf(ct, lt[e]);
-      cd = fmaxf(cd, ld[e]);
-    }
-    if (ct > mt) {
-      if (st != 0.0) st *= scaled_exp((double)mt - (double)ct, a.inv_tau, sh.tab);
-      mt = ct;
-    }
-    if (cd > md) {
-      if (sd != 0.0) sd *= scaled_exp((double)md - (double)cd, a.inv_tau, sh.tab);
-      md = cd;
-    }
-    const int base = x0 + tid * EPT, x1 = min(a.V, x0 + SUBW);
-#pragma unroll
-    for (int e = 0; e < EPT; ++e)
-      if (base + e < x1) {
-        st += scaled_exp((double)lt[e] - (double)mt, a.inv_tau, sh.tab);
-        sd += scaled_exp((double)ld[e] - (double)md, a.inv_tau, sh.tab);
+        for (int e = 0; e < EPT; ++e)
+          if (base + e < V) f(sp, e, base + e, ta[e], da[e]);
       }
-    if (sp + 1 < SUB) {
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        lt[e] = nt[e];
-        ld[e] = nd[e];
-      }
+    }
+  };
+  // n's children in index order (every piece of the row lists them the same way)
+  if (wave == 0) {
+    const int k0 = lane, k1 = lane + 64;
+    const bool c0 = k0 > n && k0 < T && a.parent[rb + k0] == n;
+    const bool c1 = k1 > n && k1 < T && a.parent[rb + k1] == n;
+    const uint64_t b0 = __ballot(c0), b1 = __ballot(c1);
+    const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+    if (c0) sh.sib[__builtin_popcountll(b0 & below)] = k0;
+    if (c1) sh.sib[__builtin_popcountll(b0) + __builtin_popcountll(b1 & below)] = k1;
+    if (lane == 0) {
+      sh.nsib = __builtin_popcountll(b0) + __builtin_popcountll(b1);
+      sh.gave_up = 0;
     }
   }
+
+  // ---- the piece's statistics: maxima and sums of exp((l - max) / tau), target and draft.  A one-part piece
+  // takes its thread's maxima first and keeps the exponentials relative to them, from which p and q follow by
+  // one factor each; a streamed piece re-references its sums when a maximum grows.
+  float mt = -INFINITY, md = -INFINITY;
+  double st = 0.0, sd = 0.0;
+  double et[EPT], ed[EPT];   // (one-part pieces)
+  if (HOLD) {
+    const int base = j * SUBW + tid * EPT;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      if (base + e < V) {
+        mt = fmaxf(mt, lt0[e]);
+        md = fmaxf(md, ld0[e]);
+      }
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const bool in = base + e < V;
+      et[e] = in ? scaled_exp((double)lt0[e] - (double)mt, a.inv_tau, sh.tab) : 0.0;
+      ed[e] = in ? scaled_exp((double)ld0[e] - (double)md, a.inv_tau, sh.tab) : 0.0;
+      st += et[e];
+      sd += ed[e];
+    }
+  } else {
+    entries([&](int, int, int, float t, float d) {
+      if (t > mt) {
+        if (st != 0.0) st *= scaled_exp((double)mt - (double)t, a.inv_tau, sh.tab);
+        mt = t;
+      }
+      if (d > md) {
+        if (sd != 0.0) sd *= scaled_exp((double)md - (double)d, a.inv_tau, sh.tab);
+        md = d;
+      }
+      st += scaled_exp((double)t - (double)mt, a.inv_tau, sh.tab);
+      sd += scaled_exp((double)d - (double)md, a.inv_tau, sh.tab);
+    });
+  }
+  const float mt_own = mt, md_own = md;
   const float bt = block_max(mt, sh), bd = block_max(md, sh);
   if (st != 0.0) st *= scaled_exp((double)mt - (double)bt, a.inv_tau, sh.tab);
   if (sd != 0.0) sd *= scaled_exp((double)md - (double)bd, a.inv_tau, sh.tab);
-  mt = bt;
-  md = bd;
   st = block_sum(st, sh);
   sd = block_sum(sd, sh);
-  uint32_t* w = stats_word(a, b, i);
   if (tid == 0) {
     double* ps = a.piece_stat + (row * a.chunks + j) * 4;
-    store_d(ps + 0, mt);
+    store_d(ps + 0, bt);
     store_d(ps + 1, st);
-    store_d(ps + 2, md);
+    store_d(ps + 2, bd);
     store_d(ps + 3, sd);
     wait_vector_memory();
-    sh.flag = arrive_last(w, (uint32_t)a.chunks);
+    uint32_t* w = stats_word(a, b, n);
+    __hip_atomic_fetch_add(w, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // every piece of the row
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)a.chunks) {
+      if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
+        raise_device_error(a.err, kErrWaitTimeout);
+        sh.gave_up = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
   }
   __syncthreads();
-  if (!sh.flag) return;
-
-  // the row's last piece: at a leaf, the token emitted if the walk ends here (the target's own distribution)
-  const int T = a.T;
-  const bool child = tid > i && tid < T && a.parent[(size_t)b * T + tid] == i;
-  if (!__syncthreads_or(child)) {
-    const RowStat rs = merge_stats(a, row, sh);
-    final_draw<VEC, SUB>(a, b, i, rs, 0.0, -1, sh);
-  }
-  row_done(a, b, sh);
-}
-
-// ------------------------------------------------------------------------------------------- pass pieces
-template <bool VEC, int SUB>
-__device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int T = a.T;
-  const size_t rb = (size_t)b * T;
-  if (tid < T) sh.par[tid] = a.parent[rb + tid];
-  if (tid == 0) sh.gave_up = 0;
-  __syncthreads();
-  const int n = sh.par[c];
-  const bool valid = n >= 0 && n < c;
-  const int x = a.tokens[rb + c];
-  double z = 0.0, C = 0.0, D = 1.0, CC = 1.0;
-  int src = -1;
-  RowStat rs{};
-  if (valid) {
-    const size_t row = rb + n;
-    const float* trow = a.target_logits + row * a.V;
-    const float* drow = a.draft_logits + row * a.V;
-    // one-sub-piece pieces: loaded now, p and q computed while the earlier siblings may still be running;
-    // larger pieces (where throughput matters more than the wait chain) are streamed after the waits
-    constexpr bool HOLD = SUB == 1;
-    const int x0 = j * SUB * SUBW, x1 = min(a.V, x0 + SUBW);
-    float lt[EPT], ld[EPT];
-    if (HOLD) {
-      load_sub<VEC>(trow, x0, x1, lt);
-      load_sub<VEC>(drow, x0, x1, ld);
-    }
-    // c's earlier siblings (in index order) and whether c is n's last child
-    if (wave == 0) {
-      const int k0 = lane, k1 = lane + 64;
-      const bool s0 = k0 > n && k0 < c && sh.par[k0] == n;
-      const bool s1 = k1 > n && k1 < c && k1 < T && sh.par[k1] == n;
-      const bool l0 = k0 > c && k0 < T && sh.par[k0] == n;
-      const bool l1 = k1 > c && k1 < T && sh.par[k1] == n;
-      const uint64_t b0 = __ballot(s0), b1 = __ballot(s1);
-      const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
-      if (s0) sh.sib[__builtin_popcountll(b0 & below)] = k0;
-      if (s1) sh.sib[__builtin_popcountll(b0) + __builtin_popcountll(b1 & below)] = k1;
-      const bool later = (__ballot(l0) | __ballot(l1)) != 0;
-      if (lane == 0) {
-        sh.nsib = __builtin_popcountll(b0) + __builtin_popcountll(b1);
-        sh.last_child = !later;
-      }
-      // every piece of n's statistics
-      if (lane == 0) {
-        const uint32_t* w = stats_word(a, b, n);
-        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)a.chunks) {
-          if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
-            raise_device_error(a.err, kErrWaitTimeout);
-            sh.gave_up = 1;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(2);
-        }
-      }
-    }
-    __syncthreads();
-    rs = merge_stats(a, row, sh);
-    double p[EPT], q[EPT];
-    if (HOLD) {
-      const int base = x0 + tid * EPT;
+  const RowStat rs = merge_stats(a, row, sh);
+  auto prob_p = [&](float t) { return scaled_exp((double)t - rs.mt, a.inv_tau, sh.tab) * rs.inv_st; };
+  auto prob_q = [&](float d) { return scaled_exp((double)d - rs.md, a.inv_tau, sh.tab) * rs.inv_sd; };
+  double pc[EPT], qc[EPT];   // (one-part pieces: the kept exponentials times one factor each)
+  if (HOLD) {
+    const double ft = mt_own == -INFINITY ? 0.0 : scaled_exp((double)mt_own - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+    const double fd = md_own == -INFINITY ? 0.0 : scaled_exp((double)md_own - rs.md, a.inv_tau, sh.tab) * rs.inv_sd;
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        const bool in = base + e < x1;
-        p[e] = in ? scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st : 0.0;
-        q[e] = in ? scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd : 0.0;
-      }
+    for (int e = 0; e < EPT; ++e) {
+      pc[e] = et[e] * ft;
+      qc[e] = ed[e] * fd;
     }
-    // the earlier siblings' residual masses: complete once their accumulators count every piece
-    const int nsib = sh.nsib;
-    if (wave == 0 && nsib > 0) {
-      const uint64_t* w0 = lane < nsib ? acc_word(a, b, sh.sib[lane]) : nullptr;
-      const uint64_t* w1 = lane + 64 < nsib ? acc_word(a, b, sh.sib[lane + 64]) : nullptr;
-      uint64_t v0 = 0, v1 = 0;
+  }
+
+  // ---- n's children in index order.  Child c (token x) is tested against the state (C, D) its earlier
+  // siblings left; its residual mass sum max(p - (C + D) q, 0) is summed over the row's pieces in its 64-bit
+  // accumulator (fixed point, so the sum does not depend on the order of arrival), and every piece waits for
+  // the whole sum before the next child.
+  const int nsib = sh.nsib;
+  double C = 0.0, D = 1.0;
+  int src = -1;
+  for (int k = 0; k < nsib; ++k) {
+    const int c = sh.sib[k];
+    const int x = a.tokens[rb + c];
+    const double CC = C + D;
+    double z = 0.0, px = 0.0, qx = 0.0;
+    bool mine = false;
+    entries([&](int, int e, int xi, float t, float d) {
+      const double pe = HOLD ? pc[e] : prob_p(t), qe = HOLD ? qc[e] : prob_q(d);
+      z += fmax(pe - CC * qe, 0.0);
+      if (xi == x) {
+        px = pe;
+        qx = qe;
+        mine = true;
+      }
+    });
+    // c's decision, by the thread holding its token (a token outside the vocabulary is never kept)
+    if (mine) store_coherent(a.kept + rb + c, (int32_t)(((double)a.uniforms[rb + c] * qx) * D < fmax(px - C * qx, 0.0)));
+    if ((x < 0 || x >= V) && j == 0 && tid == 0) store_coherent(a.kept + rb + c, 0);
+    z = block_sum(z, sh);
+    if (tid == 0) {
+      sh.zs[k] = z;   // this piece's part of c's residual mass (published after the loop if c is the last to move)
+      // A piece's mass is at most 1 (up to rounding); after a wait gave up it is meaningless and counts as 0,
+      // so that it can never carry into the arrival bits: the count, and with it the walk, still completes.
+      const double zc = sh.gave_up ? 0.0 : fmin(fmax(z, 0.0), 2.0);
+      const uint64_t fix = (uint64_t)rint(zc * kFixScale);
+      uint64_t* w = acc_word(a, b, c);
+      __hip_atomic_fetch_add(w, (1ull << kArrivalShift) + fix, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const uint64_t full = (uint64_t)a.chunks << kArrivalShift;
       const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-      while (true) {
-        if (w0) v0 = load_u64(w0);
-        if (w1) v1 = load_u64(w1);
-        const bool done = (!w0 || (v0 & ~kMassMask) == full) && (!w1 || (v1 & ~kMassMask) == full);
-        if (__ballot(!done) == 0) break;
+      uint64_t v;
+      while (((v = load_u64(w)) & ~kMassMask) != full) {
         if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
-          if (lane == 0) {
-            raise_device_error(a.err, kErrWaitTimeout);
-            sh.gave_up = 1;
-          }
+          raise_device_error(a.err, kErrWaitTimeout);
+          sh.gave_up = 1;
           break;
         }
-        __builtin_amdgcn_s_sleep(2);
+        __builtin_amdgcn_s_sleep(1);
       }
-      if (w0) sh.zs[lane] = (double)(v0 & kMassMask) * kFixUnit;
-      if (w1) sh.zs[lane + 64] = (double)(v1 & kMassMask) * kFixUnit;
+      sh.st_c = (double)(v & kMassMask) * kFixUnit;   // c's whole residual mass
     }
     __syncthreads();
-    if (tid == 0) {
-      double c_run = 0.0, d_run = 1.0;
-      int s_run = -1;
-      for (int k = 0; k < nsib; ++k) {
-        const double zk = sh.zs[k];
-        if (zk > 0.0) {
-          c_run += d_run;
-          d_run = zk;
-          s_run = sh.sib[k];
-        }
-      }
-      sh.st_c = c_run;
-      sh.st_d = d_run;
-      sh.st_slot = s_run;
+    const double Zc = sh.st_c;
+    if (Zc > 0.0) {
+      C = CC;
+      D = Zc;
+      src = c;
     }
-    __syncthreads();
-    C = sh.st_c;
-    D = sh.st_d;
-    src = sh.st_slot;
-    CC = C + D;
-    double px = 0.0, qx = 0.0;
-    bool mine = false;
-    if (HOLD) {
-      const int base = x0 + tid * EPT;
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        z += fmax(p[e] - CC * q[e], 0.0);
-        if (base + e == x && base + e < x1) {
-          px = p[e];
-          qx = q[e];
-          mine = true;
+  }
+
+  // ---- the token emitted if the walk ends at n (every child rejected, or a leaf): drawn from max(p - C q, 0)
+  // through the inverse CDF with u0; the piece masses are those of child src's residual, published now by
+  // every piece (a second round of arrivals on the row's word), or the target's own
+  if (tid == 0) {
+    if (src >= 0) {
+      int ks = 0;
+      while (sh.sib[ks] != src) ++ks;
+      store_d(a.mass + (rb + src) * a.chunks + j, sh.zs[ks]);
+      wait_vector_memory();
+    }
+    uint32_t* w = stats_word(a, b, n);
+    __hip_atomic_fetch_add(w, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (src >= 0) {
+      const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+      while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < 2u * (uint32_t)a.chunks) {
+        if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
+          raise_device_error(a.err, kErrWaitTimeout);
+          sh.gave_up = 1;
+          break;
         }
+        __builtin_amdgcn_s_sleep(1);
       }
-    } else {
-      float nt[EPT], nd[EPT];
-      int y0 = x0;
-      load_sub<VEC>(trow, y0, min(a.V, y0 + SUBW), lt);
-      load_sub<VEC>(drow, y0, min(a.V, y0 + SUBW), ld);
+    }
+  }
+  __syncthreads();
+  if (src >= 0) {
+    const double* m = a.mass + (rb + src) * a.chunks;
+    for (int k = tid; k < a.chunks; k += NT) sh.pm[k] = load_d(m + k);
+  } else {
+    const double* ps = a.piece_stat + row * a.chunks * 4;
+    for (int k = tid; k < a.chunks; k += NT)
+      sh.pm[k] = load_d(ps + 4 * k + 1) * scaled_exp(load_d(ps + 4 * k + 0) - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double total = 0.0;
+    for (int k = 0; k < a.chunks; ++k) total += sh.pm[k];
+    const double thr = (double)a.uniforms[rb] * total;
+    double cum = 0.0, before = 0.0, pos_before = 0.0;
+    int piece = -1, pos_piece = 0;
+    for (int k = 0; k < a.chunks; ++k) {
+      const double mk = sh.pm[k];
+      if (mk > 0.0) {
+        pos_piece = k;
+        pos_before = cum;
+      }
+      if (cum + mk > thr) {
+        piece = k;
+        before = cum;
+        break;
+      }
+      cum += mk;
+    }
+    if (piece < 0) {   // no crossing (an all-zero residual): the last piece of positive mass
+      piece = pos_piece;
+      before = pos_before;
+    }
+    sh.fin_piece = piece;
+    sh.fin_before = before;
+    sh.fin_thr = thr;
+  }
+  __syncthreads();
+  if (sh.fin_piece == j) {   // (one piece of the row draws)
+    const double thr = sh.fin_thr;
+    double before = sh.fin_before;
+    int pick = INT_MAX, last_pos = -1;
+    // part by part (a one-part piece has one): the block's prefix of r = max(p - C q, 0) in entry order
 #pragma unroll 1
-      for (int sp = 0; sp < SUB; ++sp, y0 += SUBW) {
-        if (sp + 1 < SUB) {   // the next sub-piece's loads in flight during this one's arithmetic
-          load_sub<VEC>(trow, y0 + SUBW, min(a.V, y0 + 2 * SUBW), nt);
-          load_sub<VEC>(drow, y0 + SUBW, min(a.V, y0 + 2 * SUBW), nd);
-        }
-        const int base = y0 + tid * EPT, y1 = min(a.V, y0 + SUBW);
+    for (int sp = 0; sp < SUB && pick == INT_MAX; ++sp) {
+      const int x0 = (j * SUB + sp) * SUBW;
+      if (x0 >= V) break;
+      const int base = x0 + tid * EPT;
+      float ta[EPT], da[EPT];
+      if (HOLD) {
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
-          if (base + e < y1) {
-            const double pe = scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
-            const double qe = scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd;
-            z += fmax(pe - CC * qe, 0.0);
-            if (base + e == x) {
-              px = pe;
-              qx = qe;
-              mine = true;
-            }
-          }
+          ta[e] = lt0[e];
+          da[e] = ld0[e];
         }
-        if (sp + 1 < SUB) {
-#pragma unroll
-          for (int e = 0; e < EPT; ++e) {
-            lt[e] = nt[e];
-            ld[e] = nd[e];
-          }
-        }
+      } else {
+        load_sub<VEC>(trow, x0, min(V, x0 + SUBW), ta);
+        load_sub<VEC>(drow, x0, min(V, x0 + SUBW), da);
       }
+      double r[EPT], mine_sum = 0.0;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        r[e] = 0.0;
+        if (base + e < V) {
+          const double pe = HOLD ? pc[e] : prob_p(ta[e]);
+          const double qe = C == 0.0 ? 0.0 : (HOLD ? qc[e] : prob_q(da[e]));
+          r[e] = fmax(pe - C * qe, 0.0);
+        }
+        mine_sum += r[e];
+      }
+      double total;
+      double cum = before + block_exclusive_scan(mine_sum, total, sh);
+      int pk = INT_MAX, lp = -1;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        cum += r[e];
+        if (pk == INT_MAX && cum > thr) pk = base + e;
+        if (r[e] > 0.0) lp = base + e;
+      }
+      pick = block_int<false>(pk, sh);
+      last_pos = max(last_pos, block_int<true>(lp, sh));
+      before += total;
     }
-    // c's decision, by the thread holding its token
-    if (mine) store_coherent(a.kept + rb + c, (int32_t)(((double)a.uniforms[rb + c] * qx) * D < fmax(px - C * qx, 0.0)));
+    // (rounding between the piece masses and this prefix can leave the crossing just outside the piece: then
+    // the piece's last entry of positive mass)
+    if (pick == INT_MAX) pick = last_pos >= 0 ? last_pos : min(V - 1, j * SUB * SUBW);
+    if (tid == 0) store_coherent(a.final_token + row, pick);
+    wait_vector_memory();
   }
-  if ((!valid || x < 0 || x >= a.V) && j == 0 && tid == 0) store_coherent(a.kept + rb + c, 0);
-  z = block_sum(z, sh);
-  if (tid == 0) store_d(a.mass + (rb + c) * a.chunks + j, z);
+  // Every piece counts itself out on the row's statistics word (which already holds two arrivals per piece),
+  // once its decisions and token are stored; the row's last piece counts the row as done, and the sequence's
+  // last row runs the walk.  (So each row is counted once even where a wait gave up and the pieces disagree on
+  // which one draws.)
   wait_vector_memory();
   __syncthreads();
   if (tid == 0) {
-    // A piece's mass is at most 1 (up to rounding); after a wait gave up it is meaningless and counts as 0, so
-    // that it can never carry into the arrival bits: the count, and with it the walk, still completes.
-    const double zc = sh.gave_up ? 0.0 : fmin(fmax(z, 0.0), 2.0);
-    const uint64_t mine = (uint64_t)rint(zc * kFixScale);
-    const uint64_t old = __hip_atomic_fetch_add(acc_word(a, b, c), (1ull << kArrivalShift) + mine, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-    sh.flag = (int)(old >> kArrivalShift) == a.chunks - 1;
-    sh.zs[0] = (double)((old & kMassMask) + mine) * kFixUnit;   // the row's whole residual mass
+    int walker = 0;
+    if (__hip_atomic_fetch_add(stats_word(a, b, n), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+        (uint32_t)(3 * a.chunks - 1))
+      walker = __hip_atomic_fetch_add(a.seq_ctr + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(T - 1);
+    sh.flag = walker;
   }
   __syncthreads();
-  if (!sh.flag) return;
-  // c's last piece: if c is n's last child, the token emitted if the walk ends at n (every child rejected)
-  if (valid && sh.last_child) {
-    const bool moved = sh.zs[0] > 0.0;
-    final_draw<VEC, SUB>(a, b, n, rs, moved ? CC : C, moved ? c : src, sh);
-    __syncthreads();
-  }
-  row_done(a, b, sh);
+  if (sh.flag) walk(a, b, sh);
 }
 
 template <bool VEC, int SUB>
@@ -637,25 +614,16 @@ __global__ __launch_bounds__(NT) void tree_accept_sampled_kernel(SampledArgs a) 
   sh.tab[threadIdx.x] = exp2((double)threadIdx.x * (1.0 / 256.0));
   __syncthreads();
   const long long t = blockIdx.x;
-  const long long stats = (long long)a.B * a.T * a.chunks;
-  if (t < stats) {
-    const int j = (int)(t % a.chunks);
-    const long long r = t / a.chunks;
-    stats_piece<VEC, SUB>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
-  } else {
-    const long long u = t - stats;
-    const long long per_child = (long long)a.B * a.chunks;
-    const int c = 1 + (int)(u / per_child);
-    const long long v = u % per_child;
-    pass_piece<VEC, SUB>(a, (int)(v / a.chunks), c, (int)(v % a.chunks), sh);
-  }
+  const int j = (int)(t % a.chunks);
+  const long long r = t / a.chunks;
+  row_piece<VEC, SUB>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
 }
 
 }  // namespace
 
 hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream) {
   static_assert(NT == 256, "the exp table is filled one entry per thread");
-  const long long grid = (long long)a.B * (2 * a.T - 1) * a.chunks;
+  const long long grid = (long long)a.B * a.T * a.chunks;
   auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(NT), 0, stream, a); };
   const bool large = a.sub_pieces == kSampledSubLarge;
   if (a.vec4) {
