@@ -89,17 +89,15 @@ __device__ __forceinline__ double scaled_exp(double d, double inv_tau, const dou
 struct Shared {
   double tab[256];                 // 2^(j/256)
   double pm[kSampledMaxChunks];    // piece masses of the emitted token's distribution
-  double zs[kMaxNodes];            // this piece's part of each child's residual mass
   double red_d[NW];
   float red_f[NW];
   int red_i[NW];
   double scan[NW];
-  int flag, nsib, last_child, depth;
+  int flag, nsib, depth;
   int par[kMaxNodes];
   int sib[kMaxNodes];
   int path[kMaxNodes];
-  double st_c, st_d;
-  int st_slot;
+  double st_c;                     // a child's whole residual mass
   int fin_piece;
   double fin_before, fin_thr;
   int gave_up;                     // a wait of this workgroup reached its bound
@@ -449,7 +447,10 @@ __device__ void row_piece(const SampledArgs& a, int b, int n, int j, Shared& sh)
     if ((x < 0 || x >= V) && j == 0 && tid == 0) store_coherent(a.kept + rb + c, 0);
     z = block_sum(z, sh);
     if (tid == 0) {
-      sh.zs[k] = z;   // this piece's part of c's residual mass (published after the loop if c is the last to move)
+      // this piece's part of c's residual mass (read by the row's draw if c is the last child to move the
+      // state); the last child's arrival waits for every such store of the piece first
+      store_d(a.mass + (rb + c) * a.chunks + j, z);
+      if (k == nsib - 1) wait_vector_memory();
       // A piece's mass is at most 1 (up to rounding); after a wait gave up it is meaningless and counts as 0,
       // so that it can never carry into the arrival bits: the count, and with it the walk, still completes.
       const double zc = sh.gave_up ? 0.0 : fmin(fmax(z, 0.0), 2.0);
@@ -479,30 +480,8 @@ __device__ void row_piece(const SampledArgs& a, int b, int n, int j, Shared& sh)
   }
 
   // ---- the token emitted if the walk ends at n (every child rejected, or a leaf): drawn from max(p - C q, 0)
-  // through the inverse CDF with u0; the piece masses are those of child src's residual, published now by
-  // every piece (a second round of arrivals on the row's word), or the target's own
-  if (tid == 0) {
-    if (src >= 0) {
-      int ks = 0;
-      while (sh.sib[ks] != src) ++ks;
-      store_d(a.mass + (rb + src) * a.chunks + j, sh.zs[ks]);
-      wait_vector_memory();
-    }
-    uint32_t* w = stats_word(a, b, n);
-    __hip_atomic_fetch_add(w, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (src >= 0) {
-      const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-      while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < 2u * (uint32_t)a.chunks) {
-        if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
-          raise_device_error(a.err, kErrWaitTimeout);
-          sh.gave_up = 1;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-    }
-  }
-  __syncthreads();
+  // through the inverse CDF with u0; the piece masses are those of child src's residual (every piece stored
+  // its part before its last arrival, which this piece has seen), or the target's own
   if (src >= 0) {
     const double* m = a.mass + (rb + src) * a.chunks;
     for (int k = tid; k < a.chunks; k += NT) sh.pm[k] = load_d(m + k);
@@ -591,7 +570,7 @@ __device__ void row_piece(const SampledArgs& a, int b, int n, int j, Shared& sh)
     if (tid == 0) store_coherent(a.final_token + row, pick);
     wait_vector_memory();
   }
-  // Every piece counts itself out on the row's statistics word (which already holds two arrivals per piece),
+  // Every piece counts itself out on the row's statistics word (which already holds one arrival per piece),
   // once its decisions and token are stored; the row's last piece counts the row as done, and the sequence's
   // last row runs the walk.  (So each row is counted once even where a wait gave up and the pieces disagree on
   // which one draws.)
@@ -600,7 +579,7 @@ __device__ void row_piece(const SampledArgs& a, int b, int n, int j, Shared& sh)
   if (tid == 0) {
     int walker = 0;
     if (__hip_atomic_fetch_add(stats_word(a, b, n), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-        (uint32_t)(3 * a.chunks - 1))
+        (uint32_t)(2 * a.chunks - 1))
       walker = __hip_atomic_fetch_add(a.seq_ctr + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(T - 1);
     sh.flag = walker;
   }
