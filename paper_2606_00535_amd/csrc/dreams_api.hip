@@ -500,7 +500,7 @@ dreams_status_t plan_sampled(int32_t B, int32_t T, int32_t V, SampledPlan* p) {
   }
   if (chunks > kSampledMaxChunks)
     return fail(DREAMS_ERR_UNSUPPORTED, "vocab = %d exceeds %lld", V, (long long)kSampledMaxChunks * large);
-  if ((long long)B * T * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
+  if ((long long)B * (2 * T - 1) * chunks > 0x7fffffffLL) return fail(DREAMS_ERR_UNSUPPORTED, "problem too large");
   // counter region: one word per sequence, then a block of 4, 8 or 16 words per row (as many as fit)
   const size_t rows = (size_t)B * T, base = ((size_t)B + 63) / 64 * 64;
   if (base + rows * 4 > kMaxCounters)

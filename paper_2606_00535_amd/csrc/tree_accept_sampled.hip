@@ -27,12 +27,18 @@
 //       counts the row as done;
 //   (4) the sequence's last row to finish walks the tree by ballots (the first kept child of each node) and
 //       emits the token prepared for the node it stops at.
+// Problems of many pieces (pieces of four 2048-entry parts) use a split form instead, with twice the workgroups:
+// first a "stats" workgroup per piece of every row (its last piece draws a leaf's token), then a "pass"
+// workgroup per piece of every child c, by c, which merges the parent's statistics, computes p and q of the
+// parent's piece and adds c's part of the residual mass once the earlier siblings' sums are complete; the last
+// piece of a node's last child draws the node's token.  (At gqa_long's 16 x 128 x 152064 it takes 1.8 ms
+// against 2.7 ms for the row-piece form, whose pieces re-stream their parts for every child.)
 // Probabilities are fp64, so that the integer outcome is decided in the precision of the definition; exp is
 // Tang's table-driven method.
 //
-// Forward progress.  A workgroup only waits for the other pieces of its own row, which are consecutive
-// workgroups and wait for nothing outside the row; workgroups are dispatched in blockIdx order, so every wait
-// ends.  Waits are nevertheless bounded (0.2 s by default), after which the results are unspecified and the
+// Forward progress.  A row piece only waits for the other pieces of its own row, which are consecutive
+// workgroups and wait for nothing outside the row; in the split form a workgroup only waits for rows whose
+// pieces all have smaller blockIdx.  Workgroups are dispatched in blockIdx order, so every wait ends.  Waits are nevertheless bounded (0.2 s by default), after which the results are unspecified and the
 // workspace's failure flag is set.  Nothing a wait that gave up leaves behind is used as a memory index (piece
 // and token positions are clamped, node indices come from the tree), and every arrival word still returns to
 // zero.
@@ -93,11 +99,13 @@ struct Shared {
   float red_f[NW];
   int red_i[NW];
   double scan[NW];
-  int flag, nsib, depth;
+  int flag, nsib, last_child, depth;
   int par[kMaxNodes];
   int sib[kMaxNodes];
   int path[kMaxNodes];
-  double st_c;                     // a child's whole residual mass
+  double zs[kMaxNodes];            // residual masses of earlier siblings (split form)
+  double st_c, st_d;               // a child's whole residual mass; the state (split form)
+  int st_slot;
   int fin_piece;
   double fin_before, fin_thr;
   int gave_up;                     // a wait of this workgroup reached its bound
@@ -249,6 +257,95 @@ __device__ RowStat merge_stats(const SampledArgs& a, size_t row, Shared& sh) {
   return RowStat{mt, 1.0 / st, md, 1.0 / sd};
 }
 
+// The token emitted if the walk ends at node n with residual max(p - C q, 0): its piece masses are those of
+// child `src`'s residual, or, for src < 0, the target's own (from n's piece statistics).  Stored to
+// final_token by thread 0 (every thread then waits for its stores).
+template <bool VEC, int SUB>
+__device__ void final_draw(const SampledArgs& a, int b, int n, const RowStat& rs, double C, int src, Shared& sh) {
+  const int tid = threadIdx.x, T = a.T, V = a.V;
+  const size_t row = (size_t)b * T + n;
+  if (src >= 0) {
+    const double* m = a.mass + ((size_t)b * T + src) * a.chunks;
+    for (int k = tid; k < a.chunks; k += NT) sh.pm[k] = load_d(m + k);
+  } else {
+    const double* ps = a.piece_stat + row * a.chunks * 4;
+    for (int k = tid; k < a.chunks; k += NT)
+      sh.pm[k] = load_d(ps + 4 * k + 1) * scaled_exp(load_d(ps + 4 * k + 0) - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double total = 0.0;
+    for (int k = 0; k < a.chunks; ++k) total += sh.pm[k];
+    const double thr = (double)a.uniforms[(size_t)b * T] * total;
+    double cum = 0.0, before = 0.0, pos_before = 0.0;
+    int piece = -1, pos_piece = 0;
+    for (int k = 0; k < a.chunks; ++k) {
+      const double mk = sh.pm[k];
+      if (mk > 0.0) {
+        pos_piece = k;
+        pos_before = cum;
+      }
+      if (cum + mk > thr) {
+        piece = k;
+        before = cum;
+        break;
+      }
+      cum += mk;
+    }
+    if (piece < 0) {   // no crossing (an all-zero residual): the last piece of positive mass
+      piece = pos_piece;
+      before = pos_before;
+    }
+    sh.fin_piece = piece;
+    sh.fin_before = before;
+    sh.fin_thr = thr;
+  }
+  __syncthreads();
+  const int piece = sh.fin_piece;
+  const double thr = sh.fin_thr;
+  double before = sh.fin_before;
+  const float* trow = a.target_logits + row * V;
+  const float* drow = a.draft_logits + row * V;
+  int pick = INT_MAX, last_pos = -1;
+#pragma unroll 1
+  for (int sp = 0; sp < SUB && pick == INT_MAX; ++sp) {
+    const int x0 = (piece * SUB + sp) * SUBW, x1 = min(V, x0 + SUBW);
+    if (x0 >= V) break;
+    float lt[EPT], ld[EPT];
+    load_sub<VEC>(trow, x0, x1, lt);
+    load_sub<VEC>(drow, x0, x1, ld);
+    const int base = x0 + tid * EPT;
+    double r[EPT], mine = 0.0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      r[e] = 0.0;
+      if (base + e < x1) {
+        const double p = scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+        const double q = C == 0.0 ? 0.0 : scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd;
+        r[e] = fmax(p - C * q, 0.0);
+      }
+      mine += r[e];
+    }
+    double total;
+    double cum = before + block_exclusive_scan(mine, total, sh);
+    int pk = INT_MAX, lp = -1;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      cum += r[e];
+      if (pk == INT_MAX && cum > thr) pk = base + e;
+      if (r[e] > 0.0) lp = base + e;
+    }
+    pick = block_int<false>(pk, sh);
+    last_pos = max(last_pos, block_int<true>(lp, sh));
+    before += total;
+  }
+  // (rounding between the piece masses and this prefix can leave the crossing just outside the piece: then
+  // the piece's last entry of positive mass)
+  if (pick == INT_MAX) pick = last_pos >= 0 ? last_pos : min(V - 1, piece * SUB * SUBW);
+  if (tid == 0) store_coherent(a.final_token + row, pick);
+  wait_vector_memory();
+}
+
 // ---------------------------------------------------------------------------------------------------- walk
 __device__ void walk(const SampledArgs& a, int b, Shared& sh) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -287,6 +384,289 @@ __device__ void walk(const SampledArgs& a, int b, Shared& sh) {
     __hip_atomic_store(acc_word(a, b, tid), (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     reset_counter(stats_word(a, b, tid));
   }
+}
+
+// ------------------------------------------------------------- split form (pieces of many sub-pieces)
+// Arrival of a finished row at its sequence; the sequence's last row runs the walk.
+__device__ __forceinline__ void row_done(const SampledArgs& a, int b, Shared& sh) {
+  __syncthreads();   // every thread has read the previous flag
+  if (threadIdx.x == 0)
+    sh.flag = __hip_atomic_fetch_add(a.seq_ctr + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              (uint32_t)(2 * a.T - 2);
+  __syncthreads();
+  if (sh.flag) walk(a, b, sh);
+}
+
+// ------------------------------------------------------------------------------------------ stats pieces
+template <bool VEC, int SUB>
+__device__ void stats_piece(const SampledArgs& a, int b, int i, int j, Shared& sh) {
+  const int tid = threadIdx.x;
+  const size_t row = (size_t)b * a.T + i;
+  const float* trow = a.target_logits + row * a.V;
+  const float* drow = a.draft_logits + row * a.V;
+  // per thread: running maxima and sums relative to them (rescaled when a maximum grows)
+  float mt = -INFINITY, md = -INFINITY;
+  double st = 0.0, sd = 0.0;
+  float lt[EPT], ld[EPT], nt[EPT], nd[EPT];
+  int x0 = j * SUB * SUBW;
+  load_sub<VEC>(trow, x0, min(a.V, x0 + SUBW), lt);
+  load_sub<VEC>(drow, x0, min(a.V, x0 + SUBW), ld);
+#pragma unroll 1
+  for (int sp = 0; sp < SUB; ++sp, x0 += SUBW) {
+    if (sp + 1 < SUB) {   // the next sub-piece's loads in flight during this one's arithmetic
+      const int y0 = x0 + SUBW;
+      load_sub<VEC>(trow, y0, min(a.V, y0 + SUBW), nt);
+      load_sub<VEC>(drow, y0, min(a.V, y0 + SUBW), nd);
+    }
+    float ct = -INFINITY, cd = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      ct = fmaxf(ct, lt[e]);
+      cd = fmaxf(cd, ld[e]);
+    }
+    if (ct > mt) {
+      if (st != 0.0) st *= scaled_exp((double)mt - (double)ct, a.inv_tau, sh.tab);
+      mt = ct;
+    }
+    if (cd > md) {
+      if (sd != 0.0) sd *= scaled_exp((double)md - (double)cd, a.inv_tau, sh.tab);
+      md = cd;
+    }
+    const int base = x0 + tid * EPT, x1 = min(a.V, x0 + SUBW);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      if (base + e < x1) {
+        st += scaled_exp((double)lt[e] - (double)mt, a.inv_tau, sh.tab);
+        sd += scaled_exp((double)ld[e] - (double)md, a.inv_tau, sh.tab);
+      }
+    if (sp + 1 < SUB) {
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        lt[e] = nt[e];
+        ld[e] = nd[e];
+      }
+    }
+  }
+  const float bt = block_max(mt, sh), bd = block_max(md, sh);
+  if (st != 0.0) st *= scaled_exp((double)mt - (double)bt, a.inv_tau, sh.tab);
+  if (sd != 0.0) sd *= scaled_exp((double)md - (double)bd, a.inv_tau, sh.tab);
+  mt = bt;
+  md = bd;
+  st = block_sum(st, sh);
+  sd = block_sum(sd, sh);
+  uint32_t* w = stats_word(a, b, i);
+  if (tid == 0) {
+    double* ps = a.piece_stat + (row * a.chunks + j) * 4;
+    store_d(ps + 0, mt);
+    store_d(ps + 1, st);
+    store_d(ps + 2, md);
+    store_d(ps + 3, sd);
+    wait_vector_memory();
+    sh.flag = arrive_last(w, (uint32_t)a.chunks);
+  }
+  __syncthreads();
+  if (!sh.flag) return;
+
+  // the row's last piece: at a leaf, the token emitted if the walk ends here (the target's own distribution)
+  const int T = a.T;
+  const bool child = tid > i && tid < T && a.parent[(size_t)b * T + tid] == i;
+  if (!__syncthreads_or(child)) {
+    const RowStat rs = merge_stats(a, row, sh);
+    final_draw<VEC, SUB>(a, b, i, rs, 0.0, -1, sh);
+  }
+  row_done(a, b, sh);
+}
+
+// ------------------------------------------------------------------------------------------- pass pieces
+template <bool VEC, int SUB>
+__device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int T = a.T;
+  const size_t rb = (size_t)b * T;
+  if (tid < T) sh.par[tid] = a.parent[rb + tid];
+  if (tid == 0) sh.gave_up = 0;
+  __syncthreads();
+  const int n = sh.par[c];
+  const bool valid = n >= 0 && n < c;
+  const int x = a.tokens[rb + c];
+  double z = 0.0, C = 0.0, D = 1.0, CC = 1.0;
+  int src = -1;
+  RowStat rs{};
+  if (valid) {
+    const size_t row = rb + n;
+    const float* trow = a.target_logits + row * a.V;
+    const float* drow = a.draft_logits + row * a.V;
+    // one-sub-piece pieces: loaded now, p and q computed while the earlier siblings may still be running;
+    // larger pieces (where throughput matters more than the wait chain) are streamed after the waits
+    constexpr bool HOLD = SUB == 1;
+    const int x0 = j * SUB * SUBW, x1 = min(a.V, x0 + SUBW);
+    float lt[EPT], ld[EPT];
+    if (HOLD) {
+      load_sub<VEC>(trow, x0, x1, lt);
+      load_sub<VEC>(drow, x0, x1, ld);
+    }
+    // c's earlier siblings (in index order) and whether c is n's last child
+    if (wave == 0) {
+      const int k0 = lane, k1 = lane + 64;
+      const bool s0 = k0 > n && k0 < c && sh.par[k0] == n;
+      const bool s1 = k1 > n && k1 < c && k1 < T && sh.par[k1] == n;
+      const bool l0 = k0 > c && k0 < T && sh.par[k0] == n;
+      const bool l1 = k1 > c && k1 < T && sh.par[k1] == n;
+      const uint64_t b0 = __ballot(s0), b1 = __ballot(s1);
+      const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+      if (s0) sh.sib[__builtin_popcountll(b0 & below)] = k0;
+      if (s1) sh.sib[__builtin_popcountll(b0) + __builtin_popcountll(b1 & below)] = k1;
+      const bool later = (__ballot(l0) | __ballot(l1)) != 0;
+      if (lane == 0) {
+        sh.nsib = __builtin_popcountll(b0) + __builtin_popcountll(b1);
+        sh.last_child = !later;
+      }
+      // every piece of n's statistics
+      if (lane == 0) {
+        const uint32_t* w = stats_word(a, b, n);
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)a.chunks) {
+          if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
+            raise_device_error(a.err, kErrWaitTimeout);
+            sh.gave_up = 1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
+      }
+    }
+    __syncthreads();
+    rs = merge_stats(a, row, sh);
+    double p[EPT], q[EPT];
+    if (HOLD) {
+      const int base = x0 + tid * EPT;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        const bool in = base + e < x1;
+        p[e] = in ? scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st : 0.0;
+        q[e] = in ? scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd : 0.0;
+      }
+    }
+    // the earlier siblings' residual masses: complete once their accumulators count every piece
+    const int nsib = sh.nsib;
+    if (wave == 0 && nsib > 0) {
+      const uint64_t* w0 = lane < nsib ? acc_word(a, b, sh.sib[lane]) : nullptr;
+      const uint64_t* w1 = lane + 64 < nsib ? acc_word(a, b, sh.sib[lane + 64]) : nullptr;
+      uint64_t v0 = 0, v1 = 0;
+      const uint64_t full = (uint64_t)a.chunks << kArrivalShift;
+      const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+      while (true) {
+        if (w0) v0 = load_u64(w0);
+        if (w1) v1 = load_u64(w1);
+        const bool done = (!w0 || (v0 & ~kMassMask) == full) && (!w1 || (v1 & ~kMassMask) == full);
+        if (__ballot(!done) == 0) break;
+        if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
+          if (lane == 0) {
+            raise_device_error(a.err, kErrWaitTimeout);
+            sh.gave_up = 1;
+          }
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+      if (w0) sh.zs[lane] = (double)(v0 & kMassMask) * kFixUnit;
+      if (w1) sh.zs[lane + 64] = (double)(v1 & kMassMask) * kFixUnit;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      double c_run = 0.0, d_run = 1.0;
+      int s_run = -1;
+      for (int k = 0; k < nsib; ++k) {
+        const double zk = sh.zs[k];
+        if (zk > 0.0) {
+          c_run += d_run;
+          d_run = zk;
+          s_run = sh.sib[k];
+        }
+      }
+      sh.st_c = c_run;
+      sh.st_d = d_run;
+      sh.st_slot = s_run;
+    }
+    __syncthreads();
+    C = sh.st_c;
+    D = sh.st_d;
+    src = sh.st_slot;
+    CC = C + D;
+    double px = 0.0, qx = 0.0;
+    bool mine = false;
+    if (HOLD) {
+      const int base = x0 + tid * EPT;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        z += fmax(p[e] - CC * q[e], 0.0);
+        if (base + e == x && base + e < x1) {
+          px = p[e];
+          qx = q[e];
+          mine = true;
+        }
+      }
+    } else {
+      float nt[EPT], nd[EPT];
+      int y0 = x0;
+      load_sub<VEC>(trow, y0, min(a.V, y0 + SUBW), lt);
+      load_sub<VEC>(drow, y0, min(a.V, y0 + SUBW), ld);
+#pragma unroll 1
+      for (int sp = 0; sp < SUB; ++sp, y0 += SUBW) {
+        if (sp + 1 < SUB) {   // the next sub-piece's loads in flight during this one's arithmetic
+          load_sub<VEC>(trow, y0 + SUBW, min(a.V, y0 + 2 * SUBW), nt);
+          load_sub<VEC>(drow, y0 + SUBW, min(a.V, y0 + 2 * SUBW), nd);
+        }
+        const int base = y0 + tid * EPT, y1 = min(a.V, y0 + SUBW);
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+          if (base + e < y1) {
+            const double pe = scaled_exp((double)lt[e] - rs.mt, a.inv_tau, sh.tab) * rs.inv_st;
+            const double qe = scaled_exp((double)ld[e] - rs.md, a.inv_tau, sh.tab) * rs.inv_sd;
+            z += fmax(pe - CC * qe, 0.0);
+            if (base + e == x) {
+              px = pe;
+              qx = qe;
+              mine = true;
+            }
+          }
+        }
+        if (sp + 1 < SUB) {
+#pragma unroll
+          for (int e = 0; e < EPT; ++e) {
+            lt[e] = nt[e];
+            ld[e] = nd[e];
+          }
+        }
+      }
+    }
+    // c's decision, by the thread holding its token
+    if (mine) store_coherent(a.kept + rb + c, (int32_t)(((double)a.uniforms[rb + c] * qx) * D < fmax(px - C * qx, 0.0)));
+  }
+  if ((!valid || x < 0 || x >= a.V) && j == 0 && tid == 0) store_coherent(a.kept + rb + c, 0);
+  z = block_sum(z, sh);
+  if (tid == 0) store_d(a.mass + (rb + c) * a.chunks + j, z);
+  wait_vector_memory();
+  __syncthreads();
+  if (tid == 0) {
+    // A piece's mass is at most 1 (up to rounding); after a wait gave up it is meaningless and counts as 0, so
+    // that it can never carry into the arrival bits: the count, and with it the walk, still completes.
+    const double zc = sh.gave_up ? 0.0 : fmin(fmax(z, 0.0), 2.0);
+    const uint64_t mine = (uint64_t)rint(zc * kFixScale);
+    const uint64_t old = __hip_atomic_fetch_add(acc_word(a, b, c), (1ull << kArrivalShift) + mine, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    sh.flag = (int)(old >> kArrivalShift) == a.chunks - 1;
+    sh.zs[0] = (double)((old & kMassMask) + mine) * kFixUnit;   // the row's whole residual mass
+  }
+  __syncthreads();
+  if (!sh.flag) return;
+  // c's last piece: if c is n's last child, the token emitted if the walk ends at n (every child rejected)
+  if (valid && sh.last_child) {
+    const bool moved = sh.zs[0] > 0.0;
+    final_draw<VEC, SUB>(a, b, n, rs, moved ? CC : C, moved ? c : src, sh);
+    __syncthreads();
+  }
+  row_done(a, b, sh);
 }
 
 // ------------------------------------------------------------------------------------------- row pieces
@@ -598,18 +978,39 @@ __global__ __launch_bounds__(NT) void tree_accept_sampled_kernel(SampledArgs a) 
   row_piece<VEC, SUB>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
 }
 
+template <bool VEC, int SUB>
+__global__ __launch_bounds__(NT) void tree_accept_sampled_split_kernel(SampledArgs a) {
+  __shared__ Shared sh;
+  sh.tab[threadIdx.x] = exp2((double)threadIdx.x * (1.0 / 256.0));
+  __syncthreads();
+  const long long t = blockIdx.x;
+  const long long stats = (long long)a.B * a.T * a.chunks;
+  if (t < stats) {
+    const int j = (int)(t % a.chunks);
+    const long long r = t / a.chunks;
+    stats_piece<VEC, SUB>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
+  } else {
+    const long long u = t - stats;
+    const long long per_child = (long long)a.B * a.chunks;
+    const int c = 1 + (int)(u / per_child);
+    const long long v = u % per_child;
+    pass_piece<VEC, SUB>(a, (int)(v / a.chunks), c, (int)(v % a.chunks), sh);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_tree_accept_sampled(const SampledArgs& a, hipStream_t stream) {
   static_assert(NT == 256, "the exp table is filled one entry per thread");
-  const long long grid = (long long)a.B * a.T * a.chunks;
-  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(NT), 0, stream, a); };
+  // one-part pieces: a workgroup per row piece; four-part pieces (problems of many pieces): the split form
   const bool large = a.sub_pieces == kSampledSubLarge;
+  const long long grid = large ? (long long)a.B * (2 * a.T - 1) * a.chunks : (long long)a.B * a.T * a.chunks;
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(NT), 0, stream, a); };
   if (a.vec4) {
-    if (large) go(tree_accept_sampled_kernel<true, kSampledSubLarge>);
+    if (large) go(tree_accept_sampled_split_kernel<true, kSampledSubLarge>);
     else go(tree_accept_sampled_kernel<true, 1>);
   } else {
-    if (large) go(tree_accept_sampled_kernel<false, kSampledSubLarge>);
+    if (large) go(tree_accept_sampled_split_kernel<false, kSampledSubLarge>);
     else go(tree_accept_sampled_kernel<false, 1>);
   }
   return hipGetLastError();
