@@ -869,6 +869,8 @@ dreams_status_t dreams_prefill_visual_importance(const dreams_prefill_desc_t* de
   a.kv_len = prompt_len;
   a.lse = lse;
   a.prefill = 1;
+  st = device_cus(&a.cus);
+  if (st != DREAMS_OK) return st;
   a.counters = (uint32_t*)workspace;
   a.counter_stride = stride;
   a.partial = (float*)((char*)workspace + kCounterBytes);

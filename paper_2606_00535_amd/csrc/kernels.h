@@ -120,6 +120,7 @@ struct VisualArgs {
   int B, Hq, Hkv, G, T, D, S_cap;
   int vis_begin, vis_count;
   float scale_log2;       // scale * log2(e)
+  int cus;                // compute units of the device (prefill rows: the workgroup order pairs long and short)
 };
 struct VisualGatherArgs {
   const void* k;
