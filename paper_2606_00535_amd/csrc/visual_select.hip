@@ -303,6 +303,8 @@ __global__ __launch_bounds__(64 * pf::kWaves, 2) void visual_importance_prefill_
     if (s0 + pf::kRows - 1 < first_slot) continue;   // (wave-uniform) no row of the stage sees the wave's tokens
     const unsigned char* st = ring + (t % pf::kStages) * STAGE;
     const float* lse_s = (const float*)(st + QBYTES);
+    // (wave-uniform) every row of the stage is a prompt row past every token of the wave: no per-score test
+    const bool inner = s0 >= first_slot + pf::kTokPerWave - 1 && s0 + pf::kRows <= L;
 #pragma unroll
     for (int c = 0; c < pf::kRows / 16; ++c) {
       // B operand: lane (col, quad) holds row 16 c + ka_row of the stage (the same order as the keys)
@@ -318,7 +320,10 @@ __global__ __launch_bounds__(64 * pf::kWaves, 2) void visual_importance_prefill_
         f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kb][ds], qf[ds], sc, 0, 0, 0);
-        if (live) {
+        if (inner) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[kb][e] += __builtin_amdgcn_exp2f(fmaf(sc[e], a.scale_log2, -lse2));
+        } else if (live) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int slot = first_slot + kb * 16 + e * 4 + quad;
