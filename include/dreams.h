@@ -67,7 +67,8 @@ typedef enum { DREAMS_F32 = 0, DREAMS_BF16 = 1 } dreams_dtype_t;
  * DREAMS_ERR_DEVICE with a message naming each flag.  The flags:
  *   attention (more than one piece per row set): the pieces of one set did not all run on one XCD, so the
  *       merge could not read their partial results from its XCD's L2 -- the rows of that set are NaN.  Not
- *       expected on an MI355X (workgroup n runs on XCD n % 8).
+ *       expected on an MI355X (consecutive workgroups of a dispatch run on consecutive XCDs, so workgroups
+ *       whose ids agree mod 8 share one).
  *   a wait for another workgroup's results gave up (dreams_set_wait_limit; attention merges, sampled
  *       acceptance): that call's results are unspecified (attention rows NaN).
  * After a flagged failure, zero the workspace's counter region before it serves another call: arrivals that

@@ -65,6 +65,12 @@ __device__ __forceinline__ void raise_device_error(uint32_t* err, uint32_t bit) 
 // group) is cut into `splits` pieces.
 constexpr int kMaxNodes = 128;
 constexpr int kAttnMaxSplits = 32;
+// Fields of a row set's 64-bit merge counter: pieces started and pieces arrived (6-bit counts), a bit per
+// arrived piece, then the sum (8 bits) and sum of squares (11 bits) of the started pieces' XCD ids (0..7).
+constexpr int kCtrCountBits = 6, kCtrArrived = 6, kCtrMask = 12, kCtrXcdSum = 44, kCtrXcdSq = 52;
+static_assert(kAttnMaxSplits < (1 << kCtrCountBits) && kCtrMask + kAttnMaxSplits <= kCtrXcdSum, "count fields");
+static_assert(kAttnMaxSplits * 7 < (1 << (kCtrXcdSq - kCtrXcdSum)) && kAttnMaxSplits * 49 < (1 << (64 - kCtrXcdSq)),
+              "XCD sum fields");
 
 struct AttnArgs {
   const void* q;          // [B, Hq, T, D]

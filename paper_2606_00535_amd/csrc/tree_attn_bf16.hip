@@ -30,11 +30,13 @@
 //     counter.  A piece whose set has fully started waits for every arrival and merges its own slice of the
 //     rows; a piece that finds its set not yet fully started leaves its slice to the piece that started last,
 //     which learnt at its start which pieces had already arrived.  So a wait is only ever for a running piece.
-//     The merge goes in piece order, so the result does not depend on which piece came last.  All pieces of a set run on one XCD (below), so their rows are exchanged through that
-//     XCD's L2: plain stores, no device-scope write-through, no second launch.
-//   * Workgroup ids are remapped so that all workgroups of one (sequence, KV head) run on the same XCD
-//     (consecutive ids are dealt round-robin over the 8 XCDs): row groups reading the same keys share them
-//     in that XCD's L2.
+//     The merge goes in piece order, so the result does not depend on which piece came last.  All pieces of
+//     a set run on one XCD (below), so their rows are exchanged through that XCD's L2: plain stores, no
+//     device-scope write-through, no second launch.  Each piece adds its XCD id (and its square) to the set's
+//     counter when it starts, and a merging piece checks that they all match its own.
+//   * Workgroup ids are remapped so that all workgroups of one (sequence, KV head) share blockIdx % 8:
+//     consecutive ids of a dispatch are dealt round-robin over the 8 XCDs, so these run on one XCD (which one
+//     takes id 0 varies between dispatches), and row groups reading the same keys share them in its L2.
 #include "kernels.h"
 
 #include <math.h>
@@ -341,13 +343,17 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   }
   const int fa = min(NSS - QSS, nsp);
   for (int j = 0; j < fa; ++j) issue_super(j);
-  // This piece has started (the merge at the end relies on knowing that every piece of the set runs).  The
-  // counter's value before this start is kept (thread 0) until the epilogue: the piece that starts last finds
-  // there the pieces that arrived before the whole set was running, whose rows it then merges.
+  // This piece has started (the merge at the end relies on knowing that every piece of the set runs), on the
+  // XCD it adds to the set's sums.  The counter's value before this start is kept (thread 0) until the
+  // epilogue: the piece that starts last finds there the pieces that arrived before the whole set was running,
+  // whose rows it then merges.
   unsigned long long start_old = 0;
-  if (a.splits > 1 && tid == 0)
-    start_old = __hip_atomic_fetch_add(a.set_ctr + ((size_t)u * a.row_groups + rg) * a.ctr_stride, 1ull,
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (a.splits > 1 && tid == 0) {
+    const unsigned long long x = xcd_id();
+    start_old = __hip_atomic_fetch_add(a.set_ctr + ((size_t)u * a.row_groups + rg) * a.ctr_stride,
+                                       1ull | (x << kCtrXcdSum) | ((x * x) << kCtrXcdSq), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  }
 
   // ---- prologue: prefix length, ancestor sets, queries (all overlapping the copies above)
   int Lp = kv_len_b;
@@ -778,35 +784,44 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   }
   if (S == 1) return;
 
-  // ---- the set's merge, spread over its pieces.  One 64-bit counter word per set: pieces started (bits
-  // 0..7), pieces arrived (bits 8..15), a bit per arrived piece (16..47) and a bit for a piece that ran off the
-  // set's XCD (63).  A piece that arrives when its whole set has started waits for every arrival and merges its
-  // own slice of the rows: every piece it waits for is running and arrives without waiting for anything.  A
-  // piece that arrives earlier leaves; the piece whose start completed the set saw it among the arrived bits
-  // then, and merges its slice too (that piece arrives after the set is complete, so it never leaves).  So
-  // every wait ends, and each slice is merged once.  The last arrival puts the word back to zero for the next
-  // call; a waiting piece takes either the full count or that zero as the end of its wait.  The pieces' rows
-  // are read from this XCD's L2 (all pieces of a set share blockIdx % 8, hence the XCD).
+  // ---- the set's merge, spread over its pieces.  One 64-bit counter word per set (fields at the kCtr*
+  // shifts): pieces started, pieces arrived, a bit per arrived piece, and the sum and the sum of squares of the
+  // started pieces' XCD ids.  A piece that arrives when its whole set has started waits for every arrival and
+  // merges its own slice of the rows: every piece it waits for is running and arrives without waiting for
+  // anything.  A piece that arrives earlier leaves; the piece whose start completed the set saw it among the
+  // arrived bits then, and merges its slice too (that piece arrives after the set is complete, so it never
+  // leaves).  So every wait ends, and each slice is merged once.  The last arrival puts the word back to zero
+  // for the next call; a waiting piece takes either the full count or that zero as the end of its wait.  The
+  // pieces' rows are read from this XCD's L2: all pieces of a set share blockIdx % 8, and consecutive
+  // workgroups of a dispatch go to consecutive XCDs (which XCD takes workgroup 0 differs, e.g. between direct
+  // and graph launches).  A merging piece checks that: S ids whose sum is S x and sum of squares S x^2 all
+  // equal x, this piece's own.
   unsigned long long* ctr = a.set_ctr + pset * a.ctr_stride;
   wait_vector_memory();   // this piece's rows have reached the L2
   __syncthreads();
   if (tid == 0) {
-    const bool off_xcd = xcd_id() != (uint32_t)xcd;
-    const unsigned long long old =
-        __hip_atomic_fetch_add(ctr, (1ull << 8) | (1ull << (16 + split)) | (off_xcd ? 1ull << 63 : 0ull),
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const bool coop = (old & 0xffull) == (unsigned long long)S;
-    const bool last = ((old >> 8) & 0xffull) == (unsigned long long)(S - 1);
+    const unsigned long long old = __hip_atomic_fetch_add(
+        ctr, (1ull << kCtrArrived) | (1ull << (kCtrMask + split)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long cnt = (1ull << kCtrCountBits) - 1;
+    const bool coop = (old & cnt) == (unsigned long long)S;
+    const bool last = ((old >> kCtrArrived) & cnt) == (unsigned long long)(S - 1);
     bool good = true;
-    bool split_xcd = off_xcd || (old >> 63) != 0;
+    if (coop) {
+      const unsigned long long x = xcd_id();
+      const unsigned long long sum = (old >> kCtrXcdSum) & ((1ull << (kCtrXcdSq - kCtrXcdSum)) - 1);
+      const unsigned long long sq = old >> kCtrXcdSq;
+      if (sum != S * x || sq != S * x * x) {
+        raise_device_error(a.err, kErrXcdSplit);
+        good = false;
+      }
+    }
     if (last) {
       __hip_atomic_store(ctr, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else if (coop) {
       const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
       for (;;) {
         const unsigned long long now = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (now >> 63) split_xcd = true;
-        if (((now >> 8) & 0xffull) == (unsigned long long)S || (now & 0xffffull) == 0ull) break;
+        if (((now >> kCtrArrived) & cnt) == (unsigned long long)S || (now & cnt) == 0ull) break;
         if (__builtin_amdgcn_s_memrealtime() - t0 > a.wait_ticks) {
           raise_device_error(a.err, kErrWaitTimeout);
           good = false;
@@ -815,14 +830,11 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
         __builtin_amdgcn_s_sleep(1);
       }
     }
-    if (split_xcd) {
-      raise_device_error(a.err, kErrXcdSplit);
-      good = false;
-    }
     // slices this workgroup merges: its own (when it waited), and those of the pieces that left before this
     // piece's start completed the set
     uint32_t slices = coop ? 1u << split : 0u;
-    if ((start_old & 0xffull) == (unsigned long long)(S - 1)) slices |= (uint32_t)((start_old >> 16) & 0xffffffffull);
+    if ((start_old & cnt) == (unsigned long long)(S - 1))
+      slices |= (uint32_t)(start_old >> kCtrMask) & (uint32_t)((1ull << S) - 1);
     merge_lds = slices;
     good_lds = good ? 1u : 0u;
   }

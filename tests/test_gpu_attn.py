@@ -377,3 +377,49 @@ def test_full_size_sampled_rows(dev, name, layers):
         assert mx <= ATTN_TOL_BF16 and worst <= 1.0 and float(np.abs(l - lref).max()) <= LSE_TOL
         # property at any size: every output row is a convex combination of V rows -> bounded by max |V|
         assert float(out.float().abs().max()) <= float(v.float().abs().max()) * (1 + 2 ** -7)
+
+
+# ------------------------------------------------------------------------- graph replay
+@pytest.mark.parametrize("name", ["small", "llava7b_layer"])
+def test_graph_replay_matches_eager(dev, name):
+    # Several pieces per row set under HIP-graph replay: a graph's kernels start their round-robin over the XCDs
+    # at another XCD than direct launches do, and the merge must not depend on which.  Each replay (with eager
+    # work of other grid sizes between replays) must equal the direct call bit for bit, leave the counters zero
+    # and set no failure flag; the direct call is held to the oracle.
+    if name == "small":
+        wl = small_wl(num_q_heads=4, num_kv_heads=2, num_nodes=60, depth=6, max_branch=4, kv_len=2000)
+        splits_req = 5
+    else:
+        wl = W.WORKLOADS[name]
+        splits_req = 0
+    batch = W.make_batch(wl, with_logits=False)
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    desc = dreams.attn_desc(q, k, num_splits=splits_req)
+    splits = dreams.tree_verify_attn_splits(desc)
+    assert splits > 1
+    ws = torch.zeros(dreams.tree_verify_attn_workspace_size(desc), dtype=torch.uint8, device=dev)
+    note("%s: graph replay, splits=%d" % (name, splits))
+    out_e, lse_e, ent_e = dreams.tree_verify_attn_entropy(q, k, v, kv, par, num_splits=splits_req, workspace=ws)
+    torch.cuda.synchronize()
+    dreams.workspace_status(ws)
+    check_bf16(out_e, lse_e, batch, 0, "%s direct" % name, splits=splits)
+    out_g, lse_g, ent_g = torch.empty_like(out_e), torch.empty_like(lse_e), torch.empty_like(ent_e)
+    out_p = torch.empty_like(out_e)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dreams.tree_verify_attn(q, k, v, kv, par, out=out_p, with_lse=False, num_splits=splits_req, workspace=ws)
+        dreams.tree_verify_attn_entropy(q, k, v, kv, par, out=out_g, lse=lse_g, entropy=ent_g,
+                                        num_splits=splits_req, workspace=ws)
+    filler = torch.zeros(7 * 64 + 3, device=dev)
+    for rep in range(4):
+        for t in (out_g, out_p):
+            t.fill_(float("nan"))
+        filler.add_(1.0)
+        g.replay()
+        torch.cuda.synchronize()
+        dreams.workspace_status(ws)
+        assert np.array_equal(out_g.view(torch.int16).cpu().numpy(), out_e.view(torch.int16).cpu().numpy()), rep
+        assert np.array_equal(out_p.view(torch.int16).cpu().numpy(), out_e.view(torch.int16).cpu().numpy()), rep
+        assert np.array_equal(lse_g.cpu().numpy(), lse_e.cpu().numpy()), rep
+        assert np.array_equal(ent_g.cpu().numpy(), ent_e.cpu().numpy()), rep
+    assert not ws[:65536].cpu().numpy().any()
