@@ -207,19 +207,23 @@ __device__ __forceinline__ void merge_pieces(const AttnArgs& a, size_t prow0, in
   }
 }
 
+__device__ __forceinline__ float vmax(float x, float y) { return __builtin_elementwise_maximum(x, y); }
+
 // LDS of a workgroup: the ring, the query rows when they sit beside it, the ancestor sets and the tree as
-// copied (static), and a few words.
-template <int D, int NST>
+// copied (static), and a few words; WPC workgroups share a compute unit's 160 KB.
+template <int D, int NST, int WPC>
 constexpr bool q_beside_ring(int R) {
-  return (size_t)NST * Rows<D>::SLOT + (size_t)R * D * 2 + 4 * kMaxNodes * 8 + 64 <= 160 * 1024;
+  return (size_t)NST * Rows<D>::SLOT + (size_t)R * D * 2 + 4 * kMaxNodes * 8 + 64 <= 160 * 1024 / WPC;
 }
-template <int D, int NST>
+template <int D, int NST, int WPC>
 constexpr size_t dynamic_lds(int R) {
-  return (size_t)NST * Rows<D>::SLOT + (q_beside_ring<D, NST>(R) ? (size_t)R * D * 2 : 0);
+  return (size_t)NST * Rows<D>::SLOT + (q_beside_ring<D, NST, WPC>(R) ? (size_t)R * D * 2 : 0);
 }
 
-template <int D, int RB, int KW, int W, int NST, bool PIPE, bool ENT>
-__global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
+// WPC: workgroups meant to share a compute unit (their waves share each SIMD, so the register budget is that
+// of WPC * W / 4 waves per SIMD).
+template <int D, int RB, int KW, int W, int NST, bool PIPE, bool ENT, int WPC>
+__global__ __launch_bounds__(64 * W, WPC * W / 4) void tree_attn_bf16_kernel(AttnArgs a) {
   constexpr int WR = W / KW;          // waves per key group; each owns a different slice of the rows
   constexpr int RW = 16 * RB;         // query rows per wave
   constexpr int R = WR * RW;          // query rows per workgroup
@@ -230,7 +234,7 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   constexpr int NSS = NST / KW;       // ring slots in super-steps (KW consecutive steps, one per key group)
   // The query rows get an LDS region of their own beside the ring where it fits (so the first copies fill the
   // whole ring); otherwise they occupy the ring's last step slots until the prologue has read them.
-  constexpr bool QSEP = q_beside_ring<D, NST>(R);
+  constexpr bool QSEP = q_beside_ring<D, NST, WPC>(R);
   constexpr int QSLOTS = QSEP ? 0 : (R * L::ROW + L::SLOT - 1) / L::SLOT;   // step slots the query rows occupy
   constexpr int QSS = (QSLOTS + KW - 1) / KW;                                // ... in super-steps
   constexpr int CPS = 4 * KW * C16 / W;   // copies per wave per super-step (4*KW blocks of 16 rows)
@@ -490,6 +494,20 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
     // as the products' starting value (0 or -inf), so nothing rewrites the scores after the matrix cores
     // have written them; only steps that reach the tree slots or the piece end need it.
     f32x4 s[RB][2];
+    auto products = [&](bool from_zero) {
+      // (the products are issued at a raised wave priority, so that the SIMD's other wave -- in its softmax --
+      // does not hold them back: gqa_long 355 -> 339 us)
+      __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb)
+            s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                op.kf[kb][ds], qf[rb][ds], (from_zero && ds == 0) ? f32x4{0.f, 0.f, 0.f, 0.f} : s[rb][kb], 0, 0, 0);
+      __builtin_amdgcn_s_setprio(0);
+    };
     if (key0 + kStep > Lp || key0 + kStep > k_end) {
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
@@ -506,28 +524,20 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
           }
         }
       }
+      products(false);
     } else {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) s[rb][0] = s[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+      products(true);   // the first products start from an inline zero (no accumulator to clear)
     }
-    // (the products are issued at a raised wave priority, so that the SIMD's other wave -- in its softmax --
-    // does not hold them back: gqa_long 355 -> 339 us)
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) s[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(op.kf[kb][ds], qf[rb][ds], s[rb][kb], 0, 0, 0);
-    __builtin_amdgcn_s_setprio(0);
 
     // this lane's maximum over its 8 keys of each row, in scaled log2 units (c > 0 keeps the order)
     float lmax[RB];
     bool grow = false;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      lmax[rb] = c_scale * fmaxf(fmaxf(fmaxf(s[rb][0][0], s[rb][0][1]), fmaxf(s[rb][0][2], s[rb][0][3])),
-                                 fmaxf(fmaxf(s[rb][1][0], s[rb][1][1]), fmaxf(s[rb][1][2], s[rb][1][3])));
+      // (NaN-propagating maximum: three-input instructions, no canonicalising of the products' results; a
+      // score is never NaN, the rows past a sequence's end being zeroed)
+      lmax[rb] = c_scale * vmax(vmax(vmax(s[rb][0][0], s[rb][0][1]), vmax(s[rb][0][2], s[rb][0][3])),
+                                vmax(vmax(s[rb][1][0], s[rb][1][1]), vmax(s[rb][1][2], s[rb][1][3])));
       grow |= lmax[rb] > m_run[rb] + kLazyLog2;
     }
     // The reference maximum m only moves when some score exceeds it by more than 2^8 (the exponentials then
@@ -622,17 +632,24 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
       if (js + 1 < nsa) half_step(js + 1, op[1], op[0]);
     }
   } else {
-    for (int js = 0; js < nsa; ++js) {
-      wait_vm_steps<CPS, NSS - 2>(issued_by(js) - 1 - js);   // this wave's copies of super-step js have landed
-      zero_tail(js);
-      barrier_lds();   // super-step js complete in LDS for every wave; the slots of super-step js-1 are free
-      if (js + NSS - 1 < nsa) issue_super(js + NSS - 1);
-      const int step = js * KW + kw;   // this wave's step
-      if (step >= nact) continue;
-      Ops op;
-      read_ops(op, js);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(op, step);
+    // One pass of the inner loop per turn of the ring: the slot is a constant in each unrolled copy, so the
+    // operand reads take it as an immediate offset (no per-step address arithmetic).
+    for (int js0 = 0; js0 < nsa; js0 += NSS) {
+#pragma unroll
+      for (int sl = 0; sl < NSS; ++sl) {
+        const int js = js0 + sl;
+        if (js >= nsa) break;
+        wait_vm_steps<CPS, NSS - 2>(issued_by(js) - 1 - js);   // this wave's copies of super-step js have landed
+        zero_tail(js);
+        barrier_lds();   // super-step js complete in LDS for every wave; the slots of super-step js-1 are free
+        if (js + NSS - 1 < nsa) issue_super(js + NSS - 1);
+        const int step = js * KW + kw;   // this wave's step
+        if (step >= nact) continue;
+        Ops op;
+        read_ops(op, sl);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(op, step);
+      }
     }
   }
   wait_vm<0>();   // copies planned past a sequence's own end land before LDS is reused
@@ -849,12 +866,12 @@ __global__ __launch_bounds__(64 * W) void tree_attn_bf16_kernel(AttnArgs a) {
   }
 }
 
-template <int D, int RB, int KW, int W, int NST, bool ENT>
+template <int D, int RB, int KW, int W, int NST, int WPC, bool ENT>
 hipError_t launch_streaming(const AttnArgs& a, hipStream_t stream) {
-  constexpr size_t lds = dynamic_lds<D, NST>(16 * RB * (W / KW));
-  static_assert(lds + 2 * kMaxNodes * 8 + 2 * kMaxNodes * 8 + 64 <= 160 * 1024, "LDS budget");
+  constexpr size_t lds = dynamic_lds<D, NST, WPC>(16 * RB * (W / KW));
+  static_assert(lds + 2 * kMaxNodes * 8 + 2 * kMaxNodes * 8 + 64 <= 160 * 1024 / WPC, "LDS budget");
   // two sets of operand registers fit beside one 16-row block's state, not beside two
-  auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST, RB == 1, ENT>;
+  auto kern = tree_attn_bf16_kernel<D, RB, KW, W, NST, RB == 1, ENT, WPC>;
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -871,10 +888,10 @@ hipError_t launch_streaming(const AttnArgs& a, hipStream_t stream) {
 }
 
 // Every configuration in two builds: with the entropy term (a.entropy given) and without (no extra work).
-template <int D, int RB, int KW, int W, int NST>
+template <int D, int RB, int KW, int W, int NST, int WPC = 1>
 hipError_t launch(const AttnArgs& a, hipStream_t stream) {
-  return a.entropy ? launch_streaming<D, RB, KW, W, NST, true>(a, stream)
-                   : launch_streaming<D, RB, KW, W, NST, false>(a, stream);
+  return a.entropy ? launch_streaming<D, RB, KW, W, NST, WPC, true>(a, stream)
+                   : launch_streaming<D, RB, KW, W, NST, WPC, false>(a, stream);
 }
 
 template <int D, int NST>
@@ -883,8 +900,7 @@ hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
     case 16: return launch<D, 1, 4, 4, NST>(a, stream);
     case 32: return launch<D, 1, 4, 8, NST>(a, stream);
     case 64: return launch<D, 1, 2, 8, NST>(a, stream);
-    case 128: return launch<D, 1, 1, 8, NST>(a, stream);
-    case 256: return launch<D, 2, 1, 8, NST>(a, stream);
+    case 128: return launch<D, 2, 1, 4, NST / 2, 2>(a, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -892,10 +908,12 @@ hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
 }  // namespace
 
 // Rows per workgroup: the narrowest of 16, 32, 64 rows (4 waves in 4 key groups; 8 waves in 4 or 2 key
-// groups) that holds every row of a KV head, else 128 (all 8 waves on the same keys, several row groups).
-// Every wave owns 16 rows; 8 waves put two on each SIMD, so one's softmax overlaps the other's products.
+// groups; every wave owns 16 rows, and 8 waves put two on each SIMD, so one's softmax overlaps the other's
+// products) that holds every row of a KV head, else 128: 4 waves of 32 rows on the same keys, several row
+// groups, two workgroups per compute unit (a wave's partner on its SIMD belongs to the other workgroup, so
+// their phases are not tied by a barrier).
 int tree_attn_bf16_rows_per_wg(int rows_total) {
-  return rows_total <= 16 ? 16 : rows_total <= 32 ? 32 : rows_total <= 64 ? 64 : rows_total <= 128 ? 128 : 256;
+  return rows_total <= 16 ? 16 : rows_total <= 32 ? 32 : rows_total <= 64 ? 64 : 128;
 }
 
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream) {
