@@ -116,7 +116,7 @@ CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits)
     (128, 4, 2, 16, 4, 3, 2100, 1),    # 32 rows
     (128, 2, 2, 60, 6, 4, 3000, 2),    # 64 rows
     (128, 4, 2, 60, 6, 4, 2000, 1),    # 128 rows
-    (128, 3, 1, 60, 6, 4, 2000, 1),    # 256 rows (180)
+    (128, 3, 1, 60, 6, 4, 2000, 1),    # 128-row workgroups, 2 row groups (180 rows)
     (64, 2, 2, 60, 6, 4, 3000, 1),     # 64 rows, head_dim 64
     (64, 4, 2, 60, 6, 4, 2000, 1),     # 128 rows, head_dim 64
 ]
@@ -143,7 +143,7 @@ FUSED_CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits): grid = 8*ceil(2*Hk
     (128, 64, 64, 16, 4, 3, 400, 4),   # 16-row workgroups (4 waves): 512 workgroups
     (64, 48, 48, 60, 6, 4, 700, 3),    # 64 rows, head_dim 64: 288
     (128, 64, 32, 60, 6, 4, 600, 5),   # G=2, 128 rows: 320
-    (128, 84, 12, 128, 8, 6, 500, 3),  # G=7, 256-row workgroups, 4 row groups: 288
+    (128, 84, 12, 128, 8, 6, 500, 3),  # G=7, 128-row workgroups, 7 row groups: 504
 ]
 
 
@@ -261,7 +261,7 @@ def test_nonancestor_perturbation_bitwise(dev):
 
 
 @pytest.mark.parametrize("hq,hkv,t", [(2, 2, 60), (4, 2, 60), (3, 1, 60), (4, 2, 16)],
-                         ids=["64rows", "128rows", "256rows", "32rows"])
+                         ids=["64rows", "128rows", "128rows_2groups", "32rows"])
 def test_garbage_past_sequence_end_bitwise(dev, hq, hkv, t):
     # cache slots at or past L_b + T are not part of the problem: infinities and NaNs there change nothing
     wl = small_wl(num_q_heads=hq, num_kv_heads=hkv, num_nodes=t, depth=4, max_branch=4, kv_len=500)

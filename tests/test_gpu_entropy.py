@@ -48,7 +48,7 @@ CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits)
     (128, 2, 2, 9, 3, 3, 400, 3),       # 16 rows (4 waves, 4 key groups)
     (128, 2, 2, 60, 6, 4, 1000, 7),     # 64 rows (2 key groups)
     (128, 4, 2, 60, 6, 4, 2000, 1),     # 128 rows, long piece
-    (128, 7, 1, 128, 8, 6, 700, 2),     # 256-row workgroups (two 16-row blocks per wave), GQA
+    (128, 7, 1, 128, 8, 6, 700, 2),     # 128-row workgroups (two 16-row blocks per wave), GQA
     (64, 2, 1, 100, 8, 6, 130, 4),      # head_dim 64, T > 64
     (64, 4, 4, 16, 4, 3, 513, 0),       # head_dim 64, library's choice
     (128, 2, 2, 33, 5, 3, 0, 2),        # empty prefix
