@@ -44,6 +44,10 @@ __device__ __forceinline__ uint32_t xcd_id() {
   return x & 7u;
 }
 
+// NaN-propagating maximum (IEEE maximum): lowers to v_maximum3_f32 chains with no canonicalising of the
+// operands, where fmaxf needs both quietened first.  For maxima of scores, which are never NaN.
+__device__ __forceinline__ float vmax(float x, float y) { return __builtin_elementwise_maximum(x, y); }
+
 // ------------------------------------------------------------------------------ device-side failures
 // The last 128 bytes of every workspace's counter region hold sticky failure flags: a kernel that detects a
 // condition it cannot complete under sets a bit (device-scope atomic OR); dreams_workspace_status reports and

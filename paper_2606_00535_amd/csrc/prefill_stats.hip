@@ -207,7 +207,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void prefill_stats_kernel(PrefillAr
       bool grow = false;
 #pragma unroll
       for (int rb = 0; rb < kRB; ++rb) {
-        zmax[rb] = c * fmaxf(fmaxf(s[rb][0], s[rb][1]), fmaxf(s[rb][2], s[rb][3]));
+        zmax[rb] = c * vmax(vmax(s[rb][0], s[rb][1]), vmax(s[rb][2], s[rb][3]));
         grow |= zmax[rb] > m[rb] + kLazyLog2;
       }
       if (__any(grow)) {
@@ -236,7 +236,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void prefill_stats_kernel(PrefillAr
         const int key = kk0 + 4 * t + quad;
         z[t] = (key > row || key >= nb) ? -INFINITY : s[rb][t] * c;
       }
-      const float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+      const float zmax = vmax(vmax(z[0], z[1]), vmax(z[2], z[3]));
       if (zmax > m[rb] + kLazyLog2) rescale(m[rb], l[rb], e[rb], zmax);
       if (m[rb] != -INFINITY) {
 #pragma unroll

@@ -207,8 +207,6 @@ __device__ __forceinline__ void merge_pieces(const AttnArgs& a, size_t prow0, in
   }
 }
 
-__device__ __forceinline__ float vmax(float x, float y) { return __builtin_elementwise_maximum(x, y); }
-
 // LDS of a workgroup: the ring, the query rows when they sit beside it, the ancestor sets and the tree as
 // copied (static), and a few words; WPC workgroups share a compute unit's 160 KB.
 template <int D, int NST, int WPC>
