@@ -83,6 +83,7 @@ struct AttnPlan {
 constexpr long long kMaxSetCounters = (long long)kMaxCounters / 2;
 
 constexpr int kPieceMinKeys = 128;   // keys per piece of the key axis, at least
+constexpr int kPlanPieceKeys = 384;  // keys per piece, at least, where the library chooses the pieces
 
 constexpr int kMaxSplitsRequest = 4096;
 
@@ -132,14 +133,20 @@ dreams_status_t plan_attn(const dreams_attn_desc_t* d, AttnPlan* p) {
     int cus = 0;
     st = device_cus(&cus);
     if (st != DREAMS_OK) return st;
-    // about one workgroup per compute unit (a workgroup holds most of a compute unit's LDS)
+    // At most one workgroup per resident slot (one or two per compute unit, as the configuration's LDS allows),
+    // in pieces of at least kPlanPieceKeys keys: shorter pieces cost more in their fixed start and merge than
+    // they gain in parallel streams (llava7b_layer: 8 pieces of 400 keys 18.5 us, 16 of 200 keys 20.4 us).
+    const long long slots = (long long)cus * tree_attn_bf16_wgs_per_cu(p->rows_per_wg);
     const long long wgs = (long long)p->units * p->row_groups;
-    splits = (int)((cus + wgs / 2) / wgs);
-    // More workgroups than compute units: a last round of workgroups that fills less than half of the chip
-    // cannot keep the memory busy, so cut the key axis until it does (or the rounds come out whole).
-    if (wgs >= cus) {
+    if (wgs < slots) {
+      splits = (int)(slots / wgs);
+      const int by_len = n_keys / kPlanPieceKeys;
+      if (splits > by_len) splits = by_len;
+    } else {
+      // More workgroups than slots: a last round of workgroups that fills less than half of the chip cannot
+      // keep the memory busy, so cut the key axis until it does (or the rounds come out whole).
       splits = 1;
-      while (splits < 4 && (wgs * splits) % cus != 0 && (wgs * splits) % cus < cus / 2) ++splits;
+      while (splits < 4 && (wgs * splits) % slots != 0 && (wgs * splits) % slots < slots / 2) ++splits;
     }
   }
   if (splits > max_splits) splits = max_splits;

@@ -108,6 +108,7 @@ struct AttnArgs {
 
 // Query rows per workgroup the bf16 kernel uses for G*T rows per KV head.
 int tree_attn_bf16_rows_per_wg(int rows_total);
+int tree_attn_bf16_wgs_per_cu(int rows_per_wg);   // workgroups of that configuration per compute unit
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_tree_attn_f32(const AttnArgs& a, hipStream_t stream);
 

@@ -897,7 +897,7 @@ hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
   switch (a.rows_per_wg) {
     case 16: return launch<D, 1, 4, 4, NST>(a, stream);
     case 32: return launch<D, 1, 4, 8, NST>(a, stream);
-    case 64: return launch<D, 1, 2, 8, NST>(a, stream);
+    case 64: return launch<D, 2, 2, 4, NST / 2, 2>(a, stream);
     case 128: return launch<D, 2, 1, 4, NST / 2, 2>(a, stream);
   }
   return hipErrorInvalidValue;
@@ -905,14 +905,17 @@ hipError_t launch_for_rows(const AttnArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-// Rows per workgroup: the narrowest of 16, 32, 64 rows (4 waves in 4 key groups; 8 waves in 4 or 2 key
-// groups; every wave owns 16 rows, and 8 waves put two on each SIMD, so one's softmax overlaps the other's
-// products) that holds every row of a KV head, else 128: 4 waves of 32 rows on the same keys, several row
-// groups, two workgroups per compute unit (a wave's partner on its SIMD belongs to the other workgroup, so
-// their phases are not tied by a barrier).
+// Rows per workgroup: the narrowest of 16 and 32 rows (4 waves in 4 key groups, 8 waves in 4 key groups; every
+// wave owns 16 rows, and 8 waves put two on each SIMD, so one's softmax overlaps the other's products) and 64
+// rows (4 waves of 32 rows in 2 key groups) that holds every row of a KV head, else 128: 4 waves of 32 rows on
+// the same keys, several row groups.  The 64- and 128-row workgroups take half a compute unit's LDS, so two
+// share a compute unit (a wave's partner on its SIMD belongs to the other workgroup, so their phases are not
+// tied by a barrier).
 int tree_attn_bf16_rows_per_wg(int rows_total) {
   return rows_total <= 16 ? 16 : rows_total <= 32 ? 32 : rows_total <= 64 ? 64 : 128;
 }
+
+int tree_attn_bf16_wgs_per_cu(int rows_per_wg) { return rows_per_wg >= 64 ? 2 : 1; }
 
 hipError_t launch_tree_attn_bf16(const AttnArgs& a, hipStream_t stream) {
   if (a.D == 128) return launch_for_rows<128, 8>(a, stream);
