@@ -323,6 +323,7 @@ dreams_status_t verify_attn(const dreams_attn_desc_t* desc, const void* q, const
   a.row_groups = p.row_groups;
   a.splits = p.splits;
   a.max_keys = (desc->max_kv_len > 0 ? desc->max_kv_len : desc->cache_capacity - desc->num_nodes) + desc->num_nodes;
+  a.piece_by_len = desc->batch > 1 && p.splits > 1 ? 1 : 0;
   a.scale_log2 = desc->scale * 1.4426950408889634f;
   hipError_t e = desc->dtype == DREAMS_F32 ? launch_tree_attn_f32(a, stream) : launch_tree_attn_bf16(a, stream);
   if (e != hipSuccess) return hip_fail(e, "tree attention launch");

@@ -103,6 +103,7 @@ struct AttnArgs {
   int row_groups;         // ceil(G*T / rows_per_wg)
   int splits;
   int max_keys;           // host-side bound on L_b + T over the batch (plans the pieces of the key axis)
+  int piece_by_len;       // 1: each sequence's pieces are cut from its own L_b + T (read before the first copies)
   float scale_log2;       // scale * log2(e)
 };
 

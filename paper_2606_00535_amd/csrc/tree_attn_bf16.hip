@@ -267,11 +267,15 @@ __global__ __launch_bounds__(64 * W, WPC * W / 4) void tree_attn_bf16_kernel(Att
   const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(lds_addr(ring));
   const int kv_len_b = a.kv_len[b];   // issued before the copies below, ahead of their traffic
 
-  // ---- this workgroup's piece of the key axis, planned from the host's bound on the key count
-  int piece = (a.max_keys + a.splits - 1) / a.splits;
+  // ---- this workgroup's piece of the key axis, planned from the host's bound on the key count, or (several
+  // sequences of different lengths) from this sequence's own count, so that a short sequence's pieces are
+  // shorter rather than its last piece nearly empty; the first copies then wait for its length
+  int keys = a.max_keys;
+  if (a.piece_by_len) keys = min(max(kv_len_b, 0), a.S_cap - T) + T;
+  int piece = (keys + a.splits - 1) / a.splits;
   piece = (piece + kStep - 1) / kStep * kStep;
   const int k_begin = split * piece;
-  const int k_end_plan = split == a.splits - 1 ? a.max_keys : min(a.max_keys, k_begin + piece);
+  const int k_end_plan = split == a.splits - 1 ? keys : min(keys, k_begin + piece);
   const int nplan = k_end_plan > k_begin ? (k_end_plan - k_begin + kStep - 1) / kStep : 0;
   const int nsp = (nplan + KW - 1) / KW;
   const unsigned char* kbase = (const unsigned char*)a.k + (size_t)u * a.S_cap * L::ROW;
