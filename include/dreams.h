@@ -346,8 +346,8 @@ dreams_status_t dreams_tree_accept(int32_t batch, int32_t num_nodes, int32_t voc
 /* Bytes of workspace dreams_tree_accept_sampled needs (0 only when batch is 0).  DREAMS_ERR_UNSUPPORTED if
  * vocab exceeds 2^23 or if the arrival counters (one word per sequence, then 16 bytes per row: batch *
  * num_nodes rows) do not fit in DREAMS_WORKSPACE_COUNTER_BYTES - 128 (about 4000 rows).  After the counters: per row
- * 8 bytes of flags plus 40 bytes per piece of the vocabulary (pieces of 2048 entries, or of 8192 once
- * batch * num_nodes * ceil(vocab / 2048) exceeds 4096). */
+ * 8 bytes of flags plus 40 bytes per piece of the vocabulary (pieces of 4096 entries, or of 8192 once
+ * batch * num_nodes * ceil(vocab / 4096) exceeds 4096). */
 dreams_status_t dreams_tree_accept_sampled_workspace_size(int32_t batch, int32_t num_nodes, int32_t vocab,
                                                           size_t* bytes);
 

@@ -193,15 +193,16 @@ struct AcceptArgs {
 hipError_t launch_tree_accept(const AcceptArgs& a, hipStream_t stream);
 
 // ------------------------------------------------------------------------------- sampled acceptance
-// Every row of B * T vocabulary rows is cut into pieces of sub_pieces * 2048 entries; in each 2048-entry
-// sub-piece a thread holds kSampledPerThread consecutive entries.  With one-part pieces the launch has one
-// workgroup per piece of every row, in row order: the piece's statistics, then the residual masses and accept
-// decisions of the row's children, then (one piece per row) the token emitted if the walk ends there.  With
-// four-part pieces (many pieces) it has, in blockIdx order, first one per piece of every row ("stats" pieces:
-// maxima and normalisers), then one per piece of every child node c, by c ("pass" pieces: the residual mass
-// after c's rejection, and c's own accept decision).
+// Every row of B * T vocabulary rows is cut into pieces.  With one-part pieces (4096 entries, a thread holding
+// kSampledPerThreadRow consecutive entries) the launch has one workgroup per piece of every row, in row order:
+// the piece's statistics, then the residual masses and accept decisions of the row's children, then (one
+// piece per row) the token emitted if the walk ends there.  With four-part pieces (many pieces: 4 sub-pieces
+// of 2048 entries, a thread holding kSampledPerThread consecutive entries of each) it has, in blockIdx order,
+// first one per piece of every row ("stats" pieces: maxima and normalisers), then one per piece of every
+// child node c, by c ("pass" pieces: the residual mass after c's rejection, and c's own accept decision).
 constexpr int kSampledThreads = 256;
 constexpr int kSampledPerThread = 8;
+constexpr int kSampledPerThreadRow = 16;
 constexpr int kSampledSubLarge = 4;         // sub-pieces per piece for problems of many pieces (else 1)
 constexpr int kSampledMaxChunks = 1024;     // pieces per row, at most
 

@@ -175,14 +175,15 @@ __device__ __forceinline__ double block_exclusive_scan(double v, double& total, 
 }
 
 // A piece is SUB sub-pieces of NT * EPT entries.  In a sub-piece starting at x0, thread t holds entries
-// x0 + t * EPT + e (e < EPT); entries at or past x1 read as -inf.
+// x0 + t * EPT + e (e < EPT); entries at or past x1 read as -inf.  (The split form's EPT; the row-piece form
+// holds kSampledPerThreadRow entries a thread.)
 constexpr int EPT = kSampledPerThread, SUBW = NT * EPT;
-template <bool VEC>
-__device__ __forceinline__ void load_sub(const float* row, int x0, int x1, float (&v)[EPT]) {
-  const int base = x0 + (int)threadIdx.x * EPT;
+template <bool VEC, int E>
+__device__ __forceinline__ void load_sub(const float* row, int x0, int x1, float (&v)[E]) {
+  const int base = x0 + (int)threadIdx.x * E;
   if (VEC) {
 #pragma unroll
-    for (int k = 0; k < EPT / 4; ++k) {
+    for (int k = 0; k < E / 4; ++k) {
       const int x = base + 4 * k;   // x0, x1 and x are multiples of 4: a vector is wholly in or out
       f32x4 r = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
       if (x < x1) r = *(const f32x4*)(row + x);
@@ -191,7 +192,7 @@ __device__ __forceinline__ void load_sub(const float* row, int x0, int x1, float
     }
   } else {
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) v[e] = base + e < x1 ? row[base + e] : -INFINITY;
+    for (int e = 0; e < E; ++e) v[e] = base + e < x1 ? row[base + e] : -INFINITY;
   }
 }
 
@@ -671,8 +672,9 @@ __device__ void pass_piece(const SampledArgs& a, int b, int c, int j, Shared& sh
 
 // ------------------------------------------------------------------------------------------- row pieces
 // Workgroup (b, n, j): piece j of row n.  Its logits stay in registers for the whole call.
-template <bool VEC, int SUB>
+template <bool VEC, int SUB, int E>
 __device__ void row_piece(const SampledArgs& a, int b, int n, int j, Shared& sh) {
+  constexpr int EPT = E, SUBW = NT * E;   // (this form's entries per thread and per sub-piece)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = a.T, V = a.V;
   const size_t rb = (size_t)b * T, row = rb + n;
@@ -975,7 +977,7 @@ __global__ __launch_bounds__(NT) void tree_accept_sampled_kernel(SampledArgs a) 
   const long long t = blockIdx.x;
   const int j = (int)(t % a.chunks);
   const long long r = t / a.chunks;
-  row_piece<VEC, SUB>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
+  row_piece<VEC, SUB, kSampledPerThreadRow>(a, (int)(r / a.T), (int)(r % a.T), j, sh);
 }
 
 template <bool VEC, int SUB>

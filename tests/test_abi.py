@@ -260,7 +260,7 @@ def test_sampled_accept_rejections_and_sizes(D):
 
     for B, T, V in [(1, 60, 32000), (16, 128, 152064), (3, 1, 1), (2, 7, 2049)]:
         assert lib.dreams_tree_accept_sampled_workspace_size(B, T, V, ctypes.byref(n)) == 0
-        rows, chunks = B * T, (V + 2047) // 2048
+        rows, chunks = B * T, (V + 4095) // 4096
         if rows * chunks > 4096:           # large pieces
             chunks = (V + 8191) // 8192
         assert n.value == 65536 + r256(rows * chunks * 32) + r256(rows * chunks * 8) + r256(rows * 8)

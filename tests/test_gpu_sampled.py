@@ -181,7 +181,7 @@ def test_large_pieces(dev, V):
     ragged last piece whose trailing sub-pieces lie wholly past the vocabulary; V = 20001 takes the scalar
     loads."""
     B, T = 30, 128
-    assert B * T * ((V + 2047) // 2048) > 4096
+    assert B * T * ((V + 4095) // 4096) > 4096
     rng = np.random.default_rng(V)
     tl, dl, tok, par, uni = random_case(rng, B, T, V, 8, 6, noise=0.7)
     run_and_compare(dev, tl, dl, tok, par, uni, 1.0, "large pieces V=%d" % V)
