@@ -95,6 +95,46 @@ def test_tiny_fp32_variants(dev, variant):
     assert err <= ATTN_TOL_F32
 
 
+
+F32_CASES = [  # (D, Hq, Hkv, T, depth, branch, L, mask input, empty row)
+    (128, 4, 2, 100, 8, 6, 300, False, False),    # head_dim 128, GQA, T > 64 (second ancestor word)
+    (64, 2, 1, 33, 5, 3, 0, True, True),          # empty prefix, mask input with an all-zero row
+    (128, 3, 3, 1, 0, 1, 1000, False, False),     # single node, more keys than a row's threads
+    (64, 6, 2, 60, 6, 4, 1300, False, False),     # head_dim 64, several rounds of keys per thread
+]
+
+
+@pytest.mark.parametrize("case", F32_CASES, ids=lambda c: "D%d_Hq%d_Hkv%d_T%d_L%d_mask%d" % (c[0], c[1], c[2], c[3], c[6], c[7]))
+def test_fp32_path(dev, case):
+    # the fp32 kernel over shapes beyond the tiny workload: every row against the oracle
+    from pins import ancestor_closure, mask_bits_from_closure
+    D, Hq, Hkv, T, depth, br, L, use_mask, empty_row = case
+    wl = small_wl(head_dim=D, num_q_heads=Hq, num_kv_heads=Hkv, num_nodes=T, depth=depth, max_branch=br,
+                  kv_len=L, dtype="f32")
+    batch = W.make_batch(wl, with_logits=False, kv_lens=[L, max(0, L - 37)])
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    note("fp32 path %s" % (case,))
+    bits = None
+    if use_mask:
+        bits = np.stack([mask_bits_from_closure(ancestor_closure(batch.parent[b])) for b in range(wl.batch)])
+        if empty_row:
+            bits[:, T // 2] = 0
+        out, lse = dreams.tree_verify_attn(q, k, v, kv, None, tree_mask=to_dev(bits.view(np.int64), dev))
+    else:
+        out, lse = dreams.tree_verify_attn(q, k, v, kv, par)
+    torch.cuda.synchronize()
+    ref, lref = oracle.tree_attn(f32(batch.q[0]), f32(batch.k_cache[0]), f32(batch.v_cache[0]), batch.kv_len,
+                                 None if use_mask else batch.parent, batch.scale, Hkv, tree_mask=bits)
+    o = out.cpu().numpy()
+    l = lse.cpu().numpy()
+    live = np.isfinite(lref)
+    assert np.array_equal(np.isfinite(l), live)
+    err = float(np.abs(o - ref).max())
+    lerr = float(np.abs(l[live] - lref[live]).max()) if live.any() else 0.0
+    note("  max_abs=%.3e lse=%.3e" % (err, lerr))
+    assert err <= ATTN_TOL_F32 and lerr <= 1e-4
+
+
 CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits)
     (128, 4, 2, 16, 4, 3, 300, 0),
     (128, 4, 2, 16, 4, 3, 300, 1),
