@@ -8,7 +8,10 @@
 //   * A workgroup of W waves (4 or 8) owns R query rows of one KV head (the rows of the G query heads sharing it
 //     are packed: row r -> head r / T, node r % T, which is also their order in memory) and one piece of that
 //     head's key axis.  Each wave owns 16*RB rows of its key group (below) for every key the group takes, and
-//     every K/V byte the workgroup reads serves all of its rows.
+//     every K/V byte the workgroup reads serves all of its rows.  The 64- and 128-row configurations take at
+//     most half of a compute unit's LDS and registers (WPC = 2), so two workgroups share a compute unit.
+//   * The pieces are cut from the host's bound on the key count (the first copies need nothing from the
+//     device), or, with several sequences, from each sequence's own count.
 //   * K/V stream through a ring of NST step slots in LDS (a step = 32 keys: 32 K rows then 32 V rows).  The
 //     waves copy their share of every step straight from global memory into LDS (global_load_lds_dwordx4: no
 //     registers in between), a whole ring ahead.  One barrier per super-step hands a landed step to all waves;
