@@ -347,6 +347,19 @@ def test_mask_input_matches_parent_and_empty_rows(dev):
     assert np.max(np.abs(o3n - ref)) <= ATTN_TOL_BF16 and np.max(np.abs(l3.cpu().numpy()[ok] - lref[ok])) <= LSE_TOL
 
 
+
+@pytest.mark.parametrize("splits", [2, 4, 7])
+def test_pieces_cut_per_sequence_length(dev, splits):
+    # several sequences of very different lengths (one with no prefix): each sequence's key axis is cut into
+    # pieces of its own length, so a short sequence has short or empty pieces; every row against the oracle
+    wl = small_wl(num_q_heads=4, num_kv_heads=2, num_nodes=60, depth=6, max_branch=4, kv_len=2600, batch=3)
+    batch = W.make_batch(wl, with_logits=False, kv_lens=[0, 2600, 45])
+    q, k, v, kv, par = layer_tensors(batch, 0, dev)
+    note("pieces per sequence length, splits=%d" % splits)
+    out, lse = dreams.tree_verify_attn(q, k, v, kv, par, num_splits=splits)
+    torch.cuda.synchronize()
+    check_bf16(out, lse, batch, 0, "pieces per sequence length S=%d" % splits, splits=splits_of(q, k, splits))
+
 def test_kv_len_clamped_into_cache(dev):
     # a prefix length past the capacity is clamped to S_cap - T: same result as that length, no stray access
     wl = small_wl(num_nodes=16, kv_len=300)
