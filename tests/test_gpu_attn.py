@@ -159,6 +159,11 @@ CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits)
     (128, 3, 1, 60, 6, 4, 2000, 1),    # 128-row workgroups, 2 row groups (180 rows)
     (64, 2, 2, 60, 6, 4, 3000, 1),     # 64 rows, head_dim 64
     (64, 4, 2, 60, 6, 4, 2000, 1),     # 128 rows, head_dim 64
+    # more (sequence, KV head) sets than compute units: 16- and 32-row workgroups in several rounds (short
+    # prefixes, so one piece each: the key-axis pieces of these shapes are covered below)
+    (128, 320, 320, 9, 3, 3, 200, 0),  # 16 rows, 640 sets
+    (128, 320, 160, 16, 4, 3, 200, 0), # 32 rows (G=2), 320 sets
+    (64, 300, 300, 16, 4, 3, 200, 0),  # 16 rows, head_dim 64
 ]
 
 
@@ -184,6 +189,8 @@ FUSED_CASES = [  # (D, Hq, Hkv, T, depth, branch, L, splits): grid = 8*ceil(2*Hk
     (64, 48, 48, 60, 6, 4, 700, 3),    # 64 rows, head_dim 64: 288
     (128, 64, 32, 60, 6, 4, 600, 5),   # G=2, 128 rows: 320
     (128, 84, 12, 128, 8, 6, 500, 3),  # G=7, 128-row workgroups, 7 row groups: 504
+    (128, 320, 320, 9, 3, 3, 900, 3),  # 16-row workgroups, 3 pieces: 1920
+    (64, 320, 160, 16, 4, 3, 800, 2),  # 32-row workgroups, head_dim 64: 640
 ]
 
 
