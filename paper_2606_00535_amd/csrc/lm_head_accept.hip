@@ -12,7 +12,8 @@
 // lm_head_argmax_big_kernel (more than 64 rows): 256 vocabulary entries by 128 or 256 rows per workgroup, both
 // operands through a shared LDS ring (see below).
 // lm_head_finish_kernel: a workgroup of 16 waves per sequence merges every row's candidates over the tiles
-// (the row's argmax) and one wave runs the greedy path scan on them.
+// (the row's argmax; 4 rows a wave with all their loads in flight) and one wave runs the greedy path scan on
+// them.
 #include "accept_scan.h"
 #include "kernels.h"
 
@@ -79,7 +80,7 @@ __device__ __forceinline__ void barrier_lds() {
 // hands a landed stage to every wave and frees the oldest.  Each operand tile is read from the caches once
 // per 64 WR rows or 64 WN entries instead of once per 64.
 
-constexpr int FIN_THREADS = 1024, FIN_WAVES = FIN_THREADS / 64, FIN_PER = 8;
+constexpr int FIN_THREADS = 1024, FIN_WAVES = FIN_THREADS / 64, FIN_PER = 4, FIN_ROWS = 4;
 
 __device__ __forceinline__ void best_of_batch(const float* pv, const int* px, int p0, int n, int lane, float& v,
                                               int& x) {
@@ -118,23 +119,30 @@ __global__ __launch_bounds__(FIN_THREADS) void lm_head_finish_kernel(LmHeadArgs 
     tok_s[threadIdx.x] = a.tokens[(size_t)b * T + threadIdx.x];
     par_s[threadIdx.x] = a.parent[(size_t)b * T + threadIdx.x];
   }
-  for (int i = wave; i < T; i += 2 * FIN_WAVES) {
-    const int j = i + FIN_WAVES;   // the second row of the pair (may be past T)
-    const size_t ri = (size_t)b * T + i, rj = (size_t)b * T + min(j, T - 1);
-    float vi = -INFINITY, vj = -INFINITY;
-    int xi = INT_MAX, xj = INT_MAX;
-    for (int p0 = 0; p0 < n; p0 += FIN_PER * 64) {
-      best_of_batch(a.part_val + ri * n, a.part_idx + ri * n, p0, n, lane, vi, xi);
-      best_of_batch(a.part_val + rj * n, a.part_idx + rj * n, p0, n, lane, vj, xj);
+  // FIN_ROWS rows a wave at a time (rows past T read row T - 1 and are dropped), every load of a batch in
+  // flight together: up to 64 rows in one round of memory latency
+  for (int i0 = wave; i0 < T; i0 += FIN_ROWS * FIN_WAVES) {
+    float v[FIN_ROWS];
+    int x[FIN_ROWS];
+#pragma unroll
+    for (int r = 0; r < FIN_ROWS; ++r) {
+      v[r] = -INFINITY;
+      x[r] = INT_MAX;
     }
-    wave_best(vi, xi);
-    wave_best(vj, xj);
-    if (lane == 0) {
-      am_s[i] = xi;
-      if (a.target_argmax) a.target_argmax[ri] = xi;
-      if (j < T) {
-        am_s[j] = xj;
-        if (a.target_argmax) a.target_argmax[rj] = xj;
+    for (int p0 = 0; p0 < n; p0 += FIN_PER * 64) {
+#pragma unroll
+      for (int r = 0; r < FIN_ROWS; ++r) {
+        const size_t ri = (size_t)b * T + min(i0 + r * FIN_WAVES, T - 1);
+        best_of_batch(a.part_val + ri * n, a.part_idx + ri * n, p0, n, lane, v[r], x[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < FIN_ROWS; ++r) {
+      const int i = i0 + r * FIN_WAVES;
+      wave_best(v[r], x[r]);
+      if (lane == 0 && i < T) {
+        am_s[i] = x[r];
+        if (a.target_argmax) a.target_argmax[(size_t)b * T + i] = x[r];
       }
     }
   }
