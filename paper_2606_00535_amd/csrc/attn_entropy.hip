@@ -13,18 +13,7 @@ constexpr int kMeanThreads = 256;
 __global__ __launch_bounds__(kMeanThreads) void attn_entropy_mean_kernel(long long count, const float* e, float* ae) {
   __shared__ double part[kMeanThreads];
   double acc = 0.0;
-  // each thread's entries in index order, 8 loads in flight at a time (the order of the adds is unchanged)
-  for (long long i0 = threadIdx.x; i0 < count; i0 += 8LL * kMeanThreads) {
-    float x[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const long long i = i0 + (long long)k * kMeanThreads;
-      x[k] = i < count ? e[i] : 0.f;
-    }
-#pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (i0 + (long long)k * kMeanThreads < count) acc += (double)x[k];
-  }
+  for (long long i = threadIdx.x; i < count; i += kMeanThreads) acc += (double)e[i];
   part[threadIdx.x] = acc;
   __syncthreads();
   for (int w = kMeanThreads / 2; w >= 1; w >>= 1) {

@@ -298,18 +298,7 @@ __global__ __launch_bounds__(1024) void prefill_entropy_mean_kernel(int B, int H
   __shared__ double part[1024];
   const long long total = (long long)B * Hq * N;
   double s = 0.0;
-  // each thread's rows in index order, 8 loads in flight at a time (the order of the adds is unchanged)
-  for (long long i0 = threadIdx.x; i0 < total; i0 += 8LL * blockDim.x) {
-    float x[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const long long i = i0 + (long long)k * blockDim.x;
-      x[k] = i < total ? entropy[i] : 0.f;
-    }
-#pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (i0 + (long long)k * blockDim.x < total) s += (double)x[k];
-  }
+  for (long long i = threadIdx.x; i < total; i += blockDim.x) s += (double)entropy[i];
   part[threadIdx.x] = s;
   __syncthreads();
   for (int w = 512; w > 0; w >>= 1) {
