@@ -1,4 +1,4 @@
-"""Every verb but the KV commit (which moves the cache, so a replay is not a repeat) under HIP-graph replay.
+"""Every verb under HIP-graph replay (the KV commit, which moves the cache in place, from a restored cache).
 
 A graph's kernels start their round-robin over the XCDs at another XCD than direct launches do, and every
 cross-workgroup hand-off here (arrival counters, pieces merged in the same launch) must not depend on which.
@@ -186,3 +186,56 @@ def test_prefill_statistics(dev):
              torch.empty((B, 1000), device=dev)]
     chain(eager)
     replay_matches_eager(dev, chain, eager, [ws], "prefill statistics")
+
+
+def test_accept_then_commit(dev):
+    # the end of a verify step in one graph: greedy acceptance, then the accepted path's K/V moved into place in
+    # every layer; the cache is restored between replays (the commit is in place, so a replay is a repeat only
+    # from the same cache)
+    NL, B, Hkv, S_cap, D, T, V = 4, 2, 8, 1024, 128, 60, 4099
+    rng = np.random.default_rng(75)
+    g = torch.Generator(device=dev)
+    g.manual_seed(75)
+    kv = to_dev(np.array([700, 650], np.int32), dev)
+    par_h = random_tree(rng, B, T, 6, 4)
+    logits = (rng.standard_normal((B, T, V)) * 3).astype(np.float32)
+    am = logits.argmax(axis=2)
+    tok = np.where(rng.random((B, T)) < 0.8, am[np.arange(B)[:, None], np.maximum(par_h, 0)],
+                   rng.integers(0, V, (B, T))).astype(np.int32)
+    tl, tk, pr = to_dev(logits, dev), to_dev(tok, dev), to_dev(par_h, dev)
+    k0 = torch.randn((NL, B, Hkv, S_cap, D), generator=g, device=dev).to(torch.bfloat16)
+    v0 = torch.randn((NL, B, Hkv, S_cap, D), generator=g, device=dev).to(torch.bfloat16)
+    ws = torch.zeros(dreams.tree_accept_workspace_size(B, T, V), dtype=torch.uint8, device=dev)
+    kc, vc = k0.clone(), v0.clone()
+
+    def chain(o):
+        alen, path, nxt, kv_out = o
+        dreams.tree_accept(tl, tk, pr, outputs=(alen, path, nxt, None), workspace=ws)
+        dreams.kv_commit(kc, vc, kv, path, alen, kv_len_out=kv_out)
+
+    eager = [torch.empty(B, dtype=torch.int32, device=dev), torch.empty((B, T), dtype=torch.int32, device=dev),
+             torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, dtype=torch.int32, device=dev)]
+    chain(eager)
+    torch.cuda.synchronize()
+    dreams.workspace_status(ws)
+    note("accept then commit: accepted %s, lengths %s" % (eager[0].cpu().numpy(), eager[3].cpu().numpy()))
+    k_ref, v_ref = bits(kc), bits(vc)
+    ref = [bits(t) for t in eager]
+    outs = [torch.empty_like(t) for t in eager]
+    kc.copy_(k0)
+    vc.copy_(v0)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        chain(outs)
+    for rep in range(REPLAYS):
+        kc.copy_(k0)
+        vc.copy_(v0)
+        for t in outs:
+            spoil(t)
+        graph.replay()
+        torch.cuda.synchronize()
+        dreams.workspace_status(ws)
+        for i, (t, r) in enumerate(zip(outs, ref)):
+            assert np.array_equal(bits(t), r), "output %d differs on replay %d" % (i, rep)
+        assert np.array_equal(bits(kc), k_ref) and np.array_equal(bits(vc), v_ref), "cache differs on replay %d" % rep
+    note("accept then commit: %d replays equal the eager call" % REPLAYS)
